@@ -1,0 +1,239 @@
+/*
+ * hoccl.h -- C ABI of libhoccl, an MI355X (gfx950) implementation of the
+ * hot path behind HOCCL's collectives: the chunked data movement and the
+ * element-wise reduction of ring reduce-scatter, all-gather and all-reduce,
+ * point-to-point send/recv and all-to-all(v).
+ *
+ * Setting.  One process drives one GPU.  A collective runs across R "virtual
+ * ranks" whose buffers all live in that GPU's memory: rank r's buffer is
+ * simply the r-th pointer of an array.  The paper's setting spans many GPUs;
+ * here every ring hop, every point-to-point flow and every all-to-all block
+ * becomes a copy or a reduction between two regions of one HBM.
+ *
+ * Two execution paths, as in the paper's design (System Design, Overview):
+ *   - pure-copy steps go to the SDMA copy engines, so they occupy no compute
+ *     unit (the zero-SM point-to-point executor, here "zero-CU");
+ *   - reduction steps, which the paper leaves to SM-side execution
+ *     (Limitations), run as gfx950 HIP kernels with an explicit workgroup
+ *     budget.
+ * Operator order with the caller's stream is kept by a stream manager
+ * (Stream Manager section): HIP event fork/join for the HIP copy path, and
+ * the start/finish flag handshake through host memory for the path in which
+ * a CPU proxy thread drives the SDMA engines itself.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  `send` and `recv` are HOST arrays of R DEVICE pointers.  The
+ *   arrays are read during the call only; the device buffers are owned by the
+ *   caller, must stay valid until the operation completes on `stream`, and
+ *   are never retained by the library after that.
+ * Counts are in elements of `dtype`.  For copy-only collectives the dtype
+ *   only sets the element size (4 bytes for int32/fp32, 2 for bf16) and the
+ *   bytes are moved bit for bit.
+ * Asynchrony.  Every call returns once the work is enqueued.  The operation
+ *   starts after all work previously enqueued on `stream` and all work
+ *   enqueued on `stream` afterwards sees its results.  No call synchronises
+ *   the host with the device except where stated (workspace growth).
+ * Errors.  Every function returns a hoccl_status_t and never throws.
+ *   Argument errors are detected before anything is enqueued.  A failing HIP
+ *   or HSA call returns HOCCL_ERR_HIP; hoccl_last_error_string() describes
+ *   it.  Faults of the device work itself surface at the caller's own
+ *   synchronisation.  `count == 0` is a successful no-op.  There is no
+ *   sticky error state.
+ * Threads.  One host thread at a time may call into the library per device.
+ *   Collectives issued on different streams that overlap in time are
+ *   ordered by the library where they share its workspace.
+ * In-place forms (the only allowed overlaps between send and recv):
+ *   all-reduce      send[r] == recv[r];
+ *   all-gather      send[r] == recv[r] + r * sendcount elements;
+ *   reduce-scatter  recv[r] == send[r] + r * recvcount elements.
+ *   All other collectives are out-of-place only.
+ * Alignment.  Any element-aligned pointer is accepted; 16-byte aligned
+ *   buffers take the vectorised fast path.
+ */
+#ifndef HOCCL_H
+#define HOCCL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HOCCL_OK = 0,
+    HOCCL_ERR_INVALID_ARG = 1, /* bad pointer, count, R, dtype, peer map or overlap */
+    HOCCL_ERR_UNSUPPORTED = 2, /* valid request this build cannot serve            */
+    HOCCL_ERR_HIP = 3,         /* a HIP / HSA runtime call failed                   */
+    HOCCL_ERR_NO_MEMORY = 4,   /* workspace or host allocation failed               */
+    HOCCL_ERR_TIMEOUT = 5,     /* the copy proxy's watchdog expired                 */
+    HOCCL_ERR_INTERNAL = 6
+} hoccl_status_t;
+
+typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2 } hoccl_dtype_t;
+
+/* Where pure-copy steps run. */
+typedef enum {
+    HOCCL_COPY_AUTO = 0,         /* SDMA_ENGINES when available, else SDMA     */
+    HOCCL_COPY_SDMA = 1,         /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
+                                    library's copy streams; HIP picks engines  */
+    HOCCL_COPY_SDMA_ENGINES = 2, /* a CPU proxy thread issues each chunk on an
+                                    explicitly chosen SDMA engine (ROCr) and
+                                    releases the stream by flag handshake      */
+    HOCCL_COPY_KERNEL = 3        /* CU copy kernel with workgroups_per_step
+                                    workgroups (comparator / fallback)         */
+} hoccl_copy_path_t;
+
+/* How reduce-scatter / all-reduce reduce. */
+typedef enum {
+    HOCCL_REDUCE_RING = 0,  /* R-1 ring steps, one kernel launch per step over
+                               all ranks; fp32 partials for bf16               */
+    HOCCL_REDUCE_DIRECT = 1 /* one launch folds all R inputs in the same ring
+                               order (bit-identical result, fewer HBM bytes)   */
+} hoccl_reduce_algo_t;
+
+typedef struct {
+    int workgroups_per_step;    /* workgroups per reduce / CU-copy launch;
+                                   0 = automatic (fills the chip)              */
+    int threads_per_workgroup;  /* 64..1024, multiple of 64; 0 = 256           */
+    size_t chunk_bytes;         /* split SDMA copies into pieces of this size;
+                                   0 = no split                                */
+    int copy_streams;           /* internal copy streams, 1..16; 0 = 8         */
+    int sdma_engines;           /* engines used by SDMA_ENGINES, 0 = all       */
+    hoccl_copy_path_t copy_path;
+    int allgather_direct;       /* 1: every rank copies each shard from its
+                                   owner; 0: ring forwarding r -> r+1          */
+    int allreduce_chunk_groups; /* split each all-reduce ring chunk into this
+                                   many groups so the gather of group g
+                                   overlaps the reduction of group g+1; 0 = 1  */
+    hoccl_reduce_algo_t reduce_algo;
+    int kernel_timing;          /* 1: record HIP events around every reduce /
+                                   copy kernel launch (hoccl_get_kernel_times) */
+    unsigned int proxy_timeout_ms; /* watchdog of the SDMA_ENGINES proxy;
+                                   0 = 10000                                   */
+} hoccl_config_t;
+
+typedef struct {
+    int reduce_launches;        /* reduction kernel launches enqueued          */
+    int copy_kernel_launches;   /* CU copy kernel launches enqueued            */
+    int copy_ops;               /* SDMA copy commands issued                   */
+    int workgroups_per_step;    /* workgroups per launch actually used         */
+    int cus_available;          /* compute units of the device                 */
+    int cus_used_max;           /* upper bound on CUs occupied by this call:
+                                   min(workgroups, CUs); 0 for pure SDMA       */
+    hoccl_copy_path_t copy_path_used;
+    hoccl_reduce_algo_t reduce_algo_used;
+    unsigned long long hbm_bytes_algorithmic; /* bytes every step must read
+                                   and write in HBM, summed over the call      */
+    unsigned long long copy_bytes;             /* bytes moved by copy steps   */
+    double host_enqueue_us;     /* host time spent inside the call             */
+} hoccl_stats_t;
+
+/* Initialise the library on `device` (the current HIP device if < 0):
+ * creates the internal copy streams, the event pool and, when the SDMA
+ * engines can be driven directly, the proxy thread and its flag pool.
+ * Reads HOCCL_* environment variables into the configuration.  Optional:
+ * every collective initialises lazily on the current device. */
+hoccl_status_t hoccl_init(int device);
+
+/* Waits for the device, then releases streams, events, workspace, the proxy
+ * thread and the flag pool.  A later call re-initialises. */
+hoccl_status_t hoccl_finalize(void);
+
+/* Replace / read the configuration.  Invalid fields give
+ * HOCCL_ERR_INVALID_ARG and leave the configuration unchanged. */
+hoccl_status_t hoccl_set_config(const hoccl_config_t *cfg);
+hoccl_status_t hoccl_get_config(hoccl_config_t *cfg);
+
+/* Statistics of the most recent collective call on this thread. */
+hoccl_status_t hoccl_get_last_stats(hoccl_stats_t *stats);
+
+/* With kernel_timing on, every kernel launch of every collective call is
+ * bracketed by a pair of timing events on the stream it is launched on.
+ * This returns the durations in milliseconds of all launches recorded since
+ * the previous read, in launch order, waits for those launches to finish and
+ * clears the record.  *n receives the number of launches; at most `cap`
+ * durations are written.  With cap == 0 it only reports the count and keeps
+ * the record. */
+hoccl_status_t hoccl_get_kernel_times(float *ms, int cap, int *n);
+
+const char *hoccl_status_string(hoccl_status_t status);
+const char *hoccl_last_error_string(void);
+
+/* Number of SDMA engines the library can drive directly (0 if none). */
+int hoccl_sdma_engine_count(void);
+
+/* ---- collectives --------------------------------------------------------
+ * Reductions are sums.  The paper leaves reductions to SM-side execution and
+ * fixes no order, so the library defines one: ring direction r -> r+1, and
+ * the fold for chunk j starts at rank j+1 and ends at rank j,
+ *     out = ((x[j+1] + x[j+2]) + ...) + x[j]      (rank indices mod R).
+ * int32 adds wrap modulo 2^32; fp32 adds are IEEE binary32 round-to-nearest-
+ * even; bf16 inputs are widened exactly to fp32, summed in fp32 in the same
+ * order and rounded once to bf16 (round to nearest even).  Every path
+ * (ring or direct, any workgroup count, any chunk grouping) follows this
+ * order, so results are identical bit for bit. */
+
+/* all-reduce of `count` elements per rank.  The ring splits count into R
+ * chunks of c = ceil(count / R) elements (the last may be short or empty);
+ * rank j's reduced chunk j is then forwarded around the ring by copy steps.
+ * send[r], recv[r]: count elements each. */
+hoccl_status_t hoccl_allreduce(const void *const *send, void *const *recv,
+                               size_t count, hoccl_dtype_t dtype, int R,
+                               hipStream_t stream);
+
+/* reduce-scatter: send[r] holds R * recvcount elements; rank r receives
+ * block r (recvcount elements) of the element-wise sum. */
+hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv,
+                                    size_t recvcount, hoccl_dtype_t dtype,
+                                    int R, hipStream_t stream);
+
+/* all-gather: send[r] holds sendcount elements; every recv[r] receives the
+ * R shards in rank order (R * sendcount elements).  Copy-only: moved by the
+ * configured copy path (SDMA by default). */
+hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv,
+                               size_t sendcount, hoccl_dtype_t dtype, int R,
+                               hipStream_t stream);
+
+/* point-to-point send/recv: rank r sends its count elements to rank
+ * peers[r] (a host array of R ints; -1 = rank r sends nothing).  A receiver
+ * named twice is an argument error; a rank may send to itself (local copy).
+ * recv[d] of a rank nobody sends to may be NULL and is left untouched. */
+hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv,
+                              const int *peers, size_t count,
+                              hoccl_dtype_t dtype, int R, hipStream_t stream);
+
+/* all-to-all with uniform blocks: block d of send[s] (count elements at
+ * offset d * count) lands at block s of recv[d]. */
+hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv,
+                              size_t count, hoccl_dtype_t dtype, int R,
+                              hipStream_t stream);
+
+/* all-to-all(v): the traffic matrix C[s][d] = sendcounts[s * R + d]
+ * elements move from send[s] + sdispls[s * R + d] to
+ * recv[d] + rdispls[s * R + d] (all in elements; host arrays of R*R).
+ * Destination ranges must not overlap. */
+hoccl_status_t hoccl_alltoallv(const void *const *send,
+                               const size_t *sendcounts, const size_t *sdispls,
+                               void *const *recv, const size_t *rdispls,
+                               hoccl_dtype_t dtype, int R, hipStream_t stream);
+
+/* ---- introspection (tests and tools) ------------------------------------
+ * Writes the schedule the planner builds for a collective as JSON into buf
+ * (NUL-terminated, truncated to len).  op: 0 all-reduce, 1 reduce-scatter,
+ * 2 all-gather, 3 send/recv (peers r -> r+1, last rank sends nothing),
+ * 4 all-to-all.  Buffers are named symbolically ("send", "recv", "ws" with
+ * rank and byte offset), so no device is needed.  Uses the current
+ * configuration.  *needed receives the full length including the NUL. */
+hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dtype,
+                                     int R, char *buf, size_t len,
+                                     size_t *needed);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HOCCL_H */

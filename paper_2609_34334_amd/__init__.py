@@ -1,0 +1,295 @@
+"""Python binding of libhoccl (ctypes).
+
+Argument marshalling only: every step of a collective runs in the HIP
+library (``libhoccl.so``, built from ``csrc/`` by ``build.py``).  PyTorch is
+used for device memory and streams; each call passes raw device pointers and
+``torch.cuda.current_stream().cuda_stream`` (or the stream given) to the
+C ABI declared in ``include/hoccl.h``.
+
+Importing fails loudly when the library has not been built: there is no
+fallback implementation.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhoccl.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is not built; run `python -m paper_2609_34334_amd.build` "
+        "(or __graft_entry__.build()) first")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NO_MEMORY, ERR_TIMEOUT, ERR_INTERNAL = range(7)
+INT32, FP32, BF16 = 0, 1, 2
+COPY_AUTO, COPY_SDMA, COPY_SDMA_ENGINES, COPY_KERNEL = range(4)
+REDUCE_RING, REDUCE_DIRECT = 0, 1
+OP_ALLREDUCE, OP_REDUCE_SCATTER, OP_ALLGATHER, OP_SENDRECV, OP_ALLTOALL = range(5)
+
+_DTYPES = {torch.int32: INT32, torch.float32: FP32, torch.bfloat16: BF16}
+COPY_PATHS = {"auto": COPY_AUTO, "sdma": COPY_SDMA, "engines": COPY_SDMA_ENGINES,
+              "kernel": COPY_KERNEL}
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("workgroups_per_step", ctypes.c_int),
+                ("threads_per_workgroup", ctypes.c_int),
+                ("chunk_bytes", ctypes.c_size_t),
+                ("copy_streams", ctypes.c_int),
+                ("sdma_engines", ctypes.c_int),
+                ("copy_path", ctypes.c_int),
+                ("allgather_direct", ctypes.c_int),
+                ("allreduce_chunk_groups", ctypes.c_int),
+                ("reduce_algo", ctypes.c_int),
+                ("kernel_timing", ctypes.c_int),
+                ("proxy_timeout_ms", ctypes.c_uint)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("reduce_launches", ctypes.c_int),
+                ("copy_kernel_launches", ctypes.c_int),
+                ("copy_ops", ctypes.c_int),
+                ("workgroups_per_step", ctypes.c_int),
+                ("cus_available", ctypes.c_int),
+                ("cus_used_max", ctypes.c_int),
+                ("copy_path_used", ctypes.c_int),
+                ("reduce_algo_used", ctypes.c_int),
+                ("hbm_bytes_algorithmic", ctypes.c_ulonglong),
+                ("copy_bytes", ctypes.c_ulonglong),
+                ("host_enqueue_us", ctypes.c_double)]
+
+
+_vpp = ctypes.POINTER(ctypes.c_void_p)
+_sz = ctypes.c_size_t
+_szp = ctypes.POINTER(ctypes.c_size_t)
+_i = ctypes.c_int
+_SIGS = {
+    "hoccl_init": [_i],
+    "hoccl_finalize": [],
+    "hoccl_set_config": [ctypes.POINTER(Config)],
+    "hoccl_get_config": [ctypes.POINTER(Config)],
+    "hoccl_get_last_stats": [ctypes.POINTER(Stats)],
+    "hoccl_get_kernel_times": [ctypes.POINTER(ctypes.c_float), _i, ctypes.POINTER(_i)],
+    "hoccl_allreduce": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
+    "hoccl_reduce_scatter": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
+    "hoccl_allgather": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
+    "hoccl_sendrecv": [_vpp, _vpp, ctypes.POINTER(_i), _sz, _i, _i, ctypes.c_void_p],
+    "hoccl_alltoall": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
+    "hoccl_alltoallv": [_vpp, _szp, _szp, _vpp, _szp, _i, _i, ctypes.c_void_p],
+    "hoccl_debug_plan_json": [_i, _sz, _i, _i, ctypes.c_char_p, _sz, _szp],
+}
+for _name, _args in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = ctypes.c_int
+_lib.hoccl_status_string.argtypes = [ctypes.c_int]
+_lib.hoccl_status_string.restype = ctypes.c_char_p
+_lib.hoccl_last_error_string.argtypes = []
+_lib.hoccl_last_error_string.restype = ctypes.c_char_p
+_lib.hoccl_sdma_engine_count.argtypes = []
+_lib.hoccl_sdma_engine_count.restype = ctypes.c_int
+
+
+class HocclError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        msg = _lib.hoccl_status_string(status).decode()
+        detail = _lib.hoccl_last_error_string().decode()
+        super().__init__(f"{where}: {msg}" + (f" ({detail})" if detail else ""))
+
+
+def _check(status, where):
+    if status != OK:
+        raise HocclError(status, where)
+
+
+def lib():
+    """The loaded ctypes library (for tests that call the C ABI directly)."""
+    return _lib
+
+
+# ---- configuration -------------------------------------------------------------
+
+def get_config():
+    c = Config()
+    _check(_lib.hoccl_get_config(ctypes.byref(c)), "hoccl_get_config")
+    return {k: getattr(c, k) for k, _ in Config._fields_}
+
+
+def set_config(**kw):
+    """Update configuration fields; copy_path also accepts a name
+    ('auto', 'sdma', 'engines', 'kernel') and reduce_algo 'ring'/'direct'."""
+    c = Config()
+    _check(_lib.hoccl_get_config(ctypes.byref(c)), "hoccl_get_config")
+    for k, v in kw.items():
+        if k == "copy_path" and isinstance(v, str):
+            v = COPY_PATHS[v]
+        if k == "reduce_algo" and isinstance(v, str):
+            v = {"ring": REDUCE_RING, "direct": REDUCE_DIRECT}[v]
+        if not hasattr(c, k):
+            raise KeyError(k)
+        setattr(c, k, v)
+    _check(_lib.hoccl_set_config(ctypes.byref(c)), "hoccl_set_config")
+
+
+class config:
+    """Context manager: temporarily change configuration fields."""
+
+    def __init__(self, **kw):
+        self.kw = kw
+
+    def __enter__(self):
+        self.saved = get_config()
+        set_config(**self.kw)
+        return self
+
+    def __exit__(self, *exc):
+        set_config(**self.saved)
+
+
+def last_stats():
+    s = Stats()
+    _check(_lib.hoccl_get_last_stats(ctypes.byref(s)), "hoccl_get_last_stats")
+    return {k: getattr(s, k) for k, _ in Stats._fields_}
+
+
+def kernel_times():
+    """Durations (ms) of the kernel launches of the last call (needs
+    kernel_timing=1); waits for them."""
+    n = ctypes.c_int(0)
+    _check(_lib.hoccl_get_kernel_times(None, 0, ctypes.byref(n)), "hoccl_get_kernel_times")
+    buf = (ctypes.c_float * max(1, n.value))()
+    _check(_lib.hoccl_get_kernel_times(buf, n.value, ctypes.byref(n)), "hoccl_get_kernel_times")
+    return list(buf[:n.value])
+
+
+def sdma_engine_count():
+    return _lib.hoccl_sdma_engine_count()
+
+
+def init(device=-1):
+    _check(_lib.hoccl_init(device), "hoccl_init")
+
+
+def finalize():
+    _check(_lib.hoccl_finalize(), "hoccl_finalize")
+
+
+def plan_json(op, count, dtype, R):
+    import json
+    need = ctypes.c_size_t(0)
+    _check(_lib.hoccl_debug_plan_json(op, count, dtype, R, None, 0, ctypes.byref(need)),
+           "hoccl_debug_plan_json")
+    buf = ctypes.create_string_buffer(need.value)
+    _check(_lib.hoccl_debug_plan_json(op, count, dtype, R, buf, need.value, ctypes.byref(need)),
+           "hoccl_debug_plan_json")
+    return json.loads(buf.value.decode())
+
+
+# ---- collectives ---------------------------------------------------------------
+
+def _dtype_of(tensors):
+    dt = tensors[0].dtype
+    if dt not in _DTYPES:
+        raise TypeError(f"unsupported dtype {dt}")
+    dev = tensors[0].device
+    for t in tensors:
+        if t.dtype != dt:
+            raise TypeError("all buffers must share one dtype")
+        if t.device != dev or t.device.type != "cuda":
+            raise ValueError("all buffers must live on the same GPU")
+        if not t.is_contiguous():
+            raise ValueError("buffers must be contiguous")
+    return _DTYPES[dt]
+
+
+def _ptrs(tensors):
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def allreduce(send, recv=None, stream=None):
+    """Sum of the R tensors `send`, written to every tensor of `recv`
+    (defaults to in place)."""
+    recv = send if recv is None else recv
+    dt = _dtype_of(list(send) + list(recv))
+    n = send[0].numel()
+    if any(t.numel() != n for t in list(send) + list(recv)):
+        raise ValueError("all buffers must have the same number of elements")
+    _check(_lib.hoccl_allreduce(_ptrs(send), _ptrs(recv), n, dt, len(send), _stream(stream)),
+           "hoccl_allreduce")
+    return recv
+
+
+def reduce_scatter(send, recv=None, stream=None):
+    """send: R tensors of R*n elements; recv[r] receives block r of the sum."""
+    R = len(send)
+    if send[0].numel() % R:
+        raise ValueError("send buffers must hold R * recvcount elements")
+    n = send[0].numel() // R
+    if recv is None:
+        recv = [torch.empty(n, dtype=send[0].dtype, device=send[0].device) for _ in range(R)]
+    dt = _dtype_of(list(send) + list(recv))
+    if any(t.numel() != R * n for t in send) or any(t.numel() != n for t in recv):
+        raise ValueError("buffer sizes do not match")
+    _check(_lib.hoccl_reduce_scatter(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
+           "hoccl_reduce_scatter")
+    return recv
+
+
+def allgather(send, recv=None, stream=None):
+    """send: R tensors of n elements; every recv[r] gets their concatenation."""
+    R = len(send)
+    n = send[0].numel()
+    if recv is None:
+        recv = [torch.empty(R * n, dtype=send[0].dtype, device=send[0].device) for _ in range(R)]
+    dt = _dtype_of(list(send) + list(recv))
+    if any(t.numel() != n for t in send) or any(t.numel() != R * n for t in recv):
+        raise ValueError("buffer sizes do not match")
+    _check(_lib.hoccl_allgather(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
+           "hoccl_allgather")
+    return recv
+
+
+def sendrecv(send, recv, peers, stream=None):
+    """Rank r sends send[r] to rank peers[r] (-1: nothing).  recv[d] may be
+    None for ranks that receive nothing."""
+    R = len(send)
+    n = send[0].numel()
+    live = [t for t in list(send) + list(recv) if t is not None]
+    dt = _dtype_of(live)
+    rp = (ctypes.c_void_p * R)(*[0 if t is None else t.data_ptr() for t in recv])
+    pp = (ctypes.c_int * R)(*peers)
+    _check(_lib.hoccl_sendrecv(_ptrs(send), rp, pp, n, dt, R, _stream(stream)), "hoccl_sendrecv")
+    return recv
+
+
+def alltoall(send, recv=None, stream=None):
+    R = len(send)
+    if send[0].numel() % R:
+        raise ValueError("send buffers must hold R blocks")
+    n = send[0].numel() // R
+    if recv is None:
+        recv = [torch.empty_like(t) for t in send]
+    dt = _dtype_of(list(send) + list(recv))
+    _check(_lib.hoccl_alltoall(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
+           "hoccl_alltoall")
+    return recv
+
+
+def alltoallv(send, counts, sdispls, recv, rdispls, stream=None):
+    """counts/sdispls/rdispls: R*R element counts and offsets, [s*R + d]."""
+    R = len(send)
+    dt = _dtype_of(list(send) + list(recv))
+    S = ctypes.c_size_t * (R * R)
+    _check(_lib.hoccl_alltoallv(_ptrs(send), S(*counts), S(*sdispls), _ptrs(recv), S(*rdispls),
+                                dt, R, _stream(stream)), "hoccl_alltoallv")
+    return recv

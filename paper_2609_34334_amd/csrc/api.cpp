@@ -1,0 +1,828 @@
+// C ABI of libhoccl: argument validation, configuration, the stream manager
+// and the schedule executor.
+//
+// Stream manager (Stream Manager section of the paper): a collective is
+// enqueued on the caller's stream `s`.  Reduction kernels run on `s` itself.
+// Copy steps run either
+//   * on the library's copy streams as hipMemcpyAsync(DeviceToDeviceNoCU),
+//     which the HIP runtime hands to an SDMA engine: `s` records a fork
+//     event that each copy stream waits on before its first copy, and `s`
+//     waits on a join event of every copy stream it used, so the collective
+//     sits in `s` exactly where it was enqueued;
+//   * by the copy proxy (proxy.cpp), which drives chosen SDMA engines itself
+//     and is ordered with `s` by the start/finish flag handshake;
+//   * or as CU copy kernels on `s`.
+// All-reduce's gather copies of group g wait on an event recorded on `s`
+// right after group g's last reduction step, so SDMA copies of one group
+// overlap the CU reduction of the next (the paper's per-chunk buffer state
+// machine, reduced to "partial ready" / "final ready").
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "hoccl_internal.h"
+#include "proxy.h"
+
+namespace hoccl {
+
+namespace {
+
+thread_local std::string t_err;
+thread_local hoccl_stats_t t_stats;
+
+struct TimingPair {
+    hipEvent_t a, b;
+};
+
+struct DeviceState {
+    int device = -1;
+    int num_cus = 0;
+    std::vector<hipStream_t> copy_streams;
+    hipEvent_t ev_fork = nullptr;
+    std::vector<hipEvent_t> ev_group;
+    std::vector<hipEvent_t> ev_join;
+    void *ws = nullptr;
+    size_t ws_cap = 0;
+    hipEvent_t ws_event = nullptr;
+    hipStream_t ws_last_stream = nullptr;
+    bool ws_used = false;
+    std::vector<TimingPair> timing_pool;
+    size_t timing_used = 0;
+    Proxy *proxy = nullptr;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceState *> g_states;
+hoccl_config_t g_cfg;
+bool g_cfg_init = false;
+
+void set_err(const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+}
+
+#define HIP_TRY(call)                                                                     \
+    do {                                                                                  \
+        hipError_t e_ = (call);                                                           \
+        if (e_ != hipSuccess) {                                                           \
+            set_err("%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, __LINE__); \
+            return HOCCL_ERR_HIP;                                                         \
+        }                                                                                 \
+    } while (0)
+
+#define TRY(expr)                          \
+    do {                                   \
+        hoccl_status_t st_ = (expr);       \
+        if (st_ != HOCCL_OK) return st_;   \
+    } while (0)
+
+hoccl_config_t default_config() {
+    hoccl_config_t c;
+    std::memset(&c, 0, sizeof c);
+    c.workgroups_per_step = 0;
+    c.threads_per_workgroup = 256;
+    c.chunk_bytes = 0;
+    c.copy_streams = 8;
+    c.sdma_engines = 0;
+    c.copy_path = HOCCL_COPY_AUTO;
+    c.allgather_direct = 0;
+    c.allreduce_chunk_groups = 1;
+    c.reduce_algo = HOCCL_REDUCE_RING;
+    c.kernel_timing = 0;
+    c.proxy_timeout_ms = 10000;
+    return c;
+}
+
+bool config_valid(const hoccl_config_t &c) {
+    if (c.workgroups_per_step < 0 || c.workgroups_per_step > (1 << 20)) return false;
+    if (c.threads_per_workgroup != 0 &&
+        (c.threads_per_workgroup < 64 || c.threads_per_workgroup > 1024 ||
+         c.threads_per_workgroup % 64 != 0))
+        return false;
+    if (c.copy_streams < 0 || c.copy_streams > 16) return false;
+    if (c.sdma_engines < 0 || c.sdma_engines > 32) return false;
+    if ((int)c.copy_path < 0 || (int)c.copy_path > 3) return false;
+    if (c.allreduce_chunk_groups < 0 || c.allreduce_chunk_groups > 1024) return false;
+    if ((int)c.reduce_algo < 0 || (int)c.reduce_algo > 1) return false;
+    if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
+    return true;
+}
+
+long env_long(const char *name, long dflt) {
+    const char *v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    char *end = nullptr;
+    long x = std::strtol(v, &end, 0);
+    return (end && *end == 0) ? x : dflt;
+}
+
+void load_config_locked() {
+    if (g_cfg_init) return;
+    hoccl_config_t c = default_config();
+    c.workgroups_per_step = (int)env_long("HOCCL_WG_PER_STEP", c.workgroups_per_step);
+    c.threads_per_workgroup = (int)env_long("HOCCL_THREADS_PER_WG", c.threads_per_workgroup);
+    c.chunk_bytes = (size_t)env_long("HOCCL_CHUNK_BYTES", (long)c.chunk_bytes);
+    c.copy_streams = (int)env_long("HOCCL_COPY_STREAMS", c.copy_streams);
+    c.sdma_engines = (int)env_long("HOCCL_SDMA_ENGINES", c.sdma_engines);
+    c.allgather_direct = (int)env_long("HOCCL_AG_DIRECT", c.allgather_direct);
+    c.allreduce_chunk_groups = (int)env_long("HOCCL_AR_GROUPS", c.allreduce_chunk_groups);
+    c.kernel_timing = (int)env_long("HOCCL_KERNEL_TIMING", c.kernel_timing);
+    if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
+        if (!std::strcmp(v, "sdma")) c.copy_path = HOCCL_COPY_SDMA;
+        else if (!std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA_ENGINES;
+        else if (!std::strcmp(v, "kernel")) c.copy_path = HOCCL_COPY_KERNEL;
+        else c.copy_path = HOCCL_COPY_AUTO;
+    }
+    if (const char *v = std::getenv("HOCCL_REDUCE_ALGO"))
+        c.reduce_algo = std::strcmp(v, "direct") ? HOCCL_REDUCE_RING : HOCCL_REDUCE_DIRECT;
+    if (!config_valid(c)) c = default_config();
+    g_cfg = c;
+    g_cfg_init = true;
+}
+
+hoccl_config_t config() {
+    std::lock_guard<std::mutex> lk(g_mu);
+    load_config_locked();
+    return g_cfg;
+}
+
+void destroy_state(DeviceState *st) {
+    if (!st) return;
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    (void)hipSetDevice(st->device);
+    (void)hipDeviceSynchronize();
+    delete st->proxy;
+    for (auto s : st->copy_streams) (void)hipStreamDestroy(s);
+    if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
+    for (auto e : st->ev_group) (void)hipEventDestroy(e);
+    for (auto e : st->ev_join) (void)hipEventDestroy(e);
+    if (st->ws_event) (void)hipEventDestroy(st->ws_event);
+    if (st->ws) (void)hipFree(st->ws);
+    for (auto &tp : st->timing_pool) {
+        (void)hipEventDestroy(tp.a);
+        (void)hipEventDestroy(tp.b);
+    }
+    (void)hipSetDevice(prev);
+    delete st;
+}
+
+hoccl_status_t create_state(int device, DeviceState **out) {
+    DeviceState *st = new DeviceState();
+    st->device = device;
+    auto fail = [&](hoccl_status_t s) {
+        destroy_state(st);
+        return s;
+    };
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) {
+        set_err("hipGetDeviceProperties(%d): %s", device, hipGetErrorString(e));
+        return fail(HOCCL_ERR_HIP);
+    }
+    st->num_cus = prop.multiProcessorCount;
+    const int K = 16;  // the most copy streams any configuration may use
+    for (int k = 0; k < K; ++k) {
+        hipStream_t s;
+        e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            set_err("hipStreamCreateWithFlags: %s", hipGetErrorString(e));
+            return fail(HOCCL_ERR_HIP);
+        }
+        st->copy_streams.push_back(s);
+        hipEvent_t ev;
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            set_err("hipEventCreateWithFlags: %s", hipGetErrorString(e));
+            return fail(HOCCL_ERR_HIP);
+        }
+        st->ev_join.push_back(ev);
+    }
+    if ((e = hipEventCreateWithFlags(&st->ev_fork, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&st->ws_event, hipEventDisableTiming)) != hipSuccess) {
+        set_err("hipEventCreateWithFlags: %s", hipGetErrorString(e));
+        return fail(HOCCL_ERR_HIP);
+    }
+    st->proxy = Proxy::create(device);  // null when the engines cannot be driven
+    *out = st;
+    return HOCCL_OK;
+}
+
+hoccl_status_t get_state(DeviceState **out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lk(g_mu);
+    load_config_locked();
+    auto it = g_states.find(dev);
+    if (it != g_states.end()) {
+        *out = it->second;
+        return HOCCL_OK;
+    }
+    DeviceState *st = nullptr;
+    TRY(create_state(dev, &st));
+    g_states[dev] = st;
+    *out = st;
+    return HOCCL_OK;
+}
+
+// ---- execution ------------------------------------------------------------------
+
+struct Buffers {
+    const void *const *send;
+    void *const *recv;
+    void *ws;
+};
+
+inline void *resolve(const BufRef &b, const Buffers &B) {
+    switch (b.kind) {
+    case BUF_SEND: return (char *)B.send[b.rank] + b.off;
+    case BUF_RECV: return (char *)B.recv[b.rank] + b.off;
+    case BUF_WS: return (char *)B.ws + b.off;
+    default: return nullptr;
+    }
+}
+
+hoccl_status_t ensure_ws(DeviceState &st, size_t bytes) {
+    if (bytes <= st.ws_cap) return HOCCL_OK;
+    // Growing the workspace waits for every user of the old one.
+    HIP_TRY(hipDeviceSynchronize());
+    if (st.ws) HIP_TRY(hipFree(st.ws));
+    st.ws = nullptr;
+    st.ws_cap = 0;
+    st.ws_last_stream = nullptr;
+    size_t cap = (bytes + (1u << 20) - 1) & ~((size_t)(1u << 20) - 1);
+    hipError_t e = hipMalloc(&st.ws, cap);
+    if (e != hipSuccess) {
+        st.ws = nullptr;
+        set_err("hipMalloc(%zu) for the workspace: %s", cap, hipGetErrorString(e));
+        return HOCCL_ERR_NO_MEMORY;
+    }
+    st.ws_cap = cap;
+    return HOCCL_OK;
+}
+
+int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg) {
+    if (cfg.workgroups_per_step > 0) return cfg.workgroups_per_step;
+    return st.num_cus * 8;
+}
+
+hoccl_status_t timed_begin(DeviceState &st, const hoccl_config_t &cfg, hipStream_t s,
+                           TimingPair **tp) {
+    *tp = nullptr;
+    if (!cfg.kernel_timing) return HOCCL_OK;
+    if (st.timing_used == st.timing_pool.size()) {
+        TimingPair p;
+        HIP_TRY(hipEventCreate(&p.a));
+        HIP_TRY(hipEventCreate(&p.b));
+        st.timing_pool.push_back(p);
+    }
+    *tp = &st.timing_pool[st.timing_used++];
+    HIP_TRY(hipEventRecord((*tp)->a, s));
+    return HOCCL_OK;
+}
+
+hoccl_status_t timed_end(TimingPair *tp, hipStream_t s) {
+    if (tp) HIP_TRY(hipEventRecord(tp->b, s));
+    return HOCCL_OK;
+}
+
+hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
+                              const Buffers &B, hipStream_t s, int wg, int threads,
+                              bool record_groups) {
+    for (size_t i = 0; i < p.reduce_steps.size(); ++i) {
+        const ReduceStep &step = p.reduce_steps[i];
+        for (size_t b = 0; b < step.segs.size(); b += kMaxReduceSegs) {
+            ReduceArgs a;
+            std::memset(&a, 0, sizeof a);
+            int ns = (int)std::min<size_t>(kMaxReduceSegs, step.segs.size() - b);
+            for (int k = 0; k < ns; ++k) {
+                const ReduceSeg &g = step.segs[b + (size_t)k];
+                a.seg[k].in0 = resolve(g.in0, B);
+                a.seg[k].in1 = resolve(g.in1, B);
+                a.seg[k].out = resolve(g.out, B);
+                a.seg[k].n = g.n;
+            }
+            a.nseg = ns;
+            TimingPair *tp;
+            TRY(timed_begin(st, cfg, s, &tp));
+            HIP_TRY(launch_reduce_step(p.dtype, step.phase, a, wg, threads, s));
+            TRY(timed_end(tp, s));
+            t_stats.reduce_launches++;
+        }
+        bool last_of_group = (i + 1 == p.reduce_steps.size()) ||
+                             p.reduce_steps[i + 1].group != step.group;
+        if (record_groups && last_of_group) {
+            while ((int)st.ev_group.size() <= step.group) {
+                hipEvent_t ev;
+                HIP_TRY(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+                st.ev_group.push_back(ev);
+            }
+            HIP_TRY(hipEventRecord(st.ev_group[(size_t)step.group], s));
+        }
+    }
+    if (p.has_fold) {
+        FoldArgs a;
+        std::memset(&a, 0, sizeof a);
+        for (int r = 0; r < p.R; ++r) {
+            a.in[r] = B.send[r];
+            a.out[r] = B.recv[r];
+        }
+        a.c = p.fold.c;
+        a.total = p.fold.total;
+        a.R = p.R;
+        a.write_all = p.fold.write_all ? 1 : 0;
+        a.out_at_chunk = p.fold.out_at_chunk ? 1 : 0;
+        TimingPair *tp;
+        TRY(timed_begin(st, cfg, s, &tp));
+        HIP_TRY(launch_fold(p.dtype, a, wg, threads, s));
+        TRY(timed_end(tp, s));
+        t_stats.reduce_launches++;
+    }
+    return HOCCL_OK;
+}
+
+hoccl_status_t run_copies_sdma(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
+                               const Buffers &B, hipStream_t s) {
+    int K = std::max(1, std::min(cfg.copy_streams ? cfg.copy_streams : 8,
+                                 (int)st.copy_streams.size()));
+    std::vector<int> q = assign_chains(p, K);
+    std::vector<int> started((size_t)K, 0), waited((size_t)K, -1);
+    for (const CopyOp &c : p.copies) {
+        int k = q[(size_t)c.chain];
+        hipStream_t cs = st.copy_streams[(size_t)k];
+        if (!started[(size_t)k]) {
+            HIP_TRY(hipStreamWaitEvent(cs, st.ev_fork, 0));
+            started[(size_t)k] = 1;
+        }
+        if (c.group >= 0 && waited[(size_t)k] < c.group) {
+            HIP_TRY(hipStreamWaitEvent(cs, st.ev_group[(size_t)c.group], 0));
+            waited[(size_t)k] = c.group;
+        }
+        HIP_TRY(hipMemcpyAsync(resolve(c.dst, B), resolve(c.src, B), c.bytes,
+                               hipMemcpyDeviceToDeviceNoCU, cs));
+        t_stats.copy_ops++;
+    }
+    for (int k = 0; k < K; ++k) {
+        if (!started[(size_t)k]) continue;
+        HIP_TRY(hipEventRecord(st.ev_join[(size_t)k], st.copy_streams[(size_t)k]));
+        HIP_TRY(hipStreamWaitEvent(s, st.ev_join[(size_t)k], 0));
+    }
+    return HOCCL_OK;
+}
+
+hoccl_status_t run_copies_kernel(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
+                                 const Buffers &B, hipStream_t s, int wg, int threads) {
+    int maxlevel = 0;
+    for (const CopyOp &c : p.copies) maxlevel = std::max(maxlevel, c.level);
+    for (int lvl = 0; lvl <= maxlevel; ++lvl) {
+        CopyArgs a;
+        std::memset(&a, 0, sizeof a);
+        auto flush = [&]() -> hoccl_status_t {
+            if (a.nseg == 0) return HOCCL_OK;
+            TimingPair *tp;
+            TRY(timed_begin(st, cfg, s, &tp));
+            HIP_TRY(launch_copy(a, wg, threads, s));
+            TRY(timed_end(tp, s));
+            t_stats.copy_kernel_launches++;
+            std::memset(&a, 0, sizeof a);
+            return HOCCL_OK;
+        };
+        for (const CopyOp &c : p.copies) {
+            if (c.level != lvl) continue;
+            a.seg[a.nseg].src = resolve(c.src, B);
+            a.seg[a.nseg].dst = resolve(c.dst, B);
+            a.seg[a.nseg].bytes = c.bytes;
+            a.nseg++;
+            if (a.nseg == kMaxCopySegs) TRY(flush());
+        }
+        TRY(flush());
+    }
+    return HOCCL_OK;
+}
+
+hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg) {
+    if (cfg.copy_path == HOCCL_COPY_AUTO) return HOCCL_COPY_SDMA;
+    if (cfg.copy_path == HOCCL_COPY_SDMA_ENGINES && !st.proxy) return HOCCL_COPY_SDMA;
+    return cfg.copy_path;
+}
+
+hoccl_status_t execute(const Plan &p, const Buffers &B0, hipStream_t s) {
+    auto t0 = std::chrono::steady_clock::now();
+    DeviceState *stp = nullptr;
+    TRY(get_state(&stp));
+    DeviceState &st = *stp;
+    hoccl_config_t cfg = config();
+    std::memset(&t_stats, 0, sizeof t_stats);
+    Buffers B = B0;
+
+    const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
+    const int wg = auto_workgroups(st, cfg);
+    const hoccl_copy_path_t path = resolve_path(st, cfg);
+    const bool has_kernels = !p.reduce_steps.empty() || p.has_fold;
+    const bool has_copies = !p.copies.empty();
+
+    if (p.ws_bytes) {
+        TRY(ensure_ws(st, p.ws_bytes));
+        B.ws = st.ws;
+        if (st.ws_last_stream && st.ws_last_stream != s)
+            HIP_TRY(hipStreamWaitEvent(s, st.ws_event, 0));
+    }
+    if (has_copies && path == HOCCL_COPY_SDMA) HIP_TRY(hipEventRecord(st.ev_fork, s));
+
+    if (has_copies && path == HOCCL_COPY_SDMA_ENGINES) {
+        // Reductions first (on s), then the proxy takes over the copies.
+        TRY(run_reductions(st, cfg, p, B, s, wg, threads, false));
+        std::vector<ProxyCopy> cps;
+        cps.reserve(p.copies.size());
+        for (const CopyOp &c : p.copies)
+            cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
+        int ne = 0;
+        hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, s, &ne,
+                                            t_err);
+        if (r != HOCCL_OK) return r;
+        t_stats.copy_ops += (int)cps.size();
+    } else {
+        TRY(run_reductions(st, cfg, p, B, s, wg, threads, has_copies && path == HOCCL_COPY_SDMA));
+        if (has_copies) {
+            if (path == HOCCL_COPY_KERNEL)
+                TRY(run_copies_kernel(st, cfg, p, B, s, wg, threads));
+            else
+                TRY(run_copies_sdma(st, cfg, p, B, s));
+        }
+    }
+    if (p.ws_bytes) {
+        HIP_TRY(hipEventRecord(st.ws_event, s));
+        st.ws_last_stream = s;
+    }
+
+    bool cu_work = has_kernels || (has_copies && path == HOCCL_COPY_KERNEL);
+    t_stats.workgroups_per_step = cu_work ? wg : 0;
+    t_stats.cus_available = st.num_cus;
+    t_stats.cus_used_max = cu_work ? std::min(wg, st.num_cus) : 0;
+    t_stats.copy_path_used = has_copies ? path : HOCCL_COPY_AUTO;
+    t_stats.reduce_algo_used = p.has_fold ? HOCCL_REDUCE_DIRECT : HOCCL_REDUCE_RING;
+    t_stats.hbm_bytes_algorithmic = p.hbm_bytes;
+    t_stats.copy_bytes = p.copy_bytes;
+    t_stats.host_enqueue_us =
+        std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+    return HOCCL_OK;
+}
+
+// ---- validation -------------------------------------------------------------------
+
+struct Range {
+    uintptr_t lo, hi;  // [lo, hi)
+    int who;           // rank
+    bool is_out;
+};
+
+bool overlaps(const Range &a, const Range &b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Outputs must be pairwise disjoint; an output may overlap an input only
+// where `allowed(out_rank, in_rank, out, in)` says it is a permitted in-place
+// form.
+template <typename Allowed>
+hoccl_status_t check_overlaps(const std::vector<Range> &outs, const std::vector<Range> &ins,
+                              Allowed allowed) {
+    std::vector<Range> o = outs;
+    std::sort(o.begin(), o.end(), [](const Range &a, const Range &b) { return a.lo < b.lo; });
+    for (size_t i = 1; i < o.size(); ++i)
+        if (o[i].lo < o[i - 1].hi) {
+            set_err("output buffers of ranks %d and %d overlap", o[i - 1].who, o[i].who);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+    for (const Range &a : outs)
+        for (const Range &b : ins)
+            if (a.hi > a.lo && b.hi > b.lo && overlaps(a, b) && !allowed(a, b)) {
+                set_err("output of rank %d overlaps input of rank %d outside the in-place form",
+                        a.who, b.who);
+                return HOCCL_ERR_INVALID_ARG;
+            }
+    return HOCCL_OK;
+}
+
+hoccl_status_t check_common(const void *send, const void *recv, hoccl_dtype_t dt, int R) {
+    if (R < 1 || R > kMaxRanks) {
+        set_err("R = %d outside [1, %d]", R, kMaxRanks);
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if (dt != HOCCL_INT32 && dt != HOCCL_FP32 && dt != HOCCL_BF16) {
+        set_err("unknown dtype %d", (int)dt);
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if (!send || !recv) {
+        set_err("send/recv pointer arrays must not be NULL");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    return HOCCL_OK;
+}
+
+hoccl_status_t check_ptrs(const void *const *arr, int R, const char *what) {
+    for (int r = 0; r < R; ++r)
+        if (!arr[r]) {
+            set_err("%s[%d] is NULL", what, r);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+    return HOCCL_OK;
+}
+
+bool size_overflows(size_t a, size_t b) { return b != 0 && a > SIZE_MAX / b; }
+
+PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
+    PlanOptions o;
+    o.allgather_direct = cfg.allgather_direct != 0;
+    o.allreduce_groups = cfg.allreduce_chunk_groups > 0 ? cfg.allreduce_chunk_groups : 1;
+    o.chunk_bytes = cfg.chunk_bytes;
+    o.in_place = in_place;
+    o.algo = cfg.reduce_algo;
+    return o;
+}
+
+}  // namespace
+}  // namespace hoccl
+
+using namespace hoccl;
+
+extern "C" {
+
+hoccl_status_t hoccl_init(int device) {
+    if (device >= 0) HIP_TRY(hipSetDevice(device));
+    DeviceState *st = nullptr;
+    return get_state(&st);
+}
+
+hoccl_status_t hoccl_finalize(void) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    for (auto &kv : g_states) destroy_state(kv.second);
+    g_states.clear();
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_set_config(const hoccl_config_t *cfg) {
+    if (!cfg || !config_valid(*cfg)) {
+        set_err("invalid configuration");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    std::lock_guard<std::mutex> lk(g_mu);
+    load_config_locked();
+    g_cfg = *cfg;
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_get_config(hoccl_config_t *cfg) {
+    if (!cfg) return HOCCL_ERR_INVALID_ARG;
+    *cfg = config();
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_get_last_stats(hoccl_stats_t *stats) {
+    if (!stats) return HOCCL_ERR_INVALID_ARG;
+    *stats = t_stats;
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_get_kernel_times(float *ms, int cap, int *n) {
+    if (!n || (cap > 0 && !ms)) return HOCCL_ERR_INVALID_ARG;
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    DeviceState *st = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_states.find(dev);
+        if (it != g_states.end()) st = it->second;
+    }
+    *n = 0;
+    if (!st) return HOCCL_OK;
+    *n = (int)st->timing_used;
+    if (cap <= 0) return HOCCL_OK;  // query the count only; keep the record
+    for (size_t i = 0; i < st->timing_used; ++i) {
+        HIP_TRY(hipEventSynchronize(st->timing_pool[i].b));
+        if ((int)i < cap) HIP_TRY(hipEventElapsedTime(&ms[i], st->timing_pool[i].a, st->timing_pool[i].b));
+    }
+    st->timing_used = 0;
+    return HOCCL_OK;
+}
+
+const char *hoccl_status_string(hoccl_status_t s) {
+    switch (s) {
+    case HOCCL_OK: return "ok";
+    case HOCCL_ERR_INVALID_ARG: return "invalid argument";
+    case HOCCL_ERR_UNSUPPORTED: return "unsupported";
+    case HOCCL_ERR_HIP: return "HIP/HSA runtime error";
+    case HOCCL_ERR_NO_MEMORY: return "out of memory";
+    case HOCCL_ERR_TIMEOUT: return "copy proxy timeout";
+    case HOCCL_ERR_INTERNAL: return "internal error";
+    }
+    return "unknown status";
+}
+
+const char *hoccl_last_error_string(void) { return t_err.c_str(); }
+
+int hoccl_sdma_engine_count(void) {
+    DeviceState *st = nullptr;
+    if (get_state(&st) != HOCCL_OK || !st->proxy) return 0;
+    return st->proxy->engine_count();
+}
+
+hoccl_status_t hoccl_allreduce(const void *const *send, void *const *recv, size_t count,
+                               hoccl_dtype_t dt, int R, hipStream_t stream) {
+    TRY(check_common(send, recv, dt, R));
+    if (count == 0) return HOCCL_OK;
+    TRY(check_ptrs(send, R, "send"));
+    TRY(check_ptrs((const void *const *)recv, R, "recv"));
+    size_t es = dtype_size(dt);
+    if (size_overflows(count, es)) return HOCCL_ERR_INVALID_ARG;
+    size_t bytes = count * es;
+    std::vector<Range> outs, ins;
+    bool in_place = true;
+    for (int r = 0; r < R; ++r) {
+        outs.push_back({(uintptr_t)recv[r], (uintptr_t)recv[r] + bytes, r, true});
+        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + bytes, r, false});
+        in_place &= (send[r] == recv[r]);
+    }
+    TRY(check_overlaps(outs, ins, [](const Range &o, const Range &i) {
+        return o.who == i.who && o.lo == i.lo;
+    }));
+    Plan p = plan_allreduce(count, dt, R, options_from(config(), in_place));
+    return execute(p, Buffers{send, recv, nullptr}, stream);
+}
+
+hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv, size_t n,
+                                    hoccl_dtype_t dt, int R, hipStream_t stream) {
+    TRY(check_common(send, recv, dt, R));
+    if (n == 0) return HOCCL_OK;
+    TRY(check_ptrs(send, R, "send"));
+    TRY(check_ptrs((const void *const *)recv, R, "recv"));
+    size_t es = dtype_size(dt);
+    if (size_overflows(n, es * (size_t)R)) return HOCCL_ERR_INVALID_ARG;
+    size_t ob = n * es, ib = (size_t)R * n * es;
+    std::vector<Range> outs, ins;
+    bool in_place = true;
+    for (int r = 0; r < R; ++r) {
+        outs.push_back({(uintptr_t)recv[r], (uintptr_t)recv[r] + ob, r, true});
+        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + ib, r, false});
+        in_place &= ((const char *)recv[r] == (const char *)send[r] + (size_t)r * ob);
+    }
+    TRY(check_overlaps(outs, ins, [ob](const Range &o, const Range &i) {
+        return o.who == i.who && o.lo == i.lo + (uintptr_t)o.who * ob;
+    }));
+    Plan p = plan_reduce_scatter(n, dt, R, options_from(config(), in_place));
+    return execute(p, Buffers{send, recv, nullptr}, stream);
+}
+
+hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv, size_t n,
+                               hoccl_dtype_t dt, int R, hipStream_t stream) {
+    TRY(check_common(send, recv, dt, R));
+    if (n == 0) return HOCCL_OK;
+    TRY(check_ptrs(send, R, "send"));
+    TRY(check_ptrs((const void *const *)recv, R, "recv"));
+    size_t es = dtype_size(dt);
+    if (size_overflows(n, es * (size_t)R)) return HOCCL_ERR_INVALID_ARG;
+    size_t ib = n * es, ob = (size_t)R * n * es;
+    std::vector<Range> outs, ins;
+    bool in_place = true;
+    for (int r = 0; r < R; ++r) {
+        outs.push_back({(uintptr_t)recv[r], (uintptr_t)recv[r] + ob, r, true});
+        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + ib, r, false});
+        in_place &= ((const char *)send[r] == (const char *)recv[r] + (size_t)r * ib);
+    }
+    TRY(check_overlaps(outs, ins, [ib](const Range &o, const Range &i) {
+        return o.who == i.who && i.lo == o.lo + (uintptr_t)o.who * ib;
+    }));
+    Plan p = plan_allgather(n, dt, R, options_from(config(), in_place));
+    return execute(p, Buffers{send, recv, nullptr}, stream);
+}
+
+hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv, const int *peers,
+                              size_t n, hoccl_dtype_t dt, int R, hipStream_t stream) {
+    TRY(check_common(send, recv, dt, R));
+    if (!peers) {
+        set_err("peers must not be NULL");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    std::vector<int> seen((size_t)R, 0);
+    for (int r = 0; r < R; ++r) {
+        int d = peers[r];
+        if (d < -1 || d >= R) {
+            set_err("peers[%d] = %d outside [-1, R)", r, d);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+        if (d >= 0 && seen[(size_t)d]++) {
+            set_err("rank %d receives from two senders", d);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+    }
+    if (n == 0) return HOCCL_OK;
+    size_t es = dtype_size(dt);
+    if (size_overflows(n, es)) return HOCCL_ERR_INVALID_ARG;
+    size_t b = n * es;
+    std::vector<Range> outs, ins;
+    for (int r = 0; r < R; ++r) {
+        int d = peers[r];
+        if (d < 0) continue;
+        if (!send[r] || !recv[d]) {
+            set_err("send[%d] or recv[%d] is NULL", r, d);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+        outs.push_back({(uintptr_t)recv[d], (uintptr_t)recv[d] + b, d, true});
+        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + b, r, false});
+    }
+    TRY(check_overlaps(outs, ins, [](const Range &, const Range &) { return false; }));
+    Plan p = plan_sendrecv(n, dt, R, peers, options_from(config(), false));
+    return execute(p, Buffers{send, recv, nullptr}, stream);
+}
+
+hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv, size_t n,
+                              hoccl_dtype_t dt, int R, hipStream_t stream) {
+    TRY(check_common(send, recv, dt, R));
+    if (n == 0) return HOCCL_OK;
+    TRY(check_ptrs(send, R, "send"));
+    TRY(check_ptrs((const void *const *)recv, R, "recv"));
+    size_t es = dtype_size(dt);
+    if (size_overflows(n, es * (size_t)R)) return HOCCL_ERR_INVALID_ARG;
+    size_t b = (size_t)R * n * es;
+    std::vector<Range> outs, ins;
+    for (int r = 0; r < R; ++r) {
+        outs.push_back({(uintptr_t)recv[r], (uintptr_t)recv[r] + b, r, true});
+        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + b, r, false});
+    }
+    TRY(check_overlaps(outs, ins, [](const Range &, const Range &) { return false; }));
+    Plan p = plan_alltoall(n, dt, R, options_from(config(), false));
+    return execute(p, Buffers{send, recv, nullptr}, stream);
+}
+
+hoccl_status_t hoccl_alltoallv(const void *const *send, const size_t *counts, const size_t *sd,
+                               void *const *recv, const size_t *rd, hoccl_dtype_t dt, int R,
+                               hipStream_t stream) {
+    TRY(check_common(send, recv, dt, R));
+    if (!counts || !sd || !rd) {
+        set_err("counts and displacements must not be NULL");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    size_t es = dtype_size(dt);
+    std::vector<Range> outs, ins;
+    for (int s = 0; s < R; ++s)
+        for (int d = 0; d < R; ++d) {
+            size_t k = (size_t)s * (size_t)R + (size_t)d;
+            if (counts[k] == 0) continue;
+            if (!send[s] || !recv[d]) {
+                set_err("send[%d] or recv[%d] is NULL", s, d);
+                return HOCCL_ERR_INVALID_ARG;
+            }
+            if (size_overflows(counts[k], es) || sd[k] > SIZE_MAX / es - counts[k] ||
+                rd[k] > SIZE_MAX / es - counts[k]) {
+                set_err("count/displacement overflow at (%d, %d)", s, d);
+                return HOCCL_ERR_INVALID_ARG;
+            }
+            uintptr_t o = (uintptr_t)recv[d] + rd[k] * es, i = (uintptr_t)send[s] + sd[k] * es;
+            outs.push_back({o, o + counts[k] * es, d, true});
+            ins.push_back({i, i + counts[k] * es, s, false});
+        }
+    if (outs.empty()) return HOCCL_OK;
+    TRY(check_overlaps(outs, ins, [](const Range &, const Range &) { return false; }));
+    Plan p = plan_alltoallv(counts, sd, rd, dt, R, options_from(config(), false));
+    return execute(p, Buffers{send, recv, nullptr}, stream);
+}
+
+hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dt, int R, char *buf,
+                                     size_t len, size_t *needed) {
+    TRY(check_common((const void *)1, (const void *)1, dt, R));
+    PlanOptions o = options_from(config(), false);
+    Plan p;
+    switch (op) {
+    case 0: p = plan_allreduce(count, dt, R, o); break;
+    case 1: p = plan_reduce_scatter(count, dt, R, o); break;
+    case 2: p = plan_allgather(count, dt, R, o); break;
+    case 3: {
+        std::vector<int> peers((size_t)R);
+        for (int r = 0; r < R; ++r) peers[(size_t)r] = r + 1 < R ? r + 1 : -1;
+        p = plan_sendrecv(count, dt, R, peers.data(), o);
+        break;
+    }
+    case 4: p = plan_alltoall(count, dt, R, o); break;
+    default: set_err("unknown op %d", op); return HOCCL_ERR_INVALID_ARG;
+    }
+    std::string js = plan_to_json(p);
+    if (needed) *needed = js.size() + 1;
+    if (buf && len) {
+        size_t k = std::min(len - 1, js.size());
+        std::memcpy(buf, js.data(), k);
+        buf[k] = 0;
+    }
+    return HOCCL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,168 @@
+// Internal types shared by the planner, the executor and the kernels.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/hoccl.h"
+
+namespace hoccl {
+
+enum class Op : int {
+    AllReduce = 0,
+    ReduceScatter = 1,
+    AllGather = 2,
+    SendRecv = 3,
+    AllToAll = 4,
+    AllToAllV = 5
+};
+
+// A symbolic buffer position: which buffer (send[rank], recv[rank] or the
+// library workspace) and a byte offset into it.  Plans are built on these so
+// the planner never touches device memory and can be dumped and replayed on
+// the host.
+enum BufKind : uint8_t { BUF_NONE = 0, BUF_SEND = 1, BUF_RECV = 2, BUF_WS = 3 };
+
+struct BufRef {
+    uint8_t kind = BUF_NONE;
+    int rank = 0;
+    size_t off = 0;  // bytes
+};
+
+// Element types a reduction step reads and writes.  The local contribution
+// (in1) is always of the collective's dtype; in0 and out are either the
+// dtype itself or the accumulator type (fp32 for bf16, the dtype otherwise).
+enum Phase : int {
+    PH_FIRST = 0,   // in0 = x[j+1] (dtype),  in1 = x[j+2],  out = partial (acc)
+    PH_MIDDLE = 1,  // in0 = partial (acc),   in1 = x[r],    out = partial (acc)
+    PH_LAST = 2,    // in0 = partial (acc),   in1 = x[j],    out = recv (dtype)
+    PH_ONLY = 3     // R == 2: in0 = x[j+1],  in1 = x[j],    out = recv (dtype)
+};
+
+struct ReduceSeg {
+    BufRef in0, in1, out;
+    size_t n = 0;  // elements
+};
+
+// One ring step: every rank adds its contribution to the partial it
+// received; one kernel launch covers all ranks' segments of the step.
+struct ReduceStep {
+    Phase phase = PH_MIDDLE;
+    int group = 0;
+    int step = 0;
+    std::vector<ReduceSeg> segs;
+};
+
+// Direct reduction: one launch folds all R inputs of every chunk in the ring
+// order.  Chunk j spans elements [j*c, min(total, (j+1)*c)) of the inputs;
+// its result goes to recv[j] at out_off(j) (reduce-scatter) or to every
+// recv[r] at the chunk's own offset (all-reduce, write_all).
+struct FoldStep {
+    size_t c = 0;        // chunk length in elements
+    size_t total = 0;    // input elements per rank covered by the fold
+    bool write_all = false;
+    bool out_at_chunk = false;  // reduce-scatter: recv[j] at 0; else j*c
+};
+
+// One copy: `bytes` from src to dst.  Copies with the same chain run in
+// order (the ring hops of one chunk); different chains are independent.  A
+// copy with group >= 0 may only start once the reduction of that group has
+// finished (all-reduce's gather phase).  `level` is the copy's position in
+// its chain, used to batch independent copies into one CU-copy launch.
+struct CopyOp {
+    BufRef dst, src;
+    size_t bytes = 0;
+    int chain = 0;
+    int group = -1;
+    int level = 0;
+};
+
+struct Plan {
+    Op op = Op::AllReduce;
+    hoccl_dtype_t dtype = HOCCL_FP32;
+    int R = 1;
+    size_t count = 0;
+    int ngroups = 1;
+    std::vector<ReduceStep> reduce_steps;  // in launch order, grouped
+    bool has_fold = false;
+    FoldStep fold;
+    std::vector<CopyOp> copies;            // in issue order
+    int nchains = 0;
+    size_t ws_bytes = 0;                   // workspace the plan needs
+    unsigned long long hbm_bytes = 0;      // algorithmic HBM bytes
+    unsigned long long copy_bytes = 0;
+};
+
+struct PlanOptions {
+    bool allgather_direct = false;
+    int allreduce_groups = 1;
+    size_t chunk_bytes = 0;
+    bool in_place = false;
+    hoccl_reduce_algo_t algo = HOCCL_REDUCE_RING;
+};
+
+size_t dtype_size(hoccl_dtype_t dt);
+size_t acc_size(hoccl_dtype_t dt);
+
+// Planner entry points (plan.cpp); pure host code.
+Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o);
+Plan plan_reduce_scatter(size_t recvcount, hoccl_dtype_t dt, int R, const PlanOptions &o);
+Plan plan_allgather(size_t sendcount, hoccl_dtype_t dt, int R, const PlanOptions &o);
+Plan plan_sendrecv(size_t count, hoccl_dtype_t dt, int R, const int *peers,
+                   const PlanOptions &o);
+Plan plan_alltoall(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o);
+Plan plan_alltoallv(const size_t *counts, const size_t *sdispls, const size_t *rdispls,
+                    hoccl_dtype_t dt, int R, const PlanOptions &o);
+
+// Assigns each chain of a plan to one of `queues` queues so that the bytes
+// per queue are balanced (largest chain first, onto the least loaded queue).
+std::vector<int> assign_chains(const Plan &p, int queues);
+
+std::string plan_to_json(const Plan &p);
+
+// ---- kernels (kernels.hip) -------------------------------------------------
+
+constexpr int kMaxReduceSegs = 64;
+constexpr int kMaxCopySegs = 128;
+constexpr int kMaxRanks = 64;
+
+struct RSegArg {
+    const void *in0;
+    const void *in1;
+    void *out;
+    uint64_t n;
+};
+struct ReduceArgs {
+    RSegArg seg[kMaxReduceSegs];
+    int nseg;
+};
+
+struct CSegArg {
+    const void *src;
+    void *dst;
+    uint64_t bytes;
+};
+struct CopyArgs {
+    CSegArg seg[kMaxCopySegs];
+    int nseg;
+};
+
+struct FoldArgs {
+    const void *in[kMaxRanks];
+    void *out[kMaxRanks];
+    uint64_t c;
+    uint64_t total;
+    int R;
+    int write_all;
+    int out_at_chunk;
+};
+
+hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg,
+                              int threads, hipStream_t s);
+hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
+                       hipStream_t s);
+hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s);
+
+}  // namespace hoccl

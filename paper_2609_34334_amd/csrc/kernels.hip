@@ -1,0 +1,346 @@
+// gfx950 kernels of the collective hot path.
+//
+// * reduce_step_kernel -- one ring reduction step for every virtual rank at
+//   once: out[i] = in0[i] + in1[i], where in0 is the partial received from
+//   the previous rank (or, on the first step, that rank's own element) and
+//   in1 is this rank's element.  bf16 partials are carried in fp32.
+// * fold_kernel        -- the direct variant: folds all R inputs of a chunk
+//   in the ring order in one pass (same result bit for bit, fewer bytes).
+// * copy_kernel        -- a CU copy of many independent (src, dst, bytes)
+//   segments; the comparator for the SDMA copy path.
+//
+// All three are HBM-bound streams (about one add per 8-12 bytes), so they
+// use 16-byte vector loads and stores, a grid-stride loop over each segment
+// with several independent vectors in flight per thread, and no LDS and no
+// MFMA: the limit is memory bandwidth, not arithmetic.
+#include <hip/hip_runtime.h>
+
+#include "hoccl_internal.h"
+
+namespace hoccl {
+namespace {
+
+// ---- element types ----------------------------------------------------------
+// S is the storage type in memory, A the accumulator type of the fold.
+struct TBF16 {
+    using S = uint16_t;
+    using A = float;
+    static __device__ __forceinline__ float widen(uint16_t v) {
+        return __uint_as_float((uint32_t)v << 16);  // exact
+    }
+    static __device__ __forceinline__ uint16_t narrow(float f) {
+        // v_cvt_pk_bf16_f32: round to nearest even, NaN stays NaN
+        return __builtin_bit_cast(uint16_t, (__bf16)f);
+    }
+};
+struct TF32 {
+    using S = float;
+    using A = float;
+    static __device__ __forceinline__ float widen(float v) { return v; }
+    static __device__ __forceinline__ float narrow(float f) { return f; }
+};
+struct TI32 {
+    using S = uint32_t;
+    using A = uint32_t;  // unsigned: adds wrap modulo 2^32
+    static __device__ __forceinline__ uint32_t widen(uint32_t v) { return v; }
+    static __device__ __forceinline__ uint32_t narrow(uint32_t v) { return v; }
+};
+
+template <typename S, int VE>
+struct alignas(16) Pack {
+    S v[VE];
+};
+
+// Splits the blocks of a launch over `nseg` segments.  With at least one
+// block per segment, block b serves segment b % nseg (consecutive blocks go
+// to different segments, so every XCD streams every segment); otherwise each
+// block walks several segments.
+template <typename F>
+__device__ __forceinline__ void for_each_segment(int nseg, F &&f) {
+    if ((int)gridDim.x >= nseg) {
+        int seg = (int)blockIdx.x % nseg;
+        int lb = (int)blockIdx.x / nseg;
+        int nb = ((int)gridDim.x - seg + nseg - 1) / nseg;
+        f(seg, lb, nb);
+    } else {
+        for (int seg = (int)blockIdx.x; seg < nseg; seg += (int)gridDim.x) f(seg, 0, 1);
+    }
+}
+
+// ---- one ring step --------------------------------------------------------------
+template <class T0, class T1, class TO, int VE, int U>
+__device__ __forceinline__ void reduce_segment(const RSegArg &s, int lb, int nb) {
+    using S0 = typename T0::S;
+    using S1 = typename T1::S;
+    using SO = typename TO::S;
+    using P0 = Pack<S0, VE>;
+    using P1 = Pack<S1, VE>;
+    using PO = Pack<SO, VE>;
+    const S0 *in0 = (const S0 *)s.in0;
+    const S1 *in1 = (const S1 *)s.in1;
+    SO *out = (SO *)s.out;
+    const uint64_t n = s.n;
+
+    // Elements before in1 reaches 16-byte alignment; the vector body needs
+    // in0, in1 and out all 16-byte aligned at the same element.
+    uint64_t h = ((16u - ((uintptr_t)in1 & 15u)) & 15u) / sizeof(S1);
+    if (h > n) h = n;
+    const bool vec = ((((uintptr_t)(in0 + h)) | ((uintptr_t)(in1 + h)) | ((uintptr_t)(out + h))) &
+                      15u) == 0;
+    if (!vec) h = n;
+    const uint64_t nv = (n - h) / VE;
+    const uint64_t tail = h + nv * VE;
+
+    const uint64_t bd = blockDim.x;
+    const uint64_t t = (uint64_t)lb * bd + threadIdx.x;
+    const uint64_t stride = (uint64_t)nb * bd;
+    for (uint64_t k = t; k < h; k += stride)
+        out[k] = TO::narrow(T0::widen(in0[k]) + T1::widen(in1[k]));
+    for (uint64_t k = tail + t; k < n; k += stride)
+        out[k] = TO::narrow(T0::widen(in0[k]) + T1::widen(in1[k]));
+
+    const P0 *v0 = (const P0 *)(in0 + h);
+    const P1 *v1 = (const P1 *)(in1 + h);
+    PO *vo = (PO *)(out + h);
+    auto one = [&](const P0 &a, const P1 &b) {
+        PO y;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) y.v[e] = TO::narrow(T0::widen(a.v[e]) + T1::widen(b.v[e]));
+        return y;
+    };
+    // Main loop: U vectors per thread, all in range, loads issued before use.
+    uint64_t base = (uint64_t)lb * bd * U + threadIdx.x;
+    for (; base + (uint64_t)(U - 1) * bd < nv; base += stride * U) {
+        P0 a[U];
+        P1 b[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            a[u] = v0[base + (uint64_t)u * bd];
+            b[u] = v1[base + (uint64_t)u * bd];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) vo[base + (uint64_t)u * bd] = one(a[u], b[u]);
+    }
+    // At most one partial iteration is left for this thread.
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        uint64_t i = base + (uint64_t)u * bd;
+        if (i < nv) vo[i] = one(v0[i], v1[i]);
+    }
+}
+
+template <typename A>
+__device__ __forceinline__ const A &kernargs();
+
+template <class T0, class T1, class TO, int VE, int U>
+__global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgs) {
+    const ReduceArgs &a = kernargs<ReduceArgs>();
+    for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
+        reduce_segment<T0, T1, TO, VE, U>(a.seg[seg], lb, nb);
+    });
+}
+
+// ---- direct fold ------------------------------------------------------------------
+// Chunk j reads x[(j+1)%R], x[(j+2)%R], ..., x[j] at the chunk's elements and
+// adds them left to right; loads are issued in batches of KB ranks so several
+// are in flight before the adds consume them in order.
+template <class T, int VE, int NR>
+__device__ __forceinline__ void fold_chunk(const FoldArgs &a, int j, int lb, int nb) {
+    using S = typename T::S;
+    using A = typename T::A;
+    using P = Pack<S, VE>;
+    const int R = NR > 0 ? NR : a.R;
+    const uint64_t e0 = (uint64_t)j * a.c;
+    if (e0 >= a.total) return;
+    const uint64_t n = (a.total - e0 < a.c) ? a.total - e0 : a.c;
+    // k-th operand of chunk j's fold (k = 0 .. R-1) is rank (j + 1 + k) mod R.
+    auto src = [&](int k) -> const S * {
+        int r = j + 1 + k;
+        if (r >= R) r -= R;
+        if (r >= R) r -= R;
+        return (const S *)a.in[r] + e0;
+    };
+    const uint64_t oe = a.out_at_chunk ? 0 : e0;
+    const int nout = a.write_all ? R : 1;
+    auto dst = [&](int q) -> S * { return (S *)a.out[a.write_all ? q : j] + oe; };
+
+    uint64_t h = ((16u - ((uintptr_t)src(0) & 15u)) & 15u) / sizeof(S);
+    if (h > n) h = n;
+    uintptr_t mis = 0;
+    for (int k = 0; k < R; ++k) mis |= (uintptr_t)(src(k) + h);
+    for (int q = 0; q < nout; ++q) mis |= (uintptr_t)(dst(q) + h);
+    if (mis & 15u) h = n;
+    const uint64_t nv = (n - h) / VE;
+    const uint64_t tail = h + nv * VE;
+
+    const uint64_t bd = blockDim.x;
+    const uint64_t t = (uint64_t)lb * bd + threadIdx.x;
+    const uint64_t stride = (uint64_t)nb * bd;
+    auto scalar = [&](uint64_t k) {
+        A acc = T::widen(src(0)[k]);
+        for (int q = 1; q < R; ++q) acc = acc + T::widen(src(q)[k]);
+        S y = T::narrow(acc);
+        for (int q = 0; q < nout; ++q) dst(q)[k] = y;
+    };
+    for (uint64_t k = t; k < h; k += stride) scalar(k);
+    for (uint64_t k = tail + t; k < n; k += stride) scalar(k);
+
+    for (uint64_t i = t; i < nv; i += stride) {
+        A acc[VE];
+        if constexpr (NR > 0) {
+            // every operand's vector is loaded before the in-order adds
+            P v[NR];
+#pragma unroll
+            for (int k = 0; k < NR; ++k) v[k] = ((const P *)(src(k) + h))[i];
+#pragma unroll
+            for (int e = 0; e < VE; ++e) acc[e] = T::widen(v[0].v[e]);
+#pragma unroll
+            for (int k = 1; k < NR; ++k)
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[k].v[e]);
+        } else {
+            constexpr int KB = 8;
+            {
+                P v0 = ((const P *)(src(0) + h))[i];
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = T::widen(v0.v[e]);
+            }
+            int k = 1;
+            for (; k + KB <= R; k += KB) {
+                P v[KB];
+#pragma unroll
+                for (int q = 0; q < KB; ++q) v[q] = ((const P *)(src(k + q) + h))[i];
+#pragma unroll
+                for (int q = 0; q < KB; ++q)
+#pragma unroll
+                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[q].v[e]);
+            }
+            for (; k < R; ++k) {
+                P v = ((const P *)(src(k) + h))[i];
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v.v[e]);
+            }
+        }
+        P y;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
+        for (int q = 0; q < nout; ++q) ((P *)(dst(q) + h))[i] = y;
+    }
+}
+
+// The argument structs are indexed with run-time rank numbers.  Reading them
+// through the kernarg segment pointer keeps those reads scalar loads from the
+// (read-only) argument buffer; indexing the by-value parameter instead makes
+// the compiler copy the whole struct into per-thread scratch memory.
+template <typename A>
+__device__ __forceinline__ const A &kernargs() {
+    return *(const A *)__builtin_amdgcn_kernarg_segment_ptr();
+}
+
+template <class T, int VE, int NR>
+__global__ void __launch_bounds__(1024) fold_kernel(FoldArgs) {
+    const FoldArgs &a = kernargs<FoldArgs>();
+    for_each_segment(a.R, [&](int j, int lb, int nb) { fold_chunk<T, VE, NR>(a, j, lb, nb); });
+}
+
+// ---- CU copy ----------------------------------------------------------------------
+template <int U>
+__device__ __forceinline__ void copy_segment(const CSegArg &s, int lb, int nb) {
+    const unsigned char *src = (const unsigned char *)s.src;
+    unsigned char *dst = (unsigned char *)s.dst;
+    const uint64_t n = s.bytes;
+    const uint64_t bd = blockDim.x;
+    const uint64_t t = (uint64_t)lb * bd + threadIdx.x;
+    const uint64_t stride = (uint64_t)nb * bd;
+    // Widest unit for which source and destination share their misalignment.
+    const uintptr_t x = (uintptr_t)src ^ (uintptr_t)dst;
+    const uint64_t w = (x & 15u) == 0 ? 16 : ((x & 3u) == 0 ? 4 : 1);
+    uint64_t h = w == 1 ? 0 : ((w - ((uintptr_t)src & (w - 1))) & (w - 1));
+    if (h > n) h = n;
+    const uint64_t nv = w == 1 ? 0 : (n - h) / w;
+    const uint64_t tail = h + nv * w;
+    for (uint64_t k = t; k < h; k += stride) dst[k] = src[k];
+    for (uint64_t k = (w == 1 ? 0 : tail) + t; k < n; k += stride) dst[k] = src[k];
+    if (w == 16) {
+        using V = Pack<uint32_t, 4>;  // HIP's uint4 is a union and defeats SROA
+        const V *vs = (const V *)(src + h);
+        V *vd = (V *)(dst + h);
+        uint64_t base = (uint64_t)lb * bd * U + threadIdx.x;
+        for (; base + (uint64_t)(U - 1) * bd < nv; base += stride * U) {
+            V v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) v[u] = vs[base + (uint64_t)u * bd];
+#pragma unroll
+            for (int u = 0; u < U; ++u) vd[base + (uint64_t)u * bd] = v[u];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            uint64_t i = base + (uint64_t)u * bd;
+            if (i < nv) vd[i] = vs[i];
+        }
+    } else if (w == 4) {
+        const uint32_t *vs = (const uint32_t *)(src + h);
+        uint32_t *vd = (uint32_t *)(dst + h);
+        for (uint64_t i = t; i < nv; i += stride) vd[i] = vs[i];
+    }
+}
+
+__global__ void __launch_bounds__(1024) copy_kernel(CopyArgs) {
+    const CopyArgs &a = kernargs<CopyArgs>();
+    for_each_segment(a.nseg, [&](int seg, int lb, int nb) { copy_segment<2>(a.seg[seg], lb, nb); });
+}
+
+}  // namespace
+
+// ---- launchers --------------------------------------------------------------------
+
+template <class T0, class T1, class TO, int VE, int U>
+static hipError_t launch_rs(const ReduceArgs &a, int wg, int threads, hipStream_t s) {
+    hipLaunchKernelGGL((reduce_step_kernel<T0, T1, TO, VE, U>), dim3((unsigned)wg), dim3((unsigned)threads),
+                       0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg, int threads,
+                              hipStream_t s) {
+    if (dt == HOCCL_BF16) {
+        switch (ph) {
+        case PH_FIRST: return launch_rs<TBF16, TBF16, TF32, 8, 2>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TF32, TBF16, TF32, 8, 2>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TF32, TBF16, TBF16, 8, 2>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, 8, 2>(a, wg, threads, s);
+        }
+    } else if (dt == HOCCL_FP32) {
+        return launch_rs<TF32, TF32, TF32, 4, 4>(a, wg, threads, s);
+    } else if (dt == HOCCL_INT32) {
+        return launch_rs<TI32, TI32, TI32, 4, 4>(a, wg, threads, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <class T, int VE>
+static hipError_t launch_fold_t(const FoldArgs &a, int wg, int threads, hipStream_t s) {
+    dim3 g((unsigned)wg), b((unsigned)threads);
+    switch (a.R) {
+    case 2: hipLaunchKernelGGL((fold_kernel<T, VE, 2>), g, b, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((fold_kernel<T, VE, 3>), g, b, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((fold_kernel<T, VE, 4>), g, b, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((fold_kernel<T, VE, 8>), g, b, 0, s, a); break;
+    default: hipLaunchKernelGGL((fold_kernel<T, VE, 0>), g, b, 0, s, a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads, hipStream_t s) {
+    if (dt == HOCCL_BF16) return launch_fold_t<TBF16, 8>(a, wg, threads, s);
+    if (dt == HOCCL_FP32) return launch_fold_t<TF32, 4>(a, wg, threads, s);
+    if (dt == HOCCL_INT32) return launch_fold_t<TI32, 4>(a, wg, threads, s);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s) {
+    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)wg), dim3((unsigned)threads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace hoccl

@@ -1,0 +1,380 @@
+// Copy proxy: the paper's CPU-driven DMA path with its stream handshake.
+//
+// The paper drives the copy engines from a CPU proxy thread and keeps them
+// in order with the surrounding kernels through two flags per operation in
+// host memory, written and awaited by the GPU stream with stream memory
+// operations (Stream Manager: CPU-GPU handshake synchronization protocol):
+//
+//   stream:  write start := START;  wait start == 0;     <- start path
+//            wait finish == FINISH; write finish := 0;   <- completion path
+//   proxy:   see start == START, write start := 0 (acknowledge),
+//            run the copies, write finish := FINISH, see finish == 0.
+//
+// Every transition is acknowledged, so a flag pair is free for reuse once
+// the stream has reset `finish`.  The flags live in a pool of slots in
+// pinned, coherent host memory (the paper's flag pool); each in-flight
+// operation holds one slot.
+//
+// The copies themselves go to SDMA engines chosen explicitly through ROCr
+// (hsa_amd_memory_async_copy_on_engine), which lets one collective use every
+// engine of the device; the HIP runtime's own device-to-device path picks
+// engines itself.  Chains of copies (the ring hops of one chunk) stay on one
+// engine and also depend on their predecessor's completion signal; chains
+// are spread over the engines so that each engine gets about the same
+// number of bytes (the paper's flow-size-aware chunk scheduling, reduced to
+// one domain).
+#include "proxy.h"
+
+#include <hip/hip_runtime.h>
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <mutex>
+#include <numeric>
+#include <thread>
+
+namespace hoccl {
+
+namespace {
+
+constexpr uint32_t kStartValue = 0x53544152u;   // written by the stream
+constexpr uint32_t kFinishValue = 0x46494e49u;  // written by the proxy
+constexpr int kSlots = 64;
+constexpr size_t kLine = 64;  // one cache line per flag
+
+struct FindAgent {
+    uint32_t bdf;
+    bool found;
+    hsa_agent_t agent;
+};
+
+hsa_status_t find_agent_cb(hsa_agent_t a, void *data) {
+    FindAgent *f = (FindAgent *)data;
+    hsa_device_type_t t;
+    if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &t) != HSA_STATUS_SUCCESS) return HSA_STATUS_SUCCESS;
+    if (t != HSA_DEVICE_TYPE_GPU) return HSA_STATUS_SUCCESS;
+    uint32_t bdf = 0;
+    if (hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_BDFID, &bdf) != HSA_STATUS_SUCCESS)
+        return HSA_STATUS_SUCCESS;
+    if ((bdf >> 3) == (f->bdf >> 3)) {  // bus and device; any function
+        f->agent = a;
+        f->found = true;
+        return HSA_STATUS_INFO_BREAK;
+    }
+    return HSA_STATUS_SUCCESS;
+}
+
+inline uint32_t load_flag(volatile uint32_t *p) {
+    return __atomic_load_n((uint32_t *)p, __ATOMIC_ACQUIRE);
+}
+inline void store_flag(volatile uint32_t *p, uint32_t v) {
+    __atomic_store_n((uint32_t *)p, v, __ATOMIC_RELEASE);
+}
+
+}  // namespace
+
+struct ProxyOp {
+    enum State { WAIT_START, COPYING, WAIT_ACK };
+    int slot = -1;
+    std::vector<ProxyCopy> copies;
+    std::vector<uint32_t> engine;  // engine id bit per copy
+    std::vector<int> dep;          // previous copy of the same chain, or -1
+    std::vector<hsa_signal_t> sig;
+    State state = WAIT_START;
+    std::chrono::steady_clock::time_point since;
+    unsigned timeout_ms = 10000;
+    bool timed_out = false;
+};
+
+class ProxyImpl {
+  public:
+    hsa_agent_t agent{};
+    std::vector<uint32_t> engines;  // id bits of usable engines
+    uint32_t *flags = nullptr;      // kSlots * 2 flags, one per cache line
+    std::mutex mu;
+    std::condition_variable cv_work, cv_slot;
+    std::deque<ProxyOp *> incoming;
+    std::vector<int> free_slots;
+    std::vector<hsa_signal_t> free_signals;
+    bool stop = false;
+    std::thread th;
+    hoccl_status_t sticky = HOCCL_OK;
+    std::string sticky_msg;
+
+    volatile uint32_t *start_flag(int s) { return (volatile uint32_t *)((char *)flags + (2 * s) * kLine); }
+    volatile uint32_t *finish_flag(int s) {
+        return (volatile uint32_t *)((char *)flags + (2 * s + 1) * kLine);
+    }
+
+    void fail(hoccl_status_t st, const char *msg) {
+        std::lock_guard<std::mutex> lk(mu);
+        if (sticky == HOCCL_OK) {
+            sticky = st;
+            sticky_msg = msg;
+        }
+    }
+
+    bool issue(ProxyOp &op) {
+        for (size_t i = 0; i < op.copies.size(); ++i) {
+            const ProxyCopy &c = op.copies[i];
+            hsa_signal_store_screlease(op.sig[i], 1);
+            const hsa_signal_t *deps = nullptr;
+            uint32_t ndep = 0;
+            if (op.dep[i] >= 0) {
+                deps = &op.sig[(size_t)op.dep[i]];
+                ndep = 1;
+            }
+            hsa_status_t e = hsa_amd_memory_async_copy_on_engine(
+                c.dst, agent, c.src, agent, c.bytes, ndep, deps, op.sig[i],
+                (hsa_amd_sdma_engine_id_t)op.engine[i], true);
+            if (e != HSA_STATUS_SUCCESS) {
+                char buf[160];
+                std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
+                fail(HOCCL_ERR_HIP, buf);
+                // Retire the copies that were never issued so the op completes.
+                for (size_t k = i; k < op.copies.size(); ++k) hsa_signal_store_screlease(op.sig[k], 0);
+                return false;
+            }
+        }
+        return true;
+    }
+
+    bool copies_done(const ProxyOp &op) {
+        for (const hsa_signal_t &s : op.sig)
+            if (hsa_signal_load_scacquire(s) != 0) return false;
+        return true;
+    }
+
+    void release(ProxyOp *op) {
+        std::lock_guard<std::mutex> lk(mu);
+        for (auto &s : op->sig) free_signals.push_back(s);
+        free_slots.push_back(op->slot);
+        cv_slot.notify_all();
+        delete op;
+    }
+
+    void loop() {
+        std::vector<ProxyOp *> active;
+        for (;;) {
+            {
+                std::unique_lock<std::mutex> lk(mu);
+                if (active.empty())
+                    cv_work.wait(lk, [&] { return stop || !incoming.empty(); });
+                while (!incoming.empty()) {
+                    active.push_back(incoming.front());
+                    incoming.pop_front();
+                }
+                if (stop && active.empty()) return;
+            }
+            bool progress = false;
+            auto now = std::chrono::steady_clock::now();
+            for (size_t i = 0; i < active.size();) {
+                ProxyOp *op = active[i];
+                bool retired = false;
+                switch (op->state) {
+                case ProxyOp::WAIT_START:
+                    // The stream has drained everything before the collective.
+                    if (load_flag(start_flag(op->slot)) == kStartValue) {
+                        store_flag(start_flag(op->slot), 0);  // acknowledge
+                        issue(*op);
+                        op->state = ProxyOp::COPYING;
+                        op->since = now;
+                        progress = true;
+                    }
+                    break;
+                case ProxyOp::COPYING:
+                    if (copies_done(*op)) {
+                        store_flag(finish_flag(op->slot), kFinishValue);
+                        op->state = ProxyOp::WAIT_ACK;
+                        op->since = now;
+                        progress = true;
+                    } else if (!op->timed_out &&
+                               now - op->since > std::chrono::milliseconds(op->timeout_ms)) {
+                        op->timed_out = true;
+                        fail(HOCCL_ERR_TIMEOUT, "SDMA copies did not complete within the proxy timeout");
+                    }
+                    break;
+                case ProxyOp::WAIT_ACK:
+                    // The stream reset `finish`: the slot may be reused.
+                    if (load_flag(finish_flag(op->slot)) == 0) {
+                        release(op);
+                        retired = true;
+                        progress = true;
+                    }
+                    break;
+                }
+                if (retired) {
+                    active[i] = active.back();
+                    active.pop_back();
+                } else {
+                    ++i;
+                }
+            }
+            if (!progress) std::this_thread::yield();
+        }
+    }
+};
+
+Proxy *Proxy::create(int device) {
+    int bus = 0, dev = 0;
+    if (hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, device) != hipSuccess ||
+        hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, device) != hipSuccess)
+        return nullptr;
+    if (hsa_init() != HSA_STATUS_SUCCESS) return nullptr;
+    FindAgent f{(uint32_t)((bus << 8) | (dev << 3)), false, {}};
+    hsa_iterate_agents(find_agent_cb, &f);
+    if (!f.found) {
+        hsa_shut_down();
+        return nullptr;
+    }
+    uint32_t mask = 0;
+    if (hsa_amd_memory_copy_engine_status(f.agent, f.agent, &mask) != HSA_STATUS_SUCCESS || mask == 0) {
+        hsa_shut_down();
+        return nullptr;
+    }
+    ProxyImpl *p = new ProxyImpl();
+    p->agent = f.agent;
+    for (int b = 0; b < 32; ++b)
+        if (mask & (1u << b)) p->engines.push_back(1u << b);
+    void *fl = nullptr;
+    if (hipHostMalloc(&fl, kSlots * 2 * kLine, hipHostMallocCoherent | hipHostMallocMapped) !=
+            hipSuccess ||
+        !fl) {
+        delete p;
+        hsa_shut_down();
+        return nullptr;
+    }
+    std::memset(fl, 0, kSlots * 2 * kLine);
+    p->flags = (uint32_t *)fl;
+    for (int s = kSlots - 1; s >= 0; --s) p->free_slots.push_back(s);
+    p->th = std::thread([p] { p->loop(); });
+    return new Proxy(p);
+}
+
+Proxy::~Proxy() {
+    {
+        std::lock_guard<std::mutex> lk(impl_->mu);
+        impl_->stop = true;
+    }
+    impl_->cv_work.notify_all();
+    if (impl_->th.joinable()) impl_->th.join();
+    for (auto &s : impl_->free_signals) hsa_signal_destroy(s);
+    if (impl_->flags) (void)hipHostFree(impl_->flags);
+    delete impl_;
+    hsa_shut_down();
+}
+
+int Proxy::engine_count() const { return (int)impl_->engines.size(); }
+
+hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
+                             unsigned timeout_ms, hipStream_t s, int *engines_used, std::string &err) {
+    ProxyImpl &P = *impl_;
+    {
+        std::lock_guard<std::mutex> lk(P.mu);
+        if (P.sticky != HOCCL_OK) {
+            hoccl_status_t st = P.sticky;
+            err = P.sticky_msg;
+            P.sticky = HOCCL_OK;
+            P.sticky_msg.clear();
+            return st;
+        }
+    }
+    ProxyOp *op = new ProxyOp();
+    op->copies = copies;
+    op->timeout_ms = timeout_ms ? timeout_ms : 10000;
+    int E = (int)P.engines.size();
+    if (max_engines > 0) E = std::min(E, max_engines);
+    // Balance bytes per engine: largest chain first onto the least loaded.
+    int nch = 0;
+    for (auto &c : copies) nch = std::max(nch, c.chain + 1);
+    std::vector<unsigned long long> cb((size_t)nch, 0);
+    for (auto &c : copies) cb[(size_t)c.chain] += c.bytes;
+    std::vector<int> order((size_t)nch);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cb[(size_t)a] > cb[(size_t)b]; });
+    std::vector<unsigned long long> load((size_t)E, 0);
+    std::vector<int> eng_of_chain((size_t)nch, 0);
+    for (int ch : order) {
+        size_t best = 0;
+        for (size_t k = 1; k < load.size(); ++k)
+            if (load[k] < load[best]) best = k;
+        eng_of_chain[(size_t)ch] = (int)best;
+        load[best] += cb[(size_t)ch];
+    }
+    std::vector<int> last((size_t)nch, -1);
+    op->engine.resize(copies.size());
+    op->dep.resize(copies.size());
+    for (size_t i = 0; i < copies.size(); ++i) {
+        int ch = copies[i].chain;
+        op->engine[i] = P.engines[(size_t)eng_of_chain[(size_t)ch]];
+        op->dep[i] = last[(size_t)ch];
+        last[(size_t)ch] = (int)i;
+    }
+    if (engines_used) {
+        int used = 0;
+        for (auto l : load) used += l > 0;
+        *engines_used = used;
+    }
+    // Signals and a flag slot.
+    {
+        std::unique_lock<std::mutex> lk(P.mu);
+        if (!P.cv_slot.wait_for(lk, std::chrono::milliseconds(op->timeout_ms),
+                                [&] { return !P.free_slots.empty(); })) {
+            delete op;
+            err = "no free handshake slot within the proxy timeout";
+            return HOCCL_ERR_TIMEOUT;
+        }
+        op->slot = P.free_slots.back();
+        P.free_slots.pop_back();
+        while (op->sig.size() < copies.size() && !P.free_signals.empty()) {
+            op->sig.push_back(P.free_signals.back());
+            P.free_signals.pop_back();
+        }
+    }
+    while (op->sig.size() < copies.size()) {
+        hsa_signal_t sg;
+        if (hsa_signal_create(1, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) {
+            err = "hsa_signal_create failed";
+            std::lock_guard<std::mutex> lk(P.mu);
+            for (auto &x : op->sig) P.free_signals.push_back(x);
+            P.free_slots.push_back(op->slot);
+            delete op;
+            return HOCCL_ERR_HIP;
+        }
+        op->sig.push_back(sg);
+    }
+    void *st = (void *)P.start_flag(op->slot);
+    void *fi = (void *)P.finish_flag(op->slot);
+    hipError_t e = hipStreamWriteValue32(s, st, kStartValue, 0);
+    if (e != hipSuccess) {
+        // Nothing reached the stream: give the slot and signals back.
+        err = std::string("hipStreamWriteValue32 failed: ") + hipGetErrorString(e);
+        std::lock_guard<std::mutex> lk(P.mu);
+        for (auto &x : op->sig) P.free_signals.push_back(x);
+        P.free_slots.push_back(op->slot);
+        delete op;
+        return HOCCL_ERR_HIP;
+    }
+    if ((e = hipStreamWaitValue32(s, st, 0, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
+        (e = hipStreamWaitValue32(s, fi, kFinishValue, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
+        (e = hipStreamWriteValue32(s, fi, 0, 0)) != hipSuccess) {
+        // Whatever part of the handshake reached the stream, the proxy must
+        // still see the op through, so hand it over regardless and report.
+        err = std::string("stream memory operation failed: ") + hipGetErrorString(e);
+    }
+    {
+        std::lock_guard<std::mutex> lk(P.mu);
+        P.incoming.push_back(op);
+    }
+    P.cv_work.notify_one();
+    return e == hipSuccess ? HOCCL_OK : HOCCL_ERR_HIP;
+}
+
+}  // namespace hoccl

@@ -1,0 +1,43 @@
+// Copy proxy: a CPU thread that drives chosen SDMA engines directly and is
+// ordered with a HIP stream by the paper's start/finish flag handshake.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstddef>
+#include <string>
+#include <vector>
+
+#include "../../include/hoccl.h"
+
+namespace hoccl {
+
+struct ProxyCopy {
+    void *dst;
+    const void *src;
+    size_t bytes;
+    int chain;  // copies of one chain run in order; chains are independent
+};
+
+class ProxyImpl;
+
+class Proxy {
+  public:
+    // Null when the device's SDMA engines cannot be driven directly.
+    static Proxy *create(int device);
+    ~Proxy();
+
+    int engine_count() const;
+
+    // Enqueues the handshake on `s` and hands the copies to the proxy
+    // thread; returns once enqueued.  Copies run on at most `max_engines`
+    // engines (0 = all), balanced by bytes per engine.
+    hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
+                          unsigned timeout_ms, hipStream_t s, int *engines_used, std::string &err);
+
+  private:
+    explicit Proxy(ProxyImpl *impl) : impl_(impl) {}
+    ProxyImpl *impl_;
+};
+
+}  // namespace hoccl

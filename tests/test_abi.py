@@ -1,0 +1,127 @@
+"""The C-ABI library loads on a machine without a GPU, exports every entry
+point include/hoccl.h declares, and rejects bad arguments before touching the
+device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_34334_amd as hc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hoccl.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hoccl_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_collectives():
+    syms = declared_symbols()
+    for s in ["hoccl_allreduce", "hoccl_reduce_scatter", "hoccl_allgather", "hoccl_sendrecv",
+              "hoccl_alltoall", "hoccl_alltoallv", "hoccl_init", "hoccl_finalize"]:
+        assert s in syms
+
+
+@pytest.mark.parametrize("sym", declared_symbols())
+def test_library_exports_symbol(sym):
+    assert hasattr(hc.lib(), sym), sym
+
+
+L = hc.lib()
+VP = ctypes.c_void_p
+
+
+def ptrs(*vals):
+    return (VP * len(vals))(*vals)
+
+
+def test_bad_rank_count_and_dtype():
+    p = ptrs(0x1000)
+    assert L.hoccl_allreduce(p, p, 4, hc.FP32, 0, None) == hc.ERR_INVALID_ARG
+    big = (VP * 65)(*([0x1000] * 65))
+    assert L.hoccl_allreduce(big, big, 4, hc.FP32, 65, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_allreduce(p, p, 4, 9, 1, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_allreduce(None, p, 4, hc.FP32, 1, None) == hc.ERR_INVALID_ARG
+
+
+def test_null_buffer_with_count():
+    s = ptrs(0x1000, 0)
+    r = ptrs(0x10000, 0x20000)
+    assert L.hoccl_allgather(s, r, 4, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+
+
+def test_zero_count_is_noop_ok():
+    s = ptrs(0, 0)
+    assert L.hoccl_allreduce(s, s, 0, hc.FP32, 2, None) == hc.OK
+    assert L.hoccl_reduce_scatter(s, s, 0, hc.BF16, 2, None) == hc.OK
+
+
+def test_sendrecv_duplicate_receiver_and_bad_peer():
+    s = ptrs(0x1000, 0x2000, 0x3000)
+    r = ptrs(0x10000, 0x20000, 0x30000)
+    dup = (ctypes.c_int * 3)(1, 1, -1)
+    assert L.hoccl_sendrecv(s, r, dup, 4, hc.FP32, 3, None) == hc.ERR_INVALID_ARG
+    bad = (ctypes.c_int * 3)(3, -1, -1)
+    assert L.hoccl_sendrecv(s, r, bad, 4, hc.FP32, 3, None) == hc.ERR_INVALID_ARG
+    neg = (ctypes.c_int * 3)(-2, -1, -1)
+    assert L.hoccl_sendrecv(s, r, neg, 4, hc.FP32, 3, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_sendrecv(s, r, None, 4, hc.FP32, 3, None) == hc.ERR_INVALID_ARG
+
+
+def test_overlapping_outputs_rejected():
+    s = ptrs(0x100000, 0x200000)
+    r = ptrs(0x300000, 0x300008)                 # 16-byte outputs 8 bytes apart
+    assert L.hoccl_allreduce(s, r, 4, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+
+
+def test_input_output_overlap_outside_in_place_form():
+    # all-reduce: recv[0] overlaps send[1]
+    s = ptrs(0x100000, 0x200000)
+    r = ptrs(0x200000, 0x300000)
+    assert L.hoccl_allreduce(s, r, 4, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+    # all-gather: send[1] must sit at recv[1] + 1*n, not at recv[1]
+    s = ptrs(0x100000, 0x300000)
+    r = ptrs(0x200000, 0x300000)
+    assert L.hoccl_allgather(s, r, 4, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+    # reduce-scatter: recv[1] must be send[1] + 1*n, not send[1] + 0
+    s = ptrs(0x100000, 0x200000)
+    r = ptrs(0x300000, 0x200000)
+    assert L.hoccl_reduce_scatter(s, r, 4, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+    # all-to-all is out-of-place only
+    s = ptrs(0x100000, 0x200000)
+    assert L.hoccl_alltoall(s, s, 4, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+
+
+def test_alltoallv_overlapping_destinations_rejected():
+    R = 2
+    s = ptrs(0x100000, 0x200000)
+    r = ptrs(0x300000, 0x400000)
+    S = ctypes.c_size_t * 4
+    counts = S(4, 4, 4, 4)
+    sd = S(0, 4, 0, 4)
+    rd = S(0, 0, 2, 4)       # (0->0) at 0..4 and (1->0) at 2..6 overlap
+    assert L.hoccl_alltoallv(s, counts, sd, r, rd, hc.FP32, R, None) == hc.ERR_INVALID_ARG
+
+
+def test_config_roundtrip_and_validation():
+    saved = hc.get_config()
+    try:
+        hc.set_config(workgroups_per_step=64, copy_path="kernel", allreduce_chunk_groups=4)
+        c = hc.get_config()
+        assert c["workgroups_per_step"] == 64 and c["copy_path"] == hc.COPY_KERNEL
+        with pytest.raises(hc.HocclError):
+            hc.set_config(threads_per_workgroup=100)
+        with pytest.raises(hc.HocclError):
+            hc.set_config(chunk_bytes=100)
+        assert hc.get_config()["workgroups_per_step"] == 64
+    finally:
+        hc.set_config(**saved)
+
+
+def test_status_strings():
+    for st in range(7):
+        assert L.hoccl_status_string(st)

@@ -1,0 +1,333 @@
+"""GPU parity: every collective through the C ABI against the CPU oracle,
+bit for bit, across dtypes, rank counts, ragged and misaligned sizes, in-place
+forms, copy paths, reduction algorithms and launch shapes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34334_amd as hc
+import workloads as W
+from gpu_util import (ES, NAME, TORCH, assert_bitwise, check_canaries, from_dev, padded,
+                      to_dev)
+
+pytestmark = pytest.mark.gpu
+
+DTS = [hc.INT32, hc.FP32, hc.BF16]
+PATHS = ["sdma", "engines", "kernel"]
+
+
+@pytest.fixture(autouse=True)
+def _fresh_config():
+    saved = hc.get_config()
+    yield
+    hc.set_config(**saved)
+
+
+def run_ar(x, dt, lead=0):
+    R, n = len(x), x[0].size
+    outs = [padded(n, dt, lead) for _ in range(R)]
+    send = [to_dev(a, dt) for a in x]
+    hc.allreduce(send, [o[1] for o in outs])
+    torch.cuda.synchronize()
+    for full, _ in outs:
+        check_canaries(full, lead, n, dt)
+    return [from_dev(o[1], dt) for o in outs]
+
+
+def run_rs(x, dt, lead=0):
+    R = len(x)
+    n = x[0].size // R
+    outs = [padded(n, dt, lead) for _ in range(R)]
+    send = [to_dev(a, dt) for a in x]
+    hc.reduce_scatter(send, [o[1] for o in outs])
+    torch.cuda.synchronize()
+    for full, _ in outs:
+        check_canaries(full, lead, n, dt)
+    return [from_dev(o[1], dt) for o in outs]
+
+
+# ---------------------------------------------------------------- reductions
+
+@pytest.mark.parametrize("algo", ["ring", "direct"])
+@pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
+@pytest.mark.parametrize("R", [1, 2, 3, 4, 8])
+def test_allreduce_and_reduce_scatter(algo, dt, R):
+    hc.set_config(reduce_algo=algo, copy_path="sdma")
+    for n in [1, 7, R * 37 + 3, 4099, 65536 + 5]:
+        seed = 9000 + 13 * R + n
+        x = [W.random_values(NAME[dt], seed, r, n) for r in range(R)]
+        ref = oracle.allreduce_new(x, dt)
+        got = run_ar(x, dt)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"allreduce R={R} n={n} r={r}")
+        x = [W.random_values(NAME[dt], seed + 1, r, R * n) for r in range(R)]
+        ref = oracle.reduce_scatter_new(x, dt)
+        got = run_rs(x, dt)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"reduce_scatter R={R} n={n} r={r}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("groups", [1, 4])
+def test_allreduce_copy_paths_and_groups(path, groups):
+    hc.set_config(copy_path=path, allreduce_chunk_groups=groups)
+    for dt in DTS:
+        R, n = 4, 262_147
+        x = [W.random_values(NAME[dt], 77, r, n) for r in range(R)]
+        ref = oracle.allreduce_new(x, dt)
+        got = run_ar(x, dt)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"{path} groups={groups} {NAME[dt]} r={r}")
+
+
+@pytest.mark.parametrize("wg,threads", [(1, 64), (7, 256), (256, 256), (2048, 512), (4096, 1024)])
+def test_launch_shapes(wg, threads):
+    hc.set_config(workgroups_per_step=wg, threads_per_workgroup=threads)
+    for algo in ["ring", "direct"]:
+        hc.set_config(reduce_algo=algo)
+        R, n = 8, 20_011
+        x = [W.random_values("bf16", 31, r, R * n) for r in range(R)]
+        ref = oracle.reduce_scatter_new(x, hc.BF16)
+        got = run_rs(x, hc.BF16)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"wg={wg} threads={threads} {algo} r={r}")
+
+
+@pytest.mark.parametrize("lead", [1, 3, 5])
+def test_misaligned_buffers(lead):
+    """Output windows that start off a 16-byte boundary take the scalar head
+    and tail paths; inputs are sub-views at an element offset too."""
+    for dt in DTS:
+        R, n = 4, 10_007
+        x = [W.random_values(NAME[dt], 41 + lead, r, n) for r in range(R)]
+        ref = oracle.allreduce_new(x, dt)
+        send_full = [to_dev(np.concatenate([np.zeros(lead, a.dtype), a]), dt) for a in x]
+        send = [t[lead:] for t in send_full]
+        outs = [padded(n, dt, lead) for _ in range(R)]
+        hc.allreduce(send, [o[1] for o in outs])
+        torch.cuda.synchronize()
+        for r in range(R):
+            check_canaries(outs[r][0], lead, n, dt)
+            assert_bitwise(from_dev(outs[r][1], dt), ref[r], f"misaligned {NAME[dt]} r={r}")
+
+
+def test_mixed_alignment_across_ranks():
+    # rank buffers with different misalignments force the all-scalar path
+    R, n, dt = 3, 5003, hc.FP32
+    x = [W.random_values("fp32", 51, r, n) for r in range(R)]
+    ref = oracle.allreduce_new(x, dt)
+    send = []
+    for r, a in enumerate(x):
+        t = to_dev(np.concatenate([np.zeros(r, a.dtype), a]), dt)
+        send.append(t[r:])
+    recv = [torch.empty(n + 4, dtype=torch.float32, device="cuda")[r:r + n] for r in range(R)]
+    hc.allreduce(send, recv)
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(recv[r], dt), ref[r], f"r={r}")
+
+
+@pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
+def test_in_place_forms(dt):
+    R, n = 4, 9001
+    # all-reduce in place
+    x = [W.random_values(NAME[dt], 61, r, n) for r in range(R)]
+    ref = oracle.allreduce_new(x, dt)
+    bufs = [to_dev(a, dt) for a in x]
+    hc.allreduce(bufs, bufs)
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(bufs[r], dt), ref[r], f"AR in place r={r}")
+    # reduce-scatter in place: recv[r] = send[r] + r*n
+    x = [W.random_values(NAME[dt], 62, r, R * n) for r in range(R)]
+    ref = oracle.reduce_scatter_new(x, dt)
+    bufs = [to_dev(a, dt) for a in x]
+    hc.reduce_scatter(bufs, [b[r * n:(r + 1) * n] for r, b in enumerate(bufs)])
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(bufs[r][r * n:(r + 1) * n], dt), ref[r], f"RS in place r={r}")
+    # all-gather in place: send[r] = recv[r] + r*n
+    x = [W.random_bits(63, r, n, ES[dt]).view(np.uint16 if dt == hc.BF16 else np.int32)
+         for r in range(R)]
+    if dt == hc.FP32:
+        x = [a.view(np.float32) for a in x]
+    ref = oracle.allgather_new(x, dt)
+    recv = [torch.zeros(R * n, dtype=TORCH[dt], device="cuda") for _ in range(R)]
+    for r in range(R):
+        recv[r][r * n:(r + 1) * n] = to_dev(x[r], dt)
+    for path in PATHS:
+        hc.set_config(copy_path=path)
+        hc.allgather([recv[r][r * n:(r + 1) * n] for r in range(R)], recv)
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(recv[r], dt), ref[r], f"AG in place {path} r={r}")
+
+
+def test_special_values_in_reductions():
+    # subnormal sums (no flush to zero), signed zeros, infinities
+    R, n = 4, 4096
+    rng = np.random.default_rng(5)
+    k = [rng.integers(0, 1 << 18, n) for _ in range(R)]
+    x = [(kr * 2.0 ** -149).astype(np.float32) for kr in k]
+    x[1][:8] = -0.0
+    x[0][:8] = -0.0
+    x[2][:8] = -0.0
+    x[3][:8] = -0.0
+    x[0][8] = np.inf
+    x[2][9] = -np.inf
+    for algo in ["ring", "direct"]:
+        hc.set_config(reduce_algo=algo)
+        ref = oracle.allreduce_new(x, hc.FP32)
+        got = run_ar(x, hc.FP32)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"special {algo} r={r}")
+    xb = [(kr % 32).astype(np.uint16) for kr in k]       # bf16 subnormals
+    ref = oracle.allreduce_new(xb, hc.BF16)
+    got = run_ar(xb, hc.BF16)
+    assert_bitwise(got[0], ref[0], "bf16 subnormal")
+
+
+# ---------------------------------------------------------------- copies
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("direct", [0, 1])
+@pytest.mark.parametrize("R", [1, 2, 3, 8])
+def test_allgather(path, direct, R):
+    hc.set_config(copy_path=path, allgather_direct=direct)
+    for dt in [hc.FP32, hc.BF16]:
+        for n in [1, 13, 100_003]:
+            x = [W.random_bits(71 + n, r, n, ES[dt]) for r in range(R)]
+            x = [a.view(np.float32) if dt == hc.FP32 else a for a in x]
+            ref = oracle.allgather_new(x, dt)
+            outs = [padded(R * n, dt, 2) for _ in range(R)]
+            hc.allgather([to_dev(a, dt) for a in x], [o[1] for o in outs])
+            torch.cuda.synchronize()
+            for r in range(R):
+                check_canaries(outs[r][0], 2, R * n, dt)
+                assert_bitwise(from_dev(outs[r][1], dt), ref[r], f"AG {path} n={n} r={r}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("chunk", [0, 65536])
+def test_sendrecv_and_alltoall(path, chunk):
+    hc.set_config(copy_path=path, chunk_bytes=chunk)
+    R = 8
+    for n in [5, 300_001]:
+        x = [W.random_bits(81, r, n, 2) for r in range(R)]
+        for peers in ([r + 1 if r + 1 < R else -1 for r in range(R)],
+                      [r - 1 for r in range(R)],
+                      [(r + 3) % R for r in range(R)],
+                      [r for r in range(R)]):
+            ref = [np.full(n, 0x7A5A, np.uint16) for _ in range(R)]
+            oracle.sendrecv(x, ref, peers, n, hc.BF16)
+            outs = [padded(n, hc.BF16, 0, 0) for _ in range(R)]
+            recv = [o[1] for o in outs]
+            hc.sendrecv([to_dev(a, hc.BF16) for a in x], recv, peers)
+            torch.cuda.synchronize()
+            for r in range(R):
+                assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"P2P {peers} r={r}")
+        xs = [W.random_bits(82, r, R * n, 4).view(np.float32) for r in range(R)]
+        ref = [np.zeros_like(a) for a in xs]
+        oracle.alltoall(xs, ref, n, hc.FP32)
+        got = hc.alltoall([to_dev(a, hc.FP32) for a in xs])
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(got[r], hc.FP32), ref[r], f"A2A n={n} r={r}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_alltoallv_routing(path):
+    hc.set_config(copy_path=path)
+    R = 8
+    send, counts, sd, rd, rsz = W.a2a_tokens(R=R, tokens=512, hidden=256)
+    ref = [np.zeros(s, np.uint16) for s in rsz]
+    oracle.alltoallv(send, counts, sd, ref, rd, hc.BF16)
+    recv = [torch.zeros(s, dtype=torch.bfloat16, device="cuda") for s in rsz]
+    hc.alltoallv([to_dev(a, hc.BF16) for a in send], counts, sd, recv, rd)
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"A2Av r={r}")
+
+
+def test_sdma_paths_dispatch_no_kernel():
+    """Copy-only collectives on an SDMA path report zero CUs."""
+    R, n = 8, 1 << 16
+    x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    for path in ["sdma", "engines"]:
+        hc.set_config(copy_path=path)
+        hc.allgather(x)
+        s = hc.last_stats()
+        assert s["cus_used_max"] == 0 and s["reduce_launches"] == 0
+        assert s["copy_kernel_launches"] == 0 and s["copy_ops"] > 0
+    torch.cuda.synchronize()
+
+
+def test_kernel_timing_reports_each_launch():
+    hc.set_config(kernel_timing=1)
+    R, n = 8, 1 << 18
+    x = [torch.randn(R * n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    hc.reduce_scatter(x)
+    t = hc.kernel_times()
+    assert len(t) == R - 1 and all(v > 0 for v in t)
+
+
+# ---------------------------------------------------------------- stream order
+
+@pytest.mark.parametrize("path", PATHS)
+def test_stream_order_with_delayed_producer(path):
+    """The inputs are written by a kernel queued behind a long spin on the
+    same stream; the collective must not start before them, and a consumer
+    queued after it must see its results."""
+    hc.set_config(copy_path=path)
+    R, n = 4, 1 << 20
+    x = [W.random_values("fp32", 91, r, n) for r in range(R)]
+    ref = oracle.allreduce_new(x, hc.FP32)
+    host = [torch.from_numpy(a).pin_memory() for a in x]
+    send = [torch.full((n,), float("nan"), device="cuda") for _ in range(R)]
+    recv = [torch.zeros(n, device="cuda") for _ in range(R)]
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        torch.cuda._sleep(50_000_000)                 # ~20 ms spin
+        for r in range(R):
+            send[r].copy_(host[r], non_blocking=True)
+        hc.allreduce(send, recv, stream=s)
+        out = [t.clone() for t in recv]
+    s.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(out[r], hc.FP32), ref[r], f"{path} r={r}")
+    # all-gather too (pure copies)
+    shards = [torch.full((n,), float("nan"), device="cuda") for _ in range(R)]
+    with torch.cuda.stream(s):
+        torch.cuda._sleep(50_000_000)
+        for r in range(R):
+            shards[r].copy_(host[r], non_blocking=True)
+        ag = hc.allgather(shards, stream=s)
+        ag = [t.clone() for t in ag]
+    s.synchronize()
+    cat = np.concatenate(x)
+    for r in range(R):
+        assert_bitwise(from_dev(ag[r], hc.FP32), cat, f"AG {path} r={r}")
+
+
+def test_back_to_back_calls_on_two_streams_share_workspace_safely():
+    R, n = 8, 1 << 18
+    xa = [W.random_values("bf16", 95, r, R * n) for r in range(R)]
+    xb = [W.random_values("bf16", 96, r, R * n) for r in range(R)]
+    ra = oracle.reduce_scatter_new(xa, hc.BF16)
+    rb = oracle.reduce_scatter_new(xb, hc.BF16)
+    da = [to_dev(a, hc.BF16) for a in xa]
+    db = [to_dev(a, hc.BF16) for a in xb]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            torch.cuda._sleep(5_000_000)
+            oa = hc.reduce_scatter(da, stream=s1)
+        with torch.cuda.stream(s2):
+            ob = hc.reduce_scatter(db, stream=s2)
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(oa[r], hc.BF16), ra[r], f"s1 r={r}")
+            assert_bitwise(from_dev(ob[r], hc.BF16), rb[r], f"s2 r={r}")

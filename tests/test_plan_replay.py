@@ -1,0 +1,201 @@
+"""Plan replay on the CPU: the planner's schedule, executed step by step with
+numpy, must equal the oracle bit for bit.
+
+This checks step order, phases, chunk offsets, workspace placement, copy
+chains and chunking without a GPU.  The replayer is scaffolding for the HIP
+path's schedules and shares nothing with the oracle: it does plain numpy
+float32 / uint32 adds and torch's fp32 -> bf16 rounding.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34334_amd as hc
+import workloads as W
+
+NP = {hc.INT32: np.int32, hc.FP32: np.float32, hc.BF16: np.uint16}
+ES = {hc.INT32: 4, hc.FP32: 4, hc.BF16: 2}
+NAME = {hc.INT32: "int32", hc.FP32: "fp32", hc.BF16: "bf16"}
+
+
+def widen(raw, dt, is_acc):
+    if dt == hc.INT32:
+        return raw.view(np.uint32)
+    if dt == hc.FP32 or is_acc:
+        return raw.view(np.float32)
+    return (raw.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def narrow(vals, dt, is_acc):
+    if dt == hc.INT32:
+        return vals.astype(np.uint32).view(np.uint8)
+    if dt == hc.FP32 or is_acc:
+        return vals.astype(np.float32).view(np.uint8)
+    t = torch.from_numpy(np.ascontiguousarray(vals, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint8)
+
+
+def replay(plan, send, recv):
+    dt = plan["dtype"]
+    es = ES[dt]
+    ws = np.zeros(plan["ws_bytes"], np.uint8)
+    bufs = {"send": send, "recv": recv, "ws": [ws]}
+
+    def region(ref, nbytes):
+        kind, rank, off = ref
+        arr = bufs[kind][0 if kind == "ws" else rank]
+        assert off + nbytes <= arr.size, (ref, nbytes, arr.size)
+        return arr[off:off + nbytes]
+
+    for st in plan["reduce_steps"]:
+        ph = st["phase"]
+        in0_acc = ph in ("middle", "last")
+        out_acc = ph in ("first", "middle")
+        for g in st["segs"]:
+            n = g["n"]
+            a = widen(region(g["in0"], n * (4 if in0_acc else es)).copy(), dt, in0_acc)
+            b = widen(region(g["in1"], n * es).copy(), dt, False)
+            if dt == hc.INT32:
+                r = (a.astype(np.uint64) + b.astype(np.uint64)) & 0xFFFFFFFF
+            else:
+                r = a + b
+            region(g["out"], n * (4 if out_acc else es))[:] = narrow(r, dt, out_acc)
+    f = plan["fold"]
+    if f is not None:
+        R = plan["R"]
+        c, total = f["c"], f["total"]
+        for j in range(R):
+            e0 = j * c
+            if e0 >= total:
+                continue
+            n = min(c, total - e0)
+            acc = None
+            for k in range(1, R + 1):
+                x = widen(send[(j + k) % R][e0 * es:(e0 + n) * es].copy(), dt, False)
+                if acc is None:
+                    acc = x.astype(np.uint64) if dt == hc.INT32 else x
+                elif dt == hc.INT32:
+                    acc = (acc + x.astype(np.uint64)) & 0xFFFFFFFF
+                else:
+                    acc = acc + x
+            y = narrow(acc, dt, False)
+            oe = 0 if f["out_at_chunk"] else e0
+            outs = range(R) if f["write_all"] else [j]
+            for r in outs:
+                recv[r][oe * es:(oe + n) * es] = y
+    for cp in plan["copies"]:
+        region(cp["dst"], cp["bytes"])[:] = region(cp["src"], cp["bytes"]).copy()
+
+
+def as_bytes(arrays):
+    return [np.ascontiguousarray(a).view(np.uint8).copy() for a in arrays]
+
+
+CONFIGS = [
+    dict(),
+    dict(allreduce_chunk_groups=3),
+    dict(chunk_bytes=4096),
+    dict(allgather_direct=1, chunk_bytes=4096, allreduce_chunk_groups=2),
+    dict(reduce_algo="direct"),
+]
+
+
+@pytest.fixture(params=range(len(CONFIGS)), ids=lambda i: "cfg%d" % i)
+def cfg(request):
+    with hc.config(**CONFIGS[request.param]):
+        yield CONFIGS[request.param]
+
+
+@pytest.mark.parametrize("dt", [hc.INT32, hc.FP32, hc.BF16], ids=lambda d: NAME[d])
+@pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 8])
+def test_reduction_plans_replay_to_oracle(cfg, dt, R):
+    for n in [1, 7, R * 5 + 3, 64, 3001]:
+        seed = 500 + R * 7 + n
+        # all-reduce of n elements
+        x = [W.random_values(NAME[dt], seed, r, n) for r in range(R)]
+        ref = oracle.allreduce_new(x, dt)
+        recv = [np.zeros(n * ES[dt], np.uint8) for _ in range(R)]
+        replay(hc.plan_json(hc.OP_ALLREDUCE, n, dt, R), as_bytes(x), recv)
+        for r in range(R):
+            assert np.array_equal(recv[r], as_bytes([ref[r]])[0]), ("allreduce", n, r)
+        # reduce-scatter with recvcount n
+        x = [W.random_values(NAME[dt], seed + 1, r, R * n) for r in range(R)]
+        ref = oracle.reduce_scatter_new(x, dt)
+        recv = [np.zeros(n * ES[dt], np.uint8) for _ in range(R)]
+        replay(hc.plan_json(hc.OP_REDUCE_SCATTER, n, dt, R), as_bytes(x), recv)
+        for r in range(R):
+            assert np.array_equal(recv[r], as_bytes([ref[r]])[0]), ("reduce_scatter", n, r)
+
+
+@pytest.mark.parametrize("R", [1, 2, 3, 8])
+def test_copy_plans_replay_to_oracle(cfg, R):
+    for dt in [hc.FP32, hc.BF16]:
+        for n in [1, 5, 3001]:
+            x = [W.random_bits(600 + n, r, n, ES[dt]) for r in range(R)]
+            # all-gather
+            ref = oracle.allgather_new(x, dt)
+            recv = [np.zeros(R * n * ES[dt], np.uint8) for _ in range(R)]
+            replay(hc.plan_json(hc.OP_ALLGATHER, n, dt, R), as_bytes(x), recv)
+            for r in range(R):
+                assert np.array_equal(recv[r], as_bytes([ref[r]])[0])
+            # all-to-all with blocks of n
+            xs = [W.random_bits(700 + n, r, R * n, ES[dt]) for r in range(R)]
+            ref = [np.zeros_like(a) for a in xs]
+            oracle.alltoall(xs, ref, n, dt)
+            recv = [np.zeros(R * n * ES[dt], np.uint8) for _ in range(R)]
+            replay(hc.plan_json(hc.OP_ALLTOALL, n, dt, R), as_bytes(xs), recv)
+            for r in range(R):
+                assert np.array_equal(recv[r], as_bytes([ref[r]])[0])
+            # send/recv pipeline r -> r+1
+            peers = [r + 1 if r + 1 < R else -1 for r in range(R)]
+            ref = [np.zeros_like(a) for a in x]
+            oracle.sendrecv(x, ref, peers, n, dt)
+            recv = [np.zeros(n * ES[dt], np.uint8) for _ in range(R)]
+            replay(hc.plan_json(hc.OP_SENDRECV, n, dt, R), as_bytes(x), recv)
+            for r in range(R):
+                assert np.array_equal(recv[r], as_bytes([ref[r]])[0])
+
+
+@pytest.mark.parametrize("op", [hc.OP_ALLGATHER, hc.OP_ALLTOALL, hc.OP_SENDRECV, hc.OP_ALLREDUCE])
+def test_copies_cover_each_destination_byte_once(cfg, op):
+    """Completeness (every flow of the traffic matrix is realised) and no
+    destination byte is written twice."""
+    R, n, dt = 8, 3001, hc.BF16
+    plan = hc.plan_json(op, n, dt, R)
+    written = {}
+    for cp in plan["copies"]:
+        kind, rank, off = cp["dst"]
+        assert kind == "recv"
+        cov = written.setdefault(rank, np.zeros(R * n * 2 + 1, np.int32))
+        cov[off:off + cp["bytes"]] += 1
+    for rank, cov in written.items():
+        assert cov.max() <= 1, rank
+    total = sum(int(c.sum()) for c in written.values())
+    expect = {hc.OP_ALLGATHER: R * R * n * 2, hc.OP_ALLTOALL: R * R * n * 2,
+              hc.OP_SENDRECV: (R - 1) * n * 2}
+    if op == hc.OP_ALLREDUCE:
+        # the ring's gather phase writes every rank's copy of every chunk but
+        # the owner's; the direct fold writes all outputs itself
+        assert total == (0 if plan["fold"] else (R - 1) * n * 2)
+    else:
+        assert total == expect[op]
+
+
+def test_chains_are_ordered_by_level():
+    with hc.config(chunk_bytes=4096):
+        plan = hc.plan_json(hc.OP_ALLGATHER, 5000, hc.BF16, 8)
+    last = {}
+    for cp in plan["copies"]:
+        ch = cp["chain"]
+        assert cp["level"] >= last.get(ch, -1)
+        last[ch] = cp["level"]
+
+
+def test_algorithmic_bytes():
+    # reduce-scatter of bf16 with fp32 partials: 8 + 10*(R-3) + 8 bytes per
+    # element of each of the R chunks, i.e. 66 n bytes at R = 8
+    n = 3_145_728
+    plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, 8)
+    assert plan["hbm_bytes"] == 8 * n * (8 + 5 * 10 + 8)
+    assert plan["ws_bytes"] == 8 * n * 4
