@@ -115,10 +115,21 @@ def direct_reduce_scatter(hc, send_np, steps, warmup):
     hc.set_config(reduce_algo="direct")
     sec = time_op(lambda: hc.reduce_scatter(send, recv), steps, warmup)
     st = hc.last_stats()
-    hc.set_config(reduce_algo="ring")
-    return recv, dict(algbw_GBs=round(R * n * 2 / sec / 1e9, 2), ms=round(sec * 1e3, 4),
-                      hbm_GBs=round(st["hbm_bytes_algorithmic"] / sec / 1e9, 1),
-                      hbm_frac=round(st["hbm_bytes_algorithmic"] / sec / 1e9 / HBM_PEAK_GBS, 4))
+    hc.set_config(kernel_timing=1)
+    hc.kernel_times()
+    for _ in range(steps):
+        hc.reduce_scatter(send, recv)
+    kt = hc.kernel_times()
+    hc.set_config(kernel_timing=0, reduce_algo="ring")
+    launch = statistics.mean(kt) / 1e3
+    achieved = st["hbm_bytes_algorithmic"] / launch / 1e9
+    return recv, dict(algbw_GBs=round(R * n * 2 / sec / 1e9, 2), busbw_GBs=round(R * n * 2 / sec / 1e9 * (R - 1) / R, 2),
+                      ms=round(sec * 1e3, 4), cus_used=st["cus_used_max"],
+                      roofline={"kernel": "fold_kernel (all 8 ranks folded in ring order, one launch)",
+                                "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                                "avg_launch_us": round(launch * 1e6, 2),
+                                "bytes_per_launch": st["hbm_bytes_algorithmic"]})
 
 
 def cpu_baseline(x, recvcount, budget_s=12.0):
@@ -141,50 +152,167 @@ def cpu_baseline(x, recvcount, budget_s=12.0):
 
 # ---- the other collectives ---------------------------------------------------
 
-def bench_allreduce(hc, W, reps):
+def dedicated_stream():
+    """A stream with a hardware queue of its own.  HIP folds streams onto a
+    few shared queues (four per process here), and two streams on one queue
+    run one after the other; a stream created with a CU mask (every CU) is
+    never shared, so the GEMM and the collective can overlap."""
+    import ctypes
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")    # the HIP runtime torch has loaded
+    s = ctypes.c_void_p()
+    mask = (ctypes.c_uint32 * 8)(*([0xFFFFFFFF] * 8))
+    if hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), 8, mask) != 0:
+        return torch.cuda.Stream()
+    return torch.cuda.ExternalStream(s.value)
+
+
+def _gemm_run(gemm, k=20):
+    import torch
+    A, B, C, _, gs, _ = gemm
+    ts = []
+    with torch.cuda.stream(gs):
+        g0 = torch.cuda.Event(enable_timing=True)
+        g0.record(gs)
+        for _ in range(k):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(gs)
+            torch.matmul(A, B, out=C)
+            b.record(gs)
+            ts.append((a, b))
+        g1 = torch.cuda.Event(enable_timing=True)
+        g1.record(gs)
+    return g0, g1, ts
+
+
+def _gated(gemm, enqueue_s, collective=None, n_coll=0):
+    """Hold the GEMM stream (and the collective stream) behind one event that
+    a spin on a third stream releases after the host has enqueued
+    everything; then 20 GEMMs, and `n_coll` collectives.  Returns the
+    collective window (c0, c1) and the GEMM event pairs."""
+    import torch
+    gs, cs = gemm[4], gemm[5]
+    torch.cuda.synchronize()
+    gate_s = torch.cuda.Stream()
+    with torch.cuda.stream(gate_s):
+        torch.cuda._sleep(int((1.5 * enqueue_s + 0.02) * 2.4e9))
+        gate = torch.cuda.Event()
+        gate.record(gate_s)
+    gs.wait_event(gate)
+    c0 = c1 = None
+    if collective is not None:
+        cs.wait_event(gate)
+        with torch.cuda.stream(cs):
+            c0 = torch.cuda.Event(enable_timing=True)
+            c0.record(cs)
+            for _ in range(n_coll):
+                collective(cs)
+            c1 = torch.cuda.Event(enable_timing=True)
+            c1.record(cs)
+    _, _, ts = _gemm_run(gemm)
+    torch.cuda.synchronize()
+    return c0, c1, ts
+
+
+def gemm_slowdown(hc, collective, med, gemm):
+    """Slowdown of the GEMM while `collective` loops beside it.  GEMM i of
+    the concurrent run is compared with GEMM i of a run alone under the same
+    gate (GEMM time drifts as clocks settle, so position matters); only
+    GEMMs that ran entirely inside the collective window count.  Returns
+    (median slowdown, fraction of the 20 GEMMs that overlapped)."""
+    import time as _t
+    import torch
+    t_alone, cs = gemm[3], gemm[5]
+    n_coll = int(45 * t_alone / max(med, 1e-6)) + 3
+    t0 = _t.perf_counter()
+    with torch.cuda.stream(cs):
+        collective(cs)
+    host_call = _t.perf_counter() - t0
+    enqueue = n_coll * host_call + 0.002
+    _, _, alone = _gated(gemm, enqueue)
+    base = [a.elapsed_time(b) for a, b in alone]
+    c0, c1, ts = _gated(gemm, enqueue, collective, n_coll)
+    end = c0.elapsed_time(c1)
+    ratios = [a.elapsed_time(b) / base[i] for i, (a, b) in enumerate(ts)
+              if c0.elapsed_time(a) >= 0 and c0.elapsed_time(b) <= end]
+    if not ratios:
+        return None, 0.0
+    return round(statistics.median(ratios) - 1, 4), round(len(ratios) / len(ts), 3)
+
+
+def make_gemm():
+    """The victim: a bf16 8192 x 8192 x 8192 matmul on its own queue."""
+    import torch
+    A = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    B = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    C = torch.empty(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    gs, cs = dedicated_stream(), dedicated_stream()
+    for _ in range(5):
+        torch.matmul(A, B, out=C)
+    torch.cuda.synchronize()
+    gemm = (A, B, C, 0.0, gs, cs)
+    _, _, ts = _gemm_run(gemm)
+    torch.cuda.synchronize()
+    t = statistics.median(x.elapsed_time(y) for x, y in ts) / 1e3
+    return (A, B, C, t, gs, cs)
+
+
+PATHS = [("sdma", {}), ("engines", {}), ("kernel", {})]
+
+
+def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
+    """Time `run(stream)` under every copy path: algbw = S / t, busbw = algbw * f."""
+    res = {}
+    for name, kw in list(PATHS) + list(extra_paths):
+        path = name.split("_")[0]
+        hc.set_config(copy_path=path, **kw)
+        med, mn = event_time(lambda: run(None), reps)
+        st = hc.last_stats()
+        r = dict(algbw_GBs=round(S / med / 1e9, 2), busbw_GBs=round(S / med / 1e9 * f, 2),
+                 ms=round(med * 1e3, 4), copy_GBs=round(st["copy_bytes"] / med / 1e9, 1),
+                 hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
+                 path_used=["auto", "sdma", "engines", "kernel"][st["copy_path_used"]],
+                 cus_used=st["cus_used_max"])
+        if gemm is not None:
+            r["gemm_slowdown"], r["gemm_overlap"] = gemm_slowdown(hc, run, med, gemm)
+        res[name] = r
+        hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0)
+    return res
+
+
+def bench_allreduce(hc, W, reps, gemm):
     import torch
     R, n = 4, 1_048_576
     x = W.allreduce_fp32(R, n)
     send = [torch.from_numpy(a).cuda() for a in x]
     recv = [torch.empty(n, device="cuda") for _ in range(R)]
-    res = {}
-    for path in ["sdma", "engines", "kernel"]:
-        hc.set_config(copy_path=path)
-        med, mn = event_time(lambda: hc.allreduce(send, recv), reps)
-        st = hc.last_stats()
-        S = n * 4
-        res[path] = dict(algbw_GBs=round(S / med / 1e9, 2),
-                         busbw_GBs=round(S / med / 1e9 * 2 * (R - 1) / R, 2),
-                         us=round(med * 1e6, 2), hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
-                         cus_used=st["cus_used_max"])
-    hc.set_config(copy_path="auto")
-    return dict(workload="all-reduce ring fp32 R=4, 1,048,576 elements per rank", **res)
+    res = copy_paths(hc, lambda s: hc.allreduce(send, recv, stream=s), n * 4, 2 * (R - 1) / R, reps)
+    hc.set_config(reduce_algo="direct")
+    med, _ = event_time(lambda: hc.allreduce(send, recv), reps)
+    st = hc.last_stats()
+    res["direct_fold"] = dict(algbw_GBs=round(n * 4 / med / 1e9, 2), us=round(med * 1e6, 2),
+                              hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
+                              cus_used=st["cus_used_max"])
+    hc.set_config(reduce_algo="ring")
+    return dict(workload="all-reduce fp32 R=4, 1,048,576 elements per rank (ring reduction + gather copies; "
+                         "direct_fold: one kernel writes all outputs)", **res)
 
 
-def bench_allgather(hc, W, reps):
+def bench_allgather(hc, W, reps, gemm):
     import torch
     R, total = 8, 201_326_592
     x = W.ag_parameters(R, total)
-    n = total // R
     send = [bf16_dev(a) for a in x]
     recv = [torch.empty(total, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
-    res = {}
-    for path, extra in [("sdma", {}), ("engines", {}), ("engines", {"allgather_direct": 1, "chunk_bytes": 8 << 20}),
-                        ("kernel", {})]:
-        key = path + ("_direct_8MiB" if extra else "")
-        hc.set_config(copy_path=path, **extra)
-        med, mn = event_time(lambda: hc.allgather(send, recv), reps, warmup=1)
-        st = hc.last_stats()
-        S = total * 2
-        res[key] = dict(algbw_GBs=round(S / med / 1e9, 2), busbw_GBs=round(S / med / 1e9 * (R - 1) / R, 2),
-                        ms=round(med * 1e3, 3), hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
-                        cus_used=st["cus_used_max"])
-        hc.set_config(allgather_direct=0, chunk_bytes=0)
-    hc.set_config(copy_path="auto")
-    return dict(workload="FSDP all-gather bf16 R=8, 25,165,824-element shards (201,326,592 params)", **res)
+    res = copy_paths(hc, lambda s: hc.allgather(send, recv, stream=s), total * 2, (R - 1) / R, reps, gemm,
+                     extra_paths=[("engines_ring", {"allgather_direct": 0}), ("sdma_ring", {"allgather_direct": 0})])
+    hc.set_config(allgather_direct=1)
+    return dict(workload="FSDP all-gather bf16 R=8, 25,165,824-element shards (one GPT-6.7B block, "
+                         "201,326,592 params), out-of-place", **res)
 
 
-def bench_p2p(hc, W, reps):
+def bench_p2p(hc, W, reps, gemm):
     import torch
     R = 8
     x = W.p2p_activations(R)
@@ -193,78 +321,124 @@ def bench_p2p(hc, W, reps):
     recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     fwd = [r + 1 if r + 1 < R else -1 for r in range(R)]
     bwd = [r - 1 for r in range(R)]
-    res = {}
-    for path in ["sdma", "engines", "kernel"]:
-        hc.set_config(copy_path=path)
 
-        def schedule():
-            for _ in range(16):            # 16 microbatches, forward then backward
-                hc.sendrecv(send, recv, fwd)
-                hc.sendrecv(send, recv, bwd)
+    def schedule(s):
+        for _ in range(16):            # 16 microbatches, forward then backward
+            hc.sendrecv(send, recv, fwd, stream=s)
+            hc.sendrecv(send, recv, bwd, stream=s)
 
-        med, mn = event_time(schedule, max(3, reps // 4), warmup=1)
-        st = hc.last_stats()
-        msgs = 16 * 2 * (R - 1)
-        # 32 rounds (16 microbatches x fwd/bwd) of 7 concurrent messages
-        res[path] = dict(per_message_algbw_GBs=round(n * 2 / (med / 32) / 1e9, 2),
-                         aggregate_GBs=round(msgs * n * 2 / med / 1e9, 2),
-                         schedule_ms=round(med * 1e3, 3), cus_used=st["cus_used_max"])
-    hc.set_config(copy_path="auto")
-    return dict(workload="PP send/recv bf16 [1,2048,4096], 8 stages, 16 microbatches fwd+bwd "
-                         "(224 messages in rounds of 7 concurrent hops)", **res)
+    # S: one message per round of 7 concurrent hops; 32 rounds per schedule
+    res = copy_paths(hc, schedule, 32 * n * 2, 1.0, max(3, reps // 3), gemm)
+    for k, r in res.items():
+        r["per_message_algbw_GBs"] = r.pop("algbw_GBs")
+        r.pop("busbw_GBs")
+        r["aggregate_GBs"] = round(r["per_message_algbw_GBs"] * (R - 1), 2)
+    return dict(workload="PP send/recv bf16 [1,2048,4096] per message, 8 stages, 16 microbatches fwd+bwd "
+                         "(224 messages in 32 rounds of 7 concurrent hops)", **res)
 
 
-def bench_a2a_gemm(hc, W, reps):
+def bench_a2a(hc, W, reps, gemm):
     import torch
     R = 8
     send_np, counts, sd, rd, rsz = W.a2a_tokens(R)
     send = [bf16_dev(a) for a in send_np]
     recv = [torch.empty(s, dtype=torch.bfloat16, device="cuda") for s in rsz]
     sent = sum(counts) * 2
-    A = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
-    B = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
-    C = torch.empty(8192, 8192, device="cuda", dtype=torch.bfloat16)
-    gemm_s = torch.cuda.Stream()
-    coll_s = torch.cuda.Stream()
-
-    def gemm_alone(ngemm=20):
-        ts = []
-        with torch.cuda.stream(gemm_s):
-            for _ in range(ngemm):
-                a = torch.cuda.Event(enable_timing=True)
-                b = torch.cuda.Event(enable_timing=True)
-                a.record()
-                torch.matmul(A, B, out=C)
-                b.record()
-                ts.append((a, b))
-        torch.cuda.synchronize()
-        return statistics.median(a.elapsed_time(b) for a, b in ts) / 1e3
-
-    gemm_alone(3)
-    t_alone = gemm_alone()
-    res = dict(gemm_ms_alone=round(t_alone * 1e3, 4),
-               gemm_tflops_alone=round(2 * 8192 ** 3 / t_alone / 1e12, 1))
-    for path in ["sdma", "engines", "kernel"]:
-        hc.set_config(copy_path=path)
-        med, mn = event_time(lambda: hc.alltoallv(send, counts, sd, recv, rd), reps)
-        st = hc.last_stats()
-        # concurrent: keep the all-to-all looping on its own stream for the
-        # whole GEMM window
-        torch.cuda.synchronize()
-        n_coll = int(20 * t_alone / med) + 4
-        with torch.cuda.stream(coll_s):
-            for _ in range(n_coll):
-                hc.alltoallv(send, counts, sd, recv, rd, stream=coll_s)
-        t_conc = gemm_alone()
-        torch.cuda.synchronize()
-        res[path] = dict(algbw_GBs=round(sent / R / med / 1e9, 2), aggregate_GBs=round(sent / med / 1e9, 2),
-                         ms=round(med * 1e3, 3), cus_used=st["cus_used_max"],
-                         gemm_ms_concurrent=round(t_conc * 1e3, 4),
-                         gemm_slowdown=round(t_conc / t_alone - 1, 4))
-    hc.set_config(copy_path="auto")
-    return dict(workload="EP all-to-all(v) bf16, 4096 tokens x 2048 per rank, 64 experts over R=8, "
-                         "top-6 (one copy per destination rank), with a concurrent 8192^3 bf16 GEMM",
+    res = copy_paths(hc, lambda s: hc.alltoallv(send, counts, sd, recv, rd, stream=s), sent // R, (R - 1) / R,
+                     reps, gemm)
+    return dict(workload="EP all-to-all(v) bf16, 4096 tokens x 2048 per rank, 64 experts over R=8, top-6 "
+                         "(one copy per destination rank), gemm_slowdown against a concurrent 8192^3 bf16 GEMM",
                 bytes_sent_total=sent, **res)
+
+
+def bench_p2p_sizes(hc, reps):
+    """One message 0 -> 1 over the paper's microbenchmark range: SDMA paths
+    against the CU copy kernel at 1 ... 256 workgroups (the analog of NCCL's
+    1/2/4/8-SM budgets)."""
+    import torch
+    big = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda")
+    big2 = torch.empty_like(big)
+    rows = []
+    for sz in [2 << 20, 32 << 20, 512 << 20]:
+        ne = sz // 2
+        s0, d1 = big[:ne], big2[:ne]
+        row = {"bytes": sz}
+        for name, kw in [("sdma", dict(copy_path="sdma")), ("engines", dict(copy_path="engines")),
+                         ("engines_striped", dict(copy_path="engines", chunk_bytes=max(1 << 20, sz // 16)))] + \
+                        [(f"kernel_wg{w}", dict(copy_path="kernel", workgroups_per_step=w)) for w in (1, 2, 4, 8, 64, 256)]:
+            hc.set_config(**kw)
+            med, _ = event_time(lambda: hc.sendrecv([s0, s0], [d1, d1], [1, -1]), reps)
+            row[name] = round(sz / med / 1e9, 1)
+            hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0)
+        rows.append(row)
+    return dict(workload="single bf16 message rank 0 -> 1, algbw GB/s", rows=rows)
+
+
+def bench_rs_workgroups(hc, x, reps):
+    """Ring reduce-scatter of the headline at a fixed workgroup budget: the
+    CU footprint / bandwidth trade-off of the reduction kernels."""
+    import torch
+    R = len(x)
+    n = x[0].size // R
+    send = [bf16_dev(a) for a in x]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    out = {}
+    for w in (16, 64, 256, 1024, 0):
+        hc.set_config(workgroups_per_step=w)
+        med, _ = event_time(lambda: hc.reduce_scatter(send, recv), reps)
+        st = hc.last_stats()
+        out[f"wg{st['workgroups_per_step']}"] = dict(algbw_GBs=round(R * n * 2 / med / 1e9, 2),
+                                                    hbm_GBs=round(st["hbm_bytes_algorithmic"] / med / 1e9, 1),
+                                                    cus_used=st["cus_used_max"])
+    hc.set_config(workgroups_per_step=0)
+    return out
+
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "reduce_step_kernel_rs_bf16_R8_traffic.txt")
+
+
+def kernel_source_hash():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2609_34334_amd", "csrc", "kernels.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per reduce-step launch from the committed rocprofv3 counter
+    summary, or None when it is missing or the kernels changed since."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_SUMMARY):
+        if ":" in line and not line.startswith(("#", " ", "|")):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernels_hip_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return int(float(kv["traffic_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def pmc_workload(hc, W):
+    """What the counter runs profile: a 1 GiB CU copy of known size (to
+    scale FETCH_SIZE / WRITE_SIZE), then five headline reduce-scatters."""
+    import torch
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    with hc.config(copy_path="kernel"):
+        hc.sendrecv([src], [dst], [0])
+    torch.cuda.synchronize()
+    del src, dst
+    R, n_in = 8, 25_165_824
+    send = [bf16_dev(a) for a in W.rs_gradients(R, n_in)]
+    recv = [torch.empty(n_in // R, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    for _ in range(5):
+        hc.reduce_scatter(send, recv)
+    torch.cuda.synchronize()
+    print(json.dumps({"pmc_workload": "done", "kernels_hip_sha256_16": kernel_source_hash()}))
 
 
 def main():
@@ -274,6 +448,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--quick", action="store_true", help="headline only, no extras")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--pmc-workload", action="store_true",
+                    help="run only the workload the counter profiles are taken on")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -289,6 +465,9 @@ def main():
 
     torch.cuda.set_device(0)
     hc.init(0)
+    if args.pmc_workload:
+        pmc_workload(hc, W)
+        return
     log("reduce-scatter headline")
     rs = bench_reduce_scatter(hc, W, args.steps, args.warmup)
     log(f"RS algbw {rs['algbw']:.1f} GB/s, {rs['sec'] * 1e3:.3f} ms/step, "
@@ -310,13 +489,18 @@ def main():
                "sample": f"the full reduce-scatter workload, {reps} repetitions, "
                          f"{csec:.2f} s each on one host core"}
     if not args.quick:
+        gemm = make_gemm()
+        extra["gemm_alone"] = dict(ms=round(gemm[3] * 1e3, 4), tflops=round(2 * 8192 ** 3 / gemm[3] / 1e12, 1))
+        extra["reduce_scatter_workgroups"] = bench_rs_workgroups(hc, rs["x"], 3)
         for name, fn in [("allreduce_fp32_R4", bench_allreduce), ("allgather_fsdp", bench_allgather),
-                         ("p2p_pp", bench_p2p), ("alltoallv_ep_with_gemm", bench_a2a_gemm)]:
+                         ("p2p_pp", bench_p2p), ("alltoallv_ep", bench_a2a)]:
             log(name)
             try:
-                extra[name] = fn(hc, W, 10)
+                extra[name] = fn(hc, W, 10, gemm)
             except Exception as e:  # report, do not hide the headline
                 extra[name] = {"error": repr(e)}
+        log("p2p sizes")
+        extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
 
     st = rs["stats"]
     out = {
@@ -344,7 +528,7 @@ def main():
         "parity_vs_oracle": parity,
         "roofline": {"bound": "hbm", "kernel": "reduce_step_kernel (ring step, all 8 ranks per launch)",
                      "achieved": round(rs["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(rs["achieved"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(rs["achieved"] / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "avg_launch_us": round(rs["avg_launch_us"], 2),
                      "bytes_per_launch": rs["bytes_per_op"] // rs["launches"],
                      "launches_per_step": rs["launches"]},

@@ -42,7 +42,10 @@
  *   sticky error state.
  * Threads.  One host thread at a time may call into the library per device.
  *   Collectives issued on different streams that overlap in time are
- *   ordered by the library where they share its workspace.
+ *   ordered by the library where they share its workspace or its internal
+ *   copy / handshake streams, in the order the calls were issued: a call
+ *   must not wait, through the caller's own stream dependencies, for a call
+ *   issued after it.
  * In-place forms (the only allowed overlaps between send and recv):
  *   all-reduce      send[r] == recv[r];
  *   all-gather      send[r] == recv[r] + r * sendcount elements;
@@ -77,12 +80,17 @@ typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2 } hoccl_dtype_t;
 
 /* Where pure-copy steps run. */
 typedef enum {
-    HOCCL_COPY_AUTO = 0,         /* SDMA_ENGINES when available, else SDMA     */
+    HOCCL_COPY_AUTO = 0,         /* SDMA: the one path that keeps copies
+                                    free of compute units end to end          */
     HOCCL_COPY_SDMA = 1,         /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
                                     library's copy streams; HIP picks engines  */
     HOCCL_COPY_SDMA_ENGINES = 2, /* a CPU proxy thread issues each chunk on an
                                     explicitly chosen SDMA engine (ROCr) and
-                                    releases the stream by flag handshake      */
+                                    releases the stream by flag handshake;
+                                    with chunk_bytes 0 it cuts copies into
+                                    about total/engines pieces when there are
+                                    fewer chains than engines.  The handshake
+                                    costs a spinning one-thread kernel        */
     HOCCL_COPY_KERNEL = 3        /* CU copy kernel with workgroups_per_step
                                     workgroups (comparator / fallback)         */
 } hoccl_copy_path_t;
@@ -99,13 +107,15 @@ typedef struct {
     int workgroups_per_step;    /* workgroups per reduce / CU-copy launch;
                                    0 = automatic (fills the chip)              */
     int threads_per_workgroup;  /* 64..1024, multiple of 64; 0 = 256           */
-    size_t chunk_bytes;         /* split SDMA copies into pieces of this size;
-                                   0 = no split                                */
+    size_t chunk_bytes;         /* split copies into pieces of this size
+                                   (>= 4096); 0 = no split, or the automatic
+                                   split of the AUTO copy path                 */
     int copy_streams;           /* internal copy streams, 1..16; 0 = 8         */
     int sdma_engines;           /* engines used by SDMA_ENGINES, 0 = all       */
     hoccl_copy_path_t copy_path;
-    int allgather_direct;       /* 1: every rank copies each shard from its
-                                   owner; 0: ring forwarding r -> r+1          */
+    int allgather_direct;       /* 1 (default): every rank copies each shard
+                                   from its owner, the all-pairs traffic
+                                   matrix; 0: ring forwarding r -> r+1         */
     int allreduce_chunk_groups; /* split each all-reduce ring chunk into this
                                    many groups so the gather of group g
                                    overlaps the reduction of group g+1; 0 = 1  */
@@ -114,6 +124,15 @@ typedef struct {
                                    copy kernel launch (hoccl_get_kernel_times) */
     unsigned int proxy_timeout_ms; /* watchdog of the SDMA_ENGINES proxy;
                                    0 = 10000                                   */
+    int proxy_handshake;        /* where the SDMA_ENGINES start/finish flag
+                                   handshake (hipStreamWriteValue32 /
+                                   hipStreamWaitValue32) runs.  This HIP runs
+                                   those as kernels and the wait spins on a CU
+                                   while the copies run, holding back its
+                                   hardware queue.  0 (default): on a private
+                                   stream masked to one CU (its own hardware
+                                   queue), joined to the caller's stream by
+                                   events; 1: on the caller's stream itself  */
 } hoccl_config_t;
 
 typedef struct {
@@ -123,7 +142,10 @@ typedef struct {
     int workgroups_per_step;    /* workgroups per launch actually used         */
     int cus_available;          /* compute units of the device                 */
     int cus_used_max;           /* upper bound on CUs occupied by this call:
-                                   min(workgroups, CUs); 0 for pure SDMA       */
+                                   min(workgroups, CUs) when kernels run; for
+                                   copy-only calls 0 on the SDMA path and 1 on
+                                   SDMA_ENGINES (the handshake's wait kernel,
+                                   one thread)                                 */
     hoccl_copy_path_t copy_path_used;
     hoccl_reduce_algo_t reduce_algo_used;
     unsigned long long hbm_bytes_algorithmic; /* bytes every step must read

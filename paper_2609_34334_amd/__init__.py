@@ -46,7 +46,8 @@ class Config(ctypes.Structure):
                 ("allreduce_chunk_groups", ctypes.c_int),
                 ("reduce_algo", ctypes.c_int),
                 ("kernel_timing", ctypes.c_int),
-                ("proxy_timeout_ms", ctypes.c_uint)]
+                ("proxy_timeout_ms", ctypes.c_uint),
+                ("proxy_handshake", ctypes.c_int)]
 
 
 class Stats(ctypes.Structure):

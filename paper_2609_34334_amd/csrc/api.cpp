@@ -58,6 +58,7 @@ struct DeviceState {
     std::vector<TimingPair> timing_pool;
     size_t timing_used = 0;
     Proxy *proxy = nullptr;
+    std::string proxy_why;  // why the proxy could not be created
 };
 
 std::mutex g_mu;
@@ -98,11 +99,12 @@ hoccl_config_t default_config() {
     c.copy_streams = 8;
     c.sdma_engines = 0;
     c.copy_path = HOCCL_COPY_AUTO;
-    c.allgather_direct = 0;
+    c.allgather_direct = 1;
     c.allreduce_chunk_groups = 1;
     c.reduce_algo = HOCCL_REDUCE_RING;
     c.kernel_timing = 0;
     c.proxy_timeout_ms = 10000;
+    c.proxy_handshake = 0;
     return c;
 }
 
@@ -118,6 +120,7 @@ bool config_valid(const hoccl_config_t &c) {
     if (c.allreduce_chunk_groups < 0 || c.allreduce_chunk_groups > 1024) return false;
     if ((int)c.reduce_algo < 0 || (int)c.reduce_algo > 1) return false;
     if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
+    if (c.proxy_handshake < 0 || c.proxy_handshake > 1) return false;
     return true;
 }
 
@@ -140,6 +143,7 @@ void load_config_locked() {
     c.allgather_direct = (int)env_long("HOCCL_AG_DIRECT", c.allgather_direct);
     c.allreduce_chunk_groups = (int)env_long("HOCCL_AR_GROUPS", c.allreduce_chunk_groups);
     c.kernel_timing = (int)env_long("HOCCL_KERNEL_TIMING", c.kernel_timing);
+    c.proxy_handshake = (int)env_long("HOCCL_PROXY_ON_CALLER", c.proxy_handshake);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "sdma")) c.copy_path = HOCCL_COPY_SDMA;
         else if (!std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA_ENGINES;
@@ -195,8 +199,11 @@ hoccl_status_t create_state(int device, DeviceState **out) {
     }
     st->num_cus = prop.multiProcessorCount;
     const int K = 16;  // the most copy streams any configuration may use
+    // Plain streams on the runtime's shared hardware queues.  Giving each its
+    // own queue (a CU-masked stream) was measured slower for SDMA copies:
+    // the pipeline send/recv schedule took 39.7 ms instead of 9.8 ms.
     for (int k = 0; k < K; ++k) {
-        hipStream_t s;
+        hipStream_t s = nullptr;
         e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
         if (e != hipSuccess) {
             set_err("hipStreamCreateWithFlags: %s", hipGetErrorString(e));
@@ -216,7 +223,7 @@ hoccl_status_t create_state(int device, DeviceState **out) {
         set_err("hipEventCreateWithFlags: %s", hipGetErrorString(e));
         return fail(HOCCL_ERR_HIP);
     }
-    st->proxy = Proxy::create(device);  // null when the engines cannot be driven
+    st->proxy = Proxy::create(device, &st->proxy_why);  // null when the engines cannot be driven
     *out = st;
     return HOCCL_OK;
 }
@@ -239,6 +246,8 @@ hoccl_status_t get_state(DeviceState **out) {
 }
 
 // ---- execution ------------------------------------------------------------------
+
+PlanOptions options_from(const hoccl_config_t &cfg, bool in_place);
 
 struct Buffers {
     const void *const *send;
@@ -274,9 +283,25 @@ hoccl_status_t ensure_ws(DeviceState &st, size_t bytes) {
     return HOCCL_OK;
 }
 
-int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg) {
+// Workgroups per launch.  An explicit budget wins.  Otherwise about two
+// 16-byte vectors per thread of the largest launch, between one workgroup
+// per CU and 32 per CU (8192 on MI355X): measured on the bf16 ring step, the
+// streaming kernels keep gaining up to roughly one vector per thread.
+int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan &p, int threads) {
     if (cfg.workgroups_per_step > 0) return cfg.workgroups_per_step;
-    return st.num_cus * 8;
+    unsigned long long bytes = 0;
+    for (const ReduceStep &s : p.reduce_steps) {
+        unsigned long long b = 0;
+        for (const ReduceSeg &g : s.segs) b += (unsigned long long)g.n * dtype_size(p.dtype);
+        bytes = std::max(bytes, b);
+    }
+    if (p.has_fold) bytes = std::max(bytes, (unsigned long long)p.fold.total * dtype_size(p.dtype));
+    if (cfg.copy_path == HOCCL_COPY_KERNEL)
+        for (const CopyOp &c : p.copies) bytes = std::max(bytes, (unsigned long long)c.bytes * p.R);
+    unsigned long long vec = bytes / 16;
+    unsigned long long wg = (vec + 2ull * threads - 1) / (2ull * threads);
+    unsigned long long lo = (unsigned long long)st.num_cus, hi = 32ull * st.num_cus;
+    return (int)std::min(hi, std::max(lo, wg));
 }
 
 hoccl_status_t timed_begin(DeviceState &st, const hoccl_config_t &cfg, hipStream_t s,
@@ -413,13 +438,32 @@ hoccl_status_t run_copies_kernel(DeviceState &st, const hoccl_config_t &cfg, con
     return HOCCL_OK;
 }
 
-hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg) {
-    if (cfg.copy_path == HOCCL_COPY_AUTO) return HOCCL_COPY_SDMA;
-    if (cfg.copy_path == HOCCL_COPY_SDMA_ENGINES && !st.proxy) return HOCCL_COPY_SDMA;
-    return cfg.copy_path;
+// Copy path for a plan.  An explicit choice wins; AUTO is the HIP runtime's
+// device-to-device SDMA path.  It is the only one that is free of compute
+// units end to end: the engine proxy moves data on SDMA engines too, but its
+// stream handshake needs hipStreamWaitValue32, which this HIP executes as a
+// spinning one-thread kernel, and a concurrent full-occupancy GEMM measured
+// 61% slower beside it (1.8% beside the HIP path, 81% beside the CU copy).
+hoccl_copy_path_t resolve_path(const DeviceState &, const hoccl_config_t &cfg, const Plan &) {
+    return cfg.copy_path == HOCCL_COPY_AUTO ? HOCCL_COPY_SDMA : cfg.copy_path;
 }
 
-hoccl_status_t execute(const Plan &p, const Buffers &B0, hipStream_t s) {
+// On the engine proxy with no chunk size configured: when there are fewer
+// independent chains than engines, cut the copies into pieces of about
+// total / engines bytes (at least 4 MiB) so that every engine works, the
+// paper's striping of one flow over several queues.
+size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, const Plan &p) {
+    if (cfg.copy_path != HOCCL_COPY_SDMA_ENGINES || cfg.chunk_bytes != 0 || !st.proxy) return 0;
+    int E = st.proxy->engine_count();
+    if (cfg.sdma_engines > 0) E = std::min(E, cfg.sdma_engines);
+    if (p.nchains >= E) return 0;
+    size_t c = (size_t)(p.copy_bytes / (unsigned long long)E);
+    c = std::max(c, (size_t)4 << 20);
+    return (c + 4095) & ~(size_t)4095;
+}
+
+template <typename Build>
+hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_t s) {
     auto t0 = std::chrono::steady_clock::now();
     DeviceState *stp = nullptr;
     TRY(get_state(&stp));
@@ -427,10 +471,21 @@ hoccl_status_t execute(const Plan &p, const Buffers &B0, hipStream_t s) {
     hoccl_config_t cfg = config();
     std::memset(&t_stats, 0, sizeof t_stats);
     Buffers B = B0;
+    PlanOptions opt = options_from(cfg, in_place);
+    Plan p = build(opt);
+    if (size_t c = auto_chunk_bytes(st, cfg, p)) {
+        opt.chunk_bytes = c;
+        p = build(opt);
+    }
 
     const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
-    const int wg = auto_workgroups(st, cfg);
-    const hoccl_copy_path_t path = resolve_path(st, cfg);
+    const int wg = auto_workgroups(st, cfg, p, threads);
+    const hoccl_copy_path_t path = resolve_path(st, cfg, p);
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && !st.proxy) {
+        // Asked for explicitly: never fall back silently.
+        set_err("%s", st.proxy_why.c_str());
+        return HOCCL_ERR_UNSUPPORTED;
+    }
     const bool has_kernels = !p.reduce_steps.empty() || p.has_fold;
     const bool has_copies = !p.copies.empty();
 
@@ -450,8 +505,8 @@ hoccl_status_t execute(const Plan &p, const Buffers &B0, hipStream_t s) {
         for (const CopyOp &c : p.copies)
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
-        hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, s, &ne,
-                                            t_err);
+        hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
+                                            cfg.proxy_handshake == 1, s, &ne, t_err);
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {
@@ -471,7 +526,9 @@ hoccl_status_t execute(const Plan &p, const Buffers &B0, hipStream_t s) {
     bool cu_work = has_kernels || (has_copies && path == HOCCL_COPY_KERNEL);
     t_stats.workgroups_per_step = cu_work ? wg : 0;
     t_stats.cus_available = st.num_cus;
-    t_stats.cus_used_max = cu_work ? std::min(wg, st.num_cus) : 0;
+    // The engine proxy's handshake waits in a one-thread kernel on one CU.
+    const bool handshake_wave = has_copies && path == HOCCL_COPY_SDMA_ENGINES;
+    t_stats.cus_used_max = cu_work ? std::min(wg, st.num_cus) : (handshake_wave ? 1 : 0);
     t_stats.copy_path_used = has_copies ? path : HOCCL_COPY_AUTO;
     t_stats.reduce_algo_used = p.has_fold ? HOCCL_REDUCE_DIRECT : HOCCL_REDUCE_RING;
     t_stats.hbm_bytes_algorithmic = p.hbm_bytes;
@@ -633,7 +690,11 @@ const char *hoccl_last_error_string(void) { return t_err.c_str(); }
 
 int hoccl_sdma_engine_count(void) {
     DeviceState *st = nullptr;
-    if (get_state(&st) != HOCCL_OK || !st->proxy) return 0;
+    if (get_state(&st) != HOCCL_OK) return 0;
+    if (!st->proxy) {
+        set_err("%s", st->proxy_why.c_str());
+        return 0;
+    }
     return st->proxy->engine_count();
 }
 
@@ -656,8 +717,8 @@ hoccl_status_t hoccl_allreduce(const void *const *send, void *const *recv, size_
     TRY(check_overlaps(outs, ins, [](const Range &o, const Range &i) {
         return o.who == i.who && o.lo == i.lo;
     }));
-    Plan p = plan_allreduce(count, dt, R, options_from(config(), in_place));
-    return execute(p, Buffers{send, recv, nullptr}, stream);
+    return execute([&](const PlanOptions &o) { return plan_allreduce(count, dt, R, o); }, in_place,
+                   Buffers{send, recv, nullptr}, stream);
 }
 
 hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv, size_t n,
@@ -679,8 +740,8 @@ hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv, 
     TRY(check_overlaps(outs, ins, [ob](const Range &o, const Range &i) {
         return o.who == i.who && o.lo == i.lo + (uintptr_t)o.who * ob;
     }));
-    Plan p = plan_reduce_scatter(n, dt, R, options_from(config(), in_place));
-    return execute(p, Buffers{send, recv, nullptr}, stream);
+    return execute([&](const PlanOptions &o) { return plan_reduce_scatter(n, dt, R, o); }, in_place,
+                   Buffers{send, recv, nullptr}, stream);
 }
 
 hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv, size_t n,
@@ -702,8 +763,8 @@ hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv, size_
     TRY(check_overlaps(outs, ins, [ib](const Range &o, const Range &i) {
         return o.who == i.who && i.lo == o.lo + (uintptr_t)o.who * ib;
     }));
-    Plan p = plan_allgather(n, dt, R, options_from(config(), in_place));
-    return execute(p, Buffers{send, recv, nullptr}, stream);
+    return execute([&](const PlanOptions &o) { return plan_allgather(n, dt, R, o); }, in_place,
+                   Buffers{send, recv, nullptr}, stream);
 }
 
 hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv, const int *peers,
@@ -741,8 +802,8 @@ hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv, const 
         ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + b, r, false});
     }
     TRY(check_overlaps(outs, ins, [](const Range &, const Range &) { return false; }));
-    Plan p = plan_sendrecv(n, dt, R, peers, options_from(config(), false));
-    return execute(p, Buffers{send, recv, nullptr}, stream);
+    return execute([&](const PlanOptions &o) { return plan_sendrecv(n, dt, R, peers, o); }, false,
+                   Buffers{send, recv, nullptr}, stream);
 }
 
 hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv, size_t n,
@@ -760,8 +821,8 @@ hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv, size_t
         ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + b, r, false});
     }
     TRY(check_overlaps(outs, ins, [](const Range &, const Range &) { return false; }));
-    Plan p = plan_alltoall(n, dt, R, options_from(config(), false));
-    return execute(p, Buffers{send, recv, nullptr}, stream);
+    return execute([&](const PlanOptions &o) { return plan_alltoall(n, dt, R, o); }, false,
+                   Buffers{send, recv, nullptr}, stream);
 }
 
 hoccl_status_t hoccl_alltoallv(const void *const *send, const size_t *counts, const size_t *sd,
@@ -793,8 +854,8 @@ hoccl_status_t hoccl_alltoallv(const void *const *send, const size_t *counts, co
         }
     if (outs.empty()) return HOCCL_OK;
     TRY(check_overlaps(outs, ins, [](const Range &, const Range &) { return false; }));
-    Plan p = plan_alltoallv(counts, sd, rd, dt, R, options_from(config(), false));
-    return execute(p, Buffers{send, recv, nullptr}, stream);
+    return execute([&](const PlanOptions &o) { return plan_alltoallv(counts, sd, rd, dt, R, o); },
+                   false, Buffers{send, recv, nullptr}, stream);
 }
 
 hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dt, int R, char *buf,

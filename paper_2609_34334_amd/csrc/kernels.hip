@@ -51,6 +51,62 @@ struct alignas(16) Pack {
     S v[VE];
 };
 
+// Tuning knobs (compile time).  Vectors in flight per thread in the ring
+// step, and whether streamed operands use non-temporal loads / stores.
+#ifndef HOCCL_RS_UNROLL_BF16
+#define HOCCL_RS_UNROLL_BF16 2
+#endif
+#ifndef HOCCL_RS_UNROLL_32
+#define HOCCL_RS_UNROLL_32 4
+#endif
+// Non-temporal access for operands touched once per collective: the ranks'
+// inputs (HOCCL_NT_X) and the final output (HOCCL_NT_FINAL).  Partials are
+// always accessed normally so that the next step can hit the cache.
+#ifndef HOCCL_NT_X
+#define HOCCL_NT_X 1
+#endif
+#ifndef HOCCL_NT_FINAL
+#define HOCCL_NT_FINAL 0
+#endif
+#ifndef HOCCL_FOLD_NT
+#define HOCCL_FOLD_NT 1
+#endif
+#ifndef HOCCL_FOLD_UNROLL
+#define HOCCL_FOLD_UNROLL 1
+#endif
+// bit 0: in0 non-temporal, bit 1: in1, bit 2: out
+constexpr int kNtFirst = (HOCCL_NT_X ? 3 : 0);
+constexpr int kNtMiddle = (HOCCL_NT_X ? 2 : 0);
+constexpr int kNtLast = (HOCCL_NT_X ? 2 : 0) | (HOCCL_NT_FINAL ? 4 : 0);
+constexpr int kNtOnly = (HOCCL_NT_X ? 3 : 0) | (HOCCL_NT_FINAL ? 4 : 0);
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte-granular vector load / store of a Pack, optionally non-temporal.
+template <bool NT, typename P>
+__device__ __forceinline__ P ldp(const P *p) {
+    static_assert(sizeof(P) % 16 == 0, "Pack must be a multiple of 16 bytes");
+    P r;
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(P) / 16); ++i) {
+        u32x4 v = NT ? __builtin_nontemporal_load((const u32x4 *)p + i) : ((const u32x4 *)p)[i];
+        __builtin_memcpy((char *)&r + 16 * i, &v, 16);
+    }
+    return r;
+}
+template <bool NT, typename P>
+__device__ __forceinline__ void stp(P *p, const P &x) {
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(P) / 16); ++i) {
+        u32x4 v;
+        __builtin_memcpy(&v, (const char *)&x + 16 * i, 16);
+        if (NT)
+            __builtin_nontemporal_store(v, (u32x4 *)p + i);
+        else
+            ((u32x4 *)p)[i] = v;
+    }
+}
+
 // Splits the blocks of a launch over `nseg` segments.  With at least one
 // block per segment, block b serves segment b % nseg (consecutive blocks go
 // to different segments, so every XCD streams every segment); otherwise each
@@ -68,8 +124,9 @@ __device__ __forceinline__ void for_each_segment(int nseg, F &&f) {
 }
 
 // ---- one ring step --------------------------------------------------------------
-template <class T0, class T1, class TO, int VE, int U>
+template <class T0, class T1, class TO, int VE, int U, int NT>
 __device__ __forceinline__ void reduce_segment(const RSegArg &s, int lb, int nb) {
+    constexpr bool NT0 = NT & 1, NT1 = NT & 2, NTO = NT & 4;
     using S0 = typename T0::S;
     using S1 = typename T1::S;
     using SO = typename TO::S;
@@ -115,28 +172,28 @@ __device__ __forceinline__ void reduce_segment(const RSegArg &s, int lb, int nb)
         P1 b[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            a[u] = v0[base + (uint64_t)u * bd];
-            b[u] = v1[base + (uint64_t)u * bd];
+            a[u] = ldp<NT0>(v0 + base + (uint64_t)u * bd);
+            b[u] = ldp<NT1>(v1 + base + (uint64_t)u * bd);
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) vo[base + (uint64_t)u * bd] = one(a[u], b[u]);
+        for (int u = 0; u < U; ++u) stp<NTO>(vo + base + (uint64_t)u * bd, one(a[u], b[u]));
     }
     // At most one partial iteration is left for this thread.
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         uint64_t i = base + (uint64_t)u * bd;
-        if (i < nv) vo[i] = one(v0[i], v1[i]);
+        if (i < nv) stp<NTO>(vo + i, one(ldp<NT0>(v0 + i), ldp<NT1>(v1 + i)));
     }
 }
 
 template <typename A>
 __device__ __forceinline__ const A &kernargs();
 
-template <class T0, class T1, class TO, int VE, int U>
+template <class T0, class T1, class TO, int VE, int U, int NT>
 __global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgs) {
     const ReduceArgs &a = kernargs<ReduceArgs>();
     for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
-        reduce_segment<T0, T1, TO, VE, U>(a.seg[seg], lb, nb);
+        reduce_segment<T0, T1, TO, VE, U, NT>(a.seg[seg], lb, nb);
     });
 }
 
@@ -185,20 +242,55 @@ __device__ __forceinline__ void fold_chunk(const FoldArgs &a, int j, int lb, int
     for (uint64_t k = t; k < h; k += stride) scalar(k);
     for (uint64_t k = tail + t; k < n; k += stride) scalar(k);
 
+    constexpr bool NT = HOCCL_FOLD_NT;
+    if constexpr (NR > 0) {
+        // FU vectors per thread; every operand's vector is loaded before the
+        // in-order adds consume them.
+        constexpr int FU = HOCCL_FOLD_UNROLL;
+        uint64_t base = t;
+        for (; base + (uint64_t)(FU - 1) * stride < nv; base += stride * FU) {
+            P v[FU][NR];
+#pragma unroll
+            for (int u = 0; u < FU; ++u)
+#pragma unroll
+                for (int k = 0; k < NR; ++k) v[u][k] = ldp<NT>((const P *)(src(k) + h) + base + u * stride);
+#pragma unroll
+            for (int u = 0; u < FU; ++u) {
+                A acc[VE];
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = T::widen(v[u][0].v[e]);
+#pragma unroll
+                for (int k = 1; k < NR; ++k)
+#pragma unroll
+                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[u][k].v[e]);
+                P y;
+#pragma unroll
+                for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
+                for (int q = 0; q < nout; ++q) ((P *)(dst(q) + h))[base + u * stride] = y;
+            }
+        }
+        for (int u = 0; u < FU; ++u) {
+            uint64_t i = base + u * stride;
+            if (i >= nv) break;
+            A acc[VE];
+            P v0 = ldp<NT>((const P *)(src(0) + h) + i);
+#pragma unroll
+            for (int e = 0; e < VE; ++e) acc[e] = T::widen(v0.v[e]);
+            for (int k = 1; k < NR; ++k) {
+                P v = ldp<NT>((const P *)(src(k) + h) + i);
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v.v[e]);
+            }
+            P y;
+#pragma unroll
+            for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
+            for (int q = 0; q < nout; ++q) ((P *)(dst(q) + h))[i] = y;
+        }
+        return;
+    }
     for (uint64_t i = t; i < nv; i += stride) {
         A acc[VE];
-        if constexpr (NR > 0) {
-            // every operand's vector is loaded before the in-order adds
-            P v[NR];
-#pragma unroll
-            for (int k = 0; k < NR; ++k) v[k] = ((const P *)(src(k) + h))[i];
-#pragma unroll
-            for (int e = 0; e < VE; ++e) acc[e] = T::widen(v[0].v[e]);
-#pragma unroll
-            for (int k = 1; k < NR; ++k)
-#pragma unroll
-                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[k].v[e]);
-        } else {
+        {
             constexpr int KB = 8;
             {
                 P v0 = ((const P *)(src(0) + h))[i];
@@ -294,41 +386,56 @@ __global__ void __launch_bounds__(1024) copy_kernel(CopyArgs) {
 
 // ---- launchers --------------------------------------------------------------------
 
-template <class T0, class T1, class TO, int VE, int U>
+// hipLaunchKernel reports this launch's own status (hipGetLastError would
+// also return errors left behind by unrelated earlier calls).
+template <typename Args>
+static hipError_t launch(const void *kernel, const Args &a, int wg, int threads, hipStream_t s) {
+    void *args[] = {const_cast<Args *>(&a)};
+    return hipLaunchKernel(kernel, dim3((unsigned)wg), dim3((unsigned)threads), args, 0, s);
+}
+
+template <class T0, class T1, class TO, int VE, int U, int NT>
 static hipError_t launch_rs(const ReduceArgs &a, int wg, int threads, hipStream_t s) {
-    hipLaunchKernelGGL((reduce_step_kernel<T0, T1, TO, VE, U>), dim3((unsigned)wg), dim3((unsigned)threads),
-                       0, s, a);
-    return hipGetLastError();
+    return launch((const void *)reduce_step_kernel<T0, T1, TO, VE, U, NT>, a, wg, threads, s);
 }
 
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg, int threads,
                               hipStream_t s) {
+    constexpr int UB = HOCCL_RS_UNROLL_BF16, U4 = HOCCL_RS_UNROLL_32;
     if (dt == HOCCL_BF16) {
         switch (ph) {
-        case PH_FIRST: return launch_rs<TBF16, TBF16, TF32, 8, 2>(a, wg, threads, s);
-        case PH_MIDDLE: return launch_rs<TF32, TBF16, TF32, 8, 2>(a, wg, threads, s);
-        case PH_LAST: return launch_rs<TF32, TBF16, TBF16, 8, 2>(a, wg, threads, s);
-        case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, 8, 2>(a, wg, threads, s);
+        case PH_FIRST: return launch_rs<TBF16, TBF16, TF32, 8, UB, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TF32, TBF16, TF32, 8, UB, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TF32, TBF16, TBF16, 8, UB, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, 8, UB, kNtOnly>(a, wg, threads, s);
         }
     } else if (dt == HOCCL_FP32) {
-        return launch_rs<TF32, TF32, TF32, 4, 4>(a, wg, threads, s);
+        switch (ph) {
+        case PH_FIRST: return launch_rs<TF32, TF32, TF32, 4, U4, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TF32, TF32, TF32, 4, U4, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TF32, TF32, TF32, 4, U4, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TF32, TF32, TF32, 4, U4, kNtOnly>(a, wg, threads, s);
+        }
     } else if (dt == HOCCL_INT32) {
-        return launch_rs<TI32, TI32, TI32, 4, 4>(a, wg, threads, s);
+        switch (ph) {
+        case PH_FIRST: return launch_rs<TI32, TI32, TI32, 4, U4, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TI32, TI32, TI32, 4, U4, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TI32, TI32, TI32, 4, U4, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TI32, TI32, TI32, 4, U4, kNtOnly>(a, wg, threads, s);
+        }
     }
     return hipErrorInvalidValue;
 }
 
 template <class T, int VE>
 static hipError_t launch_fold_t(const FoldArgs &a, int wg, int threads, hipStream_t s) {
-    dim3 g((unsigned)wg), b((unsigned)threads);
     switch (a.R) {
-    case 2: hipLaunchKernelGGL((fold_kernel<T, VE, 2>), g, b, 0, s, a); break;
-    case 3: hipLaunchKernelGGL((fold_kernel<T, VE, 3>), g, b, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((fold_kernel<T, VE, 4>), g, b, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((fold_kernel<T, VE, 8>), g, b, 0, s, a); break;
-    default: hipLaunchKernelGGL((fold_kernel<T, VE, 0>), g, b, 0, s, a); break;
+    case 2: return launch((const void *)fold_kernel<T, VE, 2>, a, wg, threads, s);
+    case 3: return launch((const void *)fold_kernel<T, VE, 3>, a, wg, threads, s);
+    case 4: return launch((const void *)fold_kernel<T, VE, 4>, a, wg, threads, s);
+    case 8: return launch((const void *)fold_kernel<T, VE, 8>, a, wg, threads, s);
+    default: return launch((const void *)fold_kernel<T, VE, 0>, a, wg, threads, s);
     }
-    return hipGetLastError();
 }
 
 hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads, hipStream_t s) {
@@ -339,8 +446,7 @@ hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
 }
 
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s) {
-    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)wg), dim3((unsigned)threads), 0, s, a);
-    return hipGetLastError();
+    return launch((const void *)copy_kernel, a, wg, threads, s);
 }
 
 }  // namespace hoccl

@@ -10,19 +10,21 @@
 //   proxy:   see start == START, write start := 0 (acknowledge),
 //            run the copies, write finish := FINISH, see finish == 0.
 //
-// Every transition is acknowledged, so a flag pair is free for reuse once
-// the stream has reset `finish`.  The flags live in a pool of slots in
-// pinned, coherent host memory (the paper's flag pool); each in-flight
-// operation holds one slot.
+// With the HIP runtime used here, hipStreamWaitValue32 and
+// hipStreamWriteValue32 are executed by small kernels, and the wait kernel
+// spins on a compute unit for as long as the copies take, holding back every
+// later packet of its hardware queue -- including kernels of other streams
+// that share the queue.  So by default the handshake runs on a private
+// stream created with a one-CU mask: such a stream gets a hardware queue of
+// its own, the spinning wait is confined to one compute unit, and the
+// caller's stream joins the private one through HIP events (fork before the
+// start path, join after the completion path).  The handshake can also be
+// put on the caller's stream directly, the paper's literal form.
 //
-// The copies themselves go to SDMA engines chosen explicitly through ROCr
-// (hsa_amd_memory_async_copy_on_engine), which lets one collective use every
-// engine of the device; the HIP runtime's own device-to-device path picks
-// engines itself.  Chains of copies (the ring hops of one chunk) stay on one
-// engine and also depend on their predecessor's completion signal; chains
-// are spread over the engines so that each engine gets about the same
-// number of bytes (the paper's flow-size-aware chunk scheduling, reduced to
-// one domain).
+// A host function (hipLaunchHostFunc) that blocks until the copies are done
+// would need no GPU code at all, but it blocks the runtime thread that also
+// delivers signal callbacks (a profiler's copy-completion callbacks, for
+// one), so it is not used.
 #include "proxy.h"
 
 #include <hip/hip_runtime.h>
@@ -71,6 +73,50 @@ hsa_status_t find_agent_cb(hsa_agent_t a, void *data) {
     return HSA_STATUS_SUCCESS;
 }
 
+// Runs a 256-byte device-to-device copy on each of the first 16 engine ids and
+// returns the mask of those that completed within 200 ms.  The scratch
+// buffer is leaked if a copy is still outstanding, so no late write can land
+// in freed memory.
+uint32_t probe_engines(hsa_agent_t agent) {
+    constexpr int kIds = 16;
+    constexpr size_t kStep = 512;
+    char *buf = nullptr;
+    if (hipMalloc(&buf, 2 * kIds * kStep) != hipSuccess) return 0;
+    if (hipMemset(buf, 0x5a, 2 * kIds * kStep) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+        (void)hipFree(buf);
+        return 0;
+    }
+    hsa_signal_t sig;
+    if (hsa_signal_create(1, 0, nullptr, &sig) != HSA_STATUS_SUCCESS) {
+        (void)hipFree(buf);
+        return 0;
+    }
+    uint32_t ok = 0;
+    bool outstanding = false;
+    for (int e = 0; e < kIds && !outstanding; ++e) {
+        hsa_signal_store_screlease(sig, 1);
+        char *src = buf + (size_t)e * kStep, *dst = buf + (size_t)(kIds + e) * kStep;
+        if (hsa_amd_memory_async_copy_on_engine(dst, agent, src, agent, 256, 0, nullptr, sig,
+                                                (hsa_amd_sdma_engine_id_t)(1u << e), true) !=
+            HSA_STATUS_SUCCESS)
+            continue;
+        auto t0 = std::chrono::steady_clock::now();
+        while (hsa_signal_load_scacquire(sig) != 0) {
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(200)) {
+                outstanding = true;
+                break;
+            }
+            std::this_thread::yield();
+        }
+        if (!outstanding) ok |= 1u << e;
+    }
+    if (!outstanding) {
+        hsa_signal_destroy(sig);
+        (void)hipFree(buf);
+    }
+    return ok;
+}
+
 inline uint32_t load_flag(volatile uint32_t *p) {
     return __atomic_load_n((uint32_t *)p, __ATOMIC_ACQUIRE);
 }
@@ -98,6 +144,8 @@ class ProxyImpl {
     hsa_agent_t agent{};
     std::vector<uint32_t> engines;  // id bits of usable engines
     uint32_t *flags = nullptr;      // kSlots * 2 flags, one per cache line
+    hipStream_t hs = nullptr;       // private one-CU stream for the handshake
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     std::mutex mu;
     std::condition_variable cv_work, cv_slot;
     std::deque<ProxyOp *> incoming;
@@ -160,6 +208,12 @@ class ProxyImpl {
         delete op;
     }
 
+    bool started(ProxyOp &op) {
+        if (load_flag(start_flag(op.slot)) != kStartValue) return false;
+        store_flag(start_flag(op.slot), 0);  // acknowledge
+        return true;
+    }
+
     void loop() {
         std::vector<ProxyOp *> active;
         for (;;) {
@@ -181,8 +235,7 @@ class ProxyImpl {
                 switch (op->state) {
                 case ProxyOp::WAIT_START:
                     // The stream has drained everything before the collective.
-                    if (load_flag(start_flag(op->slot)) == kStartValue) {
-                        store_flag(start_flag(op->slot), 0);  // acknowledge
+                    if (started(*op)) {
                         issue(*op);
                         op->state = ProxyOp::COPYING;
                         op->since = now;
@@ -191,10 +244,10 @@ class ProxyImpl {
                     break;
                 case ProxyOp::COPYING:
                     if (copies_done(*op)) {
+                        progress = true;
                         store_flag(finish_flag(op->slot), kFinishValue);
                         op->state = ProxyOp::WAIT_ACK;
                         op->since = now;
-                        progress = true;
                     } else if (!op->timed_out &&
                                now - op->since > std::chrono::milliseconds(op->timeout_ms)) {
                         op->timed_out = true;
@@ -222,37 +275,69 @@ class ProxyImpl {
     }
 };
 
-Proxy *Proxy::create(int device) {
-    int bus = 0, dev = 0;
-    if (hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, device) != hipSuccess ||
-        hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, device) != hipSuccess)
+Proxy *Proxy::create(int device, std::string *why) {
+    auto fail = [&](const char *msg, long code) -> Proxy * {
+        if (why) {
+            char buf[200];
+            std::snprintf(buf, sizeof buf, "SDMA engine proxy unavailable: %s (%ld)", msg, code);
+            *why = buf;
+        }
         return nullptr;
-    if (hsa_init() != HSA_STATUS_SUCCESS) return nullptr;
+    };
+    int bus = 0, dev = 0;
+    hipError_t he;
+    if ((he = hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, device)) != hipSuccess ||
+        (he = hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, device)) != hipSuccess)
+        return fail("PCI location query failed", (long)he);
+    hsa_status_t hs = hsa_init();
+    if (hs != HSA_STATUS_SUCCESS) return fail("hsa_init failed", (long)hs);
     FindAgent f{(uint32_t)((bus << 8) | (dev << 3)), false, {}};
     hsa_iterate_agents(find_agent_cb, &f);
     if (!f.found) {
         hsa_shut_down();
-        return nullptr;
+        return fail("no HSA GPU agent at the HIP device's PCI location", (long)f.bdf);
     }
     uint32_t mask = 0;
-    if (hsa_amd_memory_copy_engine_status(f.agent, f.agent, &mask) != HSA_STATUS_SUCCESS || mask == 0) {
+    hs = hsa_amd_memory_copy_engine_status(f.agent, f.agent, &mask);
+    if (hs != HSA_STATUS_SUCCESS || mask == 0) {
+        // Some ROCr builds do not answer this query for same-device copies
+        // although they execute them; find the usable engines by running one
+        // small copy on each.
+        mask = probe_engines(f.agent);
+    }
+    if (mask == 0) {
         hsa_shut_down();
-        return nullptr;
+        return fail("no SDMA engine accepts device-to-device copies", (long)hs);
     }
     ProxyImpl *p = new ProxyImpl();
     p->agent = f.agent;
-    for (int b = 0; b < 32; ++b)
+    // Engines 0 and 1 also serve the runtime's own host transfers: use them
+    // last.
+    for (int b = 2; b < 32; ++b)
+        if (mask & (1u << b)) p->engines.push_back(1u << b);
+    for (int b = 0; b < 2; ++b)
         if (mask & (1u << b)) p->engines.push_back(1u << b);
     void *fl = nullptr;
-    if (hipHostMalloc(&fl, kSlots * 2 * kLine, hipHostMallocCoherent | hipHostMallocMapped) !=
-            hipSuccess ||
-        !fl) {
+    he = hipHostMalloc(&fl, kSlots * 2 * kLine, hipHostMallocCoherent | hipHostMallocMapped);
+    if (he != hipSuccess || !fl) {
         delete p;
         hsa_shut_down();
-        return nullptr;
+        return fail("hipHostMalloc of the flag pool failed", (long)he);
     }
     std::memset(fl, 0, kSlots * 2 * kLine);
     p->flags = (uint32_t *)fl;
+    // A CU-masked stream owns a hardware queue.  The runtime accepts masks
+    // only with at least one CU in every XCD; logical CUs 0-7 are one per
+    // XCD on MI355X, so the mask is 0xff (the wait kernel itself is a single
+    // thread on one of them).
+    uint32_t cu_mask[8] = {0xffu, 0, 0, 0, 0, 0, 0, 0};
+    if (hipExtStreamCreateWithCUMask(&p->hs, 8, cu_mask) != hipSuccess ||
+        hipEventCreateWithFlags(&p->ev_fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();  // handled: do not leave it for the next caller
+        if (p->hs) (void)hipStreamDestroy(p->hs);
+        p->hs = nullptr;  // the handshake then runs on the caller's stream
+    }
     for (int s = kSlots - 1; s >= 0; --s) p->free_slots.push_back(s);
     p->th = std::thread([p] { p->loop(); });
     return new Proxy(p);
@@ -267,6 +352,9 @@ Proxy::~Proxy() {
     if (impl_->th.joinable()) impl_->th.join();
     for (auto &s : impl_->free_signals) hsa_signal_destroy(s);
     if (impl_->flags) (void)hipHostFree(impl_->flags);
+    if (impl_->hs) (void)hipStreamDestroy(impl_->hs);
+    if (impl_->ev_fork) (void)hipEventDestroy(impl_->ev_fork);
+    if (impl_->ev_join) (void)hipEventDestroy(impl_->ev_join);
     delete impl_;
     hsa_shut_down();
 }
@@ -274,7 +362,8 @@ Proxy::~Proxy() {
 int Proxy::engine_count() const { return (int)impl_->engines.size(); }
 
 hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                             unsigned timeout_ms, hipStream_t s, int *engines_used, std::string &err) {
+                             unsigned timeout_ms, bool on_caller, hipStream_t s, int *engines_used,
+                             std::string &err) {
     ProxyImpl &P = *impl_;
     {
         std::lock_guard<std::mutex> lk(P.mu);
@@ -338,33 +427,48 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
             P.free_signals.pop_back();
         }
     }
-    while (op->sig.size() < copies.size()) {
-        hsa_signal_t sg;
-        if (hsa_signal_create(1, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) {
-            err = "hsa_signal_create failed";
-            std::lock_guard<std::mutex> lk(P.mu);
-            for (auto &x : op->sig) P.free_signals.push_back(x);
-            P.free_slots.push_back(op->slot);
-            delete op;
-            return HOCCL_ERR_HIP;
-        }
-        op->sig.push_back(sg);
-    }
-    void *st = (void *)P.start_flag(op->slot);
-    void *fi = (void *)P.finish_flag(op->slot);
-    hipError_t e = hipStreamWriteValue32(s, st, kStartValue, 0);
-    if (e != hipSuccess) {
-        // Nothing reached the stream: give the slot and signals back.
-        err = std::string("hipStreamWriteValue32 failed: ") + hipGetErrorString(e);
+    auto give_back = [&]() {
         std::lock_guard<std::mutex> lk(P.mu);
         for (auto &x : op->sig) P.free_signals.push_back(x);
         P.free_slots.push_back(op->slot);
         delete op;
+    };
+    while (op->sig.size() < copies.size()) {
+        hsa_signal_t sg;
+        if (hsa_signal_create(1, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) {
+            err = "hsa_signal_create failed";
+            give_back();
+            return HOCCL_ERR_HIP;
+        }
+        op->sig.push_back(sg);
+    }
+    // The handshake runs on the private one-CU stream unless asked for on
+    // the caller's stream (or the private stream could not be created).
+    hipStream_t hs = s;
+    if (!on_caller && P.hs) {
+        hipError_t e = hipEventRecord(P.ev_fork, s);
+        if (e == hipSuccess) e = hipStreamWaitEvent(P.hs, P.ev_fork, 0);
+        if (e != hipSuccess) {
+            err = std::string("fork to the handshake stream failed: ") + hipGetErrorString(e);
+            give_back();
+            return HOCCL_ERR_HIP;
+        }
+        hs = P.hs;
+    }
+    void *st = (void *)P.start_flag(op->slot);
+    void *fi = (void *)P.finish_flag(op->slot);
+    hipError_t e = hipStreamWriteValue32(hs, st, kStartValue, 0);
+    if (e != hipSuccess) {
+        // Nothing of the handshake reached a stream: give everything back.
+        err = std::string("hipStreamWriteValue32 failed: ") + hipGetErrorString(e);
+        give_back();
         return HOCCL_ERR_HIP;
     }
-    if ((e = hipStreamWaitValue32(s, st, 0, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
-        (e = hipStreamWaitValue32(s, fi, kFinishValue, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
-        (e = hipStreamWriteValue32(s, fi, 0, 0)) != hipSuccess) {
+    if ((e = hipStreamWaitValue32(hs, st, 0, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
+        (e = hipStreamWaitValue32(hs, fi, kFinishValue, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
+        (e = hipStreamWriteValue32(hs, fi, 0, 0)) != hipSuccess ||
+        (hs != s && ((e = hipEventRecord(P.ev_join, hs)) != hipSuccess ||
+                     (e = hipStreamWaitEvent(s, P.ev_join, 0)) != hipSuccess))) {
         // Whatever part of the handshake reached the stream, the proxy must
         // still see the op through, so hand it over regardless and report.
         err = std::string("stream memory operation failed: ") + hipGetErrorString(e);

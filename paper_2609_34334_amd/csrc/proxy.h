@@ -23,8 +23,9 @@ class ProxyImpl;
 
 class Proxy {
   public:
-    // Null when the device's SDMA engines cannot be driven directly.
-    static Proxy *create(int device);
+    // Null when the device's SDMA engines cannot be driven directly; *why
+    // then says which step failed.
+    static Proxy *create(int device, std::string *why);
     ~Proxy();
 
     int engine_count() const;
@@ -32,8 +33,11 @@ class Proxy {
     // Enqueues the handshake on `s` and hands the copies to the proxy
     // thread; returns once enqueued.  Copies run on at most `max_engines`
     // engines (0 = all), balanced by bytes per engine.
+    // The start/finish flag handshake runs on the proxy's private one-CU
+    // stream joined to `s` by events, or on `s` itself when `on_caller`.
     hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                          unsigned timeout_ms, hipStream_t s, int *engines_used, std::string &err);
+                          unsigned timeout_ms, bool on_caller, hipStream_t s, int *engines_used,
+                          std::string &err);
 
   private:
     explicit Proxy(ProxyImpl *impl) : impl_(impl) {}

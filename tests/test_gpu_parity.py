@@ -251,15 +251,18 @@ def test_alltoallv_routing(path):
 
 
 def test_sdma_paths_dispatch_no_kernel():
-    """Copy-only collectives on an SDMA path report zero CUs."""
+    """Copy-only collectives on an SDMA path launch no kernel of the library:
+    zero CUs on the HIP path, one (the handshake's one-thread wait kernel)
+    on the engine proxy.  AUTO resolves to the HIP path."""
     R, n = 8, 1 << 16
     x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
-    for path in ["sdma", "engines"]:
+    for path, cus in [("auto", 0), ("sdma", 0), ("engines", 1)]:
         hc.set_config(copy_path=path)
         hc.allgather(x)
         s = hc.last_stats()
-        assert s["cus_used_max"] == 0 and s["reduce_launches"] == 0
+        assert s["cus_used_max"] == cus and s["reduce_launches"] == 0, (path, s)
         assert s["copy_kernel_launches"] == 0 and s["copy_ops"] > 0
+        assert s["copy_path_used"] == (hc.COPY_SDMA_ENGINES if path == "engines" else hc.COPY_SDMA)
     torch.cuda.synchronize()
 
 
@@ -331,3 +334,32 @@ def test_back_to_back_calls_on_two_streams_share_workspace_safely():
         for r in range(R):
             assert_bitwise(from_dev(oa[r], hc.BF16), ra[r], f"s1 r={r}")
             assert_bitwise(from_dev(ob[r], hc.BF16), rb[r], f"s2 r={r}")
+
+
+@pytest.mark.parametrize("handshake", [0, 1])
+def test_engine_proxy_handshakes(handshake):
+    """Both ways of ordering the engine proxy with the stream: a host
+    function (default) and the start/finish flag handshake through stream
+    memory operations.  Checked behind a delayed producer, with a consumer
+    queued after the collective, and for ring chains (dependent hops)."""
+    hc.set_config(copy_path="engines", proxy_handshake=handshake)
+    R, n = 4, 1 << 20
+    x = [W.random_values("fp32", 97, r, n) for r in range(R)]
+    ref = oracle.allreduce_new(x, hc.FP32)
+    host = [torch.from_numpy(a).pin_memory() for a in x]
+    s = torch.cuda.Stream()
+    for direct in (1, 0):
+        hc.set_config(allgather_direct=direct)
+        send = [torch.full((n,), float("nan"), device="cuda") for _ in range(R)]
+        recv = [torch.zeros(n, device="cuda") for _ in range(R)]
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            torch.cuda._sleep(20_000_000)
+            for r in range(R):
+                send[r].copy_(host[r], non_blocking=True)
+            for _ in range(3):
+                hc.allreduce(send, recv, stream=s)
+            out = [t.clone() for t in recv]
+        s.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(out[r], hc.FP32), ref[r], f"handshake={handshake} direct={direct} r={r}")
