@@ -80,29 +80,44 @@ def bench_reduce_scatter(hc, W, steps, warmup):
     send = [bf16_dev(a) for a in x]
     recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     hc.set_config(reduce_algo="ring", kernel_timing=0)
+    stream = torch.cuda.current_stream()
 
     def step():
-        hc.reduce_scatter(send, recv)
+        hc.reduce_scatter(send, recv, stream=stream)
 
-    sec = time_op(step, steps, warmup)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    # The timed region: K steps between two synchronisations, bracketed by
+    # HIP events on the stream every kernel of the step is launched on.
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / steps
     stats = hc.last_stats()
-    # Per-launch durations of the reduce-step kernel over a second timed run.
+    launches_per_op = stats["reduce_launches"]
+    bytes_per_op = stats["hbm_bytes_algorithmic"]
+    avg_launch_s = e0.elapsed_time(e1) / 1e3 / (steps * launches_per_op)
+    achieved = bytes_per_op / launches_per_op / avg_launch_s / 1e9
+    # Per-step detail: events around each launch (they add the dispatch gap).
     hc.set_config(kernel_timing=1)
     hc.kernel_times()
     for _ in range(steps):
         step()
     kt = hc.kernel_times()
     hc.set_config(kernel_timing=0)
-    launches_per_op = stats["reduce_launches"]
-    bytes_per_op = stats["hbm_bytes_algorithmic"]
-    avg_launch_s = statistics.mean(kt) / 1e3
-    achieved = bytes_per_op / launches_per_op / avg_launch_s / 1e9
+    per_step = [round(statistics.mean(kt[i::launches_per_op]) * 1e3, 2) for i in range(launches_per_op)]
     S = R * n * 2
     algbw = S / sec / 1e9
     return dict(x=x, recv=recv, sec=sec, stats=stats, S=S, algbw=algbw,
                 busbw=algbw * (R - 1) / R, bytes_per_op=bytes_per_op,
                 launches=launches_per_op, avg_launch_us=avg_launch_s * 1e6,
-                achieved=achieved, kernel_ms=kt)
+                achieved=achieved, per_step_us=per_step)
 
 
 def direct_reduce_scatter(hc, send_np, steps, warmup):
@@ -115,13 +130,16 @@ def direct_reduce_scatter(hc, send_np, steps, warmup):
     hc.set_config(reduce_algo="direct")
     sec = time_op(lambda: hc.reduce_scatter(send, recv), steps, warmup)
     st = hc.last_stats()
-    hc.set_config(kernel_timing=1)
-    hc.kernel_times()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
     for _ in range(steps):
-        hc.reduce_scatter(send, recv)
-    kt = hc.kernel_times()
-    hc.set_config(kernel_timing=0, reduce_algo="ring")
-    launch = statistics.mean(kt) / 1e3
+        hc.reduce_scatter(send, recv, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    hc.set_config(reduce_algo="ring")
+    launch = e0.elapsed_time(e1) / 1e3 / steps
     achieved = st["hbm_bytes_algorithmic"] / launch / 1e9
     return recv, dict(algbw_GBs=round(R * n * 2 / sec / 1e9, 2), busbw_GBs=round(R * n * 2 / sec / 1e9 * (R - 1) / R, 2),
                       ms=round(sec * 1e3, 4), cus_used=st["cus_used_max"],
@@ -531,7 +549,8 @@ def main():
                      "frac": round(rs["achieved"] / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "avg_launch_us": round(rs["avg_launch_us"], 2),
                      "bytes_per_launch": rs["bytes_per_op"] // rs["launches"],
-                     "launches_per_step": rs["launches"]},
+                     "launches_per_step": rs["launches"],
+                     "per_launch_event_us": rs["per_step_us"]},
         "cpu_baseline": cpu,
         "extra": extra,
     }
