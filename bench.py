@@ -392,6 +392,29 @@ def bench_p2p_sizes(hc, reps):
     return dict(workload="single bf16 message rank 0 -> 1, algbw GB/s", rows=rows)
 
 
+def bench_small_message(hc, reps):
+    """Latency of one 4 KiB send/recv (rank 0 -> 1) through each copy path:
+    the event fork/join + HIP SDMA copy, the engine proxy's flag handshake,
+    and the CU copy kernel; plus the host time of the call."""
+    import torch
+    src = torch.zeros(2048, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    out = {}
+    for name in ("sdma", "engines", "kernel"):
+        hc.set_config(copy_path=name)
+        med, mn = event_time(lambda: hc.sendrecv([src, src], [dst, dst], [1, -1]), reps, warmup=5)
+        host = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            hc.sendrecv([src, src], [dst, dst], [1, -1])
+            host.append(time.perf_counter() - t0)
+            torch.cuda.synchronize()
+        out[name] = dict(device_us=round(med * 1e6, 2), device_min_us=round(mn * 1e6, 2),
+                         host_call_us=round(statistics.median(host) * 1e6, 2))
+    hc.set_config(copy_path="auto")
+    return dict(workload="one 4 KiB message rank 0 -> 1 (stream-manager round trip)", **out)
+
+
 def bench_rs_workgroups(hc, x, reps):
     """Ring reduce-scatter of the headline at a fixed workgroup budget: the
     CU footprint / bandwidth trade-off of the reduction kernels."""
@@ -519,6 +542,7 @@ def main():
                 extra[name] = {"error": repr(e)}
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
+        extra["small_message_latency"] = bench_small_message(hc, 30)
 
     st = rs["stats"]
     out = {

@@ -38,8 +38,11 @@
  *   Argument errors are detected before anything is enqueued.  A failing HIP
  *   or HSA call returns HOCCL_ERR_HIP; hoccl_last_error_string() describes
  *   it.  Faults of the device work itself surface at the caller's own
- *   synchronisation.  `count == 0` is a successful no-op.  There is no
- *   sticky error state.
+ *   synchronisation.  `count == 0` is a successful no-op.  The only error
+ *   that outlives its call is the SDMA_ENGINES proxy's watchdog: copies of
+ *   an earlier call that did not finish within proxy_timeout_ms are reported
+ *   once, as HOCCL_ERR_TIMEOUT, by the next SDMA_ENGINES call (which then
+ *   enqueues nothing).
  * Threads.  One host thread at a time may call into the library per device.
  *   Collectives issued on different streams that overlap in time are
  *   ordered by the library where they share its workspace or its internal
@@ -253,6 +256,26 @@ hoccl_status_t hoccl_alltoallv(const void *const *send,
 hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dtype,
                                      int R, char *buf, size_t len,
                                      size_t *needed);
+
+/* The paper's collective scheduler (Collective Scheduler section) on a
+ * described multi-node topology, host only.  G GPUs; C: G*G row-major
+ * traffic matrix in bytes (C[u*G+v] = bytes from GPU u to GPU v; the
+ * diagonal is ignored); node[u]: intra-node (NVLink/xGMI) domain of GPU u;
+ * peer[u]: its symmetric peer (-1: none); bw_intra / bw_inter: bandwidth of
+ * an intra-node / inter-node edge.  Writes JSON {"T": expanded traffic
+ * matrix with forwarding copies (Eq. 2-5), "stages": stage matrices T^s from
+ * the Birkhoff-like decomposition (Algorithm 1), "tau": stage durations
+ * (Eq. 9-10), "total": their sum (Eq. 11)}.  Buffer conventions as for
+ * hoccl_debug_plan_json. */
+hoccl_status_t hoccl_debug_schedule_json(int G, const double *C, const int *node, const int *peer,
+                                         double bw_intra, double bw_inter, char *buf, size_t len,
+                                         size_t *needed);
+
+/* Flow-size-aware chunk order on one DMA engine: flows of bytes[i] are cut
+ * into chunk_bytes pieces and order[k] receives the flow of the k-th chunk
+ * (at most cap entries); *n receives the total number of chunks. */
+hoccl_status_t hoccl_debug_interleave(int nflows, const double *bytes, double chunk_bytes, int *order,
+                                      size_t cap, size_t *n);
 
 #ifdef __cplusplus
 }

@@ -82,6 +82,11 @@ _SIGS = {
     "hoccl_alltoall": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
     "hoccl_alltoallv": [_vpp, _szp, _szp, _vpp, _szp, _i, _i, ctypes.c_void_p],
     "hoccl_debug_plan_json": [_i, _sz, _i, _i, ctypes.c_char_p, _sz, _szp],
+    "hoccl_debug_schedule_json": [_i, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i),
+                                  ctypes.POINTER(_i), ctypes.c_double, ctypes.c_double,
+                                  ctypes.c_char_p, _sz, _szp],
+    "hoccl_debug_interleave": [_i, ctypes.POINTER(ctypes.c_double), ctypes.c_double,
+                               ctypes.POINTER(_i), _sz, _szp],
 }
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -189,6 +194,37 @@ def plan_json(op, count, dtype, R):
     _check(_lib.hoccl_debug_plan_json(op, count, dtype, R, buf, need.value, ctypes.byref(need)),
            "hoccl_debug_plan_json")
     return json.loads(buf.value.decode())
+
+
+def schedule(C, node, peer, bw_intra, bw_inter):
+    """The paper's collective scheduler on a described topology: returns
+    {'T', 'stages', 'tau', 'total'} (see hoccl_debug_schedule_json)."""
+    import json
+    G = len(node)
+    flat = [float(C[u][v]) for u in range(G) for v in range(G)]
+    Cm = (ctypes.c_double * (G * G))(*flat)
+    nd = (ctypes.c_int * G)(*node)
+    pr = (ctypes.c_int * G)(*peer)
+    need = ctypes.c_size_t(0)
+    _check(_lib.hoccl_debug_schedule_json(G, Cm, nd, pr, bw_intra, bw_inter, None, 0,
+                                          ctypes.byref(need)), "hoccl_debug_schedule_json")
+    buf = ctypes.create_string_buffer(need.value)
+    _check(_lib.hoccl_debug_schedule_json(G, Cm, nd, pr, bw_intra, bw_inter, buf, need.value,
+                                          ctypes.byref(need)), "hoccl_debug_schedule_json")
+    return json.loads(buf.value.decode())
+
+
+def interleave(bytes_per_flow, chunk_bytes):
+    """Flow-size-aware chunk order on one engine: list of flow indices."""
+    F = len(bytes_per_flow)
+    b = (ctypes.c_double * max(1, F))(*bytes_per_flow)
+    n = ctypes.c_size_t(0)
+    _check(_lib.hoccl_debug_interleave(F, b, chunk_bytes, None, 0, ctypes.byref(n)),
+           "hoccl_debug_interleave")
+    out = (ctypes.c_int * max(1, n.value))()
+    _check(_lib.hoccl_debug_interleave(F, b, chunk_bytes, out, n.value, ctypes.byref(n)),
+           "hoccl_debug_interleave")
+    return list(out[:n.value])
 
 
 # ---- collectives ---------------------------------------------------------------

@@ -31,6 +31,7 @@
 
 #include "hoccl_internal.h"
 #include "proxy.h"
+#include "schedule.h"
 
 namespace hoccl {
 
@@ -883,6 +884,54 @@ hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dt, int
         std::memcpy(buf, js.data(), k);
         buf[k] = 0;
     }
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_debug_schedule_json(int G, const double *C, const int *node, const int *peer,
+                                         double bw_intra, double bw_inter, char *buf, size_t len,
+                                         size_t *needed) {
+    if (G < 1 || G > 1024 || !C || !node || !peer || !(bw_intra > 0) || !(bw_inter > 0)) {
+        set_err("invalid topology or traffic matrix");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    Topology t;
+    t.G = G;
+    t.node.assign(node, node + G);
+    t.peer.assign(peer, peer + G);
+    t.bw_nvlink = bw_intra;
+    t.bw_rdma = bw_inter;
+    for (int u = 0; u < G; ++u)
+        if (t.peer[(size_t)u] < -1 || t.peer[(size_t)u] >= G) {
+            set_err("peer[%d] = %d outside [-1, G)", u, t.peer[(size_t)u]);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+    std::vector<std::vector<double>> M((size_t)G, std::vector<double>((size_t)G));
+    for (int u = 0; u < G; ++u)
+        for (int v = 0; v < G; ++v) {
+            double x = C[(size_t)u * (size_t)G + (size_t)v];
+            if (!(x >= 0)) {
+                set_err("C[%d][%d] is negative or NaN", u, v);
+                return HOCCL_ERR_INVALID_ARG;
+            }
+            M[(size_t)u][(size_t)v] = x;
+        }
+    std::string js = schedule_to_json(decompose(t, M));
+    if (needed) *needed = js.size() + 1;
+    if (buf && len) {
+        size_t k = std::min(len - 1, js.size());
+        std::memcpy(buf, js.data(), k);
+        buf[k] = 0;
+    }
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_debug_interleave(int nflows, const double *bytes, double chunk_bytes, int *order,
+                                      size_t cap, size_t *n) {
+    if (nflows < 0 || (nflows > 0 && !bytes) || !(chunk_bytes > 0) || !n) return HOCCL_ERR_INVALID_ARG;
+    std::vector<int> o = interleave_chunks(std::vector<double>(bytes, bytes + nflows), chunk_bytes);
+    *n = o.size();
+    if (order)
+        for (size_t i = 0; i < o.size() && i < cap; ++i) order[i] = o[i];
     return HOCCL_OK;
 }
 

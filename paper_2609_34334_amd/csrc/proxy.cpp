@@ -26,6 +26,7 @@
 // delivers signal callbacks (a profiler's copy-completion callbacks, for
 // one), so it is not used.
 #include "proxy.h"
+#include "schedule.h"
 
 #include <hip/hip_runtime.h>
 #include <hsa/hsa.h>
@@ -397,11 +398,36 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         eng_of_chain[(size_t)ch] = (int)best;
         load[best] += cb[(size_t)ch];
     }
+    // Issue order per engine: the chains sharing an engine are interleaved
+    // copy by copy in proportion to their length (flow-size-aware chunk
+    // scheduling), each chain keeping its own order.
+    std::vector<std::vector<size_t>> of_chain((size_t)nch);
+    for (size_t i = 0; i < copies.size(); ++i) of_chain[(size_t)copies[i].chain].push_back(i);
+    std::vector<size_t> issue;
+    issue.reserve(copies.size());
+    for (int e = 0; e < E; ++e) {
+        std::vector<int> chains;
+        std::vector<double> len;
+        for (int ch = 0; ch < nch; ++ch)
+            if (eng_of_chain[(size_t)ch] == e && !of_chain[(size_t)ch].empty()) {
+                chains.push_back(ch);
+                len.push_back((double)of_chain[(size_t)ch].size());
+            }
+        std::vector<size_t> next(chains.size(), 0);
+        for (int k : interleave_chunks(len, 1.0)) {
+            int ch = chains[(size_t)k];
+            issue.push_back(of_chain[(size_t)ch][next[(size_t)k]++]);
+        }
+    }
+    std::vector<ProxyCopy> ordered;
+    ordered.reserve(copies.size());
+    for (size_t i : issue) ordered.push_back(copies[i]);
+    op->copies = std::move(ordered);
     std::vector<int> last((size_t)nch, -1);
-    op->engine.resize(copies.size());
-    op->dep.resize(copies.size());
-    for (size_t i = 0; i < copies.size(); ++i) {
-        int ch = copies[i].chain;
+    op->engine.resize(op->copies.size());
+    op->dep.resize(op->copies.size());
+    for (size_t i = 0; i < op->copies.size(); ++i) {
+        int ch = op->copies[i].chain;
         op->engine[i] = P.engines[(size_t)eng_of_chain[(size_t)ch]];
         op->dep[i] = last[(size_t)ch];
         last[(size_t)ch] = (int)i;

@@ -363,3 +363,39 @@ def test_engine_proxy_handshakes(handshake):
         s.synchronize()
         for r in range(R):
             assert_bitwise(from_dev(out[r], hc.FP32), ref[r], f"handshake={handshake} direct={direct} r={r}")
+
+
+def test_proxy_watchdog_reports_timeout_then_recovers():
+    """Failure handling forced from the host: a 1 ms watchdog on copies that
+    take several ms.  The copies still complete (results are right), the
+    next call reports HOCCL_ERR_TIMEOUT once, and the call after that works."""
+    R, n = 8, 1 << 24
+    x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    hc.set_config(copy_path="engines", proxy_timeout_ms=1)
+    hc.allgather(x, recv)
+    torch.cuda.synchronize()
+    for r in (0, R - 1):
+        for s in range(R):
+            assert torch.equal(recv[r][s * n:(s + 1) * n], x[s])
+    with pytest.raises(hc.HocclError) as ei:
+        hc.allgather(x, recv)
+    assert ei.value.status == hc.ERR_TIMEOUT
+    torch.cuda.synchronize()
+    hc.set_config(proxy_timeout_ms=0)
+    hc.allgather(x, recv)
+    torch.cuda.synchronize()
+    assert torch.equal(recv[3][5 * n:6 * n], x[5])
+
+
+def test_finalize_and_reinit():
+    R, n = 4, 4096
+    x = [W.random_values("fp32", 98, r, n) for r in range(R)]
+    ref = oracle.allreduce_new(x, hc.FP32)
+    for _ in range(2):
+        got = run_ar(x, hc.FP32)
+        assert_bitwise(got[0], ref[0], "before finalize")
+        hc.finalize()
+    hc.init(0)
+    got = run_ar(x, hc.FP32)
+    assert_bitwise(got[3], ref[3], "after re-init")
