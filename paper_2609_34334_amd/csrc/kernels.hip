@@ -74,6 +74,9 @@ struct alignas(16) Pack {
 #ifndef HOCCL_FOLD_UNROLL
 #define HOCCL_FOLD_UNROLL 1
 #endif
+#ifndef HOCCL_FOLD_NT_OUT
+#define HOCCL_FOLD_NT_OUT 1
+#endif
 // bit 0: in0 non-temporal, bit 1: in1, bit 2: out
 constexpr int kNtFirst = (HOCCL_NT_X ? 3 : 0);
 constexpr int kNtMiddle = (HOCCL_NT_X ? 2 : 0);
@@ -243,49 +246,48 @@ __device__ __forceinline__ void fold_chunk(const FoldArgs &a, int j, int lb, int
     for (uint64_t k = tail + t; k < n; k += stride) scalar(k);
 
     constexpr bool NT = HOCCL_FOLD_NT;
+    constexpr bool NTO = HOCCL_FOLD_NT_OUT;
     if constexpr (NR > 0) {
-        // FU vectors per thread; every operand's vector is loaded before the
-        // in-order adds consume them.
-        constexpr int FU = HOCCL_FOLD_UNROLL;
-        uint64_t base = t;
-        for (; base + (uint64_t)(FU - 1) * stride < nv; base += stride * FU) {
-            P v[FU][NR];
+        // Every operand's vector is loaded before the in-order adds consume
+        // them; with HOCCL_FOLD_UNROLL == 2 two vectors per thread are in
+        // flight (two separate arrays: a 2-D array is not kept in registers).
+        auto store = [&](uint64_t i, const P &y) {
+            for (int q = 0; q < nout; ++q) stp<NTO>((P *)(dst(q) + h) + i, y);
+        };
+        // Written out (no helper taking the array) so that the operand
+        // arrays stay in registers.
+#define HOCCL_FOLD_ARRAY(ARR, OUT)                                               \
+    P OUT;                                                                       \
+    {                                                                            \
+        A acc[VE];                                                               \
+        _Pragma("unroll") for (int e = 0; e < VE; ++e) acc[e] = T::widen(ARR[0].v[e]); \
+        _Pragma("unroll") for (int k = 1; k < NR; ++k)                            \
+            _Pragma("unroll") for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(ARR[k].v[e]); \
+        _Pragma("unroll") for (int e = 0; e < VE; ++e) OUT.v[e] = T::narrow(acc[e]); \
+    }
+        uint64_t i = t;
+        if constexpr (HOCCL_FOLD_UNROLL == 2) {
+            for (; i + stride < nv; i += 2 * stride) {
+                P va[NR], vb[NR];
 #pragma unroll
-            for (int u = 0; u < FU; ++u)
-#pragma unroll
-                for (int k = 0; k < NR; ++k) v[u][k] = ldp<NT>((const P *)(src(k) + h) + base + u * stride);
-#pragma unroll
-            for (int u = 0; u < FU; ++u) {
-                A acc[VE];
-#pragma unroll
-                for (int e = 0; e < VE; ++e) acc[e] = T::widen(v[u][0].v[e]);
-#pragma unroll
-                for (int k = 1; k < NR; ++k)
-#pragma unroll
-                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[u][k].v[e]);
-                P y;
-#pragma unroll
-                for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
-                for (int q = 0; q < nout; ++q) ((P *)(dst(q) + h))[base + u * stride] = y;
+                for (int k = 0; k < NR; ++k) {
+                    va[k] = ldp<NT>((const P *)(src(k) + h) + i);
+                    vb[k] = ldp<NT>((const P *)(src(k) + h) + i + stride);
+                }
+                HOCCL_FOLD_ARRAY(va, ya)
+                HOCCL_FOLD_ARRAY(vb, yb)
+                store(i, ya);
+                store(i + stride, yb);
             }
         }
-        for (int u = 0; u < FU; ++u) {
-            uint64_t i = base + u * stride;
-            if (i >= nv) break;
-            A acc[VE];
-            P v0 = ldp<NT>((const P *)(src(0) + h) + i);
+        for (; i < nv; i += stride) {
+            P v[NR];
 #pragma unroll
-            for (int e = 0; e < VE; ++e) acc[e] = T::widen(v0.v[e]);
-            for (int k = 1; k < NR; ++k) {
-                P v = ldp<NT>((const P *)(src(k) + h) + i);
-#pragma unroll
-                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v.v[e]);
-            }
-            P y;
-#pragma unroll
-            for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
-            for (int q = 0; q < nout; ++q) ((P *)(dst(q) + h))[i] = y;
+            for (int k = 0; k < NR; ++k) v[k] = ldp<NT>((const P *)(src(k) + h) + i);
+            HOCCL_FOLD_ARRAY(v, y)
+            store(i, y);
         }
+#undef HOCCL_FOLD_ARRAY
         return;
     }
     for (uint64_t i = t; i < nv; i += stride) {
@@ -329,8 +331,11 @@ __device__ __forceinline__ const A &kernargs() {
     return *(const A *)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
+#ifndef HOCCL_FOLD_LB
+#define HOCCL_FOLD_LB 1024
+#endif
 template <class T, int VE, int NR>
-__global__ void __launch_bounds__(1024) fold_kernel(FoldArgs) {
+__global__ void __launch_bounds__(HOCCL_FOLD_LB) fold_kernel(FoldArgs) {
     const FoldArgs &a = kernargs<FoldArgs>();
     for_each_segment(a.R, [&](int j, int lb, int nb) { fold_chunk<T, VE, NR>(a, j, lb, nb); });
 }
