@@ -158,3 +158,12 @@ def a2a_tokens(R=8, tokens=4096, hidden=2048, experts=64, topk=6):
             for s in range(R)]
     recv_sizes = [sum(counts[s * R + d] for s in range(R)) for d in range(R)]
     return send, counts, sdispls, rdispls, recv_sizes
+
+
+def device_normal_bf16(seed, rank, n, std=1.0):
+    """Seeded normal(0, std) bf16 values generated on the current GPU (for
+    inputs too large to draw on the host); returns a torch tensor."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed * 1_000_003 + rank)
+    return (torch.randn(n, generator=g, device="cuda") * std).to(torch.bfloat16)
+
