@@ -291,7 +291,7 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
                  ms=round(med * 1e3, 4), copy_GBs=round(st["copy_bytes"] / med / 1e9, 1),
                  hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
                  path_used=["auto", "sdma", "engines", "kernel"][st["copy_path_used"]],
-                 cus_used=st["cus_used_max"])
+                 cus_used=st["cus_used_max"], host_enqueue_us=round(st["host_enqueue_us"], 1))
         if gemm is not None:
             r["gemm_slowdown"], r["gemm_overlap"] = gemm_slowdown(hc, run, med, gemm)
         res[name] = r
@@ -567,6 +567,7 @@ def main():
         "hbm_frac": round(rs["bytes_per_op"] / rs["sec"] / 1e9 / HBM_PEAK_GBS, 4),
         "cus_used": st["cus_used_max"],
         "cus_available": st["cus_available"],
+        "host_enqueue_us": round(st["host_enqueue_us"], 1),
         "parity_vs_oracle": parity,
         "roofline": {"bound": "hbm", "kernel": "reduce_step_kernel (ring step, all 8 ranks per launch)",
                      "achieved": round(rs["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -8,3 +8,8 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+    # Build the library only when nothing is built yet (after a source
+    # change, build again explicitly: __graft_entry__.build()).
+    if not os.path.exists(os.path.join(ROOT, "paper_2609_34334_amd", "libhoccl.so")):
+        import __graft_entry__
+        __graft_entry__.build()
