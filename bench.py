@@ -435,6 +435,49 @@ def bench_rs_workgroups(hc, x, reps):
     return out
 
 
+def size_sweep(hc):
+    """algbw against message size, 2 MiB .. 1 GiB, as in the paper's
+    microbenchmarks: send/recv (one message 0 -> 1), all-gather and
+    all-to-all over R = 8 (size = bytes each rank receives), per copy path,
+    and the CU copy kernel at 8 and 256 workgroups."""
+    import torch
+    R = 8
+    sizes = [2 << 20, 8 << 20, 32 << 20, 128 << 20, 512 << 20, 1 << 30]
+    paths = [("sdma", {}), ("engines", {}), ("kernel_wg8", {"workgroups_per_step": 8}),
+             ("kernel_wg256", {"workgroups_per_step": 256})]
+    out = {"sendrecv": [], "allgather": [], "alltoall": []}
+    big = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    big2 = torch.empty_like(big)
+    for sz in sizes:
+        row = {"bytes": sz}
+        for name, kw in paths:
+            hc.set_config(copy_path=name.split("_")[0], **kw)
+            s0, d1 = big[:sz].view(torch.int32), big2[:sz].view(torch.int32)
+            med, _ = event_time(lambda: hc.sendrecv([s0, s0], [d1, d1], [1, -1]), 5)
+            row[name] = round(sz / med / 1e9, 1)
+            hc.set_config(copy_path="auto", workgroups_per_step=0)
+        out["sendrecv"].append(row)
+    del big, big2
+    for op in ("allgather", "alltoall"):
+        for sz in sizes:
+            n = sz // 4 // R
+            send = [torch.zeros(n if op == "allgather" else R * n, dtype=torch.int32, device="cuda")
+                    for _ in range(R)]
+            recv = [torch.empty(R * n, dtype=torch.int32, device="cuda") for _ in range(R)]
+            row = {"bytes": R * n * 4}
+            for name, kw in paths:
+                hc.set_config(copy_path=name.split("_")[0], **kw)
+                fn = (lambda: hc.allgather(send, recv)) if op == "allgather" else \
+                     (lambda: hc.alltoall(send, recv))
+                med, _ = event_time(fn, 3, warmup=1)
+                row[name] = round(R * n * 4 / med / 1e9, 1)
+                hc.set_config(copy_path="auto", workgroups_per_step=0)
+            out[op].append(row)
+            del send, recv
+            torch.cuda.empty_cache()
+    return out
+
+
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "reduce_step_kernel_rs_bf16_R8_traffic.txt")
 
 
@@ -461,6 +504,30 @@ def measured_traffic():
         return int(float(kv["traffic_bytes_per_launch"]))
     except (KeyError, ValueError):
         return None
+
+
+def copy_workload(hc, W):
+    """What the zero-CU trace profiles: the FSDP all-gather, the EP
+    all-to-all(v) and one PP send/recv round, once each on the default (AUTO)
+    copy path, after the inputs are resident."""
+    import torch
+    R = 8
+    ag = [bf16_dev(a) for a in W.ag_parameters(R)]
+    send_np, counts, sd, rd, rsz = W.a2a_tokens(R)
+    a2a = [bf16_dev(a) for a in send_np]
+    a2a_out = [torch.empty(s, dtype=torch.bfloat16, device="cuda") for s in rsz]
+    act = [bf16_dev(a) for a in W.p2p_activations(R)]
+    act_out = [torch.empty_like(t) for t in act]
+    torch.cuda.synchronize()
+    marker = torch.cuda.Event()
+    hc.set_config(copy_path="auto")
+    ag_out = hc.allgather(ag)
+    hc.alltoallv(a2a, counts, sd, a2a_out, rd)
+    hc.sendrecv(act, act_out, [r + 1 if r + 1 < R else -1 for r in range(R)])
+    marker.record()
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_workload": "done", "copy_ops": hc.last_stats()["copy_ops"],
+                      "allgather_bytes": sum(t.numel() * 2 for t in ag_out)}))
 
 
 def pmc_workload(hc, W):
@@ -491,6 +558,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--pmc-workload", action="store_true",
                     help="run only the workload the counter profiles are taken on")
+    ap.add_argument("--sweep", action="store_true",
+                    help="print algbw against message size per copy path instead")
+    ap.add_argument("--copy-workload", action="store_true",
+                    help="run only the copy collectives the zero-CU trace is taken on")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -508,6 +579,12 @@ def main():
     hc.init(0)
     if args.pmc_workload:
         pmc_workload(hc, W)
+        return
+    if args.copy_workload:
+        copy_workload(hc, W)
+        return
+    if args.sweep:
+        print(json.dumps({"sweep": size_sweep(hc)}), flush=True)
         return
     log("reduce-scatter headline")
     rs = bench_reduce_scatter(hc, W, args.steps, args.warmup)

@@ -49,6 +49,19 @@
  *   copy / handshake streams, in the order the calls were issued: a call
  *   must not wait, through the caller's own stream dependencies, for a call
  *   issued after it.
+ * Stream capture.  A call on a stream that is capturing into a HIP graph
+ *   records its kernels, SDMA copies and events (never a memset) and
+ *   allocates nothing, so it returns HOCCL_ERR_UNSUPPORTED, enqueuing
+ *   nothing, when it would have to: as the first call on a device (which
+ *   creates the library's streams and probes the engines), when it needs a
+ *   larger workspace than the library holds, or when its copies would take
+ *   the SDMA_ENGINES path (a host thread issues those).  Make the same call
+ *   once outside capture first.  A workspace a graph captured stays
+ *   allocated until hoccl_finalize, after which the graph must not be
+ *   replayed.  Replays share it with the device's other workspace users
+ *   (ring reduce-scatter and all-reduce over more than two ranks) and are
+ *   not ordered with them by the library: a replay must not overlap another
+ *   such call or replay.  Kernel timing skips captured calls.
  * In-place forms (the only allowed overlaps between send and recv):
  *   all-reduce      send[r] == recv[r];
  *   all-gather      send[r] == recv[r] + r * sendcount elements;

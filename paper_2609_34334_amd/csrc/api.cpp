@@ -55,7 +55,8 @@ struct DeviceState {
     size_t ws_cap = 0;
     hipEvent_t ws_event = nullptr;
     hipStream_t ws_last_stream = nullptr;
-    bool ws_used = false;
+    bool ws_captured = false;        // a graph captured the current workspace
+    std::vector<void *> ws_retired;  // older workspaces captured graphs may replay into
     std::vector<TimingPair> timing_pool;
     size_t timing_used = 0;
     Proxy *proxy = nullptr;
@@ -177,6 +178,7 @@ void destroy_state(DeviceState *st) {
     for (auto e : st->ev_join) (void)hipEventDestroy(e);
     if (st->ws_event) (void)hipEventDestroy(st->ws_event);
     if (st->ws) (void)hipFree(st->ws);
+    for (void *w : st->ws_retired) (void)hipFree(w);
     for (auto &tp : st->timing_pool) {
         (void)hipEventDestroy(tp.a);
         (void)hipEventDestroy(tp.b);
@@ -229,7 +231,9 @@ hoccl_status_t create_state(int device, DeviceState **out) {
     return HOCCL_OK;
 }
 
-hoccl_status_t get_state(DeviceState **out) {
+// `capturing`: the caller's stream is capturing a graph.  Creating the state
+// then would synchronise the device and allocate, so it is refused.
+hoccl_status_t get_state(DeviceState **out, bool capturing = false) {
     int dev = 0;
     HIP_TRY(hipGetDevice(&dev));
     std::lock_guard<std::mutex> lk(g_mu);
@@ -238,6 +242,11 @@ hoccl_status_t get_state(DeviceState **out) {
     if (it != g_states.end()) {
         *out = it->second;
         return HOCCL_OK;
+    }
+    if (capturing) {
+        set_err("the library is not initialised on device %d and cannot be during stream "
+                "capture: call hoccl_init (or any collective) outside capture first", dev);
+        return HOCCL_ERR_UNSUPPORTED;
     }
     DeviceState *st = nullptr;
     TRY(create_state(dev, &st));
@@ -265,11 +274,28 @@ inline void *resolve(const BufRef &b, const Buffers &B) {
     }
 }
 
-hoccl_status_t ensure_ws(DeviceState &st, size_t bytes) {
-    if (bytes <= st.ws_cap) return HOCCL_OK;
+// During stream capture nothing is allocated: the call needs a workspace
+// that an earlier call outside capture already made large enough.  A
+// workspace a graph has captured is never freed before finalize, since any
+// replay of that graph still writes into it.
+hoccl_status_t ensure_ws(DeviceState &st, size_t bytes, bool capturing) {
+    if (bytes <= st.ws_cap) {
+        st.ws_captured = st.ws_captured || capturing;
+        return HOCCL_OK;
+    }
+    if (capturing) {
+        set_err("this call needs a %zu-byte workspace but %zu bytes are allocated, and the "
+                "workspace cannot grow during stream capture: make the same call once "
+                "outside capture first", bytes, st.ws_cap);
+        return HOCCL_ERR_UNSUPPORTED;
+    }
     // Growing the workspace waits for every user of the old one.
     HIP_TRY(hipDeviceSynchronize());
-    if (st.ws) HIP_TRY(hipFree(st.ws));
+    if (st.ws && st.ws_captured)
+        st.ws_retired.push_back(st.ws);
+    else if (st.ws)
+        HIP_TRY(hipFree(st.ws));
+    st.ws_captured = false;
     st.ws = nullptr;
     st.ws_cap = 0;
     st.ws_last_stream = nullptr;
@@ -493,11 +519,16 @@ size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, const 
 template <typename Build>
 hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_t s) {
     auto t0 = std::chrono::steady_clock::now();
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(s, &cap));
+    const bool capturing = cap != hipStreamCaptureStatusNone;
     DeviceState *stp = nullptr;
-    TRY(get_state(&stp));
+    TRY(get_state(&stp, capturing));
     DeviceState &st = *stp;
     hoccl_config_t cfg = config();
     std::memset(&t_stats, 0, sizeof t_stats);
+    // Timing events of a captured call would be recorded only on replay.
+    if (capturing) cfg.kernel_timing = 0;
     Buffers B = B0;
     PlanOptions opt = options_from(cfg, in_place);
     Plan p = build(opt);
@@ -514,13 +545,23 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
         set_err("%s", st.proxy_why.c_str());
         return HOCCL_ERR_UNSUPPORTED;
     }
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && capturing) {
+        // The proxy thread issues the copies at call time; a graph replay
+        // would run the handshake without them.
+        set_err("the SDMA_ENGINES copy path cannot be captured into a graph: its copies are "
+                "issued by a host thread");
+        return HOCCL_ERR_UNSUPPORTED;
+    }
     const bool has_kernels = !p.reduce_steps.empty() || p.has_fold;
     const bool has_copies = !p.copies.empty();
 
     if (p.ws_bytes) {
-        TRY(ensure_ws(st, p.ws_bytes));
+        TRY(ensure_ws(st, p.ws_bytes, capturing));
         B.ws = st.ws;
-        if (st.ws_last_stream && st.ws_last_stream != s)
+        // Calls outside capture are chained through ws_event.  A captured
+        // call joins no such chain: the order of its replays against other
+        // users of the workspace is the caller's.
+        if (!capturing && st.ws_last_stream && st.ws_last_stream != s)
             HIP_TRY(hipStreamWaitEvent(s, st.ws_event, 0));
     }
 
@@ -545,7 +586,7 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
                 TRY(run_copies_sdma(st, cfg, p, B, s));
         }
     }
-    if (p.ws_bytes) {
+    if (p.ws_bytes && !capturing) {
         HIP_TRY(hipEventRecord(st.ws_event, s));
         st.ws_last_stream = s;
     }
