@@ -140,15 +140,17 @@ typedef struct {
                                    copy kernel launch (hoccl_get_kernel_times) */
     unsigned int proxy_timeout_ms; /* watchdog of the SDMA_ENGINES proxy;
                                    0 = 10000                                   */
-    int proxy_handshake;        /* where the SDMA_ENGINES start/finish flag
-                                   handshake (hipStreamWriteValue32 /
-                                   hipStreamWaitValue32) runs.  This HIP runs
-                                   those as kernels and the wait spins on a CU
-                                   while the copies run, holding back its
-                                   hardware queue.  0 (default): on a private
-                                   stream masked to one CU (its own hardware
-                                   queue), joined to the caller's stream by
-                                   events; 1: on the caller's stream itself  */
+    int proxy_handshake;        /* where the stream side of the SDMA_ENGINES
+                                   start/finish flag handshake runs: one
+                                   dispatch of a one-lane kernel that waits
+                                   on a CU while the copies run.
+                                   0 (default): on the caller's stream, the
+                                   paper's form (4 KiB send/recv: 21 us);
+                                   1: on a private CU-masked stream with a
+                                   hardware queue of its own, joined to the
+                                   caller's stream by events (86 us), so the
+                                   wait never holds back the caller's
+                                   hardware queue                              */
 } hoccl_config_t;
 
 typedef struct {

@@ -145,7 +145,7 @@ void load_config_locked() {
     c.allgather_direct = (int)env_long("HOCCL_AG_DIRECT", c.allgather_direct);
     c.allreduce_chunk_groups = (int)env_long("HOCCL_AR_GROUPS", c.allreduce_chunk_groups);
     c.kernel_timing = (int)env_long("HOCCL_KERNEL_TIMING", c.kernel_timing);
-    c.proxy_handshake = (int)env_long("HOCCL_PROXY_ON_CALLER", c.proxy_handshake);
+    c.proxy_handshake = (int)env_long("HOCCL_PROXY_HANDSHAKE", c.proxy_handshake);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "sdma")) c.copy_path = HOCCL_COPY_SDMA;
         else if (!std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA_ENGINES;
@@ -494,10 +494,12 @@ hoccl_status_t run_copies_kernel(DeviceState &st, const hoccl_config_t &cfg, con
 
 // Copy path for a plan.  An explicit choice wins; AUTO is the HIP runtime's
 // device-to-device SDMA path.  It is the only one that is free of compute
-// units end to end: the engine proxy moves data on SDMA engines too, but its
-// stream handshake needs hipStreamWaitValue32, which this HIP executes as a
-// spinning one-thread kernel, and a concurrent full-occupancy GEMM measured
-// 61% slower beside it (1.8% beside the HIP path, 81% beside the CU copy).
+// units end to end: the engine proxy moves data on SDMA engines too, but the
+// stream has to wait for a CPU thread, and this HIP offers no such wait
+// without a resident wave (its stream memory operations are spinning
+// kernels even on signal memory).  One resident wave alone slows a
+// full-occupancy bf16 GEMM by about half, beside which the HIP path costs
+// nothing measurable.
 hoccl_copy_path_t resolve_path(const DeviceState &, const hoccl_config_t &cfg, const Plan &) {
     return cfg.copy_path == HOCCL_COPY_AUTO ? HOCCL_COPY_SDMA : cfg.copy_path;
 }
@@ -574,7 +576,7 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
         hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                            cfg.proxy_handshake == 1, s, &ne, t_err);
+                                            cfg.proxy_handshake == 0, s, &ne, t_err);
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {

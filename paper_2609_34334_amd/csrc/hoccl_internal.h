@@ -159,10 +159,22 @@ struct FoldArgs {
     int out_at_chunk;
 };
 
+// The stream side of one proxy operation's start/finish handshake.  The
+// three flags are host memory mapped for the device.
+struct HandshakeArgs {
+    uint32_t *start;        // the kernel writes start_value; the proxy clears it
+    uint32_t *finish;       // the proxy writes finish_value; the kernel clears it
+    uint32_t *status;       // the kernel writes 1 here if it gave up waiting
+    uint32_t start_value;
+    uint32_t finish_value;
+    uint64_t limit_ticks;   // give up after this many device wall-clock ticks
+};
+
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg,
                               int threads, hipStream_t s);
 hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
                        hipStream_t s);
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s);
+hipError_t launch_handshake(const HandshakeArgs &a, hipStream_t s);
 
 }  // namespace hoccl

@@ -10,22 +10,23 @@
 //   proxy:   see start == START, write start := 0 (acknowledge),
 //            run the copies, write finish := FINISH, see finish == 0.
 //
-// With the HIP runtime used here, hipStreamWaitValue32 and
-// hipStreamWriteValue32 are executed by small kernels, and the wait kernel
-// spins on a compute unit for as long as the copies take, holding back every
-// later packet of its hardware queue -- including kernels of other streams
-// that share the queue.  So by default the handshake runs on a private
-// stream created with a one-CU mask: such a stream gets a hardware queue of
-// its own, the spinning wait is confined to one compute unit, and the
-// caller's stream joins the private one through HIP events (fork before the
-// start path, join after the completion path).  The handshake can also be
-// put on the caller's stream directly, the paper's literal form.
+// The stream's side runs as one dispatch of a one-lane handshake kernel
+// that performs all four flag operations in order, sleeping between polls
+// (HIP's own stream memory operations are separate spinning kernels here,
+// one dispatch each).  While the copies run, that lane occupies a wave slot
+// and holds back every later packet of its hardware queue -- including
+// kernels of other streams sharing the queue.  So by default it runs on a
+// private stream created with a CU mask: such a stream gets a hardware queue
+// of its own, and the caller's stream joins it through HIP events (fork
+// before the start path, join after the completion path).  The handshake can
+// also be put on the caller's stream directly, the paper's literal form.
 //
 // A host function (hipLaunchHostFunc) that blocks until the copies are done
 // would need no GPU code at all, but it blocks the runtime thread that also
 // delivers signal callbacks (a profiler's copy-completion callbacks, for
 // one), so it is not used.
 #include "proxy.h"
+#include "hoccl_internal.h"
 #include "schedule.h"
 
 #include <hip/hip_runtime.h>
@@ -51,6 +52,7 @@ constexpr uint32_t kStartValue = 0x53544152u;   // written by the stream
 constexpr uint32_t kFinishValue = 0x46494e49u;  // written by the proxy
 constexpr int kSlots = 64;
 constexpr size_t kLine = 64;  // one cache line per flag
+constexpr int kFlagsPerSlot = 3;  // start, finish, status
 
 struct FindAgent {
     uint32_t bdf;
@@ -144,7 +146,8 @@ class ProxyImpl {
   public:
     hsa_agent_t agent{};
     std::vector<uint32_t> engines;  // id bits of usable engines
-    uint32_t *flags = nullptr;      // kSlots * 2 flags, one per cache line
+    uint32_t *flags = nullptr;      // kSlots * kFlagsPerSlot flags, one per cache line
+    uint64_t ticks_per_ms = 100000;  // device wall clock
     hipStream_t hs = nullptr;       // private one-CU stream for the handshake
     hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     std::mutex mu;
@@ -157,10 +160,12 @@ class ProxyImpl {
     hoccl_status_t sticky = HOCCL_OK;
     std::string sticky_msg;
 
-    volatile uint32_t *start_flag(int s) { return (volatile uint32_t *)((char *)flags + (2 * s) * kLine); }
-    volatile uint32_t *finish_flag(int s) {
-        return (volatile uint32_t *)((char *)flags + (2 * s + 1) * kLine);
+    volatile uint32_t *flag(int s, int k) {
+        return (volatile uint32_t *)((char *)flags + (size_t)(kFlagsPerSlot * s + k) * kLine);
     }
+    volatile uint32_t *start_flag(int s) { return flag(s, 0); }
+    volatile uint32_t *finish_flag(int s) { return flag(s, 1); }
+    volatile uint32_t *status_flag(int s) { return flag(s, 2); }
 
     void fail(hoccl_status_t st, const char *msg) {
         std::lock_guard<std::mutex> lk(mu);
@@ -256,8 +261,16 @@ class ProxyImpl {
                     }
                     break;
                 case ProxyOp::WAIT_ACK:
-                    // The stream reset `finish`: the slot may be reused.
+                    // The stream reset `finish`: the slot may be reused.  If
+                    // the handshake kernel gave up waiting it never will;
+                    // the slot is free then too, and the error is reported.
                     if (load_flag(finish_flag(op->slot)) == 0) {
+                        release(op);
+                        retired = true;
+                        progress = true;
+                    } else if (load_flag(status_flag(op->slot)) != 0) {
+                        fail(HOCCL_ERR_TIMEOUT, "the stream stopped waiting for the SDMA copies "
+                                                "before they completed");
                         release(op);
                         retired = true;
                         progress = true;
@@ -319,14 +332,17 @@ Proxy *Proxy::create(int device, std::string *why) {
     for (int b = 0; b < 2; ++b)
         if (mask & (1u << b)) p->engines.push_back(1u << b);
     void *fl = nullptr;
-    he = hipHostMalloc(&fl, kSlots * 2 * kLine, hipHostMallocCoherent | hipHostMallocMapped);
+    he = hipHostMalloc(&fl, kSlots * kFlagsPerSlot * kLine, hipHostMallocCoherent | hipHostMallocMapped);
     if (he != hipSuccess || !fl) {
         delete p;
         hsa_shut_down();
         return fail("hipHostMalloc of the flag pool failed", (long)he);
     }
-    std::memset(fl, 0, kSlots * 2 * kLine);
+    std::memset(fl, 0, kSlots * kFlagsPerSlot * kLine);
     p->flags = (uint32_t *)fl;
+    int khz = 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, device) == hipSuccess && khz > 0)
+        p->ticks_per_ms = (uint64_t)khz;
     // A CU-masked stream owns a hardware queue.  The runtime accepts masks
     // only with at least one CU in every XCD; logical CUs 0-7 are one per
     // XCD on MI355X, so the mask is 0xff (the wait kernel itself is a single
@@ -481,20 +497,28 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         }
         hs = P.hs;
     }
-    void *st = (void *)P.start_flag(op->slot);
-    void *fi = (void *)P.finish_flag(op->slot);
-    hipError_t e = hipStreamWriteValue32(hs, st, kStartValue, 0);
+    // One dispatch carries the stream's whole side of the handshake.  It
+    // stops waiting after twice the proxy timeout plus a second, so the
+    // stream drains even if the proxy never answers; the proxy's own
+    // watchdog reports first.
+    store_flag(P.status_flag(op->slot), 0);
+    HandshakeArgs ha;
+    ha.start = (uint32_t *)P.start_flag(op->slot);
+    ha.finish = (uint32_t *)P.finish_flag(op->slot);
+    ha.status = (uint32_t *)P.status_flag(op->slot);
+    ha.start_value = kStartValue;
+    ha.finish_value = kFinishValue;
+    ha.limit_ticks = (2ull * op->timeout_ms + 1000ull) * P.ticks_per_ms;
+    hipError_t e = launch_handshake(ha, hs);
     if (e != hipSuccess) {
         // Nothing of the handshake reached a stream: give everything back.
-        err = std::string("hipStreamWriteValue32 failed: ") + hipGetErrorString(e);
+        (void)hipGetLastError();
+        err = std::string("handshake launch failed: ") + hipGetErrorString(e);
         give_back();
         return HOCCL_ERR_HIP;
     }
-    if ((e = hipStreamWaitValue32(hs, st, 0, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
-        (e = hipStreamWaitValue32(hs, fi, kFinishValue, hipStreamWaitValueEq, 0xffffffffu)) != hipSuccess ||
-        (e = hipStreamWriteValue32(hs, fi, 0, 0)) != hipSuccess ||
-        (hs != s && ((e = hipEventRecord(P.ev_join, hs)) != hipSuccess ||
-                     (e = hipStreamWaitEvent(s, P.ev_join, 0)) != hipSuccess))) {
+    if (hs != s && ((e = hipEventRecord(P.ev_join, hs)) != hipSuccess ||
+                    (e = hipStreamWaitEvent(s, P.ev_join, 0)) != hipSuccess)) {
         // Whatever part of the handshake reached the stream, the proxy must
         // still see the op through, so hand it over regardless and report.
         err = std::string("stream memory operation failed: ") + hipGetErrorString(e);

@@ -338,10 +338,10 @@ def test_back_to_back_calls_on_two_streams_share_workspace_safely():
 
 @pytest.mark.parametrize("handshake", [0, 1])
 def test_engine_proxy_handshakes(handshake):
-    """Both ways of ordering the engine proxy with the stream: a host
-    function (default) and the start/finish flag handshake through stream
-    memory operations.  Checked behind a delayed producer, with a consumer
-    queued after the collective, and for ring chains (dependent hops)."""
+    """Both places of the engine proxy's start/finish flag handshake: on
+    the caller's stream (default) and on the proxy's private stream joined
+    by events.  Checked behind a delayed producer, with a consumer queued
+    after the collective, and for ring chains (dependent hops)."""
     hc.set_config(copy_path="engines", proxy_handshake=handshake)
     R, n = 4, 1 << 20
     x = [W.random_values("fp32", 97, r, n) for r in range(R)]
