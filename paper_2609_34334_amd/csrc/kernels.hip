@@ -8,10 +8,8 @@
 //   in the ring order in one pass (same result bit for bit, fewer bytes).
 // * copy_kernel        -- a CU copy of many independent (src, dst, bytes)
 //   segments; the comparator for the SDMA copy path.
-// * handshake_kernel   -- the stream side of the copy proxy's start/finish
-//   flag handshake, one lane of one wave.
 //
-// The first three are HBM-bound streams (about one add per 8-12 bytes), so they
+// All three are HBM-bound streams (about one add per 8-12 bytes), so they
 // use 16-byte vector loads and stores, a grid-stride loop over each segment
 // with several independent vectors in flight per thread, and no LDS and no
 // MFMA: the limit is memory bandwidth, not arithmetic.
@@ -389,42 +387,6 @@ __global__ void __launch_bounds__(1024) copy_kernel(CopyArgs) {
     for_each_segment(a.nseg, [&](int seg, int lb, int nb) { copy_segment<2>(a.seg[seg], lb, nb); });
 }
 
-// ---- handshake ----------------------------------------------------------------
-// The Stream Manager section's handshake, seen from the stream, in a single
-// dispatch: publish START once everything before it is visible to the copy
-// engines (a system-scope release), wait until the proxy acknowledges by
-// clearing START, wait until it writes FINISH after the copies completed,
-// then acquire at system scope (later work sees the copied bytes) and clear
-// FINISH.  Every flag access is a system-scope vector atomic on host memory.
-// The lane sleeps between polls, and both waits give up once limit_ticks of
-// the constant-rate device wall clock have passed, recording that in
-// *status, so the dispatch always ends.
-__device__ inline uint32_t poll_flag(uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-}
-
-__device__ inline bool wait_flag(uint32_t *p, uint32_t want, uint64_t t0, uint64_t limit) {
-    while (poll_flag(p) != want) {
-        if ((uint64_t)wall_clock64() - t0 > limit) return false;
-        __builtin_amdgcn_s_sleep(4);
-    }
-    return true;
-}
-
-__global__ void __launch_bounds__(64) handshake_kernel(HandshakeArgs) {
-    const HandshakeArgs &a = kernargs<HandshakeArgs>();
-    if (threadIdx.x != 0) return;
-    __hip_atomic_store(a.start, a.start_value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-    const uint64_t t0 = (uint64_t)wall_clock64();
-    if (!wait_flag(a.start, 0u, t0, a.limit_ticks) ||
-        !wait_flag(a.finish, a.finish_value, t0, a.limit_ticks)) {
-        __hip_atomic_store(a.status, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-        return;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-    __hip_atomic_store(a.finish, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-}
-
 }  // namespace
 
 // ---- launchers --------------------------------------------------------------------
@@ -490,10 +452,6 @@ hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
 
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s) {
     return launch((const void *)copy_kernel, a, wg, threads, s);
-}
-
-hipError_t launch_handshake(const HandshakeArgs &a, hipStream_t s) {
-    return launch((const void *)handshake_kernel, a, 1, 64, s);
 }
 
 }  // namespace hoccl
