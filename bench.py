@@ -549,6 +549,32 @@ def pmc_workload(hc, W):
     print(json.dumps({"pmc_workload": "done", "kernels_hip_sha256_16": kernel_source_hash()}))
 
 
+def occupancy_workload(hc, W):
+    """What the occupancy counter pass profiles, in this order: the headline
+    reduce-scatter three times at each workgroup budget 8, 16, 64, 256 and
+    automatic (7 ring-step launches each), then a 512 MiB CU-kernel copy at
+    8 workgroups and at the automatic budget."""
+    import torch
+    R, n_in = 8, 25_165_824
+    send = [bf16_dev(a) for a in W.rs_gradients(R, n_in)]
+    recv = [torch.empty(n_in // R, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    budgets = [8, 16, 64, 256, 0]
+    for wg in budgets:
+        with hc.config(workgroups_per_step=wg):
+            for _ in range(3):
+                hc.reduce_scatter(send, recv)
+    torch.cuda.synchronize()
+    del send, recv
+    src = torch.empty(1 << 27, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for wg in (8, 0):
+        with hc.config(copy_path="kernel", workgroups_per_step=wg):
+            hc.sendrecv([src], [dst], [0])
+    torch.cuda.synchronize()
+    print(json.dumps({"occupancy_workload": "done", "rs_budgets": budgets, "copy_budgets": [8, 0],
+                      "kernels_hip_sha256_16": kernel_source_hash()}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -558,6 +584,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--pmc-workload", action="store_true",
                     help="run only the workload the counter profiles are taken on")
+    ap.add_argument("--occupancy-workload", action="store_true",
+                    help="run only the workload the occupancy counter pass is taken on")
     ap.add_argument("--sweep", action="store_true",
                     help="print algbw against message size per copy path instead")
     ap.add_argument("--copy-workload", action="store_true",
@@ -579,6 +607,9 @@ def main():
     hc.init(0)
     if args.pmc_workload:
         pmc_workload(hc, W)
+        return
+    if args.occupancy_workload:
+        occupancy_workload(hc, W)
         return
     if args.copy_workload:
         copy_workload(hc, W)
