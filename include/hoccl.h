@@ -151,6 +151,11 @@ typedef struct {
                                    caller's stream by events (86 us), so the
                                    wait never holds back the caller's
                                    hardware queue                              */
+    unsigned int proxy_wait_limit_us; /* the handshake kernel stops waiting
+                                   after this long, so its dispatch always
+                                   ends; the proxy then reports
+                                   HOCCL_ERR_TIMEOUT at the next SDMA_ENGINES
+                                   call.  0 = 2 * proxy_timeout_ms + 1 s       */
 } hoccl_config_t;
 
 typedef struct {

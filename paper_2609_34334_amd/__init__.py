@@ -47,7 +47,8 @@ class Config(ctypes.Structure):
                 ("reduce_algo", ctypes.c_int),
                 ("kernel_timing", ctypes.c_int),
                 ("proxy_timeout_ms", ctypes.c_uint),
-                ("proxy_handshake", ctypes.c_int)]
+                ("proxy_handshake", ctypes.c_int),
+                ("proxy_wait_limit_us", ctypes.c_uint)]
 
 
 class Stats(ctypes.Structure):

@@ -107,6 +107,7 @@ hoccl_config_t default_config() {
     c.kernel_timing = 0;
     c.proxy_timeout_ms = 10000;
     c.proxy_handshake = 0;
+    c.proxy_wait_limit_us = 0;
     return c;
 }
 
@@ -146,6 +147,7 @@ void load_config_locked() {
     c.allreduce_chunk_groups = (int)env_long("HOCCL_AR_GROUPS", c.allreduce_chunk_groups);
     c.kernel_timing = (int)env_long("HOCCL_KERNEL_TIMING", c.kernel_timing);
     c.proxy_handshake = (int)env_long("HOCCL_PROXY_HANDSHAKE", c.proxy_handshake);
+    c.proxy_wait_limit_us = (unsigned)env_long("HOCCL_PROXY_WAIT_LIMIT_US", c.proxy_wait_limit_us);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "sdma")) c.copy_path = HOCCL_COPY_SDMA;
         else if (!std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA_ENGINES;
@@ -576,7 +578,8 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
         hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                            cfg.proxy_handshake == 0, s, &ne, t_err);
+                                            cfg.proxy_wait_limit_us, cfg.proxy_handshake == 0, s,
+                                            &ne, t_err);
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {

@@ -379,8 +379,8 @@ Proxy::~Proxy() {
 int Proxy::engine_count() const { return (int)impl_->engines.size(); }
 
 hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                             unsigned timeout_ms, bool on_caller, hipStream_t s, int *engines_used,
-                             std::string &err) {
+                             unsigned timeout_ms, unsigned wait_limit_us, bool on_caller,
+                             hipStream_t s, int *engines_used, std::string &err) {
     ProxyImpl &P = *impl_;
     {
         std::lock_guard<std::mutex> lk(P.mu);
@@ -498,9 +498,13 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         hs = P.hs;
     }
     // One dispatch carries the stream's whole side of the handshake.  It
-    // stops waiting after twice the proxy timeout plus a second, so the
-    // stream drains even if the proxy never answers; the proxy's own
-    // watchdog reports first.
+    // stops waiting after wait_limit_us, by default twice the proxy timeout
+    // plus a second, so the stream drains even if the proxy never answers
+    // (the proxy's own watchdog reports first).  A free slot belongs to the
+    // proxy; its flags are cleared here because a handshake that gave up
+    // leaves FINISH set, which must never release a later wait early.
+    store_flag(P.start_flag(op->slot), 0);
+    store_flag(P.finish_flag(op->slot), 0);
     store_flag(P.status_flag(op->slot), 0);
     HandshakeArgs ha;
     ha.start = (uint32_t *)P.start_flag(op->slot);
@@ -508,7 +512,9 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     ha.status = (uint32_t *)P.status_flag(op->slot);
     ha.start_value = kStartValue;
     ha.finish_value = kFinishValue;
-    ha.limit_ticks = (2ull * op->timeout_ms + 1000ull) * P.ticks_per_ms;
+    ha.limit_ticks = wait_limit_us
+                         ? std::max<uint64_t>(1, (uint64_t)wait_limit_us * P.ticks_per_ms / 1000)
+                         : (2ull * op->timeout_ms + 1000ull) * P.ticks_per_ms;
     hipError_t e = launch_handshake(ha, hs);
     if (e != hipSuccess) {
         // Nothing of the handshake reached a stream: give everything back.

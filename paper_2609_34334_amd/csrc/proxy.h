@@ -33,11 +33,13 @@ class Proxy {
     // Enqueues the handshake on `s` and hands the copies to the proxy
     // thread; returns once enqueued.  Copies run on at most `max_engines`
     // engines (0 = all), balanced by bytes per engine.
-    // The start/finish flag handshake runs on the proxy's private one-CU
-    // stream joined to `s` by events, or on `s` itself when `on_caller`.
+    // The stream side of the start/finish flag handshake runs on `s` itself
+    // when `on_caller`, else on the proxy's private CU-masked stream joined
+    // to `s` by events; it stops waiting after wait_limit_us (0: twice the
+    // timeout plus a second).
     hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                          unsigned timeout_ms, bool on_caller, hipStream_t s, int *engines_used,
-                          std::string &err);
+                          unsigned timeout_ms, unsigned wait_limit_us, bool on_caller,
+                          hipStream_t s, int *engines_used, std::string &err);
 
   private:
     explicit Proxy(ProxyImpl *impl) : impl_(impl) {}

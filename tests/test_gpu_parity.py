@@ -1,6 +1,8 @@
 """GPU parity: every collective through the C ABI against the CPU oracle,
 bit for bit, across dtypes, rank counts, ragged and misaligned sizes, in-place
 forms, copy paths, reduction algorithms and launch shapes."""
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -399,3 +401,49 @@ def test_finalize_and_reinit():
     hc.init(0)
     got = run_ar(x, hc.FP32)
     assert_bitwise(got[3], ref[3], "after re-init")
+
+
+def test_handshake_wait_gives_up_then_recovers():
+    """Failure handling forced from the host: a 1 us limit on the handshake
+    kernel's own bounded wait.  The kernel stops waiting at once, so its
+    dispatch ends and the stream drains; the proxy still runs the copies
+    through, reports HOCCL_ERR_TIMEOUT at the next engine call, clears the
+    slot, and the calls after that are correct again."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    R, n = 8, 1 << 22
+    x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    hc.set_config(copy_path="engines", proxy_wait_limit_us=1)
+    hc.allgather(x, recv)
+    torch.cuda.synchronize()                     # returns: the wait gave up
+    err = None
+    t0 = time.time()
+    while err is None and time.time() - t0 < 10:  # the proxy retires the op
+        time.sleep(0.05)
+        try:
+            hc.allgather(x, recv)
+        except hc.HocclError as e:
+            err = e
+        torch.cuda.synchronize()
+    assert err is not None and err.status == hc.ERR_TIMEOUT, err
+    assert "stopped waiting" in str(err)
+    hc.set_config(proxy_wait_limit_us=0)
+    time.sleep(0.2)                               # every limited call retires
+    for _ in range(5):                            # late reports, if any, first
+        try:
+            hc.allgather(x, recv)
+            break
+        except hc.HocclError as e:
+            assert e.status == hc.ERR_TIMEOUT
+    else:
+        raise AssertionError("the proxy kept reporting timeouts")
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for t in recv:
+            t.fill_(0)
+        hc.allgather(x, recv)
+        torch.cuda.synchronize()
+        for r in (0, 5, R - 1):
+            for s in range(R):
+                assert torch.equal(recv[r][s * n:(s + 1) * n], x[s])
