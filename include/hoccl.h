@@ -180,8 +180,16 @@ typedef struct {
 /* Initialise the library on `device` (the current HIP device if < 0):
  * creates the internal copy streams, the event pool and, when the SDMA
  * engines can be driven directly, the proxy thread and its flag pool.
- * Reads HOCCL_* environment variables into the configuration.  Optional:
- * every collective initialises lazily on the current device. */
+ * Reads HOCCL_* environment variables into the configuration:
+ *   HOCCL_WG_PER_STEP, HOCCL_THREADS_PER_WG, HOCCL_CHUNK_BYTES,
+ *   HOCCL_COPY_STREAMS, HOCCL_SDMA_ENGINES, HOCCL_AG_DIRECT,
+ *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
+ *   HOCCL_PROXY_WAIT_LIMIT_US (the fields of the same meaning),
+ *   HOCCL_COPY_PATH = auto | sdma | engines | kernel,
+ *   HOCCL_REDUCE_ALGO = ring | direct,
+ *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr).
+ * A set of values that fails validation falls back to the defaults.
+ * Optional: every collective initialises lazily on the current device. */
 hoccl_status_t hoccl_init(int device);
 
 /* Waits for the device, then releases streams, events, workspace, the proxy

@@ -67,6 +67,7 @@ std::mutex g_mu;
 std::map<int, DeviceState *> g_states;
 hoccl_config_t g_cfg;
 bool g_cfg_init = false;
+bool g_debug = false;  // HOCCL_DEBUG=1: log every executed plan to stderr
 
 void set_err(const char *fmt, ...) {
     char buf[512];
@@ -157,6 +158,7 @@ void load_config_locked() {
     if (const char *v = std::getenv("HOCCL_REDUCE_ALGO"))
         c.reduce_algo = std::strcmp(v, "direct") ? HOCCL_REDUCE_RING : HOCCL_REDUCE_DIRECT;
     if (!config_valid(c)) c = default_config();
+    g_debug = env_long("HOCCL_DEBUG", 0) != 0;
     g_cfg = c;
     g_cfg_init = true;
 }
@@ -544,6 +546,10 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
     const int wg = auto_workgroups(st, cfg, p, threads);
     const hoccl_copy_path_t path = resolve_path(st, cfg, p);
+    if (g_debug)
+        std::fprintf(stderr, "hoccl: device %d stream %p workgroups %d copy_path %d%s plan %s\n",
+                     st.device, (void *)s, wg, (int)path, capturing ? " (captured)" : "",
+                     plan_to_json(p).c_str());
     if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && !st.proxy) {
         // Asked for explicitly: never fall back silently.
         set_err("%s", st.proxy_why.c_str());

@@ -125,3 +125,18 @@ def test_config_roundtrip_and_validation():
 def test_status_strings():
     for st in range(7):
         assert L.hoccl_status_string(st)
+
+
+def test_debug_env_logs_plans_without_a_gpu_call():
+    """HOCCL_DEBUG is read with the rest of the environment; with no GPU the
+    library still loads and reports its configuration."""
+    import subprocess
+    import sys
+    code = ("import paper_2609_34334_amd as hc; c = hc.get_config(); "
+            "print(c['copy_path'], c['reduce_algo'], c['proxy_wait_limit_us'])")
+    env = dict(os.environ, HOCCL_DEBUG="1", HOCCL_COPY_PATH="kernel", HOCCL_REDUCE_ALGO="direct",
+               HOCCL_PROXY_WAIT_LIMIT_US="250")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                       cwd=ROOT)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == ["3", "1", "250"], r.stdout
