@@ -70,6 +70,34 @@ def event_time(fn, reps, warmup=2):
     return statistics.median(ts), min(ts)
 
 
+_FLUSH = []
+
+
+def queued_time(fn, reps, flush, warmup=2):
+    """Device time of fn alone: each timed call is enqueued behind a 50 us
+    spin, so the host's launch latency stays outside the events.  With
+    `flush`, 1 GiB (four times the 256 MB Infinity Cache) is written before
+    the spin, so the call starts with a cold last-level cache."""
+    import torch
+    if flush and not _FLUSH:
+        _FLUSH.append(torch.empty(1 << 28, dtype=torch.float32, device="cuda"))
+    for _ in range(warmup):
+        fn()
+    ts = []
+    for k in range(reps):
+        if flush:
+            _FLUSH[0].fill_(float(k))
+        torch.cuda._sleep(120_000)
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        ts.append(a.elapsed_time(b) / 1e3)
+    return statistics.median(ts), min(ts)
+
+
 # ---- the headline: reduce-scatter ------------------------------------------
 
 def bench_reduce_scatter(hc, W, steps, warmup):
@@ -313,6 +341,18 @@ def bench_allreduce(hc, W, reps, gemm):
                               hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
                               cus_used=st["cus_used_max"])
     hc.set_config(reduce_algo="ring")
+    # The 33.6 MB working set fits the last-level cache.  Device time alone
+    # (each call queued behind a spin), with the cache warm and flushed.
+    dev = {}
+    for name, kw in (("kernel", {"copy_path": "kernel"}), ("sdma", {"copy_path": "sdma"}),
+                     ("direct_fold", {"reduce_algo": "direct"})):
+        with hc.config(**kw):
+            warm, _ = queued_time(lambda: hc.allreduce(send, recv), reps, flush=False)
+            cold, _ = queued_time(lambda: hc.allreduce(send, recv), reps, flush=True)
+        dev[name] = dict(warm_us=round(warm * 1e6, 2), flushed_us=round(cold * 1e6, 2),
+                         warm_algbw_GBs=round(n * 4 / warm / 1e9, 2),
+                         flushed_algbw_GBs=round(n * 4 / cold / 1e9, 2))
+    res["device_only"] = dev
     return dict(workload="all-reduce fp32 R=4, 1,048,576 elements per rank (ring reduction + gather copies; "
                          "direct_fold: one kernel writes all outputs)", **res)
 
@@ -475,6 +515,22 @@ def size_sweep(hc):
             out[op].append(row)
             del send, recv
             torch.cuda.empty_cache()
+    # Reduce-scatter, bf16, R = 8 (size = each rank's input): the ring at the
+    # automatic budget and at 8 workgroups, and the direct fold.
+    out["reduce_scatter"] = []
+    for sz in sizes:
+        n = sz // 2 // R
+        send = [torch.zeros(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+        recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+        row = {"bytes": R * n * 2}
+        for name, kw in (("ring", {}), ("ring_wg8", {"workgroups_per_step": 8}),
+                         ("direct", {"reduce_algo": "direct"})):
+            with hc.config(**kw):
+                med, _ = event_time(lambda: hc.reduce_scatter(send, recv), 3, warmup=1)
+            row[name] = round(R * n * 2 / med / 1e9, 1)
+        out["reduce_scatter"].append(row)
+        del send, recv
+        torch.cuda.empty_cache()
     return out
 
 
