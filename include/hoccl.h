@@ -151,6 +151,14 @@ typedef struct {
                                    caller's stream by events (86 us), so the
                                    wait never holds back the caller's
                                    hardware queue                              */
+    size_t ring_group_bytes;    /* ring reduce-scatter / all-reduce run their
+                                   R-1 steps group by group over slices of
+                                   every chunk, one group's fp32 partials
+                                   taking at most this many bytes, so they
+                                   stay in the 256 MB last-level cache from
+                                   step to step (same fold order, same bits).
+                                   0 = the library default; SIZE_MAX = one
+                                   group                                       */
     unsigned int proxy_wait_limit_us; /* the handshake kernel stops waiting
                                    after this long, so its dispatch always
                                    ends; the proxy then reports
@@ -184,7 +192,8 @@ typedef struct {
  *   HOCCL_WG_PER_STEP, HOCCL_THREADS_PER_WG, HOCCL_CHUNK_BYTES,
  *   HOCCL_COPY_STREAMS, HOCCL_SDMA_ENGINES, HOCCL_AG_DIRECT,
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
- *   HOCCL_PROXY_WAIT_LIMIT_US (the fields of the same meaning),
+ *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES (the fields of the
+ *   same meaning),
  *   HOCCL_COPY_PATH = auto | sdma | engines | kernel,
  *   HOCCL_REDUCE_ALGO = ring | direct,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr).

@@ -48,6 +48,7 @@ class Config(ctypes.Structure):
                 ("kernel_timing", ctypes.c_int),
                 ("proxy_timeout_ms", ctypes.c_uint),
                 ("proxy_handshake", ctypes.c_int),
+                ("ring_group_bytes", ctypes.c_size_t),
                 ("proxy_wait_limit_us", ctypes.c_uint)]
 
 

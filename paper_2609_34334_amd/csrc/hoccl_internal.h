@@ -101,6 +101,10 @@ struct PlanOptions {
     size_t chunk_bytes = 0;
     bool in_place = false;
     hoccl_reduce_algo_t algo = HOCCL_REDUCE_RING;
+    // Ring reductions run group by group, each group's fp32 partials taking
+    // at most this many bytes (0: one group), so that they stay in the
+    // last-level cache from one step to the next.
+    size_t group_partial_bytes = 0;
 };
 
 size_t dtype_size(hoccl_dtype_t dt);

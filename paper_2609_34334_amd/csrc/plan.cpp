@@ -144,6 +144,17 @@ static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
     }
 }
 
+// Groups a ring reduction over chunks of c elements is split into so that
+// one group's partials (R chunk slices of acc-size elements) take at most
+// `limit` bytes.  Two ranks keep no partials.
+static int cache_groups(int R, size_t c, hoccl_dtype_t dt, size_t limit) {
+    if (limit == 0 || R <= 2 || c == 0) return 1;
+    unsigned long long bytes = (unsigned long long)R * c * acc_size(dt);
+    unsigned long long G = (bytes + limit - 1) / limit;
+    if (G > c) G = c;
+    return (int)std::max(1ull, std::min(G, 1ull << 20));
+}
+
 Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o) {
     Plan p;
     p.op = Op::ReduceScatter;
@@ -169,7 +180,10 @@ Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o
         return p;
     }
     std::vector<size_t> len((size_t)R, n);
-    ring_reduce(p, dt, R, n, len, 0, n, 0, true);
+    const int G = cache_groups(R, n, dt, o.group_partial_bytes);
+    const size_t gl = (n + (size_t)G - 1) / (size_t)G;
+    p.ngroups = G;
+    for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, n, len, (size_t)g * gl, gl, g, true);
     p.ws_bytes = (R > 2) ? (size_t)R * n * acc_size(dt) : 0;
     return p;
 }
@@ -204,7 +218,7 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
         p.hbm_bytes = (unsigned long long)count * (R * es + R * es);
         return p;
     }
-    int G = std::max(1, o.allreduce_groups);
+    int G = std::max(std::max(1, o.allreduce_groups), cache_groups(R, c, dt, o.group_partial_bytes));
     if ((size_t)G > c) G = (int)c;
     size_t cg = (c + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;

@@ -51,6 +51,27 @@ def run_rs(x, dt, lead=0):
 
 # ---------------------------------------------------------------- reductions
 
+@pytest.mark.parametrize("dt", [hc.INT32, hc.FP32, hc.BF16], ids=lambda d: NAME[d])
+@pytest.mark.parametrize("R", [3, 8])
+def test_ring_in_cache_groups(dt, R):
+    """The ring run group by group (a tiny partial budget forces many groups
+    with a ragged last one) gives the oracle's bits, for reduce-scatter and
+    all-reduce, also with the all-reduce's own gather groups."""
+    n = 30_011
+    for budget, ar_groups in ((1 << 16, 1), (12_345, 3)):
+        with hc.config(ring_group_bytes=budget, allreduce_chunk_groups=ar_groups):
+            x = [W.random_values(NAME[dt], 700 + R, r, R * n) for r in range(R)]
+            ref = oracle.reduce_scatter_new(x, dt)
+            got = run_rs(x, dt, lead=3)
+            for r in range(R):
+                assert_bitwise(got[r], ref[r], f"grouped RS budget={budget} r={r}")
+            xa = [W.random_values(NAME[dt], 710 + R, r, n) for r in range(R)]
+            refa = oracle.allreduce_new(xa, dt)
+            gota = run_ar(xa, dt, lead=5)
+            for r in range(R):
+                assert_bitwise(gota[r], refa[r], f"grouped AR budget={budget} r={r}")
+
+
 @pytest.mark.parametrize("algo", ["ring", "direct"])
 @pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
 @pytest.mark.parametrize("R", [1, 2, 3, 4, 8])

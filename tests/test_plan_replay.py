@@ -98,6 +98,8 @@ CONFIGS = [
     dict(chunk_bytes=4096),
     dict(allgather_direct=1, chunk_bytes=4096, allreduce_chunk_groups=2),
     dict(reduce_algo="direct"),
+    dict(ring_group_bytes=1000),                      # many cache groups, ragged last group
+    dict(ring_group_bytes=4096, allreduce_chunk_groups=2, chunk_bytes=4096),
 ]
 
 
@@ -199,3 +201,23 @@ def test_algorithmic_bytes():
     plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, 8)
     assert plan["hbm_bytes"] == 8 * n * (8 + 5 * 10 + 8)
     assert plan["ws_bytes"] == 8 * n * 4
+
+
+def test_cache_groups_bound_partials_and_keep_bytes():
+    """Ring groups: each group's fp32 partials stay within the budget, the
+    algorithmic bytes do not change, and every group runs its R-1 steps in
+    order before the next group starts."""
+    R, n = 8, 3_145_728
+    with hc.config(ring_group_bytes=(1 << 64) - 1):
+        one = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, R)
+    with hc.config(ring_group_bytes=16 << 20):
+        p = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, R)
+    assert one["ngroups"] == 1 and p["ngroups"] == 6            # 96 MiB of partials / 16 MiB
+    assert p["hbm_bytes"] == one["hbm_bytes"]
+    steps = p["reduce_steps"]
+    assert [s["group"] for s in steps] == [g for g in range(6) for _ in range(R - 1)]
+    for s in steps:
+        assert sum(seg["n"] for seg in s["segs"]) * 4 <= 16 << 20
+    with hc.config(ring_group_bytes=16 << 20):
+        ar = hc.plan_json(hc.OP_ALLREDUCE, R * n, hc.BF16, R)
+    assert ar["ngroups"] == 6
