@@ -364,7 +364,9 @@ def bench_allgather(hc, W, reps, gemm):
     send = [bf16_dev(a) for a in x]
     recv = [torch.empty(total, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     res = copy_paths(hc, lambda s: hc.allgather(send, recv, stream=s), total * 2, (R - 1) / R, reps, gemm,
-                     extra_paths=[("engines_ring", {"allgather_direct": 0}), ("sdma_ring", {"allgather_direct": 0})])
+                     extra_paths=[("engines_ring", {"allgather_direct": 0}), ("sdma_ring", {"allgather_direct": 0}),
+                                  ("kernel_wg8", {"workgroups_per_step": 8}),
+                                  ("kernel_wg64", {"workgroups_per_step": 64})])
     hc.set_config(allgather_direct=1)
     return dict(workload="FSDP all-gather bf16 R=8, 25,165,824-element shards (one GPT-6.7B block, "
                          "201,326,592 params), out-of-place", **res)
@@ -403,7 +405,8 @@ def bench_a2a(hc, W, reps, gemm):
     recv = [torch.empty(s, dtype=torch.bfloat16, device="cuda") for s in rsz]
     sent = sum(counts) * 2
     res = copy_paths(hc, lambda s: hc.alltoallv(send, counts, sd, recv, rd, stream=s), sent // R, (R - 1) / R,
-                     reps, gemm)
+                     reps, gemm, extra_paths=[("kernel_wg8", {"workgroups_per_step": 8}),
+                                              ("kernel_wg64", {"workgroups_per_step": 64})])
     return dict(workload="EP all-to-all(v) bf16, 4096 tokens x 2048 per rank, 64 experts over R=8, top-6 "
                          "(one copy per destination rank), gemm_slowdown against a concurrent 8192^3 bf16 GEMM",
                 bytes_sent_total=sent, **res)
