@@ -357,6 +357,33 @@ def bench_allreduce(hc, W, reps, gemm):
                          "direct_fold: one kernel writes all outputs)", **res)
 
 
+def bench_allreduce_bucket(hc, W, reps):
+    """All-reduce of one GPT-6.7B gradient bucket (bf16, R=8, 25,165,824
+    elements per rank): the ring reduction on CUs, then the gather as copies.
+    With G chunk groups the gather of group g overlaps the reduction of
+    group g+1 (SDMA copies beside CU kernels); the direct fold for scale."""
+    import torch
+    R, n = 8, 25_165_824
+    x = W.rs_gradients(R, n)
+    send = [bf16_dev(a) for a in x]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    S = n * 2
+    out = {}
+    for path in ("sdma", "kernel"):
+        for G in (1, 2, 4, 8):
+            with hc.config(copy_path=path, allreduce_chunk_groups=G):
+                med, _ = event_time(lambda: hc.allreduce(send, recv), reps)
+                st = hc.last_stats()
+            out[f"{path}_groups{G}"] = dict(ms=round(med * 1e3, 4), algbw_GBs=round(S / med / 1e9, 1),
+                                            busbw_GBs=round(S / med / 1e9 * 2 * (R - 1) / R, 1),
+                                            copy_ops=st["copy_ops"], reduce_launches=st["reduce_launches"])
+    with hc.config(reduce_algo="direct"):
+        med, _ = event_time(lambda: hc.allreduce(send, recv), reps)
+    out["direct_fold"] = dict(ms=round(med * 1e3, 4), algbw_GBs=round(S / med / 1e9, 1))
+    return dict(workload="all-reduce bf16 R=8, 25,165,824 elements per rank (ring reduction + gather; "
+                         "G chunk groups overlap the gather of group g with the reduction of group g+1)", **out)
+
+
 def bench_allgather(hc, W, reps, gemm):
     import torch
     R, total = 8, 201_326_592
@@ -707,6 +734,11 @@ def main():
                 extra[name] = fn(hc, W, 10, gemm)
             except Exception as e:  # report, do not hide the headline
                 extra[name] = {"error": repr(e)}
+        log("allreduce bucket")
+        try:
+            extra["allreduce_bf16_R8_bucket"] = bench_allreduce_bucket(hc, W, 10)
+        except Exception as e:
+            extra["allreduce_bf16_R8_bucket"] = {"error": repr(e)}
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
         extra["small_message_latency"] = bench_small_message(hc, 30)
