@@ -85,7 +85,7 @@ extern "C" {
 typedef enum {
     HOCCL_OK = 0,
     HOCCL_ERR_INVALID_ARG = 1, /* bad pointer, count, R, dtype, peer map or overlap */
-    HOCCL_ERR_UNSUPPORTED = 2, /* valid request this build cannot serve            */
+    HOCCL_ERR_UNSUPPORTED = 2, /* valid request the library cannot serve here     */
     HOCCL_ERR_HIP = 3,         /* a HIP / HSA runtime call failed                   */
     HOCCL_ERR_NO_MEMORY = 4,   /* workspace or host allocation failed               */
     HOCCL_ERR_TIMEOUT = 5,     /* the copy proxy's watchdog expired                 */
