@@ -304,12 +304,13 @@ def make_gemm():
     return (A, B, C, t, gs, cs)
 
 
-PATHS = [("sdma", {}), ("engines", {}), ("kernel", {})]
+PATHS = [("sdma", {}), ("engines", {}), ("engines_hostfn", {"proxy_handshake": 2}), ("kernel", {})]
 
 
 def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
     """Time `run(stream)` under every copy path: algbw = S / t, busbw = algbw * f."""
     res = {}
+    saved = hc.get_config()
     for name, kw in list(PATHS) + list(extra_paths):
         path = name.split("_")[0]
         hc.set_config(copy_path=path, **kw)
@@ -323,7 +324,7 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
         if gemm is not None:
             r["gemm_slowdown"], r["gemm_overlap"] = gemm_slowdown(hc, run, med, gemm)
         res[name] = r
-        hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0)
+        hc.set_config(**saved)
     return res
 
 
@@ -470,8 +471,8 @@ def bench_small_message(hc, reps):
     src = torch.zeros(2048, dtype=torch.bfloat16, device="cuda")
     dst = torch.empty_like(src)
     out = {}
-    for name in ("sdma", "engines", "kernel"):
-        hc.set_config(copy_path=name)
+    for name in ("sdma", "engines", "engines_hostfn", "kernel"):
+        hc.set_config(copy_path=name.split("_")[0], proxy_handshake=2 if name.endswith("hostfn") else 0)
         med, mn = event_time(lambda: hc.sendrecv([src, src], [dst, dst], [1, -1]), reps, warmup=5)
         host = []
         for _ in range(reps):
@@ -481,7 +482,7 @@ def bench_small_message(hc, reps):
             torch.cuda.synchronize()
         out[name] = dict(device_us=round(med * 1e6, 2), device_min_us=round(mn * 1e6, 2),
                          host_call_us=round(statistics.median(host) * 1e6, 2))
-    hc.set_config(copy_path="auto")
+    hc.set_config(copy_path="auto", proxy_handshake=0)
     return dict(workload="one 4 KiB message rank 0 -> 1 (stream-manager round trip)", **out)
 
 

@@ -140,17 +140,23 @@ typedef struct {
                                    copy kernel launch (hoccl_get_kernel_times) */
     unsigned int proxy_timeout_ms; /* watchdog of the SDMA_ENGINES proxy;
                                    0 = 10000                                   */
-    int proxy_handshake;        /* where the stream side of the SDMA_ENGINES
-                                   start/finish flag handshake runs: one
-                                   dispatch of a one-lane kernel that waits
-                                   on a CU while the copies run.
-                                   0 (default): on the caller's stream, the
-                                   paper's form (4 KiB send/recv: 21 us);
-                                   1: on a private CU-masked stream with a
-                                   hardware queue of its own, joined to the
-                                   caller's stream by events (86 us), so the
-                                   wait never holds back the caller's
-                                   hardware queue                              */
+    int proxy_handshake;        /* the stream side of the SDMA_ENGINES
+                                   start/finish flag handshake:
+                                   0 (default): a one-lane kernel on the
+                                   caller's stream that waits on a CU while
+                                   the copies run (4 KiB send/recv: 23 us);
+                                   1: that kernel on a private CU-masked
+                                   stream with a hardware queue of its own,
+                                   joined to the caller's stream by events
+                                   (86 us), so the wait never holds back the
+                                   caller's hardware queue;
+                                   2: a host function on the caller's stream
+                                   (hipLaunchHostFunc): no GPU code waits and
+                                   no CU is used, but the HIP runtime's
+                                   callback thread is blocked while the
+                                   copies run.  Not for use under a profiler
+                                   that hooks copy completion: a run under
+                                   rocprofv3 hung                          */
     size_t ring_group_bytes;    /* ring reduce-scatter / all-reduce run their
                                    R-1 steps group by group over slices of
                                    every chunk, one group's fp32 partials

@@ -125,7 +125,7 @@ bool config_valid(const hoccl_config_t &c) {
     if (c.allreduce_chunk_groups < 0 || c.allreduce_chunk_groups > 1024) return false;
     if ((int)c.reduce_algo < 0 || (int)c.reduce_algo > 1) return false;
     if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
-    if (c.proxy_handshake < 0 || c.proxy_handshake > 1) return false;
+    if (c.proxy_handshake < 0 || c.proxy_handshake > 2) return false;
     return true;
 }
 
@@ -586,8 +586,8 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
         hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                            cfg.proxy_wait_limit_us, cfg.proxy_handshake == 0, s,
-                                            &ne, t_err);
+                                            cfg.proxy_wait_limit_us, cfg.proxy_handshake, s, &ne,
+                                            t_err);
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {
@@ -607,8 +607,10 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     bool cu_work = has_kernels || (has_copies && path == HOCCL_COPY_KERNEL);
     t_stats.workgroups_per_step = cu_work ? wg : 0;
     t_stats.cus_available = st.num_cus;
-    // The engine proxy's handshake waits in a one-thread kernel on one CU.
-    const bool handshake_wave = has_copies && path == HOCCL_COPY_SDMA_ENGINES;
+    // The engine proxy's handshake kernel waits as one lane on one CU; the
+    // host-function form needs none.
+    const bool handshake_wave =
+        has_copies && path == HOCCL_COPY_SDMA_ENGINES && cfg.proxy_handshake != 2;
     t_stats.cus_used_max = cu_work ? std::min(wg, st.num_cus) : (handshake_wave ? 1 : 0);
     t_stats.copy_path_used = has_copies ? path : HOCCL_COPY_AUTO;
     t_stats.reduce_algo_used = p.has_fold ? HOCCL_REDUCE_DIRECT : HOCCL_REDUCE_RING;

@@ -378,8 +378,36 @@ Proxy::~Proxy() {
 
 int Proxy::engine_count() const { return (int)impl_->engines.size(); }
 
+// The stream side of the handshake run as a host function: the HIP runtime
+// holds every later operation of the stream until it returns, so the stream
+// waits without any GPU code.  It performs the same four flag steps as the
+// handshake kernel, on the runtime's callback thread, and gives up (status
+// = 1) after the same bounded time.  It must not call into HIP.
+struct HostSide {
+    volatile uint32_t *start, *finish, *status;
+    std::chrono::microseconds limit;
+};
+
+void host_side_handshake(void *arg) {
+    HostSide *h = (HostSide *)arg;
+    const auto t0 = std::chrono::steady_clock::now();
+    auto wait = [&](volatile uint32_t *f, uint32_t want) {
+        while (load_flag(f) != want) {
+            if (std::chrono::steady_clock::now() - t0 > h->limit) return false;
+            std::this_thread::yield();
+        }
+        return true;
+    };
+    store_flag(h->start, kStartValue);
+    if (!wait(h->start, 0) || !wait(h->finish, kFinishValue))
+        store_flag(h->status, 1);
+    else
+        store_flag(h->finish, 0);
+    delete h;
+}
+
 hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                             unsigned timeout_ms, unsigned wait_limit_us, bool on_caller,
+                             unsigned timeout_ms, unsigned wait_limit_us, int handshake,
                              hipStream_t s, int *engines_used, std::string &err) {
     ProxyImpl &P = *impl_;
     {
@@ -484,10 +512,10 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         }
         op->sig.push_back(sg);
     }
-    // The handshake runs on the private one-CU stream unless asked for on
-    // the caller's stream (or the private stream could not be created).
+    // The handshake kernel runs on the caller's stream, or on the private
+    // CU-masked stream when asked for (and that stream exists).
     hipStream_t hs = s;
-    if (!on_caller && P.hs) {
+    if (handshake == 1 && P.hs) {
         hipError_t e = hipEventRecord(P.ev_fork, s);
         if (e == hipSuccess) e = hipStreamWaitEvent(P.hs, P.ev_fork, 0);
         if (e != hipSuccess) {
@@ -506,6 +534,27 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     store_flag(P.start_flag(op->slot), 0);
     store_flag(P.finish_flag(op->slot), 0);
     store_flag(P.status_flag(op->slot), 0);
+    if (handshake == 2) {
+        HostSide *h = new HostSide{P.start_flag(op->slot), P.finish_flag(op->slot),
+                                   P.status_flag(op->slot),
+                                   std::chrono::microseconds(
+                                       wait_limit_us ? (uint64_t)wait_limit_us
+                                                     : (2ull * op->timeout_ms + 1000ull) * 1000ull)};
+        hipError_t e = hipLaunchHostFunc(s, host_side_handshake, h);
+        if (e != hipSuccess) {
+            delete h;
+            (void)hipGetLastError();
+            err = std::string("hipLaunchHostFunc failed: ") + hipGetErrorString(e);
+            give_back();
+            return HOCCL_ERR_HIP;
+        }
+        {
+            std::lock_guard<std::mutex> lk(P.mu);
+            P.incoming.push_back(op);
+        }
+        P.cv_work.notify_one();
+        return HOCCL_OK;
+    }
     HandshakeArgs ha;
     ha.start = (uint32_t *)P.start_flag(op->slot);
     ha.finish = (uint32_t *)P.finish_flag(op->slot);

@@ -33,12 +33,14 @@ class Proxy {
     // Enqueues the handshake on `s` and hands the copies to the proxy
     // thread; returns once enqueued.  Copies run on at most `max_engines`
     // engines (0 = all), balanced by bytes per engine.
-    // The stream side of the start/finish flag handshake runs on `s` itself
-    // when `on_caller`, else on the proxy's private CU-masked stream joined
-    // to `s` by events; it stops waiting after wait_limit_us (0: twice the
-    // timeout plus a second).
+    // The stream side of the start/finish flag handshake (`handshake`, as
+    // hoccl_config_t.proxy_handshake): 0, a one-lane kernel on `s`; 1, that
+    // kernel on the proxy's private CU-masked stream joined to `s` by
+    // events; 2, a host function on `s` run by the HIP runtime's callback
+    // thread.  It stops waiting after wait_limit_us (0: twice the timeout
+    // plus a second).
     hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                          unsigned timeout_ms, unsigned wait_limit_us, bool on_caller,
+                          unsigned timeout_ms, unsigned wait_limit_us, int handshake,
                           hipStream_t s, int *engines_used, std::string &err);
 
   private:

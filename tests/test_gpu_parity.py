@@ -359,11 +359,11 @@ def test_back_to_back_calls_on_two_streams_share_workspace_safely():
             assert_bitwise(from_dev(ob[r], hc.BF16), rb[r], f"s2 r={r}")
 
 
-@pytest.mark.parametrize("handshake", [0, 1])
+@pytest.mark.parametrize("handshake", [0, 1, 2])
 def test_engine_proxy_handshakes(handshake):
-    """Both places of the engine proxy's start/finish flag handshake: on
-    the caller's stream (default) and on the proxy's private stream joined
-    by events.  Checked behind a delayed producer, with a consumer queued
+    """Every form of the engine proxy's start/finish flag handshake: the
+    kernel on the caller's stream (default), the kernel on the proxy's
+    private stream joined by events, and a host function.  Checked behind a delayed producer, with a consumer queued
     after the collective, and for ring chains (dependent hops)."""
     hc.set_config(copy_path="engines", proxy_handshake=handshake)
     R, n = 4, 1 << 20
@@ -424,7 +424,8 @@ def test_finalize_and_reinit():
     assert_bitwise(got[3], ref[3], "after re-init")
 
 
-def test_handshake_wait_gives_up_then_recovers():
+@pytest.mark.parametrize("handshake", [0, 2])
+def test_handshake_wait_gives_up_then_recovers(handshake):
     """Failure handling forced from the host: a 1 us limit on the handshake
     kernel's own bounded wait.  The kernel stops waiting at once, so its
     dispatch ends and the stream drains; the proxy still runs the copies
@@ -435,7 +436,7 @@ def test_handshake_wait_gives_up_then_recovers():
     R, n = 8, 1 << 22
     x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
     recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
-    hc.set_config(copy_path="engines", proxy_wait_limit_us=1)
+    hc.set_config(copy_path="engines", proxy_wait_limit_us=1, proxy_handshake=handshake)
     hc.allgather(x, recv)
     torch.cuda.synchronize()                     # returns: the wait gave up
     err = None
