@@ -154,9 +154,11 @@ typedef struct {
                                    (hipLaunchHostFunc): no GPU code waits and
                                    no CU is used, but the HIP runtime's
                                    callback thread is blocked while the
-                                   copies run.  Not for use under a profiler
-                                   that hooks copy completion: a run under
-                                   rocprofv3 hung                          */
+                                   copies run.  A run under rocprofv3 hung
+                                   once, so with a ROCm profiler loaded
+                                   (rocprofiler-sdk preloaded, or
+                                   HSA_TOOLS_LIB set) such calls return
+                                   HOCCL_ERR_UNSUPPORTED                    */
     size_t ring_group_bytes;    /* ring reduce-scatter / all-reduce run their
                                    R-1 steps group by group over slices of
                                    every chunk, one group's fp32 partials

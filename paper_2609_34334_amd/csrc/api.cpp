@@ -498,6 +498,21 @@ hoccl_status_t run_copies_kernel(DeviceState &st, const hoccl_config_t &cfg, con
     return HOCCL_OK;
 }
 
+// Whether a ROCm profiler is loaded into this process (rocprofiler-sdk is
+// preloaded and announces its tool library; the older interface uses
+// HSA_TOOLS_LIB).  The host-function handshake blocks the runtime's callback
+// thread, which a profiler may need to complete copies, so it is refused
+// then rather than risk a stall.
+bool profiler_present() {
+    static const bool present = [] {
+        const char *pre = std::getenv("LD_PRELOAD");
+        if (pre && std::strstr(pre, "rocprofiler")) return true;
+        return std::getenv("ROCP_TOOL_LIBRARIES") != nullptr || std::getenv("HSA_TOOLS_LIB") != nullptr ||
+               env_long("HOCCL_ASSUME_PROFILER", 0) != 0;  // lets a test check the refusal
+    }();
+    return present;
+}
+
 // Copy path for a plan.  An explicit choice wins; AUTO is the HIP runtime's
 // device-to-device SDMA path.  It is the only one that is free of compute
 // units end to end: the engine proxy moves data on SDMA engines too, but the
@@ -555,6 +570,12 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && !st.proxy) {
         // Asked for explicitly: never fall back silently.
         set_err("%s", st.proxy_why.c_str());
+        return HOCCL_ERR_UNSUPPORTED;
+    }
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && cfg.proxy_handshake == 2 &&
+        profiler_present()) {
+        set_err("the host-function handshake (proxy_handshake = 2) is refused while a profiler is "
+                "loaded: it blocks the runtime thread the profiler may need");
         return HOCCL_ERR_UNSUPPORTED;
     }
     if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && capturing) {

@@ -140,3 +140,4 @@ def test_debug_env_logs_plans_without_a_gpu_call():
                        cwd=ROOT)
     assert r.returncode == 0, r.stderr
     assert r.stdout.split() == ["3", "1", "250"], r.stdout
+

@@ -469,3 +469,31 @@ def test_handshake_wait_gives_up_then_recovers(handshake):
         for r in (0, 5, R - 1):
             for s in range(R):
                 assert torch.equal(recv[r][s * n:(s + 1) * n], x[s])
+
+
+def test_host_function_handshake_refused_under_a_profiler():
+    """With a profiler announced (HOCCL_ASSUME_PROFILER stands in for one in
+    a child process) the host-function handshake is refused before anything
+    is enqueued; the kernel handshake still works there."""
+    import subprocess
+    import sys
+    import os
+    code = (
+        "import torch, paper_2609_34334_amd as hc\n"
+        "x = [torch.ones(4096, device='cuda') for _ in range(4)]\n"
+        "hc.set_config(copy_path='engines', proxy_handshake=2)\n"
+        "try:\n"
+        "    hc.allgather(x)\n"
+        "    print('not refused')\n"
+        "except hc.HocclError as e:\n"
+        "    print('refused', e.status, 'profiler' in str(e))\n"
+        "hc.set_config(proxy_handshake=0)\n"
+        "y = hc.allgather(x); torch.cuda.synchronize()\n"
+        "print('kernel handshake ok', bool(torch.equal(y[2][:4096], x[0])))\n")
+    env = dict(os.environ, HOCCL_ASSUME_PROFILER="1")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0, r.stderr[-2000:]
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    assert f"refused {hc.ERR_UNSUPPORTED} True" in r.stdout, r.stdout
+    assert "kernel handshake ok True" in r.stdout, r.stdout
