@@ -204,7 +204,9 @@ typedef struct {
  *   same meaning),
  *   HOCCL_COPY_PATH = auto | sdma | engines | kernel,
  *   HOCCL_REDUCE_ALGO = ring | direct,
- *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr).
+ *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),
+ *   HOCCL_SDMA_ENGINE_IDS = "i,j,..." (the SDMA engines the SDMA_ENGINES
+ *   proxy may use, in that order; read when the proxy is created).
  * A set of values that fails validation falls back to the defaults.
  * Optional: every collective initialises lazily on the current device. */
 hoccl_status_t hoccl_init(int device);

@@ -38,6 +38,7 @@
 #include <chrono>
 #include <condition_variable>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <deque>
 #include <mutex>
@@ -326,11 +327,27 @@ Proxy *Proxy::create(int device, std::string *why) {
     ProxyImpl *p = new ProxyImpl();
     p->agent = f.agent;
     // Engines 0 and 1 also serve the runtime's own host transfers: use them
-    // last.
-    for (int b = 2; b < 32; ++b)
-        if (mask & (1u << b)) p->engines.push_back(1u << b);
-    for (int b = 0; b < 2; ++b)
-        if (mask & (1u << b)) p->engines.push_back(1u << b);
+    // last.  HOCCL_SDMA_ENGINE_IDS ("3,0,7") restricts the proxy to the
+    // listed usable engines, in that order.
+    if (const char *ids = std::getenv("HOCCL_SDMA_ENGINE_IDS")) {
+        for (const char *c = ids; *c;) {
+            char *end = nullptr;
+            long b = std::strtol(c, &end, 10);
+            if (end == c) break;
+            if (b >= 0 && b < 32 && (mask & (1u << b))) p->engines.push_back(1u << b);
+            c = (*end == ',') ? end + 1 : end;
+        }
+    } else {
+        for (int b = 2; b < 32; ++b)
+            if (mask & (1u << b)) p->engines.push_back(1u << b);
+        for (int b = 0; b < 2; ++b)
+            if (mask & (1u << b)) p->engines.push_back(1u << b);
+    }
+    if (p->engines.empty()) {
+        delete p;
+        hsa_shut_down();
+        return fail("HOCCL_SDMA_ENGINE_IDS names no usable engine", (long)mask);
+    }
     void *fl = nullptr;
     he = hipHostMalloc(&fl, kSlots * kFlagsPerSlot * kLine, hipHostMallocCoherent | hipHostMallocMapped);
     if (he != hipSuccess || !fl) {
