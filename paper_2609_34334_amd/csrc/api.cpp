@@ -700,7 +700,13 @@ hoccl_status_t check_ptrs(const void *const *arr, int R, const char *what) {
     return HOCCL_OK;
 }
 
-bool size_overflows(size_t a, size_t b) { return b != 0 && a > SIZE_MAX / b; }
+bool size_overflows(size_t a, size_t b) {
+    if (b != 0 && a > SIZE_MAX / b) {
+        set_err("count %zu times %zu bytes does not fit in size_t", a, b);
+        return true;
+    }
+    return false;
+}
 
 // Budget of one ring group's fp32 partials when ring_group_bytes is 0: the
 // 256 MB last-level cache.  Measured on the bf16 R=8 reduce-scatter: at 1 GiB

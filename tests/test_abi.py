@@ -141,3 +141,15 @@ def test_debug_env_logs_plans_without_a_gpu_call():
     assert r.returncode == 0, r.stderr
     assert r.stdout.split() == ["3", "1", "250"], r.stdout
 
+
+
+def test_size_overflow_rejected_with_a_reason():
+    """Counts whose byte size does not fit in size_t are argument errors,
+    reported before anything touches a device, with their own message."""
+    L = hc.lib()
+    send = (ctypes.c_void_p * 2)(1 << 40, 2 << 40)
+    recv = (ctypes.c_void_p * 2)(3 << 40, 4 << 40)
+    huge = ctypes.c_size_t((1 << 64) - 1)
+    for fn in (L.hoccl_allreduce, L.hoccl_reduce_scatter, L.hoccl_allgather, L.hoccl_alltoall):
+        assert fn(send, recv, huge, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
+        assert b"does not fit" in L.hoccl_last_error_string()
