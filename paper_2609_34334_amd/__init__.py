@@ -255,6 +255,20 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _on_send_device(fn):
+    """Runs a collective with its buffers' GPU current (and that GPU's
+    current stream as the default): the library keeps its streams and
+    workspace per device and acts on the current one."""
+    import functools
+
+    @functools.wraps(fn)
+    def wrapper(send, *args, **kwargs):
+        with torch.cuda.device(send[0].device):
+            return fn(send, *args, **kwargs)
+    return wrapper
+
+
+@_on_send_device
 def allreduce(send, recv=None, stream=None):
     """Sum of the R tensors `send`, written to every tensor of `recv`
     (defaults to in place)."""
@@ -268,6 +282,7 @@ def allreduce(send, recv=None, stream=None):
     return recv
 
 
+@_on_send_device
 def reduce_scatter(send, recv=None, stream=None):
     """send: R tensors of R*n elements; recv[r] receives block r of the sum."""
     R = len(send)
@@ -284,6 +299,7 @@ def reduce_scatter(send, recv=None, stream=None):
     return recv
 
 
+@_on_send_device
 def allgather(send, recv=None, stream=None):
     """send: R tensors of n elements; every recv[r] gets their concatenation."""
     R = len(send)
@@ -298,6 +314,7 @@ def allgather(send, recv=None, stream=None):
     return recv
 
 
+@_on_send_device
 def sendrecv(send, recv, peers, stream=None):
     """Rank r sends send[r] to rank peers[r] (-1: nothing).  recv[d] may be
     None for ranks that receive nothing."""
@@ -311,6 +328,7 @@ def sendrecv(send, recv, peers, stream=None):
     return recv
 
 
+@_on_send_device
 def alltoall(send, recv=None, stream=None):
     R = len(send)
     if send[0].numel() % R:
@@ -324,6 +342,7 @@ def alltoall(send, recv=None, stream=None):
     return recv
 
 
+@_on_send_device
 def alltoallv(send, counts, sdispls, recv, rdispls, stream=None):
     """counts/sdispls/rdispls: R*R element counts and offsets, [s*R + d]."""
     R = len(send)
