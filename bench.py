@@ -174,6 +174,7 @@ def direct_reduce_scatter(hc, send_np, steps, warmup):
                       roofline={"kernel": "fold_kernel (all 8 ranks folded in ring order, one launch)",
                                 "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                                "traffic": measured_traffic(FOLD_TRAFFIC_SUMMARY),
                                 "avg_launch_us": round(launch * 1e6, 2),
                                 "bytes_per_launch": st["hbm_bytes_algorithmic"]})
 
@@ -592,6 +593,7 @@ def size_sweep(hc):
 
 
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "reduce_step_kernel_rs_bf16_R8_traffic.txt")
+FOLD_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "fold_kernel_rs_bf16_R8_traffic.txt")
 
 
 def kernel_source_hash():
@@ -601,13 +603,13 @@ def kernel_source_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per reduce-step launch from the committed rocprofv3 counter
-    summary, or None when it is missing or the kernels changed since."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+def measured_traffic(summary=TRAFFIC_SUMMARY):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, or
+    None when it is missing or the kernels changed since."""
+    if not os.path.exists(summary):
         return None
     kv = {}
-    for line in open(TRAFFIC_SUMMARY):
+    for line in open(summary):
         if ":" in line and not line.startswith(("#", " ", "|")):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
@@ -645,7 +647,8 @@ def copy_workload(hc, W):
 
 def pmc_workload(hc, W):
     """What the counter runs profile: a 1 GiB CU copy of known size (to
-    scale FETCH_SIZE / WRITE_SIZE), then five headline reduce-scatters."""
+    scale FETCH_SIZE / WRITE_SIZE), then five headline reduce-scatters on
+    the ring and five with the direct fold."""
     import torch
     src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
@@ -658,6 +661,9 @@ def pmc_workload(hc, W):
     recv = [torch.empty(n_in // R, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     for _ in range(5):
         hc.reduce_scatter(send, recv)
+    with hc.config(reduce_algo="direct"):
+        for _ in range(5):
+            hc.reduce_scatter(send, recv)
     torch.cuda.synchronize()
     print(json.dumps({"pmc_workload": "done", "kernels_hip_sha256_16": kernel_source_hash()}))
 
