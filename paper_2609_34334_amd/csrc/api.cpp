@@ -459,11 +459,13 @@ hoccl_status_t run_copies_sdma(DeviceState &st, const hoccl_config_t &cfg, const
                                hipMemcpyDeviceToDeviceNoCU, cs));
         t_stats.copy_ops++;
     }
+    // Queue k >= 1 is copy stream k - 1, joined back by that stream's event.
     for (int k = 1; k < K; ++k) {
         if (!started[(size_t)k]) continue;
         hipStream_t cs = st.copy_streams[(size_t)(k - 1)];
-        HIP_TRY(hipEventRecord(st.ev_join[(size_t)k], cs));
-        HIP_TRY(hipStreamWaitEvent(s, st.ev_join[(size_t)k], 0));
+        hipEvent_t ev = st.ev_join[(size_t)(k - 1)];
+        HIP_TRY(hipEventRecord(ev, cs));
+        HIP_TRY(hipStreamWaitEvent(s, ev, 0));
     }
     return HOCCL_OK;
 }

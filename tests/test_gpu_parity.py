@@ -497,3 +497,29 @@ def test_host_function_handshake_refused_under_a_profiler():
         pytest.skip("engine proxy unavailable")
     assert f"refused {hc.ERR_UNSUPPORTED} True" in r.stdout, r.stdout
     assert "kernel handshake ok True" in r.stdout, r.stdout
+
+
+@pytest.mark.parametrize("streams", [1, 2, 16])
+def test_sdma_copy_stream_counts(streams):
+    """Every copy collective on the HIP SDMA path with 1, 2 and all 16 copy
+    streams (the largest count joins through the last copy stream's event)."""
+    R, n = 8, 20_011
+    with hc.config(copy_path="sdma", copy_streams=streams):
+        x = [W.random_bits(800 + streams, r, n, 2) for r in range(R)]
+        ref = oracle.allgather_new(x, hc.BF16)
+        got = hc.allgather([to_dev(a, hc.BF16) for a in x])
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(got[r], hc.BF16), ref[r], f"allgather streams={streams} r={r}")
+        xa = [W.random_bits(810 + streams, r, R * n, 4).view(np.int32) for r in range(R)]
+        refa = [np.zeros(R * n, np.int32) for _ in range(R)]
+        oracle.alltoall(xa, refa, n, hc.INT32)
+        gota = hc.alltoall([to_dev(a, hc.INT32) for a in xa])
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(gota[r], hc.INT32), refa[r], f"alltoall streams={streams} r={r}")
+        xr = [W.random_values("fp32", 820 + streams, r, n) for r in range(R)]
+        refr = oracle.allreduce_new(xr, hc.FP32)
+        gotr = run_ar(xr, hc.FP32)
+        for r in range(R):
+            assert_bitwise(gotr[r], refr[r], f"allreduce streams={streams} r={r}")
