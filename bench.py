@@ -179,22 +179,39 @@ def direct_reduce_scatter(hc, send_np, steps, warmup):
                                 "bytes_per_launch": st["hbm_bytes_algorithmic"]})
 
 
+def host_cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(x, recvcount, budget_s=12.0):
     """The oracle (single-threaded C) on the same reduce-scatter, repeated
-    until about budget_s seconds of CPU work."""
+    until about budget_s seconds of CPU work, with this thread pinned to one
+    host core for the timing."""
     import numpy as np
     import oracle
     R = len(x)
     out = [np.empty(recvcount, np.uint16) for _ in range(R)]
-    t0 = time.perf_counter()
-    reps = 0
-    while True:
-        oracle.reduce_scatter(x, out, recvcount, oracle.BF16)
-        reps += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
-    sec = (time.perf_counter() - t0) / reps
-    return out, sec, reps
+    saved = os.sched_getaffinity(0)
+    core = min(saved)
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            oracle.reduce_scatter(x, out, recvcount, oracle.BF16)
+            reps += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+        sec = (time.perf_counter() - t0) / reps
+    finally:
+        os.sched_setaffinity(0, saved)
+    return out, sec, reps, core, len(saved)
 
 
 # ---- the other collectives ---------------------------------------------------
@@ -750,12 +767,13 @@ def main():
     parity = None
     if not args.no_cpu:
         log("oracle CPU baseline")
-        ref, csec, reps = cpu_baseline(rs["x"], 25_165_824 // 8)
+        ref, csec, reps, core, ncores = cpu_baseline(rs["x"], 25_165_824 // 8)
         parity = all(np.array_equal(got[r], ref[r]) and np.array_equal(dgot[r], ref[r])
                      for r in range(8))
         cpu = {"value": round(rs["S"] / csec / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                "sample": f"the full reduce-scatter workload, {reps} repetitions, "
-                         f"{csec:.2f} s each on one host core"}
+                         f"{csec:.2f} s each, pinned to host core {core}",
+               "host_cpu": host_cpu_model(), "host_cores_available": ncores}
     if not args.quick:
         gemm = make_gemm()
         extra["gemm_alone"] = dict(ms=round(gemm[3] * 1e3, 4), tflops=round(2 * 8192 ** 3 / gemm[3] / 1e12, 1))
