@@ -206,7 +206,10 @@ typedef struct {
  *   HOCCL_REDUCE_ALGO = ring | direct,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),
  *   HOCCL_SDMA_ENGINE_IDS = "i,j,..." (the SDMA engines the SDMA_ENGINES
- *   proxy may use, in that order; read when the proxy is created).
+ *   proxy may use, in that order; read when the proxy is created),
+ *   HOCCL_PROXY_SCHEDULE = round_robin (ablation: chain c on engine c mod E
+ *   in plan order, instead of the byte-balanced, flow-size-interleaved
+ *   schedule).
  * A set of values that fails validation falls back to the defaults.
  * Optional: every collective initialises lazily on the current device. */
 hoccl_status_t hoccl_init(int device);

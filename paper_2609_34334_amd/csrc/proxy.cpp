@@ -452,10 +452,20 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cb[(size_t)a] > cb[(size_t)b]; });
     std::vector<unsigned long long> load((size_t)E, 0);
     std::vector<int> eng_of_chain((size_t)nch, 0);
+    // HOCCL_PROXY_SCHEDULE=round_robin is the ablation baseline: chain c on
+    // engine c mod E, each engine's copies in plan order.
+    static const bool round_robin = [] {
+        const char *v = std::getenv("HOCCL_PROXY_SCHEDULE");
+        return v && std::strcmp(v, "round_robin") == 0;
+    }();
     for (int ch : order) {
         size_t best = 0;
-        for (size_t k = 1; k < load.size(); ++k)
-            if (load[k] < load[best]) best = k;
+        if (round_robin) {
+            best = (size_t)(ch % E);
+        } else {
+            for (size_t k = 1; k < load.size(); ++k)
+                if (load[k] < load[best]) best = k;
+        }
         eng_of_chain[(size_t)ch] = (int)best;
         load[best] += cb[(size_t)ch];
     }
@@ -475,6 +485,11 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
                 len.push_back((double)of_chain[(size_t)ch].size());
             }
         std::vector<size_t> next(chains.size(), 0);
+        if (round_robin) {
+            for (size_t k = 0; k < chains.size(); ++k)
+                for (size_t i : of_chain[(size_t)chains[k]]) issue.push_back(i);
+            continue;
+        }
         for (int k : interleave_chunks(len, 1.0)) {
             int ch = chains[(size_t)k];
             issue.push_back(of_chain[(size_t)ch][next[(size_t)k]++]);
