@@ -481,6 +481,42 @@ def bench_p2p_sizes(hc, reps):
     return dict(workload="single bf16 message rank 0 -> 1, algbw GB/s", rows=rows)
 
 
+def bench_rs_variants(hc, reps):
+    """The ring reduce-scatter beyond the headline: the same 25,165,824
+    elements per rank in fp32 and int32 (12 bytes per element per step), and
+    bf16 at R = 2 ... 64 virtual ranks with the same bytes per rank."""
+    import torch
+    n_in = 25_165_824
+    out = {"dtypes": {}, "ranks": {}}
+
+    def run(send, recv, R, dt_bytes):
+        med, _ = event_time(lambda: hc.reduce_scatter(send, recv), reps)
+        st = hc.last_stats()
+        return dict(ms=round(med * 1e3, 4), algbw_GBs=round(n_in * dt_bytes / med / 1e9, 1),
+                    hbm_TBs=round(st["hbm_bytes_algorithmic"] / med / 1e12, 3),
+                    hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
+                    launches=st["reduce_launches"])
+    for name, dtype in (("fp32", torch.float32), ("int32", torch.int32)):
+        R = 8
+        if dtype == torch.int32:
+            send = [torch.randint(-1000, 1000, (n_in,), dtype=dtype, device="cuda") for _ in range(R)]
+        else:
+            send = [torch.randn(n_in, device="cuda") for _ in range(R)]
+        recv = [torch.empty(n_in // R, dtype=dtype, device="cuda") for _ in range(R)]
+        out["dtypes"][name] = run(send, recv, R, 4)
+        del send, recv
+    for R in (2, 4, 16, 32, 64):
+        n = n_in // R
+        send = [torch.randn(R * n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+        recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+        out["ranks"][f"R{R}"] = run(send, recv, R, 2)
+        del send, recv
+        torch.cuda.empty_cache()
+    out["workload"] = ("ring reduce-scatter, 25,165,824 elements per rank: fp32 and int32 at R=8; "
+                       "bf16 at other R (the headline is bf16 at R=8)")
+    return out
+
+
 def copy_ceiling(hc):
     """The measured streaming ceiling the reduction kernels are also judged
     against: the library's CU copy kernel at its automatic budget moving
@@ -790,6 +826,11 @@ def main():
             extra["allreduce_bf16_R8_bucket"] = bench_allreduce_bucket(hc, W, 10)
         except Exception as e:
             extra["allreduce_bf16_R8_bucket"] = {"error": repr(e)}
+        log("reduce-scatter variants")
+        try:
+            extra["reduce_scatter_variants"] = bench_rs_variants(hc, 10)
+        except Exception as e:
+            extra["reduce_scatter_variants"] = {"error": repr(e)}
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
         extra["small_message_latency"] = bench_small_message(hc, 30)
