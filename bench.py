@@ -520,7 +520,7 @@ def bench_rs_variants(hc, reps):
 def copy_ceiling(hc):
     """The measured streaming ceiling the reduction kernels are also judged
     against: the library's CU copy kernel at its automatic budget moving
-    1 GiB (2 GiB of HBM traffic per copy), ten copies back to back between
+    2 GiB (4 GiB of HBM traffic per copy), ten copies back to back between
     two events; 2 GiB per buffer keeps the data well outside the 256 MB
     last-level cache.  Returns HBM GB/s."""
     import torch
@@ -650,10 +650,16 @@ FOLD_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "fold_kernel_rs_bf16_R8_tr
 
 
 def kernel_source_hash():
+    """SHA-256 (16 hex digits) of kernels.hip without its // comments and
+    blank lines: any change to the code voids the committed counter figures,
+    an edit of a comment does not."""
     import hashlib
+    import re
     path = os.path.join(ROOT, "paper_2609_34334_amd", "csrc", "kernels.hip")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    with open(path, encoding="utf-8") as f:
+        lines = [re.sub(r"//.*", "", line).rstrip() for line in f]
+    code = "\n".join(line for line in lines if line)
+    return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
 def measured_traffic(summary=TRAFFIC_SUMMARY):

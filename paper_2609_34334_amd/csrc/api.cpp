@@ -316,24 +316,27 @@ hoccl_status_t ensure_ws(DeviceState &st, size_t bytes, bool capturing) {
     return HOCCL_OK;
 }
 
-// Workgroups per launch.  An explicit budget wins.  Otherwise about two
-// 16-byte vectors per thread of the largest launch, between one workgroup
-// per CU and 32 per CU (8192 on MI355X): measured on the bf16 ring step, the
-// streaming kernels keep gaining up to roughly one vector per thread.
+// Workgroups per launch.  An explicit budget wins.  Otherwise enough for
+// about one pass of the kernel's main loop per thread in the largest launch,
+// between one workgroup per CU and 64 per CU (16384 on MI355X): measured on
+// the headline bf16 ring and fold, the streaming kernels keep gaining up to
+// about one pass per thread and lose nothing beyond.
 int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan &p, int threads) {
     if (cfg.workgroups_per_step > 0) return cfg.workgroups_per_step;
-    unsigned long long bytes = 0;
+    unsigned long long passes = 0;  // thread passes of the largest launch
+    auto need = [&](unsigned long long work, size_t per_thread) {
+        passes = std::max(passes, (work + per_thread - 1) / per_thread);
+    };
     for (const ReduceStep &s : p.reduce_steps) {
-        unsigned long long b = 0;
-        for (const ReduceSeg &g : s.segs) b += (unsigned long long)g.n * dtype_size(p.dtype);
-        bytes = std::max(bytes, b);
+        unsigned long long n = 0;
+        for (const ReduceSeg &g : s.segs) n += g.n;
+        need(n, reduce_step_elems_per_thread(p.dtype, s.phase));
     }
-    if (p.has_fold) bytes = std::max(bytes, (unsigned long long)p.fold.total * dtype_size(p.dtype));
+    if (p.has_fold) need(p.fold.total, fold_elems_per_thread(p.dtype));
     if (cfg.copy_path == HOCCL_COPY_KERNEL)
-        for (const CopyOp &c : p.copies) bytes = std::max(bytes, (unsigned long long)c.bytes * p.R);
-    unsigned long long vec = bytes / 16;
-    unsigned long long wg = (vec + 2ull * threads - 1) / (2ull * threads);
-    unsigned long long lo = (unsigned long long)st.num_cus, hi = 32ull * st.num_cus;
+        for (const CopyOp &c : p.copies) need((unsigned long long)c.bytes * p.R, copy_bytes_per_thread());
+    unsigned long long wg = (passes + (unsigned long long)threads - 1) / (unsigned long long)threads;
+    unsigned long long lo = (unsigned long long)st.num_cus, hi = 64ull * st.num_cus;
     return (int)std::min(hi, std::max(lo, wg));
 }
 

@@ -179,6 +179,12 @@ hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, i
 hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
                        hipStream_t s);
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s);
+
+// Work one thread does in one pass of each kernel's main loop (elements of
+// the collective's dtype, or bytes for the copy kernel).
+size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph);
+size_t fold_elems_per_thread(hoccl_dtype_t dt);
+size_t copy_bytes_per_thread();
 hipError_t launch_handshake(const HandshakeArgs &a, hipStream_t s);
 
 }  // namespace hoccl

@@ -15,6 +15,8 @@
 // MFMA: the limit is memory bandwidth, not arithmetic.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "hoccl_internal.h"
 
 namespace hoccl {
@@ -46,8 +48,10 @@ struct TI32 {
     static __device__ __forceinline__ uint32_t narrow(uint32_t v) { return v; }
 };
 
+// VE elements in one vector register group; aligned to its size (at most
+// 16 bytes) so that it loads as one 8- or 16-byte access per piece.
 template <typename S, int VE>
-struct alignas(16) Pack {
+struct alignas(sizeof(S) * VE < 16 ? sizeof(S) * VE : 16) Pack {
     S v[VE];
 };
 
@@ -71,9 +75,6 @@ struct alignas(16) Pack {
 #ifndef HOCCL_FOLD_NT
 #define HOCCL_FOLD_NT 1
 #endif
-#ifndef HOCCL_FOLD_UNROLL
-#define HOCCL_FOLD_UNROLL 1
-#endif
 #ifndef HOCCL_FOLD_NT_OUT
 #define HOCCL_FOLD_NT_OUT 1
 #endif
@@ -83,30 +84,57 @@ constexpr int kNtMiddle = (HOCCL_NT_X ? 2 : 0);
 constexpr int kNtLast = (HOCCL_NT_X ? 2 : 0) | (HOCCL_NT_FINAL ? 4 : 0);
 constexpr int kNtOnly = (HOCCL_NT_X ? 3 : 0) | (HOCCL_NT_FINAL ? 4 : 0);
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// Lane layout of the ring step.  A lane holds VE consecutive elements of
+// every operand.  Where bf16 meets fp32 partials, VE = 4: a lane moves 8 B
+// of bf16 and 16 B of fp32, so each load or store instruction of a wave
+// covers one contiguous span (512 B or 1 KiB).  With VE = 8 the fp32 side
+// would take two 16-byte accesses 32 B apart per lane, each instruction
+// touching every line of a 2 KiB span half; that layout ran the headline
+// reduce-scatter about 5% slower.  bf16-only steps keep 16-byte vectors.
+constexpr int kVeBf16Partial = 4;
+constexpr int kVeBf16Only = 8;
+constexpr int kVe32 = 4;
 
-// 16-byte-granular vector load / store of a Pack, optionally non-temporal.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Vector load / store of a Pack in 16-byte pieces (8 bytes for an 8-byte
+// Pack), optionally non-temporal.
 template <bool NT, typename P>
 __device__ __forceinline__ P ldp(const P *p) {
-    static_assert(sizeof(P) % 16 == 0, "Pack must be a multiple of 16 bytes");
+    static_assert(sizeof(P) == 8 || sizeof(P) % 16 == 0, "Pack must be 8 bytes or a multiple of 16");
     P r;
+    if constexpr (sizeof(P) == 8) {
+        u32x2 v = NT ? __builtin_nontemporal_load((const u32x2 *)p) : *(const u32x2 *)p;
+        __builtin_memcpy(&r, &v, 8);
+    } else {
 #pragma unroll
-    for (int i = 0; i < (int)(sizeof(P) / 16); ++i) {
-        u32x4 v = NT ? __builtin_nontemporal_load((const u32x4 *)p + i) : ((const u32x4 *)p)[i];
-        __builtin_memcpy((char *)&r + 16 * i, &v, 16);
+        for (int i = 0; i < (int)(sizeof(P) / 16); ++i) {
+            u32x4 v = NT ? __builtin_nontemporal_load((const u32x4 *)p + i) : ((const u32x4 *)p)[i];
+            __builtin_memcpy((char *)&r + 16 * i, &v, 16);
+        }
     }
     return r;
 }
 template <bool NT, typename P>
 __device__ __forceinline__ void stp(P *p, const P &x) {
-#pragma unroll
-    for (int i = 0; i < (int)(sizeof(P) / 16); ++i) {
-        u32x4 v;
-        __builtin_memcpy(&v, (const char *)&x + 16 * i, 16);
+    if constexpr (sizeof(P) == 8) {
+        u32x2 v;
+        __builtin_memcpy(&v, &x, 8);
         if (NT)
-            __builtin_nontemporal_store(v, (u32x4 *)p + i);
+            __builtin_nontemporal_store(v, (u32x2 *)p);
         else
-            ((u32x4 *)p)[i] = v;
+            *(u32x2 *)p = v;
+    } else {
+#pragma unroll
+        for (int i = 0; i < (int)(sizeof(P) / 16); ++i) {
+            u32x4 v;
+            __builtin_memcpy(&v, (const char *)&x + 16 * i, 16);
+            if (NT)
+                __builtin_nontemporal_store(v, (u32x4 *)p + i);
+            else
+                ((u32x4 *)p)[i] = v;
+        }
     }
 }
 
@@ -248,46 +276,41 @@ __device__ __forceinline__ void fold_chunk(const FoldArgs &a, int j, int lb, int
     constexpr bool NT = HOCCL_FOLD_NT;
     constexpr bool NTO = HOCCL_FOLD_NT_OUT;
     if constexpr (NR > 0) {
-        // Every operand's vector is loaded before the in-order adds consume
-        // them; with HOCCL_FOLD_UNROLL == 2 two vectors per thread are in
-        // flight (two separate arrays: a 2-D array is not kept in registers).
-        auto store = [&](uint64_t i, const P &y) {
-            for (int q = 0; q < nout; ++q) stp<NTO>((P *)(dst(q) + h) + i, y);
-        };
-        // Written out (no helper taking the array) so that the operand
-        // arrays stay in registers.
-#define HOCCL_FOLD_ARRAY(ARR, OUT)                                               \
-    P OUT;                                                                       \
-    {                                                                            \
-        A acc[VE];                                                               \
-        _Pragma("unroll") for (int e = 0; e < VE; ++e) acc[e] = T::widen(ARR[0].v[e]); \
-        _Pragma("unroll") for (int k = 1; k < NR; ++k)                            \
-            _Pragma("unroll") for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(ARR[k].v[e]); \
-        _Pragma("unroll") for (int e = 0; e < VE; ++e) OUT.v[e] = T::narrow(acc[e]); \
-    }
-        uint64_t i = t;
-        if constexpr (HOCCL_FOLD_UNROLL == 2) {
-            for (; i + stride < nv; i += 2 * stride) {
-                P va[NR], vb[NR];
+        // The operand and output pointers are computed once, outside the
+        // loop; every operand's vector is loaded before the in-order adds
+        // consume them.  Reading an output pointer from the argument buffer
+        // inside the loop put a scalar load and its wait in front of every
+        // store (about 7% of the headline fold's time).
+        const P *sp[NR];
 #pragma unroll
-                for (int k = 0; k < NR; ++k) {
-                    va[k] = ldp<NT>((const P *)(src(k) + h) + i);
-                    vb[k] = ldp<NT>((const P *)(src(k) + h) + i + stride);
-                }
-                HOCCL_FOLD_ARRAY(va, ya)
-                HOCCL_FOLD_ARRAY(vb, yb)
-                store(i, ya);
-                store(i + stride, yb);
+        for (int k = 0; k < NR; ++k) sp[k] = (const P *)(src(k) + h);
+        auto run = [&](auto outs) {
+            constexpr int NO = decltype(outs)::value;
+            P *dp[NO];
+#pragma unroll
+            for (int q = 0; q < NO; ++q) dp[q] = (P *)(dst(q) + h);
+            for (uint64_t i = t; i < nv; i += stride) {
+                P v[NR];
+#pragma unroll
+                for (int k = 0; k < NR; ++k) v[k] = ldp<NT>(sp[k] + i);
+                A acc[VE];
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = T::widen(v[0].v[e]);
+#pragma unroll
+                for (int k = 1; k < NR; ++k)
+#pragma unroll
+                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[k].v[e]);
+                P y;
+#pragma unroll
+                for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
+#pragma unroll
+                for (int q = 0; q < NO; ++q) stp<NTO>(dp[q] + i, y);
             }
-        }
-        for (; i < nv; i += stride) {
-            P v[NR];
-#pragma unroll
-            for (int k = 0; k < NR; ++k) v[k] = ldp<NT>((const P *)(src(k) + h) + i);
-            HOCCL_FOLD_ARRAY(v, y)
-            store(i, y);
-        }
-#undef HOCCL_FOLD_ARRAY
+        };
+        if (a.write_all)
+            run(std::integral_constant<int, NR>{});
+        else
+            run(std::integral_constant<int, 1>{});
         return;
     }
     for (uint64_t i = t; i < nv; i += stride) {
@@ -331,11 +354,8 @@ __device__ __forceinline__ const A &kernargs() {
     return *(const A *)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
-#ifndef HOCCL_FOLD_LB
-#define HOCCL_FOLD_LB 1024
-#endif
 template <class T, int VE, int NR>
-__global__ void __launch_bounds__(HOCCL_FOLD_LB) fold_kernel(FoldArgs) {
+__global__ void __launch_bounds__(1024) fold_kernel(FoldArgs) {
     const FoldArgs &a = kernargs<FoldArgs>();
     for_each_segment(a.R, [&](int j, int lb, int nb) { fold_chunk<T, VE, NR>(a, j, lb, nb); });
 }
@@ -382,9 +402,13 @@ __device__ __forceinline__ void copy_segment(const CSegArg &s, int lb, int nb) {
     }
 }
 
+constexpr int kCopyUnroll = 2;
+
 __global__ void __launch_bounds__(1024) copy_kernel(CopyArgs) {
     const CopyArgs &a = kernargs<CopyArgs>();
-    for_each_segment(a.nseg, [&](int seg, int lb, int nb) { copy_segment<2>(a.seg[seg], lb, nb); });
+    for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
+        copy_segment<kCopyUnroll>(a.seg[seg], lb, nb);
+    });
 }
 
 }  // namespace
@@ -407,30 +431,57 @@ static hipError_t launch_rs(const ReduceArgs &a, int wg, int threads, hipStream_
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg, int threads,
                               hipStream_t s) {
     constexpr int UB = HOCCL_RS_UNROLL_BF16, U4 = HOCCL_RS_UNROLL_32;
+    constexpr int VP = kVeBf16Partial, VB = kVeBf16Only, V4 = kVe32;
     if (dt == HOCCL_BF16) {
+        // A launch that leaves each thread several passes (a small
+        // workgroup budget) keeps twice the vectors in flight per thread:
+        // there the bytes in flight per wave, not the number of waves, set
+        // the rate (8 workgroups: 777 us per headline step with 2 vectors,
+        // 497 us with 4).
+        uint64_t n = 0;
+        for (int k = 0; k < a.nseg; ++k) n += a.seg[k].n;
+        const bool deep = n > (uint64_t)wg * (uint64_t)threads * (uint64_t)(VP * UB);
+        if (deep) {
+            switch (ph) {
+            case PH_FIRST: return launch_rs<TBF16, TBF16, TF32, VP, 2 * UB, kNtFirst>(a, wg, threads, s);
+            case PH_MIDDLE: return launch_rs<TF32, TBF16, TF32, VP, 2 * UB, kNtMiddle>(a, wg, threads, s);
+            case PH_LAST: return launch_rs<TF32, TBF16, TBF16, VP, 2 * UB, kNtLast>(a, wg, threads, s);
+            case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, VB, UB, kNtOnly>(a, wg, threads, s);
+            }
+        }
         switch (ph) {
-        case PH_FIRST: return launch_rs<TBF16, TBF16, TF32, 8, UB, kNtFirst>(a, wg, threads, s);
-        case PH_MIDDLE: return launch_rs<TF32, TBF16, TF32, 8, UB, kNtMiddle>(a, wg, threads, s);
-        case PH_LAST: return launch_rs<TF32, TBF16, TBF16, 8, UB, kNtLast>(a, wg, threads, s);
-        case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, 8, UB, kNtOnly>(a, wg, threads, s);
+        case PH_FIRST: return launch_rs<TBF16, TBF16, TF32, VP, UB, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TF32, TBF16, TF32, VP, UB, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TF32, TBF16, TBF16, VP, UB, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, VB, UB, kNtOnly>(a, wg, threads, s);
         }
     } else if (dt == HOCCL_FP32) {
         switch (ph) {
-        case PH_FIRST: return launch_rs<TF32, TF32, TF32, 4, U4, kNtFirst>(a, wg, threads, s);
-        case PH_MIDDLE: return launch_rs<TF32, TF32, TF32, 4, U4, kNtMiddle>(a, wg, threads, s);
-        case PH_LAST: return launch_rs<TF32, TF32, TF32, 4, U4, kNtLast>(a, wg, threads, s);
-        case PH_ONLY: return launch_rs<TF32, TF32, TF32, 4, U4, kNtOnly>(a, wg, threads, s);
+        case PH_FIRST: return launch_rs<TF32, TF32, TF32, V4, U4, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TF32, TF32, TF32, V4, U4, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TF32, TF32, TF32, V4, U4, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TF32, TF32, TF32, V4, U4, kNtOnly>(a, wg, threads, s);
         }
     } else if (dt == HOCCL_INT32) {
         switch (ph) {
-        case PH_FIRST: return launch_rs<TI32, TI32, TI32, 4, U4, kNtFirst>(a, wg, threads, s);
-        case PH_MIDDLE: return launch_rs<TI32, TI32, TI32, 4, U4, kNtMiddle>(a, wg, threads, s);
-        case PH_LAST: return launch_rs<TI32, TI32, TI32, 4, U4, kNtLast>(a, wg, threads, s);
-        case PH_ONLY: return launch_rs<TI32, TI32, TI32, 4, U4, kNtOnly>(a, wg, threads, s);
+        case PH_FIRST: return launch_rs<TI32, TI32, TI32, V4, U4, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TI32, TI32, TI32, V4, U4, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TI32, TI32, TI32, V4, U4, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TI32, TI32, TI32, V4, U4, kNtOnly>(a, wg, threads, s);
         }
     }
     return hipErrorInvalidValue;
 }
+
+// Elements one thread covers in one pass of each kernel's main loop; the
+// executor sizes automatic launches to about one pass per thread.
+size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph) {
+    if (dt == HOCCL_BF16)
+        return (size_t)(ph == PH_ONLY ? kVeBf16Only : kVeBf16Partial) * HOCCL_RS_UNROLL_BF16;
+    return (size_t)kVe32 * HOCCL_RS_UNROLL_32;
+}
+size_t fold_elems_per_thread(hoccl_dtype_t dt) { return 16 / dtype_size(dt); }
+size_t copy_bytes_per_thread() { return 16 * kCopyUnroll; }
 
 template <class T, int VE>
 static hipError_t launch_fold_t(const FoldArgs &a, int wg, int threads, hipStream_t s) {
