@@ -517,6 +517,55 @@ def bench_rs_variants(hc, reps):
     return out
 
 
+def bench_rs_graph(hc, send_np, steps):
+    """The headline ring reduce-scatter captured ten steps at a time into a
+    HIP graph and replayed, against the same steps issued eagerly on the
+    same stream; the replayed results must equal the eager ones bit for
+    bit."""
+    import torch
+    R = len(send_np)
+    n = send_np[0].size // R
+    send = [bf16_dev(a) for a in send_np]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    s = torch.cuda.Stream()
+
+    def step():
+        hc.reduce_scatter(send, recv, stream=s)
+
+    def timed(fn, k):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(k):
+            fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 1e3 / k
+
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        eager = timed(step, steps)
+    ref = [t.clone() for t in recv]
+    per_graph = 10
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(per_graph):
+            step()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        g.replay()
+        torch.cuda.synchronize()
+        replay = timed(g.replay, max(1, steps // per_graph)) / per_graph
+    same = all(torch.equal(a.view(torch.int16), b.view(torch.int16)) for a, b in zip(ref, recv))
+    S = R * n * 2
+    return {"workload": "headline ring reduce-scatter, 10 steps per captured graph",
+            "eager_us": round(eager * 1e6, 1), "graph_replay_us": round(replay * 1e6, 1),
+            "eager_algbw_GBs": round(S / eager / 1e9, 1), "graph_algbw_GBs": round(S / replay / 1e9, 1),
+            "same_bits": same}
+
+
 def copy_ceiling(hc):
     """The measured streaming ceiling the reduction kernels are also judged
     against: the library's CU copy kernel at its automatic budget moving
@@ -837,6 +886,11 @@ def main():
             extra["reduce_scatter_variants"] = bench_rs_variants(hc, 10)
         except Exception as e:
             extra["reduce_scatter_variants"] = {"error": repr(e)}
+        log("reduce-scatter in a graph")
+        try:
+            extra["reduce_scatter_graph"] = bench_rs_graph(hc, rs["x"], args.steps)
+        except Exception as e:
+            extra["reduce_scatter_graph"] = {"error": repr(e)}
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
         extra["small_message_latency"] = bench_small_message(hc, 30)
