@@ -10,21 +10,23 @@
 //   proxy:   see start == START, write start := 0 (acknowledge),
 //            run the copies, write finish := FINISH, see finish == 0.
 //
-// The stream's side runs as one dispatch of a one-lane handshake kernel
-// that performs all four flag operations in order, sleeping between polls
-// (HIP's own stream memory operations are separate spinning kernels here,
-// one dispatch each).  While the copies run, that lane occupies a wave slot
-// and holds back every later packet of its hardware queue -- including
-// kernels of other streams sharing the queue.  So by default it runs on a
-// private stream created with a CU mask: such a stream gets a hardware queue
-// of its own, and the caller's stream joins it through HIP events (fork
-// before the start path, join after the completion path).  The handshake can
-// also be put on the caller's stream directly, the paper's literal form.
-//
-// A host function (hipLaunchHostFunc) that blocks until the copies are done
-// would need no GPU code at all, but it blocks the runtime thread that also
-// delivers signal callbacks (a profiler's copy-completion callbacks, for
-// one), so it is not used.
+// The stream's side of the handshake takes one of three forms
+// (hoccl_config_t.proxy_handshake):
+//   0 (default)  one dispatch of a one-lane handshake kernel on the caller's
+//                stream, performing all four flag operations in order and
+//                sleeping between polls.  HIP's own stream memory operations
+//                are separate spinning kernels here, one dispatch each.
+//                While the copies run, that lane holds a wave slot on one CU.
+//   1            the same kernel on a private stream created with a CU mask,
+//                which gets a hardware queue of its own; the caller's stream
+//                joins it through HIP events (fork before the start path,
+//                join after the completion path).
+//   2            a host function (hipLaunchHostFunc) that performs the four
+//                steps on the runtime's callback thread: no GPU code waits.
+//                It blocks that thread while the copies run, and a profiler
+//                may need the same thread to complete copies, so the library
+//                refuses this form while a profiler is loaded.
+// Every form gives up after a bounded time, so the stream always drains.
 #include "proxy.h"
 #include "hoccl_internal.h"
 #include "schedule.h"
@@ -149,7 +151,7 @@ class ProxyImpl {
     std::vector<uint32_t> engines;  // id bits of usable engines
     uint32_t *flags = nullptr;      // kSlots * kFlagsPerSlot flags, one per cache line
     uint64_t ticks_per_ms = 100000;  // device wall clock
-    hipStream_t hs = nullptr;       // private one-CU stream for the handshake
+    hipStream_t hs = nullptr;       // private CU-masked stream for handshake form 1
     hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     std::mutex mu;
     std::condition_variable cv_work, cv_slot;
