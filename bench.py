@@ -250,59 +250,123 @@ def _gemm_run(gemm, k=20):
     return g0, g1, ts
 
 
-def _gated(gemm, enqueue_s, collective=None, n_coll=0):
-    """Hold the GEMM stream (and the collective stream) behind one event that
-    a spin on a third stream releases after the host has enqueued
-    everything; then 20 GEMMs, and `n_coll` collectives.  Returns the
-    collective window (c0, c1) and the GEMM event pairs."""
+_GATE = {}
+
+
+def host_gate():
+    """A gate the host opens: returns (event, open).  `event` completes once
+    `open()` has been called, so work on several streams that waits on it
+    starts together, however long the host takes to enqueue that work.  An
+    own-queue stream waits (hipStreamWaitValue32, equality) on a token in
+    coherent host memory; a timer opens the gate after 30 s in any case, so
+    the wait always ends."""
+    import ctypes
+    import threading
+    import torch
+    if not _GATE:
+        hip = ctypes.CDLL("libamdhip64.so.7")    # the HIP runtime torch has loaded
+        V = ctypes.c_void_p
+        hip.hipHostMalloc.argtypes = [ctypes.POINTER(V), ctypes.c_size_t, ctypes.c_uint]
+        hip.hipStreamWaitValue32.argtypes = [V, V, ctypes.c_uint32, ctypes.c_uint, ctypes.c_uint32]
+        p = V()
+        if hip.hipHostMalloc(ctypes.byref(p), 64, 0x2 | 0x40000000) != 0:   # mapped | coherent
+            raise RuntimeError("hipHostMalloc of the gate flag failed")
+        _GATE.update(hip=hip, flag=p.value, cell=ctypes.c_uint32.from_address(p.value),
+                     stream=dedicated_stream(), token=0)
+    g = _GATE
+    g["token"] = g["token"] % 1_000_000 + 1
+    k = g["token"]
+    g["cell"].value = 0
+    s = g["stream"]
+    if g["hip"].hipStreamWaitValue32(ctypes.c_void_p(s.cuda_stream), ctypes.c_void_p(g["flag"]), k,
+                                     0x1, 0xFFFFFFFF) != 0:
+        raise RuntimeError("hipStreamWaitValue32 failed")
+    ev = torch.cuda.Event()
+    ev.record(s)
+    timer = threading.Timer(30.0, lambda: setattr(g["cell"], "value", k))
+    timer.start()
+
+    def open_gate():
+        timer.cancel()
+        g["cell"].value = k
+
+    return ev, open_gate
+
+
+def _gated(gemm, collective=None, n_coll=0):
+    """20 GEMMs and the first of `n_coll` collectives, both held behind one
+    host gate so that they start together; the remaining collectives are
+    enqueued after the gate opens, as fast as the host issues them (a
+    collective's host cost is part of what runs beside the GEMMs, and the
+    engine proxy accepts only so many operations ahead).  An event follows
+    each collective.  Returns the collective window start c0, the
+    collective's end events and the GEMM event pairs."""
     import torch
     gs, cs = gemm[4], gemm[5]
     torch.cuda.synchronize()
-    gate_s = torch.cuda.Stream()
-    with torch.cuda.stream(gate_s):
-        torch.cuda._sleep(int((1.5 * enqueue_s + 0.02) * 2.4e9))
-        gate = torch.cuda.Event()
-        gate.record(gate_s)
-    gs.wait_event(gate)
-    c0 = c1 = None
+    gate, open_gate = host_gate()
+    c0 = None
+    ends = []
+
+    def one():
+        collective(cs)
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(cs)
+        ends.append(e)
+
+    try:
+        gs.wait_event(gate)
+        if collective is not None:
+            cs.wait_event(gate)
+            with torch.cuda.stream(cs):
+                c0 = torch.cuda.Event(enable_timing=True)
+                c0.record(cs)
+                one()
+        _, _, ts = _gemm_run(gemm)
+    finally:
+        open_gate()
     if collective is not None:
-        cs.wait_event(gate)
         with torch.cuda.stream(cs):
-            c0 = torch.cuda.Event(enable_timing=True)
-            c0.record(cs)
-            for _ in range(n_coll):
-                collective(cs)
-            c1 = torch.cuda.Event(enable_timing=True)
-            c1.record(cs)
-    _, _, ts = _gemm_run(gemm)
+            for _ in range(n_coll - 1):
+                one()
     torch.cuda.synchronize()
-    return c0, c1, ts
+    return c0, ends, ts
 
 
 def gemm_slowdown(hc, collective, med, gemm):
-    """Slowdown of the GEMM while `collective` loops beside it.  GEMM i of
-    the concurrent run is compared with GEMM i of a run alone under the same
-    gate (GEMM time drifts as clocks settle, so position matters); only
-    GEMMs that ran entirely inside the collective window count.  Returns
-    (median slowdown, fraction of the 20 GEMMs that overlapped)."""
-    import time as _t
+    """Interference between `collective` looping on one queue and a bf16
+    GEMM loop on another.  GEMM i of the concurrent run is compared with
+    GEMM i of runs alone under the same gate, one before and one after
+    (GEMM time drifts as clocks settle, so position matters); only GEMMs
+    that ran entirely inside the collective window count.  The collective's own slowdown is its time per
+    call while the GEMMs ran (the calls that finished before the last GEMM,
+    from the common start) against `med`, its median time alone.  Returns
+    (median GEMM slowdown, fraction of the 20 GEMMs that overlapped,
+    collective slowdown)."""
     import torch
     t_alone, cs = gemm[3], gemm[5]
     n_coll = int(45 * t_alone / max(med, 1e-6)) + 3
-    t0 = _t.perf_counter()
     with torch.cuda.stream(cs):
         collective(cs)
-    host_call = _t.perf_counter() - t0
-    enqueue = n_coll * host_call + 0.002
-    _, _, alone = _gated(gemm, enqueue)
-    base = [a.elapsed_time(b) for a, b in alone]
-    c0, c1, ts = _gated(gemm, enqueue, collective, n_coll)
-    end = c0.elapsed_time(c1)
+    _, _, before = _gated(gemm)
+    c0, ends, ts = _gated(gemm, collective, n_coll)
+    _, _, after = _gated(gemm)
+    # GEMM i alone, averaged over a run before and a run after the
+    # concurrent one, so that a drift of the clocks across the three runs
+    # does not read as a slowdown or a speed-up.
+    base = [(a.elapsed_time(b) + c.elapsed_time(d)) / 2 for (a, b), (c, d) in zip(before, after)]
+    end = c0.elapsed_time(ends[-1])
     ratios = [a.elapsed_time(b) / base[i] for i, (a, b) in enumerate(ts)
               if c0.elapsed_time(a) >= 0 and c0.elapsed_time(b) <= end]
     if not ratios:
-        return None, 0.0
-    return round(statistics.median(ratios) - 1, 4), round(len(ratios) / len(ts), 3)
+        return None, 0.0, None
+    # The collective's calls that finished while the GEMMs still ran, timed
+    # from the common start: their mean time per call against `med`.  None
+    # when not even the first call finished before the last GEMM.
+    g_hi = c0.elapsed_time(ts[-1][1])
+    done = [t for t in (c0.elapsed_time(e) for e in ends) if t <= g_hi]
+    coll = round(done[-1] / len(done) / 1e3 / med - 1, 4) if done else None
+    return (round(statistics.median(ratios) - 1, 4), round(len(ratios) / len(ts), 3), coll)
 
 
 def make_gemm():
@@ -340,7 +404,7 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
                  path_used=["auto", "sdma", "engines", "kernel"][st["copy_path_used"]],
                  cus_used=st["cus_used_max"], host_enqueue_us=round(st["host_enqueue_us"], 1))
         if gemm is not None:
-            r["gemm_slowdown"], r["gemm_overlap"] = gemm_slowdown(hc, run, med, gemm)
+            r["gemm_slowdown"], r["gemm_overlap"], r["collective_slowdown"] = gemm_slowdown(hc, run, med, gemm)
         res[name] = r
         hc.set_config(**saved)
     return res
@@ -615,22 +679,27 @@ def bench_small_message(hc, reps):
     return dict(workload="one 4 KiB message rank 0 -> 1 (stream-manager round trip)", **out)
 
 
-def bench_rs_workgroups(hc, x, reps):
+def bench_rs_workgroups(hc, x, reps, gemm=None):
     """Ring reduce-scatter of the headline at a fixed workgroup budget: the
-    CU footprint / bandwidth trade-off of the reduction kernels."""
+    CU footprint / bandwidth trade-off of the reduction kernels, and, with
+    `gemm`, the slowdown of a bf16 8192^3 GEMM running beside it."""
     import torch
     R = len(x)
     n = x[0].size // R
     send = [bf16_dev(a) for a in x]
     recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     out = {}
-    for w in (16, 64, 256, 1024, 0):
+    for w in (8, 16, 64, 256, 1024, 0):
         hc.set_config(workgroups_per_step=w)
         med, _ = event_time(lambda: hc.reduce_scatter(send, recv), reps)
         st = hc.last_stats()
-        out[f"wg{st['workgroups_per_step']}"] = dict(algbw_GBs=round(R * n * 2 / med / 1e9, 2),
-                                                    hbm_GBs=round(st["hbm_bytes_algorithmic"] / med / 1e9, 1),
-                                                    cus_used=st["cus_used_max"])
+        row = dict(ms=round(med * 1e3, 4), algbw_GBs=round(R * n * 2 / med / 1e9, 2),
+                   hbm_GBs=round(st["hbm_bytes_algorithmic"] / med / 1e9, 1),
+                   cus_used=st["cus_used_max"])
+        if gemm is not None:
+            row["gemm_slowdown"], row["gemm_overlap"], row["collective_slowdown"] = gemm_slowdown(
+                hc, lambda s: hc.reduce_scatter(send, recv, stream=s), med, gemm)
+        out[f"wg{st['workgroups_per_step']}"] = row
     hc.set_config(workgroups_per_step=0)
     return out
 
@@ -868,7 +937,7 @@ def main():
     if not args.quick:
         gemm = make_gemm()
         extra["gemm_alone"] = dict(ms=round(gemm[3] * 1e3, 4), tflops=round(2 * 8192 ** 3 / gemm[3] / 1e12, 1))
-        extra["reduce_scatter_workgroups"] = bench_rs_workgroups(hc, rs["x"], 3)
+        extra["reduce_scatter_workgroups"] = bench_rs_workgroups(hc, rs["x"], 3, gemm)
         for name, fn in [("allreduce_fp32_R4", bench_allreduce), ("allgather_fsdp", bench_allgather),
                          ("p2p_pp", bench_p2p), ("alltoallv_ep", bench_a2a)]:
             log(name)

@@ -519,13 +519,14 @@ bool profiler_present() {
 }
 
 // Copy path for a plan.  An explicit choice wins; AUTO is the HIP runtime's
-// device-to-device SDMA path.  It is the only one that is free of compute
-// units end to end: the engine proxy moves data on SDMA engines too, but the
-// stream has to wait for a CPU thread, and this HIP offers no such wait
-// without a resident wave (its stream memory operations are spinning
-// kernels even on signal memory).  One resident wave alone slows a
-// full-occupancy bf16 GEMM by about half, beside which the HIP path costs
-// nothing measurable.
+// device-to-device SDMA path.  It runs no GPU code, is the fastest path alone
+// for large transfers, needs no host thread, can be captured into a graph
+// and is safe under a profiler.  The engine proxy with the host-function
+// handshake runs no GPU code either, and keeps its copy rate beside a
+// full-occupancy GEMM where the HIP path's copies slow down several times;
+// callers that overlap copies with heavy compute select it explicitly.  The
+// proxy's default handshake kernel keeps one wave resident, which alone
+// costs such a GEMM about half its speed.
 hoccl_copy_path_t resolve_path(const DeviceState &, const hoccl_config_t &cfg, const Plan &) {
     return cfg.copy_path == HOCCL_COPY_AUTO ? HOCCL_COPY_SDMA : cfg.copy_path;
 }
