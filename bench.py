@@ -386,7 +386,12 @@ def make_gemm():
     return (A, B, C, t, gs, cs)
 
 
-PATHS = [("sdma", {}), ("engines", {}), ("engines_hostfn", {"proxy_handshake": 2}), ("kernel", {})]
+# Copy paths compared by the copy workloads.  "engines" is the engine proxy
+# with its default host-function handshake: what AUTO resolves to.
+PATHS = [("engines", {"copy_path": "engines"}),
+         ("engines_kernel_handshake", {"copy_path": "engines", "proxy_handshake": 0}),
+         ("hip", {"copy_path": "hip"}),
+         ("kernel", {"copy_path": "kernel"})]
 
 
 def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
@@ -394,14 +399,13 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
     res = {}
     saved = hc.get_config()
     for name, kw in list(PATHS) + list(extra_paths):
-        path = name.split("_")[0]
-        hc.set_config(copy_path=path, **kw)
+        hc.set_config(**kw)
         med, mn = event_time(lambda: run(None), reps)
         st = hc.last_stats()
         r = dict(algbw_GBs=round(S / med / 1e9, 2), busbw_GBs=round(S / med / 1e9 * f, 2),
                  ms=round(med * 1e3, 4), copy_GBs=round(st["copy_bytes"] / med / 1e9, 1),
                  hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
-                 path_used=["auto", "sdma", "engines", "kernel"][st["copy_path_used"]],
+                 path_used=["auto", "hip", "engines", "kernel"][st["copy_path_used"]],
                  cus_used=st["cus_used_max"], host_enqueue_us=round(st["host_enqueue_us"], 1))
         if gemm is not None:
             r["gemm_slowdown"], r["gemm_overlap"], r["collective_slowdown"] = gemm_slowdown(hc, run, med, gemm)
@@ -427,8 +431,8 @@ def bench_allreduce(hc, W, reps, gemm):
     # The 33.6 MB working set fits the last-level cache.  Device time alone
     # (each call queued behind a spin), with the cache warm and flushed.
     dev = {}
-    for name, kw in (("kernel", {"copy_path": "kernel"}), ("sdma", {"copy_path": "sdma"}),
-                     ("direct_fold", {"reduce_algo": "direct"})):
+    for name, kw in (("kernel", {"copy_path": "kernel"}), ("hip", {"copy_path": "hip"}),
+                     ("engines", {"copy_path": "engines"}), ("direct_fold", {"reduce_algo": "direct"})):
         with hc.config(**kw):
             warm, _ = queued_time(lambda: hc.allreduce(send, recv), reps, flush=False)
             cold, _ = queued_time(lambda: hc.allreduce(send, recv), reps, flush=True)
@@ -444,7 +448,7 @@ def bench_allreduce_bucket(hc, W, reps):
     """All-reduce of one GPT-6.7B gradient bucket (bf16, R=8, 25,165,824
     elements per rank): the ring reduction on CUs, then the gather as copies.
     With G chunk groups the gather of group g overlaps the reduction of
-    group g+1 (SDMA copies beside CU kernels); the direct fold for scale."""
+    group g+1 (copies beside CU kernels); the direct fold for scale."""
     import torch
     R, n = 8, 25_165_824
     x = W.rs_gradients(R, n)
@@ -452,7 +456,7 @@ def bench_allreduce_bucket(hc, W, reps):
     recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     S = n * 2
     out = {}
-    for path in ("sdma", "kernel"):
+    for path in ("engines", "hip", "kernel"):
         for G in (1, 2, 4, 8):
             with hc.config(copy_path=path, allreduce_chunk_groups=G):
                 med, _ = event_time(lambda: hc.allreduce(send, recv), reps)
@@ -474,9 +478,10 @@ def bench_allgather(hc, W, reps, gemm):
     send = [bf16_dev(a) for a in x]
     recv = [torch.empty(total, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
     res = copy_paths(hc, lambda s: hc.allgather(send, recv, stream=s), total * 2, (R - 1) / R, reps, gemm,
-                     extra_paths=[("engines_ring", {"allgather_direct": 0}), ("sdma_ring", {"allgather_direct": 0}),
-                                  ("kernel_wg8", {"workgroups_per_step": 8}),
-                                  ("kernel_wg64", {"workgroups_per_step": 64})])
+                     extra_paths=[("engines_ring", {"copy_path": "engines", "allgather_direct": 0}),
+                                  ("hip_ring", {"copy_path": "hip", "allgather_direct": 0}),
+                                  ("kernel_wg8", {"copy_path": "kernel", "workgroups_per_step": 8}),
+                                  ("kernel_wg64", {"copy_path": "kernel", "workgroups_per_step": 64})])
     hc.set_config(allgather_direct=1)
     return dict(workload="FSDP all-gather bf16 R=8, 25,165,824-element shards (one GPT-6.7B block, "
                          "201,326,592 params), out-of-place", **res)
@@ -515,17 +520,17 @@ def bench_a2a(hc, W, reps, gemm):
     recv = [torch.empty(s, dtype=torch.bfloat16, device="cuda") for s in rsz]
     sent = sum(counts) * 2
     res = copy_paths(hc, lambda s: hc.alltoallv(send, counts, sd, recv, rd, stream=s), sent // R, (R - 1) / R,
-                     reps, gemm, extra_paths=[("kernel_wg8", {"workgroups_per_step": 8}),
-                                              ("kernel_wg64", {"workgroups_per_step": 64})])
+                     reps, gemm, extra_paths=[("kernel_wg8", {"copy_path": "kernel", "workgroups_per_step": 8}),
+                                              ("kernel_wg64", {"copy_path": "kernel", "workgroups_per_step": 64})])
     return dict(workload="EP all-to-all(v) bf16, 4096 tokens x 2048 per rank, 64 experts over R=8, top-6 "
                          "(one copy per destination rank), gemm_slowdown against a concurrent 8192^3 bf16 GEMM",
                 bytes_sent_total=sent, **res)
 
 
 def bench_p2p_sizes(hc, reps):
-    """One message 0 -> 1 over the paper's microbenchmark range: SDMA paths
-    against the CU copy kernel at 1 ... 256 workgroups (the analog of NCCL's
-    1/2/4/8-SM budgets)."""
+    """One message 0 -> 1 over the paper's microbenchmark range: the engine
+    proxy and the HIP runtime's copies against the CU copy kernel at 1 ... 256
+    workgroups (the analog of NCCL's 1/2/4/8-SM budgets)."""
     import torch
     big = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda")
     big2 = torch.empty_like(big)
@@ -534,7 +539,7 @@ def bench_p2p_sizes(hc, reps):
         ne = sz // 2
         s0, d1 = big[:ne], big2[:ne]
         row = {"bytes": sz}
-        for name, kw in [("sdma", dict(copy_path="sdma")), ("engines", dict(copy_path="engines")),
+        for name, kw in [("hip", dict(copy_path="hip")), ("engines", dict(copy_path="engines")),
                          ("engines_striped", dict(copy_path="engines", chunk_bytes=max(1 << 20, sz // 16)))] + \
                         [(f"kernel_wg{w}", dict(copy_path="kernel", workgroups_per_step=w)) for w in (1, 2, 4, 8, 64, 256)]:
             hc.set_config(**kw)
@@ -658,14 +663,15 @@ def copy_ceiling(hc):
 
 def bench_small_message(hc, reps):
     """Latency of one 4 KiB send/recv (rank 0 -> 1) through each copy path:
-    the event fork/join + HIP SDMA copy, the engine proxy's flag handshake,
-    and the CU copy kernel; plus the host time of the call."""
+    the engine proxy's flag handshake (host function, and the one-lane
+    kernel), the HIP runtime's copy, and the CU copy kernel; plus the host
+    time of the call."""
     import torch
     src = torch.zeros(2048, dtype=torch.bfloat16, device="cuda")
     dst = torch.empty_like(src)
     out = {}
-    for name in ("sdma", "engines", "engines_hostfn", "kernel"):
-        hc.set_config(copy_path=name.split("_")[0], proxy_handshake=2 if name.endswith("hostfn") else 0)
+    for name, kw in PATHS:
+        hc.set_config(**kw)
         med, mn = event_time(lambda: hc.sendrecv([src, src], [dst, dst], [1, -1]), reps, warmup=5)
         host = []
         for _ in range(reps):
@@ -675,7 +681,7 @@ def bench_small_message(hc, reps):
             torch.cuda.synchronize()
         out[name] = dict(device_us=round(med * 1e6, 2), device_min_us=round(mn * 1e6, 2),
                          host_call_us=round(statistics.median(host) * 1e6, 2))
-    hc.set_config(copy_path="auto", proxy_handshake=0)
+    hc.set_config(copy_path="auto", proxy_handshake=-1)
     return dict(workload="one 4 KiB message rank 0 -> 1 (stream-manager round trip)", **out)
 
 
@@ -712,15 +718,16 @@ def size_sweep(hc):
     import torch
     R = 8
     sizes = [2 << 20, 8 << 20, 32 << 20, 128 << 20, 512 << 20, 1 << 30]
-    paths = [("sdma", {}), ("engines", {}), ("kernel_wg8", {"workgroups_per_step": 8}),
-             ("kernel_wg256", {"workgroups_per_step": 256})]
+    paths = [("hip", {"copy_path": "hip"}), ("engines", {"copy_path": "engines"}),
+             ("kernel_wg8", {"copy_path": "kernel", "workgroups_per_step": 8}),
+             ("kernel_wg256", {"copy_path": "kernel", "workgroups_per_step": 256})]
     out = {"sendrecv": [], "allgather": [], "alltoall": []}
     big = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     big2 = torch.empty_like(big)
     for sz in sizes:
         row = {"bytes": sz}
         for name, kw in paths:
-            hc.set_config(copy_path=name.split("_")[0], **kw)
+            hc.set_config(**kw)
             s0, d1 = big[:sz].view(torch.int32), big2[:sz].view(torch.int32)
             med, _ = event_time(lambda: hc.sendrecv([s0, s0], [d1, d1], [1, -1]), 5)
             row[name] = round(sz / med / 1e9, 1)
@@ -735,7 +742,7 @@ def size_sweep(hc):
             recv = [torch.empty(R * n, dtype=torch.int32, device="cuda") for _ in range(R)]
             row = {"bytes": R * n * 4}
             for name, kw in paths:
-                hc.set_config(copy_path=name.split("_")[0], **kw)
+                hc.set_config(**kw)
                 fn = (lambda: hc.allgather(send, recv)) if op == "allgather" else \
                      (lambda: hc.alltoall(send, recv))
                 med, _ = event_time(fn, 3, warmup=1)

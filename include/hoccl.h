@@ -12,14 +12,15 @@
  *
  * Two execution paths, as in the paper's design (System Design, Overview):
  *   - pure-copy steps go to the SDMA copy engines, so they occupy no compute
- *     unit (the zero-SM point-to-point executor, here "zero-CU");
+ *     unit (the zero-SM point-to-point executor, here "zero-CU"): a CPU
+ *     proxy thread issues them on chosen engines through ROCr;
  *   - reduction steps, which the paper leaves to SM-side execution
  *     (Limitations), run as gfx950 HIP kernels with an explicit workgroup
  *     budget.
  * Operator order with the caller's stream is kept by a stream manager
- * (Stream Manager section): HIP event fork/join for the HIP copy path, and
- * the start/finish flag handshake through host memory for the path in which
- * a CPU proxy thread drives the SDMA engines itself.
+ * (Stream Manager section): the start/finish flag handshake through host
+ * memory for the engine proxy, and HIP event fork/join for the copies the
+ * HIP runtime issues (HOCCL_COPY_HIP).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -50,13 +51,15 @@
  *   must not wait, through the caller's own stream dependencies, for a call
  *   issued after it.
  * Stream capture.  A call on a stream that is capturing into a HIP graph
- *   records its kernels, SDMA copies and events (never a memset) and
- *   allocates nothing, so it returns HOCCL_ERR_UNSUPPORTED, enqueuing
- *   nothing, when it would have to: as the first call on a device (which
- *   creates the library's streams and probes the engines), when it needs a
- *   larger workspace than the library holds, or when its copies would take
- *   the SDMA_ENGINES path (a host thread issues those).  Make the same call
- *   once outside capture first.  A workspace a graph captured stays
+ *   records its kernels, HIP runtime copies and events (never a memset) and
+ *   allocates nothing.  The copy path AUTO takes the HIP runtime's copies
+ *   while capturing, since the engine proxy's copies are issued by a host
+ *   thread at call time.  A call returns HOCCL_ERR_UNSUPPORTED, enqueuing
+ *   nothing, when it would have to allocate or issue such copies: as the
+ *   first call on a device (which creates the library's streams and probes
+ *   the engines), when it needs a larger workspace than the library holds,
+ *   or when copy_path is SDMA_ENGINES explicitly.  Make the same call once
+ *   outside capture first.  A workspace a graph captured stays
  *   allocated until hoccl_finalize, after which the graph must not be
  *   replayed.  Replays share it with the device's other workspace users
  *   (ring reduce-scatter and all-reduce over more than two ranks) and are
@@ -96,17 +99,26 @@ typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2 } hoccl_dtype_t;
 
 /* Where pure-copy steps run. */
 typedef enum {
-    HOCCL_COPY_AUTO = 0,         /* SDMA: the one path that keeps copies
-                                    free of compute units end to end          */
-    HOCCL_COPY_SDMA = 1,         /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
-                                    library's copy streams; HIP picks engines  */
+    HOCCL_COPY_AUTO = 0,         /* SDMA_ENGINES, the path that keeps copies
+                                    off the compute units; HIP while the
+                                    stream is capturing a graph or when the
+                                    engines cannot be driven                  */
+    HOCCL_COPY_HIP = 1,          /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
+                                    library's copy streams.  Where the copy
+                                    runs is the HIP runtime's choice: in the
+                                    runtime PyTorch bundles it runs on the
+                                    compute units (it cannot finish while
+                                    every CU is busy), in ROCm 7.2's on one
+                                    SDMA engine.  Graph-capturable            */
     HOCCL_COPY_SDMA_ENGINES = 2, /* a CPU proxy thread issues each chunk on an
-                                    explicitly chosen SDMA engine (ROCr) and
-                                    releases the stream by flag handshake;
-                                    with chunk_bytes 0 it cuts copies into
-                                    about total/engines pieces when there are
-                                    fewer chains than engines.  The handshake
-                                    costs a spinning one-thread kernel        */
+                                    explicitly chosen SDMA engine (ROCr,
+                                    hsa_amd_memory_async_copy_on_engine) and
+                                    releases the stream by flag handshake
+                                    (proxy_handshake); with chunk_bytes 0 it
+                                    cuts copies into about total/engines
+                                    pieces when there are fewer chains than
+                                    engines.  Its copies finish while every
+                                    CU is busy                                */
     HOCCL_COPY_KERNEL = 3        /* CU copy kernel with workgroups_per_step
                                     workgroups (comparator / fallback)         */
 } hoccl_copy_path_t;
@@ -126,7 +138,7 @@ typedef struct {
     size_t chunk_bytes;         /* split copies into pieces of this size
                                    (>= 4096); 0 = no split, or the automatic
                                    split of the AUTO copy path                 */
-    int copy_streams;           /* internal copy streams, 1..16; 0 = 8         */
+    int copy_streams;           /* copy streams of the HIP path, 1..16; 0 = 8  */
     int sdma_engines;           /* engines used by SDMA_ENGINES, 0 = all       */
     hoccl_copy_path_t copy_path;
     int allgather_direct;       /* 1 (default): every rank copies each shard
@@ -142,9 +154,11 @@ typedef struct {
                                    0 = 10000                                   */
     int proxy_handshake;        /* the stream side of the SDMA_ENGINES
                                    start/finish flag handshake:
-                                   0 (default): a one-lane kernel on the
-                                   caller's stream that waits on a CU while
-                                   the copies run (4 KiB send/recv: 23 us);
+                                   -1 (default): 2, or 0 while a ROCm
+                                   profiler is loaded;
+                                   0: a one-lane kernel on the caller's
+                                   stream that waits on a CU while the
+                                   copies run (4 KiB send/recv: 23 us);
                                    1: that kernel on a private CU-masked
                                    stream with a hardware queue of its own,
                                    joined to the caller's stream by events
@@ -152,13 +166,13 @@ typedef struct {
                                    caller's hardware queue;
                                    2: a host function on the caller's stream
                                    (hipLaunchHostFunc): no GPU code waits and
-                                   no CU is used, but the HIP runtime's
-                                   callback thread is blocked while the
-                                   copies run.  A run under rocprofv3 hung
-                                   once, so with a ROCm profiler loaded
-                                   (rocprofiler-sdk preloaded, or
-                                   HSA_TOOLS_LIB set) such calls return
-                                   HOCCL_ERR_UNSUPPORTED                    */
+                                   no CU is used (4 KiB send/recv: 57 us),
+                                   but the HIP runtime's callback thread is
+                                   blocked while the copies run.  A run
+                                   under rocprofv3 hung once, so with a ROCm
+                                   profiler loaded (rocprofiler-sdk
+                                   preloaded, or HSA_TOOLS_LIB set) an
+                                   explicit 2 returns HOCCL_ERR_UNSUPPORTED */
     size_t ring_group_bytes;    /* ring reduce-scatter / all-reduce run their
                                    R-1 steps group by group over slices of
                                    every chunk, one group's fp32 partials
@@ -177,14 +191,18 @@ typedef struct {
 typedef struct {
     int reduce_launches;        /* reduction kernel launches enqueued          */
     int copy_kernel_launches;   /* CU copy kernel launches enqueued            */
-    int copy_ops;               /* SDMA copy commands issued                   */
+    int copy_ops;               /* copy commands issued to the engine proxy
+                                   or the HIP runtime                          */
     int workgroups_per_step;    /* workgroups per launch actually used         */
     int cus_available;          /* compute units of the device                 */
     int cus_used_max;           /* upper bound on CUs occupied by this call:
-                                   min(workgroups, CUs) when kernels run; for
-                                   copy-only calls 0 on the SDMA path and 1 on
-                                   SDMA_ENGINES (the handshake's wait kernel,
-                                   one thread)                                 */
+                                   min(workgroups, CUs) when kernels run; at
+                                   least 1 when the SDMA_ENGINES handshake is
+                                   the one-lane kernel; all CUs when copies go
+                                   through the HIP runtime (HOCCL_COPY_HIP),
+                                   which may run them as a kernel of its own;
+                                   0 for copy-only calls on SDMA_ENGINES with
+                                   the host-function handshake                 */
     hoccl_copy_path_t copy_path_used;
     hoccl_reduce_algo_t reduce_algo_used;
     unsigned long long hbm_bytes_algorithmic; /* bytes every step must read
@@ -202,7 +220,7 @@ typedef struct {
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
  *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES (the fields of the
  *   same meaning),
- *   HOCCL_COPY_PATH = auto | sdma | engines | kernel,
+ *   HOCCL_COPY_PATH = auto | hip | engines | kernel,
  *   HOCCL_REDUCE_ALGO = ring | direct,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),
  *   HOCCL_SDMA_ENGINE_IDS = "i,j,..." (the SDMA engines the SDMA_ENGINES
@@ -268,7 +286,7 @@ hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv,
 
 /* all-gather: send[r] holds sendcount elements; every recv[r] receives the
  * R shards in rank order (R * sendcount elements).  Copy-only: moved by the
- * configured copy path (SDMA by default). */
+ * configured copy path (the SDMA engines by default). */
 hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv,
                                size_t sendcount, hoccl_dtype_t dtype, int R,
                                hipStream_t stream);

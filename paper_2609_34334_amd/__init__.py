@@ -26,12 +26,12 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NO_MEMORY, ERR_TIMEOUT, ERR_INTERNAL = range(7)
 INT32, FP32, BF16 = 0, 1, 2
-COPY_AUTO, COPY_SDMA, COPY_SDMA_ENGINES, COPY_KERNEL = range(4)
+COPY_AUTO, COPY_HIP, COPY_SDMA_ENGINES, COPY_KERNEL = range(4)
 REDUCE_RING, REDUCE_DIRECT = 0, 1
 OP_ALLREDUCE, OP_REDUCE_SCATTER, OP_ALLGATHER, OP_SENDRECV, OP_ALLTOALL = range(5)
 
 _DTYPES = {torch.int32: INT32, torch.float32: FP32, torch.bfloat16: BF16}
-COPY_PATHS = {"auto": COPY_AUTO, "sdma": COPY_SDMA, "engines": COPY_SDMA_ENGINES,
+COPY_PATHS = {"auto": COPY_AUTO, "hip": COPY_HIP, "engines": COPY_SDMA_ENGINES,
               "kernel": COPY_KERNEL}
 
 
@@ -130,7 +130,7 @@ def get_config():
 
 def set_config(**kw):
     """Update configuration fields; copy_path also accepts a name
-    ('auto', 'sdma', 'engines', 'kernel') and reduce_algo 'ring'/'direct'."""
+    ('auto', 'hip', 'engines', 'kernel') and reduce_algo 'ring'/'direct'."""
     c = Config()
     _check(_lib.hoccl_get_config(ctypes.byref(c)), "hoccl_get_config")
     for k, v in kw.items():

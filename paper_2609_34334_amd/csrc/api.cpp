@@ -4,16 +4,17 @@
 // Stream manager (Stream Manager section of the paper): a collective is
 // enqueued on the caller's stream `s`.  Reduction kernels run on `s` itself.
 // Copy steps run either
-//   * on the library's copy streams as hipMemcpyAsync(DeviceToDeviceNoCU),
-//     which the HIP runtime hands to an SDMA engine: `s` records a fork
-//     event that each copy stream waits on before its first copy, and `s`
-//     waits on a join event of every copy stream it used, so the collective
-//     sits in `s` exactly where it was enqueued;
 //   * by the copy proxy (proxy.cpp), which drives chosen SDMA engines itself
-//     and is ordered with `s` by the start/finish flag handshake;
+//     and is ordered with `s` by the start/finish flag handshake -- the
+//     default, and the only path whose copies occupy no compute unit;
+//   * on the library's copy streams as hipMemcpyAsync(DeviceToDeviceNoCU),
+//     where the HIP runtime decides what executes the copy: `s` records a
+//     fork event that each copy stream waits on before its first copy, and
+//     `s` waits on a join event of every copy stream it used, so the
+//     collective sits in `s` exactly where it was enqueued;
 //   * or as CU copy kernels on `s`.
 // All-reduce's gather copies of group g wait on an event recorded on `s`
-// right after group g's last reduction step, so SDMA copies of one group
+// right after group g's last reduction step, so the copies of one group
 // overlap the CU reduction of the next (the paper's per-chunk buffer state
 // machine, reduced to "partial ready" / "final ready").
 #include <hip/hip_runtime.h>
@@ -107,7 +108,7 @@ hoccl_config_t default_config() {
     c.reduce_algo = HOCCL_REDUCE_RING;
     c.kernel_timing = 0;
     c.proxy_timeout_ms = 10000;
-    c.proxy_handshake = 0;
+    c.proxy_handshake = -1;
     c.ring_group_bytes = 0;
     c.proxy_wait_limit_us = 0;
     return c;
@@ -125,7 +126,7 @@ bool config_valid(const hoccl_config_t &c) {
     if (c.allreduce_chunk_groups < 0 || c.allreduce_chunk_groups > 1024) return false;
     if ((int)c.reduce_algo < 0 || (int)c.reduce_algo > 1) return false;
     if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
-    if (c.proxy_handshake < 0 || c.proxy_handshake > 2) return false;
+    if (c.proxy_handshake < -1 || c.proxy_handshake > 2) return false;
     return true;
 }
 
@@ -152,7 +153,7 @@ void load_config_locked() {
     c.proxy_wait_limit_us = (unsigned)env_long("HOCCL_PROXY_WAIT_LIMIT_US", c.proxy_wait_limit_us);
     if (const char *v = std::getenv("HOCCL_RING_GROUP_BYTES")) c.ring_group_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
-        if (!std::strcmp(v, "sdma")) c.copy_path = HOCCL_COPY_SDMA;
+        if (!std::strcmp(v, "hip")) c.copy_path = HOCCL_COPY_HIP;
         else if (!std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA_ENGINES;
         else if (!std::strcmp(v, "kernel")) c.copy_path = HOCCL_COPY_KERNEL;
         else c.copy_path = HOCCL_COPY_AUTO;
@@ -423,7 +424,7 @@ hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const 
 // by the event of the reduction group they wait for, and joined back by one
 // event each; keeping one of them on the caller's stream was measured
 // 5-30% slower for those.
-hoccl_status_t run_copies_sdma(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
+hoccl_status_t run_copies_hip(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
                                const Buffers &B, hipStream_t s) {
     int K = std::max(1, std::min(cfg.copy_streams ? cfg.copy_streams : 8,
                                  (int)st.copy_streams.size()));
@@ -518,25 +519,33 @@ bool profiler_present() {
     return present;
 }
 
-// Copy path for a plan.  An explicit choice wins; AUTO is the HIP runtime's
-// device-to-device SDMA path.  It runs no GPU code, is the fastest path alone
-// for large transfers, needs no host thread, can be captured into a graph
-// and is safe under a profiler.  The engine proxy with the host-function
-// handshake runs no GPU code either, and keeps its copy rate beside a
-// full-occupancy GEMM where the HIP path's copies slow down several times;
-// callers that overlap copies with heavy compute select it explicitly.  The
-// proxy's default handshake kernel keeps one wave resident, which alone
-// costs such a GEMM about half its speed.
-hoccl_copy_path_t resolve_path(const DeviceState &, const hoccl_config_t &cfg, const Plan &) {
-    return cfg.copy_path == HOCCL_COPY_AUTO ? HOCCL_COPY_SDMA : cfg.copy_path;
+// Copy path for a plan.  An explicit choice wins.  AUTO takes the engine
+// proxy: its copies run on SDMA engines chosen through ROCr, and finish while
+// every CU is busy.  The HIP runtime's device-to-device copy does not: in the
+// runtime PyTorch bundles it waits for free CUs, whatever the copy kind
+// asks.  AUTO falls back to the HIP runtime's copies while the stream is
+// capturing a graph (the proxy issues copies from a host thread at call
+// time) and when no engine can be driven.
+hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg, bool capturing) {
+    if (cfg.copy_path != HOCCL_COPY_AUTO) return cfg.copy_path;
+    return (st.proxy && !capturing) ? HOCCL_COPY_SDMA_ENGINES : HOCCL_COPY_HIP;
+}
+
+// The engine proxy's handshake form: an explicit choice, else the host
+// function, which runs no GPU code, or the one-lane kernel while a profiler
+// is loaded (the host function is refused then).
+int resolve_handshake(const hoccl_config_t &cfg) {
+    if (cfg.proxy_handshake >= 0) return cfg.proxy_handshake;
+    return profiler_present() ? 0 : 2;
 }
 
 // On the engine proxy with no chunk size configured: when there are fewer
 // independent chains than engines, cut the copies into pieces of about
 // total / engines bytes (at least 4 MiB) so that every engine works, the
 // paper's striping of one flow over several queues.
-size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, const Plan &p) {
-    if (cfg.copy_path != HOCCL_COPY_SDMA_ENGINES || cfg.chunk_bytes != 0 || !st.proxy) return 0;
+size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, hoccl_copy_path_t path,
+                        const Plan &p) {
+    if (path != HOCCL_COPY_SDMA_ENGINES || cfg.chunk_bytes != 0 || !st.proxy) return 0;
     int E = st.proxy->engine_count();
     if (cfg.sdma_engines > 0) E = std::min(E, cfg.sdma_engines);
     if (p.nchains >= E) return 0;
@@ -560,15 +569,16 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     if (capturing) cfg.kernel_timing = 0;
     Buffers B = B0;
     PlanOptions opt = options_from(cfg, in_place);
+    const hoccl_copy_path_t path = resolve_path(st, cfg, capturing);
+    const int handshake = resolve_handshake(cfg);
     Plan p = build(opt);
-    if (size_t c = auto_chunk_bytes(st, cfg, p)) {
+    if (size_t c = auto_chunk_bytes(st, cfg, path, p)) {
         opt.chunk_bytes = c;
         p = build(opt);
     }
 
     const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
     const int wg = auto_workgroups(st, cfg, p, threads);
-    const hoccl_copy_path_t path = resolve_path(st, cfg, p);
     if (g_debug)
         std::fprintf(stderr, "hoccl: device %d stream %p workgroups %d copy_path %d%s plan %s\n",
                      st.device, (void *)s, wg, (int)path, capturing ? " (captured)" : "",
@@ -578,7 +588,7 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
         set_err("%s", st.proxy_why.c_str());
         return HOCCL_ERR_UNSUPPORTED;
     }
-    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && cfg.proxy_handshake == 2 &&
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && handshake == 2 &&
         profiler_present()) {
         set_err("the host-function handshake (proxy_handshake = 2) is refused while a profiler is "
                 "loaded: it blocks the runtime thread the profiler may need");
@@ -613,17 +623,17 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
         hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                            cfg.proxy_wait_limit_us, cfg.proxy_handshake, s, &ne,
+                                            cfg.proxy_wait_limit_us, handshake, s, &ne,
                                             t_err);
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {
-        TRY(run_reductions(st, cfg, p, B, s, wg, threads, has_copies && path == HOCCL_COPY_SDMA));
+        TRY(run_reductions(st, cfg, p, B, s, wg, threads, has_copies && path == HOCCL_COPY_HIP));
         if (has_copies) {
             if (path == HOCCL_COPY_KERNEL)
                 TRY(run_copies_kernel(st, cfg, p, B, s, wg, threads));
             else
-                TRY(run_copies_sdma(st, cfg, p, B, s));
+                TRY(run_copies_hip(st, cfg, p, B, s));
         }
     }
     if (p.ws_bytes && !capturing) {
@@ -637,8 +647,13 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     // The engine proxy's handshake kernel waits as one lane on one CU; the
     // host-function form needs none.
     const bool handshake_wave =
-        has_copies && path == HOCCL_COPY_SDMA_ENGINES && cfg.proxy_handshake != 2;
-    t_stats.cus_used_max = cu_work ? std::min(wg, st.num_cus) : (handshake_wave ? 1 : 0);
+        has_copies && path == HOCCL_COPY_SDMA_ENGINES && handshake != 2;
+    int cus = cu_work ? std::min(wg, st.num_cus) : 0;
+    if (handshake_wave) cus = std::max(cus, 1);
+    // The HIP runtime may run its device-to-device copies as a kernel of its
+    // own, on any CU (the runtime PyTorch bundles does).
+    if (has_copies && path == HOCCL_COPY_HIP) cus = st.num_cus;
+    t_stats.cus_used_max = cus;
     t_stats.copy_path_used = has_copies ? path : HOCCL_COPY_AUTO;
     t_stats.reduce_algo_used = p.has_fold ? HOCCL_REDUCE_DIRECT : HOCCL_REDUCE_RING;
     t_stats.hbm_bytes_algorithmic = p.hbm_bytes;

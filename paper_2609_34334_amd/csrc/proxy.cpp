@@ -11,8 +11,9 @@
 //            run the copies, write finish := FINISH, see finish == 0.
 //
 // The stream's side of the handshake takes one of three forms
-// (hoccl_config_t.proxy_handshake):
-//   0 (default)  one dispatch of a one-lane handshake kernel on the caller's
+// (hoccl_config_t.proxy_handshake; by default 2, or 0 while a profiler is
+// loaded):
+//   0            one dispatch of a one-lane handshake kernel on the caller's
 //                stream, performing all four flag operations in order and
 //                sleeping between polls.  HIP's own stream memory operations
 //                are separate spinning kernels here, one dispatch each.

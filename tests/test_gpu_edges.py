@@ -21,7 +21,7 @@ def _defaults():
     hc.set_config(**saved)
 
 
-@pytest.mark.parametrize("path", ["sdma", "kernel"])
+@pytest.mark.parametrize("path", ["auto", "hip", "kernel"])
 @pytest.mark.parametrize("algo", ["ring", "direct"])
 def test_max_ranks(path, algo):
     R = 64

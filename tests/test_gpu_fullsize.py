@@ -32,7 +32,7 @@ def test_reduce_scatter_gradient_bucket(algo):
         assert_bitwise(from_dev(out[r], hc.BF16), ref[r], f"{algo} rank {r}")
 
 
-@pytest.mark.parametrize("path", ["sdma", "engines", "kernel"])
+@pytest.mark.parametrize("path", ["hip", "engines", "kernel"])
 @pytest.mark.parametrize("algo", ["ring", "direct"])
 def test_allreduce_fp32_R4(path, algo):
     hc.set_config(copy_path=path, reduce_algo=algo)
@@ -46,7 +46,7 @@ def test_allreduce_fp32_R4(path, algo):
         assert_bitwise(from_dev(recv[r], hc.FP32), ref[r], f"rank {r}")
 
 
-@pytest.mark.parametrize("path", ["sdma", "engines"])
+@pytest.mark.parametrize("path", ["hip", "engines"])
 def test_allgather_fsdp_block(path):
     """201,326,592 bf16 parameters over R=8: each rank's output is compared
     with the concatenation of the shards (the oracle's definition)."""
@@ -62,7 +62,7 @@ def test_allgather_fsdp_block(path):
             assert np.array_equal(got[s * n:(s + 1) * n], x[s]), (r, s)
 
 
-@pytest.mark.parametrize("path", ["sdma", "engines", "kernel"])
+@pytest.mark.parametrize("path", ["hip", "engines", "kernel"])
 def test_pp_activation_round(path):
     hc.set_config(copy_path=path)
     R = 8
@@ -78,7 +78,7 @@ def test_pp_activation_round(path):
             assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"{peers} rank {r}")
 
 
-@pytest.mark.parametrize("path", ["sdma", "engines"])
+@pytest.mark.parametrize("path", ["hip", "engines"])
 def test_alltoallv_ep_dispatch(path):
     hc.set_config(copy_path=path)
     R = 8

@@ -54,7 +54,7 @@ def test_reduce_scatter_in_a_graph(algo):
     replay_check(lambda s: hc.reduce_scatter(send, outs, stream=s), outs, ref, hc.BF16, algo)
 
 
-@pytest.mark.parametrize("path", ["sdma", "kernel"])
+@pytest.mark.parametrize("path", ["auto", "hip", "kernel"])
 def test_allgather_and_allreduce_in_a_graph(path):
     hc.set_config(copy_path=path)
     R, n = 8, 50_021

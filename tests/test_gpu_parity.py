@@ -16,7 +16,7 @@ from gpu_util import (ES, NAME, TORCH, assert_bitwise, check_canaries, from_dev,
 pytestmark = pytest.mark.gpu
 
 DTS = [hc.INT32, hc.FP32, hc.BF16]
-PATHS = ["sdma", "engines", "kernel"]
+PATHS = ["hip", "engines", "kernel"]
 
 
 @pytest.fixture(autouse=True)
@@ -76,7 +76,7 @@ def test_ring_in_cache_groups(dt, R):
 @pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
 @pytest.mark.parametrize("R", [1, 2, 3, 4, 8])
 def test_allreduce_and_reduce_scatter(algo, dt, R):
-    hc.set_config(reduce_algo=algo, copy_path="sdma")
+    hc.set_config(reduce_algo=algo, copy_path="hip")
     for n in [1, 7, R * 37 + 3, 4099, 65536 + 5]:
         seed = 9000 + 13 * R + n
         x = [W.random_values(NAME[dt], seed, r, n) for r in range(R)]
@@ -273,19 +273,26 @@ def test_alltoallv_routing(path):
         assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"A2Av r={r}")
 
 
-def test_sdma_paths_dispatch_no_kernel():
-    """Copy-only collectives on an SDMA path launch no kernel of the library:
-    zero CUs on the HIP path, one (the handshake's one-thread wait kernel)
-    on the engine proxy.  AUTO resolves to the HIP path."""
+def test_copy_paths_report_their_cus():
+    """Copy-only collectives launch no kernel of the library on the engine
+    proxy or the HIP runtime path.  The stats report the CUs each path may
+    occupy: none for the engine proxy with the host-function handshake
+    (the default, and what AUTO resolves to), one for its handshake
+    kernel, and every CU for the HIP runtime's copies, which the runtime may
+    run as a kernel of its own."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
     R, n = 8, 1 << 16
     x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
-    for path, cus in [("auto", 0), ("sdma", 0), ("engines", 1)]:
-        hc.set_config(copy_path=path)
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    for path, hs, cus, used in [("auto", -1, 0, hc.COPY_SDMA_ENGINES), ("engines", -1, 0, hc.COPY_SDMA_ENGINES),
+                                ("engines", 0, 1, hc.COPY_SDMA_ENGINES), ("hip", -1, ncu, hc.COPY_HIP)]:
+        hc.set_config(copy_path=path, proxy_handshake=hs)
         hc.allgather(x)
         s = hc.last_stats()
-        assert s["cus_used_max"] == cus and s["reduce_launches"] == 0, (path, s)
+        assert s["cus_used_max"] == cus and s["reduce_launches"] == 0, (path, hs, s)
         assert s["copy_kernel_launches"] == 0 and s["copy_ops"] > 0
-        assert s["copy_path_used"] == (hc.COPY_SDMA_ENGINES if path == "engines" else hc.COPY_SDMA)
+        assert s["copy_path_used"] == used, (path, s)
     torch.cuda.synchronize()
 
 
@@ -504,7 +511,7 @@ def test_sdma_copy_stream_counts(streams):
     """Every copy collective on the HIP SDMA path with 1, 2 and all 16 copy
     streams (the largest count joins through the last copy stream's event)."""
     R, n = 8, 20_011
-    with hc.config(copy_path="sdma", copy_streams=streams):
+    with hc.config(copy_path="hip", copy_streams=streams):
         x = [W.random_bits(800 + streams, r, n, 2) for r in range(R)]
         ref = oracle.allgather_new(x, hc.BF16)
         got = hc.allgather([to_dev(a, hc.BF16) for a in x])

@@ -25,7 +25,7 @@ def draw(i):
         op=str(g.choice(["allreduce", "reduce_scatter", "allgather", "sendrecv", "alltoall", "alltoallv"])),
         dt=[hc.INT32, hc.FP32, hc.BF16][int(g.integers(0, 3))], R=R, n=n,
         lead=int(g.choice([0, 1, 3, 8])),
-        cfg=dict(copy_path=str(g.choice(["sdma", "engines", "kernel"])),
+        cfg=dict(copy_path=str(g.choice(["auto", "hip", "engines", "kernel"])),
                  reduce_algo=str(g.choice(["ring", "direct"])),
                  workgroups_per_step=int(g.choice([0, 0, 1, 7, 300])),
                  threads_per_workgroup=int(g.choice([64, 256, 256, 1024])),
@@ -57,7 +57,7 @@ def test_random_case(i):
     c = draw(i)
     op, dt, R, n, lead, seed = c["op"], c["dt"], c["R"], c["n"], c["lead"], c["seed"]
     if c["cfg"]["copy_path"] == "engines" and hc.sdma_engine_count() == 0:
-        c["cfg"]["copy_path"] = "sdma"
+        c["cfg"]["copy_path"] = "hip"
     es = ES[dt]
     with hc.config(**c["cfg"]):
         if op == "allreduce":

@@ -106,11 +106,11 @@ def gated(run, outs, dt):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("path", ["sdma", "engines", "engines_hostfn", "kernel"])
+@pytest.mark.parametrize("path", ["hip", "engines", "engines_kernel", "kernel"])
 def test_copy_collectives_wait_for_the_gate(path):
     if path.startswith("engines") and hc.sdma_engine_count() == 0:
         pytest.skip("engine proxy unavailable")
-    hc.set_config(copy_path=path.split("_")[0], proxy_handshake=2 if path.endswith("hostfn") else 0)
+    hc.set_config(copy_path=path.split("_")[0], proxy_handshake=0 if path == "engines_kernel" else -1)
     R, n = 8, 70_001
     x = [W.random_bits(401, r, n, 2) for r in range(R)]
     ref = oracle.allgather_new(x, hc.BF16)
