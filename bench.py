@@ -806,9 +806,12 @@ def measured_traffic(summary=TRAFFIC_SUMMARY):
 
 
 def copy_workload(hc, W):
-    """What the zero-CU trace profiles: the FSDP all-gather, the EP
+    """What the copy-path kernel trace profiles: the FSDP all-gather, the EP
     all-to-all(v) and one PP send/recv round, once each on the default (AUTO)
-    copy path, after the inputs are resident."""
+    copy path, after the inputs are resident.  Under a profiler AUTO's
+    engine proxy uses its one-lane handshake kernel, which the trace shows;
+    the copies themselves are SDMA commands.  Whether copies need CUs is
+    shown by tests/test_gpu_zero_cu.py, not by a trace."""
     import torch
     R = 8
     ag = [bf16_dev(a) for a in W.ag_parameters(R)]
