@@ -54,7 +54,10 @@ namespace {
 
 constexpr uint32_t kStartValue = 0x53544152u;   // written by the stream
 constexpr uint32_t kFinishValue = 0x46494e49u;  // written by the proxy
-constexpr int kSlots = 64;
+// Operations that may be in flight at once: a caller that enqueues many
+// collectives ahead of the GPU (a pipeline schedule of 32 send/recv rounds,
+// several times over) waits for a free slot only beyond this many.
+constexpr int kSlots = 512;
 constexpr size_t kLine = 64;  // one cache line per flag
 constexpr int kFlagsPerSlot = 3;  // start, finish, status
 
@@ -472,14 +475,14 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         eng_of_chain[(size_t)ch] = (int)best;
         load[best] += cb[(size_t)ch];
     }
-    // Issue order per engine: the chains sharing an engine are interleaved
-    // copy by copy in proportion to their length (flow-size-aware chunk
-    // scheduling), each chain keeping its own order.
+    // Order per engine: the chains sharing an engine are interleaved copy by
+    // copy in proportion to their length (flow-size-aware chunk scheduling),
+    // each chain keeping its own order.
     std::vector<std::vector<size_t>> of_chain((size_t)nch);
     for (size_t i = 0; i < copies.size(); ++i) of_chain[(size_t)copies[i].chain].push_back(i);
-    std::vector<size_t> issue;
-    issue.reserve(copies.size());
+    std::vector<std::vector<size_t>> per_engine((size_t)E);
     for (int e = 0; e < E; ++e) {
+        std::vector<size_t> &q = per_engine[(size_t)e];
         std::vector<int> chains;
         std::vector<double> len;
         for (int ch = 0; ch < nch; ++ch)
@@ -490,14 +493,23 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         std::vector<size_t> next(chains.size(), 0);
         if (round_robin) {
             for (size_t k = 0; k < chains.size(); ++k)
-                for (size_t i : of_chain[(size_t)chains[k]]) issue.push_back(i);
+                for (size_t i : of_chain[(size_t)chains[k]]) q.push_back(i);
             continue;
         }
         for (int k : interleave_chunks(len, 1.0)) {
             int ch = chains[(size_t)k];
-            issue.push_back(of_chain[(size_t)ch][next[(size_t)k]++]);
+            q.push_back(of_chain[(size_t)ch][next[(size_t)k]++]);
         }
     }
+    // Issue order: one copy per engine in turn, so that every engine has work
+    // after the first E host calls instead of the last engine waiting for
+    // all the others' copies to be issued (each issue costs the proxy thread
+    // some microseconds).  Each engine's own order is kept.
+    std::vector<size_t> issue;
+    issue.reserve(copies.size());
+    for (size_t r = 0; issue.size() < copies.size(); ++r)
+        for (int e = 0; e < E; ++e)
+            if (r < per_engine[(size_t)e].size()) issue.push_back(per_engine[(size_t)e][r]);
     std::vector<ProxyCopy> ordered;
     ordered.reserve(copies.size());
     for (size_t i : issue) ordered.push_back(copies[i]);
