@@ -159,3 +159,44 @@ def test_debug_log_names_the_plan(tmp_path):
                        timeout=120)
     assert r.returncode == 0, r.stderr[-2000:]
     assert "hoccl: device 0" in r.stderr and "plan {" in r.stderr, r.stderr[-2000:]
+
+
+def test_many_engine_operations_in_flight():
+    """300 engine-proxy send/recv operations queued behind a closed gate
+    (more than the old pool of 64 handshake slots), each copying buffer k
+    into buffer k+1: when the gate opens they must run in stream order, so
+    every buffer ends up holding buffer 0's bits and none keeps its
+    canary."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    hc.set_config(copy_path="engines")
+    K, n = 300, 2048
+    bufs = [torch.full((n,), 0x7A5A, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+            for _ in range(K + 1)]
+    first = to_dev(W.random_bits(405, 0, n, 2), hc.BF16)
+    bufs[0].copy_(first)
+    s, _ = own_queue_streams()
+    hc.sendrecv([bufs[0], bufs[0]], [bufs[1], bufs[1]], [1, -1], stream=s)   # warm path
+    torch.cuda.synchronize()
+    bufs[1].view(torch.int16).fill_(0x7A5A)
+    torch.cuda.synchronize()
+    f = flag()
+    cell = ctypes.c_uint32.from_address(f)
+    cell.value = 0
+    k = int(time.time() * 1000) % 1_000_000 + 1
+    release = threading.Timer(5.0, lambda: setattr(cell, "value", k))
+    release.start()
+    try:
+        assert HIP.hipStreamWaitValue32(V(s.cuda_stream), V(f), k, WAIT_EQ, 0xFFFFFFFF) == 0
+        with torch.cuda.stream(s):
+            for i in range(K):
+                hc.sendrecv([bufs[i], bufs[i]], [bufs[i + 1], bufs[i + 1]], [1, -1], stream=s)
+        assert not s.query(), "the stream finished while its gate was closed"
+    finally:
+        release.cancel()
+        cell.value = k
+    s.synchronize()
+    torch.cuda.synchronize()
+    want = from_dev(first, hc.BF16)
+    for i in (1, K // 2, K):
+        assert_bitwise(from_dev(bufs[i], hc.BF16), want, f"buffer {i}")
