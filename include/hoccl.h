@@ -51,15 +51,18 @@
  *   must not wait, through the caller's own stream dependencies, for a call
  *   issued after it.
  * Stream capture.  A call on a stream that is capturing into a HIP graph
- *   records its kernels, HIP runtime copies and events (never a memset) and
- *   allocates nothing.  The copy path AUTO takes the HIP runtime's copies
- *   while capturing, since the engine proxy's copies are issued by a host
- *   thread at call time.  A call returns HOCCL_ERR_UNSUPPORTED, enqueuing
- *   nothing, when it would have to allocate or issue such copies: as the
- *   first call on a device (which creates the library's streams and probes
- *   the engines), when it needs a larger workspace than the library holds,
- *   or when copy_path is SDMA_ENGINES explicitly.  Make the same call once
- *   outside capture first.  A workspace a graph captured stays
+ *   records its kernels, events and copies (never a memset) and allocates
+ *   no device memory.  Engine-proxy copies are recorded as a host node that
+ *   issues them on the SDMA engines at every replay and returns once they
+ *   have completed (no GPU code); this needs the host-function handshake,
+ *   so while a profiler is loaded AUTO records the HIP runtime's copies
+ *   instead.  A call returns HOCCL_ERR_UNSUPPORTED, enqueuing nothing, as
+ *   the first call on a device (which creates the library's streams and
+ *   probes the engines), when it needs a larger workspace than the library
+ *   holds, or when copy_path is SDMA_ENGINES with the handshake kernel
+ *   (proxy_handshake 0 or 1).  Make the same call once outside capture
+ *   first.  The copy lists of recorded host nodes stay allocated until
+ *   hoccl_finalize.  A workspace a graph captured stays
  *   allocated until hoccl_finalize, after which the graph must not be
  *   replayed.  Replays share it with the device's other workspace users
  *   (ring reduce-scatter and all-reduce over more than two ranks) and are
@@ -100,9 +103,9 @@ typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2 } hoccl_dtype_t;
 /* Where pure-copy steps run. */
 typedef enum {
     HOCCL_COPY_AUTO = 0,         /* SDMA_ENGINES, the path that keeps copies
-                                    off the compute units; HIP while the
-                                    stream is capturing a graph or when the
-                                    engines cannot be driven                  */
+                                    off the compute units; HIP when the
+                                    engines cannot be driven, or while
+                                    capturing under a profiler                */
     HOCCL_COPY_HIP = 1,          /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
                                     library's copy streams.  Where the copy
                                     runs is the HIP runtime's choice: in the

@@ -519,24 +519,27 @@ bool profiler_present() {
     return present;
 }
 
-// Copy path for a plan.  An explicit choice wins.  AUTO takes the engine
-// proxy: its copies run on SDMA engines chosen through ROCr, and finish while
-// every CU is busy.  The HIP runtime's device-to-device copy does not: in the
-// runtime PyTorch bundles it waits for free CUs, whatever the copy kind
-// asks.  AUTO falls back to the HIP runtime's copies while the stream is
-// capturing a graph (the proxy issues copies from a host thread at call
-// time) and when no engine can be driven.
-hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg, bool capturing) {
-    if (cfg.copy_path != HOCCL_COPY_AUTO) return cfg.copy_path;
-    return (st.proxy && !capturing) ? HOCCL_COPY_SDMA_ENGINES : HOCCL_COPY_HIP;
-}
-
 // The engine proxy's handshake form: an explicit choice, else the host
 // function, which runs no GPU code, or the one-lane kernel while a profiler
 // is loaded (the host function is refused then).
 int resolve_handshake(const hoccl_config_t &cfg) {
     if (cfg.proxy_handshake >= 0) return cfg.proxy_handshake;
     return profiler_present() ? 0 : 2;
+}
+
+// Copy path for a plan.  An explicit choice wins.  AUTO takes the engine
+// proxy: its copies run on SDMA engines chosen through ROCr, and finish while
+// every CU is busy.  The HIP runtime's device-to-device copy does not: in the
+// runtime PyTorch bundles it waits for free CUs, whatever the copy kind
+// asks.  While the stream is capturing a graph, the engine path is recorded
+// as a host node that issues the copies at every replay, which needs the
+// host-function handshake; AUTO then falls back to the HIP runtime's copies
+// when that form is not available (under a profiler), and whenever no engine
+// can be driven.
+hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg, bool capturing) {
+    if (cfg.copy_path != HOCCL_COPY_AUTO) return cfg.copy_path;
+    if (!st.proxy || (capturing && resolve_handshake(cfg) != 2)) return HOCCL_COPY_HIP;
+    return HOCCL_COPY_SDMA_ENGINES;
 }
 
 // On the engine proxy with no chunk size configured: when there are fewer
@@ -594,11 +597,13 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
                 "loaded: it blocks the runtime thread the profiler may need");
         return HOCCL_ERR_UNSUPPORTED;
     }
-    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && capturing) {
-        // The proxy thread issues the copies at call time; a graph replay
-        // would run the handshake without them.
-        set_err("the SDMA_ENGINES copy path cannot be captured into a graph: its copies are "
-                "issued by a host thread");
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && capturing && handshake != 2) {
+        // A replay would run the handshake kernel without the proxy thread
+        // issuing the copies; only the host-function form is recorded as a
+        // node that issues them itself.
+        set_err("the SDMA_ENGINES copy path is captured into a graph only with the host-function "
+                "handshake (proxy_handshake 2 or -1): the handshake kernel waits for copies the "
+                "proxy thread issues at call time");
         return HOCCL_ERR_UNSUPPORTED;
     }
     const bool has_kernels = !p.reduce_steps.empty() || p.has_fold;
@@ -622,9 +627,11 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
         for (const CopyOp &c : p.copies)
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
-        hoccl_status_t r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                            cfg.proxy_wait_limit_us, handshake, s, &ne,
-                                            t_err);
+        hoccl_status_t r =
+            capturing ? st.proxy->capture(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
+                                          cfg.proxy_wait_limit_us, s, &ne, t_err)
+                      : st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
+                                         cfg.proxy_wait_limit_us, handshake, s, &ne, t_err);
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {

@@ -149,6 +149,8 @@ struct ProxyOp {
     bool timed_out = false;
 };
 
+struct CapturedOp;
+
 class ProxyImpl {
   public:
     hsa_agent_t agent{};
@@ -166,6 +168,7 @@ class ProxyImpl {
     std::thread th;
     hoccl_status_t sticky = HOCCL_OK;
     std::string sticky_msg;
+    std::vector<CapturedOp *> captured;  // kept until the proxy is destroyed
 
     volatile uint32_t *flag(int s, int k) {
         return (volatile uint32_t *)((char *)flags + (size_t)(kFlagsPerSlot * s + k) * kLine);
@@ -383,6 +386,52 @@ Proxy *Proxy::create(int device, std::string *why) {
     return new Proxy(p);
 }
 
+// A copy operation recorded into a HIP graph.  The graph holds a host node
+// that runs `run_captured` at every replay: it issues the operation's
+// copies on their engines itself and returns once they have completed, so
+// the stream waits without GPU code and without the proxy thread, which
+// only ever sees operations submitted at call time.  The copy list and its
+// completion signals stay allocated until the proxy is destroyed
+// (hoccl_finalize), after which such a graph must not be replayed.
+struct CapturedOp {
+    ProxyImpl *P = nullptr;
+    std::vector<ProxyCopy> copies;
+    std::vector<uint32_t> engine;
+    std::vector<int> dep;
+    std::vector<hsa_signal_t> sig;
+    std::chrono::microseconds limit{0};
+};
+
+// Runs on the HIP runtime's callback thread, so it calls no HIP function.
+// A failure is reported by the next call into the proxy, and the function
+// always returns within `limit`, so the stream drains.
+void run_captured(void *arg) {
+    CapturedOp &op = *(CapturedOp *)arg;
+    ProxyImpl &P = *op.P;
+    size_t issued = 0;
+    for (size_t i = 0; i < op.copies.size(); ++i, ++issued) {
+        const ProxyCopy &c = op.copies[i];
+        hsa_signal_store_screlease(op.sig[i], 1);
+        const hsa_signal_t *deps = op.dep[i] >= 0 ? &op.sig[(size_t)op.dep[i]] : nullptr;
+        if (hsa_amd_memory_async_copy_on_engine(c.dst, P.agent, c.src, P.agent, c.bytes, deps ? 1 : 0,
+                                                deps, op.sig[i], (hsa_amd_sdma_engine_id_t)op.engine[i],
+                                                true) != HSA_STATUS_SUCCESS) {
+            hsa_signal_store_screlease(op.sig[i], 0);
+            P.fail(HOCCL_ERR_HIP, "hsa_amd_memory_async_copy_on_engine failed in a graph replay");
+            break;
+        }
+    }
+    const auto t0 = std::chrono::steady_clock::now();
+    for (size_t i = 0; i < issued; ++i)
+        while (hsa_signal_load_scacquire(op.sig[i]) != 0) {
+            if (std::chrono::steady_clock::now() - t0 > op.limit) {
+                P.fail(HOCCL_ERR_TIMEOUT, "SDMA copies of a graph replay did not complete in time");
+                return;
+            }
+            std::this_thread::yield();
+        }
+}
+
 Proxy::~Proxy() {
     {
         std::lock_guard<std::mutex> lk(impl_->mu);
@@ -390,6 +439,10 @@ Proxy::~Proxy() {
     }
     impl_->cv_work.notify_all();
     if (impl_->th.joinable()) impl_->th.join();
+    for (CapturedOp *op : impl_->captured) {
+        for (auto &sg : op->sig) hsa_signal_destroy(sg);
+        delete op;
+    }
     for (auto &s : impl_->free_signals) hsa_signal_destroy(s);
     if (impl_->flags) (void)hipHostFree(impl_->flags);
     if (impl_->hs) (void)hipStreamDestroy(impl_->hs);
@@ -429,23 +482,21 @@ void host_side_handshake(void *arg) {
     delete h;
 }
 
-hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
-                             unsigned timeout_ms, unsigned wait_limit_us, int handshake,
-                             hipStream_t s, int *engines_used, std::string &err) {
-    ProxyImpl &P = *impl_;
-    {
-        std::lock_guard<std::mutex> lk(P.mu);
-        if (P.sticky != HOCCL_OK) {
-            hoccl_status_t st = P.sticky;
-            err = P.sticky_msg;
-            P.sticky = HOCCL_OK;
-            P.sticky_msg.clear();
-            return st;
-        }
-    }
-    ProxyOp *op = new ProxyOp();
-    op->copies = copies;
-    op->timeout_ms = timeout_ms ? timeout_ms : 10000;
+// The copies of one operation in issue order, each with its engine and the
+// earlier copy of its chain it must wait for.  Chains are balanced over at
+// most `max_engines` engines by bytes, largest first onto the least loaded;
+// the chains sharing an engine are interleaved copy by copy in proportion
+// to their length (flow-size-aware chunk scheduling), each chain keeping
+// its own order.
+struct EngineSchedule {
+    std::vector<ProxyCopy> copies;
+    std::vector<uint32_t> engine;  // engine id bit per copy
+    std::vector<int> dep;          // previous copy of the same chain, or -1
+    int engines_used = 0;
+};
+
+EngineSchedule schedule_copies(const ProxyImpl &P, const std::vector<ProxyCopy> &copies,
+                               int max_engines) {
     int E = (int)P.engines.size();
     if (max_engines > 0) E = std::min(E, max_engines);
     // Balance bytes per engine: largest chain first onto the least loaded.
@@ -510,23 +561,44 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     for (size_t r = 0; issue.size() < copies.size(); ++r)
         for (int e = 0; e < E; ++e)
             if (r < per_engine[(size_t)e].size()) issue.push_back(per_engine[(size_t)e][r]);
-    std::vector<ProxyCopy> ordered;
-    ordered.reserve(copies.size());
-    for (size_t i : issue) ordered.push_back(copies[i]);
-    op->copies = std::move(ordered);
+    EngineSchedule out;
+    out.copies.reserve(copies.size());
+    for (size_t i : issue) out.copies.push_back(copies[i]);
     std::vector<int> last((size_t)nch, -1);
-    op->engine.resize(op->copies.size());
-    op->dep.resize(op->copies.size());
-    for (size_t i = 0; i < op->copies.size(); ++i) {
-        int ch = op->copies[i].chain;
-        op->engine[i] = P.engines[(size_t)eng_of_chain[(size_t)ch]];
-        op->dep[i] = last[(size_t)ch];
+    out.engine.resize(out.copies.size());
+    out.dep.resize(out.copies.size());
+    for (size_t i = 0; i < out.copies.size(); ++i) {
+        int ch = out.copies[i].chain;
+        out.engine[i] = P.engines[(size_t)eng_of_chain[(size_t)ch]];
+        out.dep[i] = last[(size_t)ch];
         last[(size_t)ch] = (int)i;
     }
-    if (engines_used) {
-        int used = 0;
-        for (auto l : load) used += l > 0;
-        *engines_used = used;
+    for (auto l : load) out.engines_used += l > 0;
+    return out;
+}
+
+hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
+                             unsigned timeout_ms, unsigned wait_limit_us, int handshake,
+                             hipStream_t s, int *engines_used, std::string &err) {
+    ProxyImpl &P = *impl_;
+    {
+        std::lock_guard<std::mutex> lk(P.mu);
+        if (P.sticky != HOCCL_OK) {
+            hoccl_status_t st = P.sticky;
+            err = P.sticky_msg;
+            P.sticky = HOCCL_OK;
+            P.sticky_msg.clear();
+            return st;
+        }
+    }
+    ProxyOp *op = new ProxyOp();
+    op->timeout_ms = timeout_ms ? timeout_ms : 10000;
+    {
+        EngineSchedule sch = schedule_copies(P, copies, max_engines);
+        op->copies = std::move(sch.copies);
+        op->engine = std::move(sch.engine);
+        op->dep = std::move(sch.dep);
+        if (engines_used) *engines_used = sch.engines_used;
     }
     // Signals and a flag slot.
     {
@@ -631,6 +703,56 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     }
     P.cv_work.notify_one();
     return e == hipSuccess ? HOCCL_OK : HOCCL_ERR_HIP;
+}
+
+hoccl_status_t Proxy::capture(const std::vector<ProxyCopy> &copies, int max_engines,
+                              unsigned timeout_ms, unsigned wait_limit_us, hipStream_t s,
+                              int *engines_used, std::string &err) {
+    ProxyImpl &P = *impl_;
+    {
+        std::lock_guard<std::mutex> lk(P.mu);
+        if (P.sticky != HOCCL_OK) {
+            hoccl_status_t st = P.sticky;
+            err = P.sticky_msg;
+            P.sticky = HOCCL_OK;
+            P.sticky_msg.clear();
+            return st;
+        }
+    }
+    CapturedOp *op = new CapturedOp();
+    op->P = &P;
+    {
+        EngineSchedule sch = schedule_copies(P, copies, max_engines);
+        op->copies = std::move(sch.copies);
+        op->engine = std::move(sch.engine);
+        op->dep = std::move(sch.dep);
+        if (engines_used) *engines_used = sch.engines_used;
+    }
+    const uint64_t t = timeout_ms ? timeout_ms : 10000;
+    op->limit = std::chrono::microseconds(wait_limit_us ? (uint64_t)wait_limit_us : (2 * t + 1000) * 1000);
+    auto drop = [&]() {
+        for (auto &sg : op->sig) hsa_signal_destroy(sg);
+        delete op;
+    };
+    while (op->sig.size() < op->copies.size()) {
+        hsa_signal_t sg;
+        if (hsa_signal_create(0, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) {
+            err = "hsa_signal_create failed";
+            drop();
+            return HOCCL_ERR_HIP;
+        }
+        op->sig.push_back(sg);
+    }
+    hipError_t e = hipLaunchHostFunc(s, run_captured, op);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        err = std::string("capturing the copy host function failed: ") + hipGetErrorString(e);
+        drop();
+        return HOCCL_ERR_HIP;
+    }
+    std::lock_guard<std::mutex> lk(P.mu);
+    P.captured.push_back(op);
+    return HOCCL_OK;
 }
 
 }  // namespace hoccl

@@ -43,6 +43,14 @@ class Proxy {
                           unsigned timeout_ms, unsigned wait_limit_us, int handshake,
                           hipStream_t s, int *engines_used, std::string &err);
 
+    // For a stream that is capturing a graph: records a host node on `s`
+    // that, at every replay, issues the copies on their engines and returns
+    // once they have completed (no GPU code, no proxy thread).  The copy
+    // list stays allocated until the proxy is destroyed.
+    hoccl_status_t capture(const std::vector<ProxyCopy> &copies, int max_engines,
+                           unsigned timeout_ms, unsigned wait_limit_us, hipStream_t s,
+                           int *engines_used, std::string &err);
+
   private:
     explicit Proxy(ProxyImpl *impl) : impl_(impl) {}
     ProxyImpl *impl_;

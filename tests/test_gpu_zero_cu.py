@@ -132,3 +132,36 @@ def test_cu_copy_kernel_waits_for_the_cus():
     assert done_ms >= round_ms - 2, f"the CU copy kernel finished at {done_ms:.1f} ms, inside the spin"
     for r in range(len(outs)):
         assert_bitwise(from_dev(outs[r], hc.BF16), ref[r], f"kernel {name} rank {r}")
+
+
+def test_graph_replay_on_auto_finishes_while_every_cu_is_busy():
+    """A graph captured on AUTO records the engine copies as a host node:
+    its replay, too, needs no CU.  The replayed all-gather is bit-exact."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    hc.set_config(copy_path="auto")
+    name, run, outs, ref = _copy_workloads()[0]
+    o = occupy()
+    coll_s = o["streams"][1]
+    run(coll_s)                                # eager first: library state
+    torch.cuda.synchronize()
+    assert hc.last_stats()["copy_path_used"] == hc.COPY_SDMA_ENGINES
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=coll_s):
+        run(coll_s)
+    torch.cuda.synchronize()
+    assert hc.last_stats()["copy_path_used"] == hc.COPY_SDMA_ENGINES
+    for t in outs:
+        t.zero_()
+    torch.cuda.synchronize()
+
+    def replay(s):
+        with torch.cuda.stream(s):
+            g.replay()
+
+    done_ms, round_ms = finish_time_beside_spin(replay)
+    assert done_ms < round_ms - 10, (
+        f"the replay finished {done_ms:.1f} ms after the spin began: its copies needed a CU")
+    for r in range(len(outs)):
+        assert_bitwise(from_dev(outs[r], hc.BF16), ref[r], f"replayed {name} rank {r}")
+    del g
