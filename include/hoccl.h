@@ -34,7 +34,13 @@
  * Asynchrony.  Every call returns once the work is enqueued.  The operation
  *   starts after all work previously enqueued on `stream` and all work
  *   enqueued on `stream` afterwards sees its results.  No call synchronises
- *   the host with the device except where stated (workspace growth).
+ *   the host with the device except where stated (workspace growth).  The
+ *   HIP runtime itself makes the enqueueing thread wait once too much work
+ *   is pending behind unfinished work: on MI355X about 1000 of this
+ *   library's kernel launches (some 150 ring reduce-scatters at R = 8),
+ *   or 32 of the HIP runtime's own copies of 1 MiB or more on the
+ *   HOCCL_COPY_HIP path.  The engine proxy admits 512 operations in flight
+ *   and waits up to its timeout for a free one.
  * Errors.  Every function returns a hoccl_status_t and never throws.
  *   Argument errors are detected before anything is enqueued.  A failing HIP
  *   or HSA call returns HOCCL_ERR_HIP; hoccl_last_error_string() describes

@@ -132,36 +132,50 @@ constexpr int kMaxReduceSegs = 64;
 constexpr int kMaxCopySegs = 128;
 constexpr int kMaxRanks = 64;
 
+// Each kernel's argument struct has a fixed number of slots.  The executor
+// fills the largest form; the launchers pass the smallest form that holds the
+// launch's segments.  The HIP runtime stages the arguments of every launch
+// that has not started yet, and the enqueueing thread waits once about 1 MB
+// of them is pending (measured on MI355X).  With 2 KiB of slots, some 450
+// launches queued behind unfinished work stall the caller; an 8-rank ring
+// step passes 264 bytes (plus the runtime's own 256 bytes of hidden
+// arguments), and about 1000 fit.
 struct RSegArg {
     const void *in0;
     const void *in1;
     void *out;
     uint64_t n;
 };
-struct ReduceArgs {
-    RSegArg seg[kMaxReduceSegs];
+template <int CAP>
+struct ReduceArgsT {
+    RSegArg seg[CAP];
     int nseg;
 };
+using ReduceArgs = ReduceArgsT<kMaxReduceSegs>;
 
 struct CSegArg {
     const void *src;
     void *dst;
     uint64_t bytes;
 };
-struct CopyArgs {
-    CSegArg seg[kMaxCopySegs];
+template <int CAP>
+struct CopyArgsT {
+    CSegArg seg[CAP];
     int nseg;
 };
+using CopyArgs = CopyArgsT<kMaxCopySegs>;
 
-struct FoldArgs {
-    const void *in[kMaxRanks];
-    void *out[kMaxRanks];
+template <int CAP>
+struct FoldArgsT {
+    const void *in[CAP];
+    void *out[CAP];
     uint64_t c;
     uint64_t total;
     int R;
     int write_all;
     int out_at_chunk;
 };
+using FoldArgs = FoldArgsT<kMaxRanks>;
 
 // The stream side of one proxy operation's start/finish handshake.  The
 // three flags are host memory mapped for the device.

@@ -220,9 +220,9 @@ __device__ __forceinline__ void reduce_segment(const RSegArg &s, int lb, int nb)
 template <typename A>
 __device__ __forceinline__ const A &kernargs();
 
-template <class T0, class T1, class TO, int VE, int U, int NT>
-__global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgs) {
-    const ReduceArgs &a = kernargs<ReduceArgs>();
+template <class T0, class T1, class TO, int VE, int U, int NT, int CAP>
+__global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgsT<CAP>) {
+    const ReduceArgsT<CAP> &a = kernargs<ReduceArgsT<CAP>>();
     for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
         reduce_segment<T0, T1, TO, VE, U, NT>(a.seg[seg], lb, nb);
     });
@@ -232,8 +232,8 @@ __global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgs) {
 // Chunk j reads x[(j+1)%R], x[(j+2)%R], ..., x[j] at the chunk's elements and
 // adds them left to right; loads are issued in batches of KB ranks so several
 // are in flight before the adds consume them in order.
-template <class T, int VE, int NR>
-__device__ __forceinline__ void fold_chunk(const FoldArgs &a, int j, int lb, int nb) {
+template <class T, int VE, int NR, class FA>
+__device__ __forceinline__ void fold_chunk(const FA &a, int j, int lb, int nb) {
     using S = typename T::S;
     using A = typename T::A;
     using P = Pack<S, VE>;
@@ -354,9 +354,9 @@ __device__ __forceinline__ const A &kernargs() {
     return *(const A *)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
-template <class T, int VE, int NR>
-__global__ void __launch_bounds__(1024) fold_kernel(FoldArgs) {
-    const FoldArgs &a = kernargs<FoldArgs>();
+template <class T, int VE, int NR, int CAP>
+__global__ void __launch_bounds__(1024) fold_kernel(FoldArgsT<CAP>) {
+    const FoldArgsT<CAP> &a = kernargs<FoldArgsT<CAP>>();
     for_each_segment(a.R, [&](int j, int lb, int nb) { fold_chunk<T, VE, NR>(a, j, lb, nb); });
 }
 
@@ -404,8 +404,9 @@ __device__ __forceinline__ void copy_segment(const CSegArg &s, int lb, int nb) {
 
 constexpr int kCopyUnroll = 2;
 
-__global__ void __launch_bounds__(1024) copy_kernel(CopyArgs) {
-    const CopyArgs &a = kernargs<CopyArgs>();
+template <int CAP>
+__global__ void __launch_bounds__(1024) copy_kernel(CopyArgsT<CAP>) {
+    const CopyArgsT<CAP> &a = kernargs<CopyArgsT<CAP>>();
     for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
         copy_segment<kCopyUnroll>(a.seg[seg], lb, nb);
     });
@@ -423,9 +424,46 @@ static hipError_t launch(const void *kernel, const Args &a, int wg, int threads,
     return hipLaunchKernel(kernel, dim3((unsigned)wg), dim3((unsigned)threads), args, 0, s);
 }
 
+// The first a.nseg slots of `a` in an argument struct of CAP slots.
+template <int CAP>
+static ReduceArgsT<CAP> fit(const ReduceArgs &a) {
+    ReduceArgsT<CAP> b{};
+    for (int k = 0; k < a.nseg; ++k) b.seg[k] = a.seg[k];
+    b.nseg = a.nseg;
+    return b;
+}
+template <int CAP>
+static CopyArgsT<CAP> fit(const CopyArgs &a) {
+    CopyArgsT<CAP> b{};
+    for (int k = 0; k < a.nseg; ++k) b.seg[k] = a.seg[k];
+    b.nseg = a.nseg;
+    return b;
+}
+template <int CAP>
+static FoldArgsT<CAP> fit(const FoldArgs &a) {
+    FoldArgsT<CAP> b{};
+    for (int r = 0; r < a.R; ++r) {
+        b.in[r] = a.in[r];
+        b.out[r] = a.out[r];
+    }
+    b.c = a.c;
+    b.total = a.total;
+    b.R = a.R;
+    b.write_all = a.write_all;
+    b.out_at_chunk = a.out_at_chunk;
+    return b;
+}
+
+// Ring steps of up to 8 ranks (264 bytes of arguments) or up to 64 (2 KiB).
+constexpr int kSmallSegs = 8;
+
 template <class T0, class T1, class TO, int VE, int U, int NT>
 static hipError_t launch_rs(const ReduceArgs &a, int wg, int threads, hipStream_t s) {
-    return launch((const void *)reduce_step_kernel<T0, T1, TO, VE, U, NT>, a, wg, threads, s);
+    if (a.nseg <= kSmallSegs)
+        return launch((const void *)reduce_step_kernel<T0, T1, TO, VE, U, NT, kSmallSegs>,
+                      fit<kSmallSegs>(a), wg, threads, s);
+    return launch((const void *)reduce_step_kernel<T0, T1, TO, VE, U, NT, kMaxReduceSegs>, a, wg,
+                  threads, s);
 }
 
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg, int threads,
@@ -483,14 +521,20 @@ size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph) {
 size_t fold_elems_per_thread(hoccl_dtype_t dt) { return 16 / dtype_size(dt); }
 size_t copy_bytes_per_thread() { return 16 * kCopyUnroll; }
 
+// R = 2, 3, 4 and 8 have kernels of their own, whose arguments hold R ranks.
+template <class T, int VE, int NR>
+static hipError_t launch_fold_r(const FoldArgs &a, int wg, int threads, hipStream_t s) {
+    return launch((const void *)fold_kernel<T, VE, NR, NR>, fit<NR>(a), wg, threads, s);
+}
+
 template <class T, int VE>
 static hipError_t launch_fold_t(const FoldArgs &a, int wg, int threads, hipStream_t s) {
     switch (a.R) {
-    case 2: return launch((const void *)fold_kernel<T, VE, 2>, a, wg, threads, s);
-    case 3: return launch((const void *)fold_kernel<T, VE, 3>, a, wg, threads, s);
-    case 4: return launch((const void *)fold_kernel<T, VE, 4>, a, wg, threads, s);
-    case 8: return launch((const void *)fold_kernel<T, VE, 8>, a, wg, threads, s);
-    default: return launch((const void *)fold_kernel<T, VE, 0>, a, wg, threads, s);
+    case 2: return launch_fold_r<T, VE, 2>(a, wg, threads, s);
+    case 3: return launch_fold_r<T, VE, 3>(a, wg, threads, s);
+    case 4: return launch_fold_r<T, VE, 4>(a, wg, threads, s);
+    case 8: return launch_fold_r<T, VE, 8>(a, wg, threads, s);
+    default: return launch((const void *)fold_kernel<T, VE, 0, kMaxRanks>, a, wg, threads, s);
     }
 }
 
@@ -501,8 +545,11 @@ hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
     return hipErrorInvalidValue;
 }
 
+// Copy launches of up to 8, 32 or 128 segments (200 bytes to 3 KiB of arguments).
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s) {
-    return launch((const void *)copy_kernel, a, wg, threads, s);
+    if (a.nseg <= 8) return launch((const void *)copy_kernel<8>, fit<8>(a), wg, threads, s);
+    if (a.nseg <= 32) return launch((const void *)copy_kernel<32>, fit<32>(a), wg, threads, s);
+    return launch((const void *)copy_kernel<kMaxCopySegs>, a, wg, threads, s);
 }
 
 }  // namespace hoccl

@@ -200,3 +200,61 @@ def test_many_engine_operations_in_flight():
     want = from_dev(first, hc.BF16)
     for i in (1, K // 2, K):
         assert_bitwise(from_dev(bufs[i], hc.BF16), want, f"buffer {i}")
+
+
+@pytest.mark.parametrize("case,calls", [("ring_reduce_scatter", 100), ("kernel_sendrecv", 500)])
+def test_many_launches_queue_without_stalling_the_host(case, calls):
+    """Hundreds of collectives queued behind a closed gate, as a training
+    step queues its gradient reductions behind unfinished compute: the
+    enqueueing thread must not wait for the GPU.  The HIP runtime stages
+    the arguments of every launch that has not started and makes the
+    caller wait once about 1 MB of them is pending.  100 ring
+    reduce-scatters (700 launches of an 8-rank step) or 500 CU-kernel
+    send/recvs fit only with arguments sized to the launch (with a fixed
+    2 KiB of slots, some 450 launches fill it).  The timer opens the gate
+    after 10 s in any case; the results must equal the oracle bit for bit."""
+    s, _ = own_queue_streams()
+    R = 8
+    if case == "ring_reduce_scatter":
+        n = 4096
+        x = [W.random_values("bf16", 406, r, R * n) for r in range(R)]
+        ref = oracle.reduce_scatter_new(x, hc.BF16)
+        send = [to_dev(a, hc.BF16) for a in x]
+        outs = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+        run = lambda: hc.reduce_scatter(send, outs, stream=s)
+    else:
+        hc.set_config(copy_path="kernel")
+        n = 2048
+        a = to_dev(W.random_bits(407, 0, n, 2), hc.BF16)
+        outs = [torch.empty(n, dtype=torch.bfloat16, device="cuda")]
+        ref = [from_dev(a, hc.BF16)]
+        run = lambda: hc.sendrecv([a, a], [outs[0], outs[0]], [1, -1], stream=s)
+    run()                                       # library state and workspace
+    torch.cuda.synchronize()
+    for o in outs:
+        fill_canary(o, hc.BF16)
+    torch.cuda.synchronize()
+    f = flag()
+    cell = ctypes.c_uint32.from_address(f)
+    cell.value = 0
+    k = int(time.time() * 1000) % 1_000_000 + 1
+    fired = []
+    release = threading.Timer(10.0, lambda: (fired.append(True), setattr(cell, "value", k)))
+    release.start()
+    try:
+        assert HIP.hipStreamWaitValue32(V(s.cuda_stream), V(f), k, WAIT_EQ, 0xFFFFFFFF) == 0
+        t0 = time.perf_counter()
+        with torch.cuda.stream(s):
+            for _ in range(calls):
+                run()
+        enqueue_s = time.perf_counter() - t0
+        assert enqueue_s < 2.0 and not fired, (
+            f"enqueueing {calls} calls took {enqueue_s:.1f} s: the host waited for the GPU")
+        assert not s.query(), "the stream ran before the gate opened"
+    finally:
+        release.cancel()
+        cell.value = k
+    s.synchronize()
+    torch.cuda.synchronize()
+    for r in range(len(outs)):
+        assert_bitwise(from_dev(outs[r], hc.BF16), ref[r], f"{case} rank {r}")
