@@ -29,8 +29,11 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, GB/s
 
 
+_T0 = time.perf_counter()
+
+
 def log(*a):
-    print("[bench]", *a, file=sys.stderr, flush=True)
+    print(f"[bench {time.perf_counter() - _T0:6.1f} s]", *a, file=sys.stderr, flush=True)
 
 
 def bf16_dev(a):
@@ -258,8 +261,11 @@ def host_gate():
     `open()` has been called, so work on several streams that waits on it
     starts together, however long the host takes to enqueue that work.  An
     own-queue stream waits (hipStreamWaitValue32, equality) on a token in
-    coherent host memory; a timer opens the gate after 30 s in any case, so
-    the wait always ends."""
+    coherent host memory; a timer opens the gate after 5 s in any case, so
+    the wait always ends.  `open()` returns True when the timer had opened
+    it: the host was held up while enqueueing (the HIP runtime makes the
+    enqueueing thread wait once too much work is queued), the streams did
+    not start together and the measurement is void."""
     import ctypes
     import threading
     import torch
@@ -283,12 +289,19 @@ def host_gate():
         raise RuntimeError("hipStreamWaitValue32 failed")
     ev = torch.cuda.Event()
     ev.record(s)
-    timer = threading.Timer(30.0, lambda: setattr(g["cell"], "value", k))
+    fired = []
+
+    def on_timer():
+        fired.append(True)
+        g["cell"].value = k
+
+    timer = threading.Timer(5.0, on_timer)
     timer.start()
 
     def open_gate():
         timer.cancel()
         g["cell"].value = k
+        return bool(fired)
 
     return ev, open_gate
 
@@ -300,8 +313,8 @@ def _gated(gemm, collective=None, n_coll=0):
     thing while the GPU runs whether or not collectives are enqueued: GEMM
     time depends on it by several percent (a host that sleeps, spins or
     records events while the GEMMs run sees 0.80-0.87 ms).  Returns the
-    collective window start c0, the collective's end events and the GEMM
-    event pairs."""
+    collective window start c0, the collective's end events, the GEMM
+    event pairs and whether the gate's timer had to open it."""
     import torch
     gs, cs = gemm[4], gemm[5]
     torch.cuda.synchronize()
@@ -322,9 +335,9 @@ def _gated(gemm, collective=None, n_coll=0):
                     ends.append(e)
         _, _, ts = _gemm_run(gemm)
     finally:
-        open_gate()
+        blocked = open_gate()
     torch.cuda.synchronize()
-    return c0, ends, ts
+    return c0, ends, ts, blocked
 
 
 def gemm_slowdown(hc, collective, med, gemm):
@@ -336,15 +349,26 @@ def gemm_slowdown(hc, collective, med, gemm):
     call while the GEMMs ran (the calls that finished before the last GEMM,
     from the common start) against `med`, its median time alone.  Returns
     (median GEMM slowdown, fraction of the 20 GEMMs that overlapped,
-    collective slowdown)."""
+    collective slowdown, collectives queued).  A run whose enqueue held up
+    the host is void: it is repeated with half the collectives, twice at
+    most, and otherwise all three figures are None."""
     import torch
     t_alone, cs = gemm[3], gemm[5]
     n_coll = int(45 * t_alone / max(med, 1e-6)) + 3
     with torch.cuda.stream(cs):
         collective(cs)
-    _, _, before = _gated(gemm)
-    c0, ends, ts = _gated(gemm, collective, n_coll)
-    _, _, after = _gated(gemm)
+    for attempt in range(3):
+        _, _, before, b0 = _gated(gemm)
+        c0, ends, ts, b1 = _gated(gemm, collective, n_coll)
+        _, _, after, b2 = _gated(gemm)
+        if not (b0 or b1 or b2):
+            break
+        log(f"  the host was held up enqueueing {n_coll} collectives behind the gate: void")
+        if n_coll == 1:
+            break
+        n_coll = max(1, n_coll // 2)
+    if b0 or b1 or b2:
+        return None, None, None, n_coll
     # GEMM i alone, averaged over a run before and a run after the
     # concurrent one, so that a drift of the clocks across the three runs
     # does not read as a slowdown or a speed-up.
@@ -353,14 +377,14 @@ def gemm_slowdown(hc, collective, med, gemm):
     ratios = [a.elapsed_time(b) / base[i] for i, (a, b) in enumerate(ts)
               if c0.elapsed_time(a) >= 0 and c0.elapsed_time(b) <= end]
     if not ratios:
-        return None, 0.0, None
+        return None, 0.0, None, n_coll
     # The collective's calls that finished while the GEMMs still ran, timed
     # from the common start: their mean time per call against `med`.  None
     # when not even the first call finished before the last GEMM.
     g_hi = c0.elapsed_time(ts[-1][1])
     done = [t for t in (c0.elapsed_time(e) for e in ends) if t <= g_hi]
     coll = round(done[-1] / len(done) / 1e3 / med - 1, 4) if done else None
-    return (round(statistics.median(ratios) - 1, 4), round(len(ratios) / len(ts), 3), coll)
+    return (round(statistics.median(ratios) - 1, 4), round(len(ratios) / len(ts), 3), coll, n_coll)
 
 
 def make_gemm():
@@ -402,7 +426,11 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
                  path_used=["auto", "hip", "engines", "kernel"][st["copy_path_used"]],
                  cus_used=st["cus_used_max"], host_enqueue_us=round(st["host_enqueue_us"], 1))
         if gemm is not None:
-            r["gemm_slowdown"], r["gemm_overlap"], r["collective_slowdown"] = gemm_slowdown(hc, run, med, gemm)
+            (r["gemm_slowdown"], r["gemm_overlap"], r["collective_slowdown"],
+             r["collectives_queued"]) = gemm_slowdown(hc, run, med, gemm)
+            if r["gemm_overlap"] is None:
+                r["gemm_slowdown_void"] = ("the enqueueing thread was held up with the collectives queued "
+                                           "behind the gate, so they could not start with the GEMMs")
         res[name] = r
         hc.set_config(**saved)
     return res
@@ -697,8 +725,9 @@ def bench_rs_workgroups(hc, x, reps, gemm=None):
                    hbm_GBs=round(st["hbm_bytes_algorithmic"] / med / 1e9, 1),
                    cus_used=st["cus_used_max"])
         if gemm is not None:
-            row["gemm_slowdown"], row["gemm_overlap"], row["collective_slowdown"] = gemm_slowdown(
-                hc, lambda s: hc.reduce_scatter(send, recv, stream=s), med, gemm)
+            (row["gemm_slowdown"], row["gemm_overlap"], row["collective_slowdown"],
+             row["collectives_queued"]) = gemm_slowdown(hc, lambda s: hc.reduce_scatter(send, recv, stream=s),
+                                                        med, gemm)
         out[f"wg{st['workgroups_per_step']}"] = row
     hc.set_config(workgroups_per_step=0)
     return out
@@ -769,14 +798,16 @@ FOLD_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "fold_kernel_rs_bf16_R8_tr
 
 
 def kernel_source_hash():
-    """SHA-256 (16 hex digits) of kernels.hip without its // comments and
-    blank lines: any change to the code voids the committed counter figures,
-    an edit of a comment does not."""
+    """SHA-256 (16 hex digits) of the kernels' source (kernels.hip and the
+    header with their argument structs) without // comments and blank
+    lines: any change to the code voids the committed counter figures, an
+    edit of a comment does not."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "paper_2609_34334_amd", "csrc", "kernels.hip")
-    with open(path, encoding="utf-8") as f:
-        lines = [re.sub(r"//.*", "", line).rstrip() for line in f]
+    lines = []
+    for name in ("kernels.hip", "hoccl_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_34334_amd", "csrc", name), encoding="utf-8") as f:
+            lines += [re.sub(r"//.*", "", line).rstrip() for line in f]
     code = "\n".join(line for line in lines if line)
     return hashlib.sha256(code.encode()).hexdigest()[:16]
 
@@ -791,7 +822,7 @@ def measured_traffic(summary=TRAFFIC_SUMMARY):
         if ":" in line and not line.startswith(("#", " ", "|")):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("kernels_hip_sha256_16") != kernel_source_hash():
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     try:
         return int(float(kv["traffic_bytes_per_launch"]))
@@ -846,7 +877,7 @@ def pmc_workload(hc, W):
         for _ in range(5):
             hc.reduce_scatter(send, recv)
     torch.cuda.synchronize()
-    print(json.dumps({"pmc_workload": "done", "kernels_hip_sha256_16": kernel_source_hash()}))
+    print(json.dumps({"pmc_workload": "done", "kernel_source_sha256_16": kernel_source_hash()}))
 
 
 def occupancy_workload(hc, W):
@@ -872,7 +903,7 @@ def occupancy_workload(hc, W):
             hc.sendrecv([src], [dst], [0])
     torch.cuda.synchronize()
     print(json.dumps({"occupancy_workload": "done", "rs_budgets": budgets, "copy_budgets": [8, 0],
-                      "kernels_hip_sha256_16": kernel_source_hash()}))
+                      "kernel_source_sha256_16": kernel_source_hash()}))
 
 
 def main():
