@@ -557,7 +557,8 @@ def bench_p2p_sizes(hc, reps):
     big = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda")
     big2 = torch.empty_like(big)
     rows = []
-    for sz in [2 << 20, 32 << 20, 512 << 20]:
+    # 50,331,648 B: one all-gather hop, a 25,165,824-element bf16 shard.
+    for sz in [2 << 20, 32 << 20, 50_331_648, 512 << 20]:
         ne = sz // 2
         s0, d1 = big[:ne], big2[:ne]
         row = {"bytes": sz}
@@ -570,6 +571,40 @@ def bench_p2p_sizes(hc, reps):
             hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0)
         rows.append(row)
     return dict(workload="single bf16 message rank 0 -> 1, algbw GB/s", rows=rows)
+
+
+def bench_ring_hop(hc, x, reps):
+    """One rank's share of a ring step: the unit each GPU would run per hop
+    with the ranks on separate GPUs.  The middle hop over one 3,145,728-
+    element block of the headline input (fp32 partial updated in place with
+    a bf16 local block: 10 bytes per element, 31.5 MB) at several workgroup
+    budgets, and the first and last hops at the automatic budget; device
+    time alone (each call queued behind a spin), with the last-level cache
+    warm and after writing 1 GiB (flushed)."""
+    import torch
+    R = len(x)
+    n = x[0].size // R
+    j = 3
+    loc = bf16_dev(x[j][j * n:(j + 1) * n])
+    prev = bf16_dev(x[j - 1][j * n:(j + 1) * n])
+    part = loc.float()
+    dst = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    cases = [("middle_auto" if w == 0 else f"middle_wg{w}", w,
+              lambda: hc.ring_hop(part, loc, out=part, hop="middle")) for w in (0, 256, 64, 8)]
+    cases += [("first", 0, lambda: hc.ring_hop(prev, loc, out=part, hop="first")),
+              ("last", 0, lambda: hc.ring_hop(part, loc, out=dst, hop="last"))]
+    out = {}
+    for name, w, fn in cases:
+        with hc.config(workgroups_per_step=w):
+            warm, _ = queued_time(fn, reps, flush=False)
+            cold, _ = queued_time(fn, reps, flush=True)
+            st = hc.last_stats()
+        b = st["hbm_bytes_algorithmic"]
+        out[name] = dict(bytes=b, warm_us=round(warm * 1e6, 2), flushed_us=round(cold * 1e6, 2),
+                        warm_GBs=round(b / warm / 1e9, 1), flushed_GBs=round(b / cold / 1e9, 1),
+                        workgroups=st["workgroups_per_step"], cus_used=st["cus_used_max"])
+    return dict(workload="one rank's ring hop of the headline reduce-scatter: 3,145,728 elements, "
+                         "bf16 local block, fp32 partial (hoccl_ring_hop)", **out)
 
 
 def bench_rs_variants(hc, reps):
@@ -995,6 +1030,11 @@ def main():
             extra["reduce_scatter_graph"] = bench_rs_graph(hc, rs["x"], args.steps)
         except Exception as e:
             extra["reduce_scatter_graph"] = {"error": repr(e)}
+        log("ring hop, one rank")
+        try:
+            extra["ring_hop_one_rank"] = bench_ring_hop(hc, rs["x"], 20)
+        except Exception as e:
+            extra["ring_hop_one_rank"] = {"error": repr(e)}
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
         extra["small_message_latency"] = bench_small_message(hc, 30)

@@ -323,6 +323,38 @@ hoccl_status_t hoccl_alltoallv(const void *const *send,
                                void *const *recv, const size_t *rdispls,
                                hoccl_dtype_t dtype, int R, hipStream_t stream);
 
+/* One ring hop of one rank: out[i] = partial[i] + local[i] for i < count,
+ * in the arithmetic of the ring fold above, with `partial` the earlier
+ * ranks' sum (or, on the first hop, the previous rank's own element) and
+ * `local` this rank's contribution.  This is the step each GPU runs per hop
+ * when the ranks are GPUs (each hop of the ring reduce-scatter of the
+ * paper's collective set), exposed on its own so that one rank's share can
+ * be run and timed; the collectives above run it for all R ranks in one
+ * launch.  `hop` selects the operand types of a bf16 fold:
+ *   HOCCL_HOP_FIRST   partial bf16, out fp32
+ *   HOCCL_HOP_MIDDLE  partial fp32, out fp32
+ *   HOCCL_HOP_LAST    partial fp32, out bf16 (rounded to nearest even)
+ *   HOCCL_HOP_ONLY    partial bf16, out bf16 (a two-rank fold, rounded once)
+ * `local` is bf16 throughout.  For int32 and fp32 every operand has the
+ * dtype and the four hops compute the same thing.  All three are device
+ * pointers of count elements, any alignment (16-byte aligned runs at full
+ * speed).  `out` may be `partial` or `local` itself when its element size
+ * is the same (the in-place update of a partial); any other overlap is
+ * HOCCL_ERR_INVALID_ARG.  Launch shape from workgroups_per_step and
+ * threads_per_workgroup as for the collectives; no workspace, no copies,
+ * no allocation, so the call may be captured into a graph.  Statistics as
+ * for a collective (one reduction launch). */
+typedef enum {
+    HOCCL_HOP_FIRST = 0,
+    HOCCL_HOP_MIDDLE = 1,
+    HOCCL_HOP_LAST = 2,
+    HOCCL_HOP_ONLY = 3
+} hoccl_hop_t;
+
+hoccl_status_t hoccl_ring_hop(const void *partial, const void *local, void *out,
+                              size_t count, hoccl_dtype_t dtype, hoccl_hop_t hop,
+                              hipStream_t stream);
+
 /* ---- introspection (tests and tools) ------------------------------------
  * Writes the schedule the planner builds for a collective as JSON into buf
  * (NUL-terminated, truncated to len).  op: 0 all-reduce, 1 reduce-scatter,

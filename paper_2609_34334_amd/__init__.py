@@ -31,6 +31,8 @@ REDUCE_RING, REDUCE_DIRECT = 0, 1
 OP_ALLREDUCE, OP_REDUCE_SCATTER, OP_ALLGATHER, OP_SENDRECV, OP_ALLTOALL = range(5)
 
 _DTYPES = {torch.int32: INT32, torch.float32: FP32, torch.bfloat16: BF16}
+HOP_FIRST, HOP_MIDDLE, HOP_LAST, HOP_ONLY = range(4)
+HOPS = {"first": HOP_FIRST, "middle": HOP_MIDDLE, "last": HOP_LAST, "only": HOP_ONLY}
 COPY_PATHS = {"auto": COPY_AUTO, "hip": COPY_HIP, "engines": COPY_SDMA_ENGINES,
               "kernel": COPY_KERNEL}
 
@@ -83,6 +85,7 @@ _SIGS = {
     "hoccl_sendrecv": [_vpp, _vpp, ctypes.POINTER(_i), _sz, _i, _i, ctypes.c_void_p],
     "hoccl_alltoall": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
     "hoccl_alltoallv": [_vpp, _szp, _szp, _vpp, _szp, _i, _i, ctypes.c_void_p],
+    "hoccl_ring_hop": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _sz, _i, _i, ctypes.c_void_p],
     "hoccl_debug_plan_json": [_i, _sz, _i, _i, ctypes.c_char_p, _sz, _szp],
     "hoccl_debug_schedule_json": [_i, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i),
                                   ctypes.POINTER(_i), ctypes.c_double, ctypes.c_double,
@@ -351,3 +354,32 @@ def alltoallv(send, counts, sdispls, recv, rdispls, stream=None):
     _check(_lib.hoccl_alltoallv(_ptrs(send), S(*counts), S(*sdispls), _ptrs(recv), S(*rdispls),
                                 dt, R, _stream(stream)), "hoccl_alltoallv")
     return recv
+
+
+def ring_hop(partial, local, out=None, hop="middle", stream=None):
+    """One ring hop of one rank: out = partial + local in the ring fold's
+    arithmetic (hoccl_ring_hop).  With bf16 `local`, `partial` and `out`
+    are fp32 or bf16 by hop: "first" bf16 -> fp32, "middle" fp32 -> fp32,
+    "last" fp32 -> bf16, "only" bf16 -> bf16; int32 and fp32 use their own
+    dtype throughout.  `out` defaults to a new tensor and may be `partial`
+    (same dtype) for an in-place update."""
+    h = HOPS[hop] if isinstance(hop, str) else int(hop)
+    dt = _dtype_of([local])
+    bf = local.dtype == torch.bfloat16
+    want_in = torch.float32 if bf and h in (HOP_MIDDLE, HOP_LAST) else local.dtype
+    want_out = torch.float32 if bf and h in (HOP_FIRST, HOP_MIDDLE) else local.dtype
+    if out is None:
+        out = torch.empty(local.numel(), dtype=want_out, device=local.device)
+    for t, want, name in ((partial, want_in, "partial"), (out, want_out, "out")):
+        if t.dtype != want:
+            raise TypeError(f"{name} must be {want} for this hop, not {t.dtype}")
+        if t.device != local.device:
+            raise ValueError("all buffers must live on the same GPU")
+        if not t.is_contiguous():
+            raise ValueError("buffers must be contiguous")
+        if t.numel() != local.numel():
+            raise ValueError("partial, local and out must have the same number of elements")
+    with torch.cuda.device(local.device):
+        _check(_lib.hoccl_ring_hop(partial.data_ptr(), local.data_ptr(), out.data_ptr(), local.numel(),
+                                   dt, h, _stream(stream)), "hoccl_ring_hop")
+    return out

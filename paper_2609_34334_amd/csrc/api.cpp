@@ -322,6 +322,14 @@ hoccl_status_t ensure_ws(DeviceState &st, size_t bytes, bool capturing) {
 // between one workgroup per CU and 64 per CU (16384 on MI355X): measured on
 // the headline bf16 ring and fold, the streaming kernels keep gaining up to
 // about one pass per thread and lose nothing beyond.
+int workgroups_for(const DeviceState &st, const hoccl_config_t &cfg, unsigned long long passes,
+                   int threads) {
+    if (cfg.workgroups_per_step > 0) return cfg.workgroups_per_step;
+    unsigned long long wg = (passes + (unsigned long long)threads - 1) / (unsigned long long)threads;
+    unsigned long long lo = (unsigned long long)st.num_cus, hi = 64ull * st.num_cus;
+    return (int)std::min(hi, std::max(lo, wg));
+}
+
 int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan &p, int threads) {
     if (cfg.workgroups_per_step > 0) return cfg.workgroups_per_step;
     unsigned long long passes = 0;  // thread passes of the largest launch
@@ -336,9 +344,7 @@ int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan
     if (p.has_fold) need(p.fold.total, fold_elems_per_thread(p.dtype));
     if (cfg.copy_path == HOCCL_COPY_KERNEL)
         for (const CopyOp &c : p.copies) need((unsigned long long)c.bytes * p.R, copy_bytes_per_thread());
-    unsigned long long wg = (passes + (unsigned long long)threads - 1) / (unsigned long long)threads;
-    unsigned long long lo = (unsigned long long)st.num_cus, hi = 64ull * st.num_cus;
-    return (int)std::min(hi, std::max(lo, wg));
+    return workgroups_for(st, cfg, passes, threads);
 }
 
 hoccl_status_t timed_begin(DeviceState &st, const hoccl_config_t &cfg, hipStream_t s,
@@ -842,6 +848,76 @@ int hoccl_sdma_engine_count(void) {
         return 0;
     }
     return st->proxy->engine_count();
+}
+
+hoccl_status_t hoccl_ring_hop(const void *partial, const void *local, void *out, size_t count,
+                              hoccl_dtype_t dt, hoccl_hop_t hop, hipStream_t stream) {
+    auto t0 = std::chrono::steady_clock::now();
+    if (dt != HOCCL_INT32 && dt != HOCCL_FP32 && dt != HOCCL_BF16) {
+        set_err("unknown dtype %d", (int)dt);
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if ((int)hop < HOCCL_HOP_FIRST || (int)hop > HOCCL_HOP_ONLY) {
+        set_err("unknown hop %d", (int)hop);
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if (count == 0) return HOCCL_OK;
+    if (!partial || !local || !out) {
+        set_err("partial, local and out must not be NULL");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    // Element sizes of partial, local and out (see Phase).
+    const size_t es = dtype_size(dt);
+    size_t s0 = es, so = es;
+    if (dt == HOCCL_BF16) {
+        s0 = (hop == HOCCL_HOP_MIDDLE || hop == HOCCL_HOP_LAST) ? 4 : 2;
+        so = (hop == HOCCL_HOP_FIRST || hop == HOCCL_HOP_MIDDLE) ? 4 : 2;
+    }
+    if (size_overflows(count, 4)) return HOCCL_ERR_INVALID_ARG;
+    const Range r0{(uintptr_t)partial, (uintptr_t)partial + count * s0, 0, false};
+    const Range r1{(uintptr_t)local, (uintptr_t)local + count * es, 0, false};
+    const Range ro{(uintptr_t)out, (uintptr_t)out + count * so, 0, true};
+    // Exact aliasing with an input of the same element size is an in-place
+    // update: each element is read and then written by the same thread.
+    if ((overlaps(ro, r0) && !(ro.lo == r0.lo && so == s0)) ||
+        (overlaps(ro, r1) && !(ro.lo == r1.lo && so == es))) {
+        set_err("out overlaps an input other than as the same buffer of the same element type");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(stream, &cap));
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    DeviceState *stp = nullptr;
+    TRY(get_state(&stp, capturing));
+    DeviceState &st = *stp;
+    hoccl_config_t cfg = config();
+    if (capturing) cfg.kernel_timing = 0;
+    std::memset(&t_stats, 0, sizeof t_stats);
+    const Phase ph = (Phase)hop;
+    const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
+    const size_t per = reduce_step_elems_per_thread(dt, ph);
+    const int wg = workgroups_for(st, cfg, (count + per - 1) / per, threads);
+    ReduceArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.seg[0].in0 = partial;
+    a.seg[0].in1 = local;
+    a.seg[0].out = out;
+    a.seg[0].n = count;
+    a.nseg = 1;
+    TimingPair *tp;
+    TRY(timed_begin(st, cfg, stream, &tp));
+    HIP_TRY(launch_reduce_step(dt, ph, a, wg, threads, stream));
+    TRY(timed_end(tp, stream));
+    t_stats.reduce_launches = 1;
+    t_stats.workgroups_per_step = wg;
+    t_stats.cus_available = st.num_cus;
+    t_stats.cus_used_max = std::min(wg, st.num_cus);
+    t_stats.copy_path_used = HOCCL_COPY_AUTO;
+    t_stats.reduce_algo_used = HOCCL_REDUCE_RING;
+    t_stats.hbm_bytes_algorithmic = (unsigned long long)count * (s0 + es + so);
+    t_stats.host_enqueue_us =
+        std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+    return HOCCL_OK;
 }
 
 hoccl_status_t hoccl_allreduce(const void *const *send, void *const *recv, size_t count,

@@ -153,3 +153,19 @@ def test_size_overflow_rejected_with_a_reason():
     for fn in (L.hoccl_allreduce, L.hoccl_reduce_scatter, L.hoccl_allgather, L.hoccl_alltoall):
         assert fn(send, recv, huge, hc.FP32, 2, None) == hc.ERR_INVALID_ARG
         assert b"does not fit" in L.hoccl_last_error_string()
+
+
+def test_ring_hop_rejects_bad_arguments_before_the_device():
+    a, b, o = 0x100000, 0x200000, 0x300000
+    assert L.hoccl_ring_hop(a, b, o, 4, 9, hc.HOP_MIDDLE, None) == hc.ERR_INVALID_ARG      # dtype
+    assert L.hoccl_ring_hop(a, b, o, 4, hc.BF16, 4, None) == hc.ERR_INVALID_ARG            # hop
+    assert L.hoccl_ring_hop(a, b, o, 4, hc.BF16, -1, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_ring_hop(None, b, o, 4, hc.FP32, hc.HOP_MIDDLE, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_ring_hop(a, b, None, 4, hc.FP32, hc.HOP_MIDDLE, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_ring_hop(0, 0, 0, 0, hc.FP32, hc.HOP_MIDDLE, None) == hc.OK             # no work
+    # bf16 middle hop: out (fp32, 16 bytes) may be the partial itself, but not
+    # the bf16 local (other element size) nor half-overlap the partial.
+    assert L.hoccl_ring_hop(a, b, b, 4, hc.BF16, hc.HOP_MIDDLE, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_ring_hop(a, b, a + 8, 4, hc.BF16, hc.HOP_MIDDLE, None) == hc.ERR_INVALID_ARG
+    # last hop: bf16 out aliasing the fp32 partial is a different element size
+    assert L.hoccl_ring_hop(a, b, a, 4, hc.BF16, hc.HOP_LAST, None) == hc.ERR_INVALID_ARG
