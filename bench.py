@@ -234,6 +234,23 @@ def dedicated_stream():
     return torch.cuda.ExternalStream(s.value)
 
 
+def masked_stream(cus):
+    """A stream with a hardware queue of its own whose kernels run only on
+    the logical CUs in `cus` (bit i of the runtime's 256-bit CU mask); None
+    if the runtime refuses the mask (it needs a CU in every XCD: logical
+    CUs 0-7 are one per XCD)."""
+    import ctypes
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")    # the HIP runtime torch has loaded
+    words = [0] * 8
+    for c in cus:
+        words[c // 32] |= 1 << (c % 32)
+    s = ctypes.c_void_p()
+    if hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), 8, (ctypes.c_uint32 * 8)(*words)) != 0:
+        return None
+    return torch.cuda.ExternalStream(s.value)
+
+
 def _gemm_run(gemm, k=20):
     import torch
     A, B, C, _, gs, _ = gemm
@@ -768,6 +785,45 @@ def bench_rs_workgroups(hc, x, reps, gemm=None):
     return out
 
 
+def bench_cu_partition(hc, x, gemm):
+    """CUs set aside for the reduction, the analog of a collective library
+    that owns a fixed set of SMs: the GEMM's stream is masked to the other
+    CUs, and the headline ring reduce-scatter runs with K workgroups per
+    step on a stream masked to K CUs of its own (two or four per XCD).
+    Reports the masked GEMM alone against the full chip, the reduction alone
+    on its K CUs, and the gated pair: the GEMM against the masked GEMM
+    alone, the reduction against itself alone."""
+    import torch
+    R = len(x)
+    n = x[0].size // R
+    send = [bf16_dev(a) for a in x]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    A, B, C, t_full = gemm[:4]
+    out = {"gemm_full_chip_ms": round(t_full * 1e3, 4)}
+    for K in (16, 32):
+        gs, cs = masked_stream(range(K, ncu)), masked_stream(range(K))
+        if gs is None or cs is None:
+            out[f"cus{K}"] = {"error": "CU mask refused"}
+            continue
+        _, _, ts = _gemm_run((A, B, C, 0.0, gs, cs))
+        torch.cuda.synchronize()
+        t_masked = statistics.median(a.elapsed_time(b) for a, b in ts) / 1e3
+        g2 = (A, B, C, t_masked, gs, cs)
+        with hc.config(workgroups_per_step=K):
+            with torch.cuda.stream(cs):
+                med, _ = event_time(lambda: hc.reduce_scatter(send, recv, stream=cs), 5)
+            row = dict(gemm_masked_ms=round(t_masked * 1e3, 4),
+                       gemm_cost_of_the_mask=round(t_masked / t_full - 1, 4),
+                       reduce_scatter_alone_ms=round(med * 1e3, 4))
+            (row["gemm_slowdown"], row["gemm_overlap"], row["collective_slowdown"],
+             row["collectives_queued"]) = gemm_slowdown(
+                hc, lambda s: hc.reduce_scatter(send, recv, stream=s), med, g2)
+        out[f"cus{K}"] = row
+    return dict(workload="headline ring reduce-scatter on K reserved CUs (K workgroups per step) beside "
+                         "a bf16 8192^3 GEMM masked to the other CUs", **out)
+
+
 def size_sweep(hc):
     """algbw against message size, 2 MiB .. 1 GiB, as in the paper's
     microbenchmarks: send/recv (one message 0 -> 1), all-gather and
@@ -1008,6 +1064,11 @@ def main():
         gemm = make_gemm()
         extra["gemm_alone"] = dict(ms=round(gemm[3] * 1e3, 4), tflops=round(2 * 8192 ** 3 / gemm[3] / 1e12, 1))
         extra["reduce_scatter_workgroups"] = bench_rs_workgroups(hc, rs["x"], 3, gemm)
+        log("reduce-scatter on reserved CUs")
+        try:
+            extra["reduce_scatter_reserved_cus"] = bench_cu_partition(hc, rs["x"], gemm)
+        except Exception as e:
+            extra["reduce_scatter_reserved_cus"] = {"error": repr(e)}
         for name, fn in [("allreduce_fp32_R4", bench_allreduce), ("allgather_fsdp", bench_allgather),
                          ("p2p_pp", bench_p2p), ("alltoallv_ep", bench_a2a)]:
             log(name)
