@@ -146,6 +146,20 @@ int main(void) {
         for (size_t i = 0; i < N; ++i) CHECK(g[i] == (int32_t)((d - 1) * 1000003 + i), "send/recv %d", d);
     }
 
+    /* one ring hop, int32 (wrapping): out[i] = a[i] + b[i] mod 2^32, written
+     * in place over a */
+    for (size_t i = 0; i < N; ++i) h[i] = (int32_t)(0x7ffffff0u + (uint32_t)i);
+    HIP_OK(hipMemcpy(send[0], h, sizeof(int32_t) * N, hipMemcpyHostToDevice));
+    for (size_t i = 0; i < N; ++i) h[i] = (int32_t)(3u * (uint32_t)i + 1u);
+    HIP_OK(hipMemcpy(send[1], h, sizeof(int32_t) * N, hipMemcpyHostToDevice));
+    HOCCL_OK_(hoccl_ring_hop(send[0], send[1], send[0], N, HOCCL_INT32, HOCCL_HOP_MIDDLE, s));
+    HIP_OK(hipStreamSynchronize(s));
+    HIP_OK(hipMemcpy(g, send[0], sizeof(int32_t) * N, hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < N; ++i)
+        CHECK(g[i] == (int32_t)(0x7ffffff0u + (uint32_t)i + 3u * (uint32_t)i + 1u), "ring hop %zu", i);
+    CHECK(hoccl_ring_hop(send[0], send[1], send[0], N, HOCCL_INT32, (hoccl_hop_t)7, s) ==
+              HOCCL_ERR_INVALID_ARG, "unknown hop accepted");
+
     /* documented argument errors enqueue nothing and say why */
     CHECK(hoccl_allreduce((const void *const *)send, (void *const *)recv, N, HOCCL_INT32, 0, s) ==
               HOCCL_ERR_INVALID_ARG, "R = 0 accepted");

@@ -1,7 +1,7 @@
 """The C ABI from plain C: tests/native/c_abi_check (built by build()) links
 libhoccl.so, allocates with hipMalloc and runs every collective without
-Python or torch in the process, checking closed forms and the argument
-errors."""
+Python or torch in the process, checking closed forms (also for one ring
+hop) and the argument errors."""
 import os
 import subprocess
 
