@@ -566,13 +566,25 @@ def bench_a2a(hc, W, reps, gemm):
                 bytes_sent_total=sent, **res)
 
 
-def bench_p2p_sizes(hc, reps):
+def bench_p2p_sizes(hc, reps, bufs=None):
     """One message 0 -> 1 over the paper's microbenchmark range: the engine
     proxy and the HIP runtime's copies against the CU copy kernel at 1 ... 256
-    workgroups (the analog of NCCL's 1/2/4/8-SM budgets)."""
+    workgroups (the analog of NCCL's 1/2/4/8-SM budgets).  `bufs`: two 1 GiB
+    bf16 device buffers to copy between (allocated here if not given)."""
     import torch
-    big = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda")
-    big2 = torch.empty_like(big)
+    if bufs is None:
+        bufs = [torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    big, big2 = bufs
+    # The first pass over the sizes sometimes caught the engine copies of
+    # 32-48 MiB at less than half their rate for some milliseconds (a
+    # transient of the engines themselves: the handshake kernel saw it too);
+    # a second pass never did.  The loop runs twice and the second is kept.
+    for _ in range(2):
+        rows = _p2p_size_rows(hc, reps, big, big2)
+    return dict(workload="single bf16 message rank 0 -> 1, algbw GB/s", rows=rows)
+
+
+def _p2p_size_rows(hc, reps, big, big2):
     rows = []
     # 50,331,648 B: one all-gather hop, a 25,165,824-element bf16 shard.
     for sz in [2 << 20, 32 << 20, 50_331_648, 512 << 20]:
@@ -580,14 +592,15 @@ def bench_p2p_sizes(hc, reps):
         s0, d1 = big[:ne], big2[:ne]
         row = {"bytes": sz}
         for name, kw in [("hip", dict(copy_path="hip")), ("engines", dict(copy_path="engines")),
+                         ("engines_kernel_handshake", dict(copy_path="engines", proxy_handshake=0)),
                          ("engines_striped", dict(copy_path="engines", chunk_bytes=max(1 << 20, sz // 16)))] + \
                         [(f"kernel_wg{w}", dict(copy_path="kernel", workgroups_per_step=w)) for w in (1, 2, 4, 8, 64, 256)]:
             hc.set_config(**kw)
             med, _ = event_time(lambda: hc.sendrecv([s0, s0], [d1, d1], [1, -1]), reps)
             row[name] = round(sz / med / 1e9, 1)
-            hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0)
+            hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0, proxy_handshake=-1)
         rows.append(row)
-    return dict(workload="single bf16 message rank 0 -> 1, algbw GB/s", rows=rows)
+    return rows
 
 
 def bench_ring_hop(hc, x, reps):
@@ -1097,7 +1110,7 @@ def main():
         except Exception as e:
             extra["ring_hop_one_rank"] = {"error": repr(e)}
         log("p2p sizes")
-        extra["p2p_single_message"] = bench_p2p_sizes(hc, 5)
+        extra["p2p_single_message"] = bench_p2p_sizes(hc, 11)
         extra["small_message_latency"] = bench_small_message(hc, 30)
 
     ceiling = round(copy_ceiling(hc), 1)

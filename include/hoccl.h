@@ -123,11 +123,11 @@ typedef enum {
                                     explicitly chosen SDMA engine (ROCr,
                                     hsa_amd_memory_async_copy_on_engine) and
                                     releases the stream by flag handshake
-                                    (proxy_handshake); with chunk_bytes 0 it
-                                    cuts copies into about total/engines
-                                    pieces when there are fewer chains than
-                                    engines.  Its copies finish while every
-                                    CU is busy                                */
+                                    (proxy_handshake); with chunk_bytes 0 and
+                                    fewer chains than engines it cuts every
+                                    copy into engines/chains equal pieces of
+                                    at least 512 KiB.  Its copies finish
+                                    while every CU is busy                    */
     HOCCL_COPY_KERNEL = 3        /* CU copy kernel with workgroups_per_step
                                     workgroups (comparator / fallback)         */
 } hoccl_copy_path_t;

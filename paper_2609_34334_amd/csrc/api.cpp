@@ -549,18 +549,27 @@ hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg,
 }
 
 // On the engine proxy with no chunk size configured: when there are fewer
-// independent chains than engines, cut the copies into pieces of about
-// total / engines bytes (at least 4 MiB) so that every engine works, the
-// paper's striping of one flow over several queues.
+// independent chains than engines, cut every copy into k = engines / chains
+// equal pieces, each a chain of its own, so that every engine works: the
+// paper's striping of one flow over several queues.  Pieces stay at least
+// 512 KiB (an engine copy starts in about 7 us and then moves about
+// 60 GB/s).  Measured on one message with the default handshake: 8 MiB in
+// 82 us as 16 pieces against 122 us as 2 pieces of 4 MiB; 48 MiB in 132 us
+// as 16 pieces against 154 us as 12 pieces of 4 MiB.
+constexpr size_t kMinPieceBytes = (size_t)512 << 10;
+
 size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, hoccl_copy_path_t path,
                         const Plan &p) {
     if (path != HOCCL_COPY_SDMA_ENGINES || cfg.chunk_bytes != 0 || !st.proxy) return 0;
     int E = st.proxy->engine_count();
     if (cfg.sdma_engines > 0) E = std::min(E, cfg.sdma_engines);
-    if (p.nchains >= E) return 0;
-    size_t c = (size_t)(p.copy_bytes / (unsigned long long)E);
-    c = std::max(c, (size_t)4 << 20);
-    return (c + 4095) & ~(size_t)4095;
+    if (p.nchains <= 0 || p.nchains >= E) return 0;
+    size_t big = 0;
+    for (const CopyOp &c : p.copies) big = std::max(big, c.bytes);
+    const size_t k = (size_t)(E / p.nchains);
+    size_t c = std::max((big + k - 1) / k, kMinPieceBytes);
+    c = (c + 4095) & ~(size_t)4095;
+    return c < big ? c : 0;
 }
 
 template <typename Build>
