@@ -1,8 +1,8 @@
 """Large copies on the engine proxy, bit for bit against the definitions
 the oracle implements (all-gather: the shards concatenated in rank order;
 all-to-all: block d of rank s lands at block s of rank d): chains of
-dependent 50.3 MB copies, one copy of 16 MiB plus a ragged tail, and 64 MiB
-blocks lying a power of two apart."""
+dependent 50.3 MB copies, one copy of 16 MiB plus a ragged tail, and an
+all-to-all of 64 MiB blocks."""
 import pytest
 import torch
 
@@ -58,9 +58,9 @@ def test_large_ragged_copy(extra):
 
 
 def test_alltoall_of_power_of_two_blocks():
-    """All-to-all over R = 8 with 64 MiB blocks lying a power of two apart
-    (the layout on which the engines run slowest): every block must land
-    where the definition puts it."""
+    """All-to-all over R = 8 with 64 MiB blocks (the layout of the size
+    sweep's 512 MiB point): every block must land where the definition puts
+    it."""
     hc.set_config(copy_path="engines")
     R, blk = 8, 32 << 20                     # bf16 elements: 64 MiB blocks
     send = [torch.empty(R * blk, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
