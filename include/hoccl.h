@@ -155,7 +155,10 @@ typedef struct {
                                    matrix; 0: ring forwarding r -> r+1         */
     int allreduce_chunk_groups; /* split each all-reduce ring chunk into this
                                    many groups so the gather of group g
-                                   overlaps the reduction of group g+1; 0 = 1  */
+                                   overlaps the reduction of group g+1 (on
+                                   SDMA_ENGINES the proxy issues group g's
+                                   copies once an event the stream records
+                                   after its reduction has completed); 0 = 1 */
     hoccl_reduce_algo_t reduce_algo;
     int kernel_timing;          /* 1: record HIP events around every reduce /
                                    copy kernel launch (hoccl_get_kernel_times) */

@@ -367,9 +367,11 @@ hoccl_status_t timed_end(TimingPair *tp, hipStream_t s) {
     return HOCCL_OK;
 }
 
+// With record_groups, an event is recorded on s after each group's last
+// reduction step: gates[g] when given, else the library's ev_group[g].
 hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
                               const Buffers &B, hipStream_t s, int wg, int threads,
-                              bool record_groups) {
+                              bool record_groups, const std::vector<hipEvent_t> *gates = nullptr) {
     for (size_t i = 0; i < p.reduce_steps.size(); ++i) {
         const ReduceStep &step = p.reduce_steps[i];
         for (size_t b = 0; b < step.segs.size(); b += kMaxReduceSegs) {
@@ -392,7 +394,9 @@ hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const 
         }
         bool last_of_group = (i + 1 == p.reduce_steps.size()) ||
                              p.reduce_steps[i + 1].group != step.group;
-        if (record_groups && last_of_group) {
+        if (record_groups && last_of_group && gates) {
+            HIP_TRY(hipEventRecord((*gates)[(size_t)step.group], s));
+        } else if (record_groups && last_of_group) {
             while ((int)st.ev_group.size() <= step.group) {
                 hipEvent_t ev;
                 HIP_TRY(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
@@ -478,6 +482,40 @@ hoccl_status_t run_copies_hip(DeviceState &st, const hoccl_config_t &cfg, const 
         HIP_TRY(hipStreamWaitEvent(s, ev, 0));
     }
     return HOCCL_OK;
+}
+
+// All-reduce in chunk groups on the engine proxy.  After each group's last
+// reduction step the caller's stream records one of the proxy's gate
+// events; the proxy thread polls them and issues group g's gather copies as
+// soon as its gate has completed, so the engines copy group g while the CUs
+// reduce group g + 1 (the paper's per-chunk buffer states, reduced to
+// "final ready").  One handshake at the end of the call releases the stream
+// once every copy has completed.  A handshake per group, each on a stream
+// of its own, was measured slower: every host-function handshake waits for
+// the runtime's callback thread, and with 8 groups that cost more than the
+// overlap gained.
+hoccl_status_t run_engine_groups(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
+                                 const Buffers &B, hipStream_t s, int wg, int threads, int handshake) {
+    std::vector<hipEvent_t> gates;
+    hoccl_status_t r = st.proxy->acquire_events(p.ngroups, gates, t_err);
+    if (r != HOCCL_OK) return r;
+    r = run_reductions(st, cfg, p, B, s, wg, threads, true, &gates);
+    if (r != HOCCL_OK) {
+        st.proxy->release_events(gates);
+        return r;
+    }
+    std::vector<ProxyCopy> cps;
+    cps.reserve(p.copies.size());
+    for (const CopyOp &c : p.copies) {
+        ProxyCopy pc{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain};
+        pc.gate = c.group;
+        cps.push_back(pc);
+    }
+    int ne = 0;
+    r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, handshake,
+                         s, &ne, t_err, std::move(gates));
+    if (r == HOCCL_OK) t_stats.copy_ops += (int)cps.size();
+    return r;
 }
 
 hoccl_status_t run_copies_kernel(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
@@ -634,7 +672,10 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
             HIP_TRY(hipStreamWaitEvent(s, st.ws_event, 0));
     }
 
-    if (has_copies && path == HOCCL_COPY_SDMA_ENGINES) {
+    if (has_copies && path == HOCCL_COPY_SDMA_ENGINES && !capturing && p.ngroups > 1 &&
+        !p.reduce_steps.empty()) {
+        TRY(run_engine_groups(st, cfg, p, B, s, wg, threads, handshake));
+    } else if (has_copies && path == HOCCL_COPY_SDMA_ENGINES) {
         // Reductions first (on s), then the proxy takes over the copies.
         TRY(run_reductions(st, cfg, p, B, s, wg, threads, false));
         std::vector<ProxyCopy> cps;

@@ -28,6 +28,13 @@
 //                may need the same thread to complete copies, so the library
 //                refuses this form while a profiler is loaded.
 // Every form gives up after a bounded time, so the stream always drains.
+//
+// Copy gates: an operation's copies may also be tied to events the caller
+// records on its stream before the handshake (an all-reduce's gather of
+// chunk group g behind group g's reduction).  The proxy thread polls those
+// events and issues each gate's copies as soon as it completes, before the
+// stream reaches the handshake; the handshake still releases the stream
+// only once every copy of the operation has completed.
 #include "proxy.h"
 #include "hoccl_internal.h"
 #include "schedule.h"
@@ -137,14 +144,18 @@ inline void store_flag(volatile uint32_t *p, uint32_t v) {
 }  // namespace
 
 struct ProxyOp {
-    enum State { WAIT_START, COPYING, WAIT_ACK };
+    enum State { ACTIVE, WAIT_ACK };
     int slot = -1;
-    std::vector<ProxyCopy> copies;
-    std::vector<uint32_t> engine;  // engine id bit per copy
-    std::vector<int> dep;          // previous copy of the same chain, or -1
+    std::vector<ProxyCopy> copies;  // in issue order: the gates' blocks, then the ungated
+    std::vector<uint32_t> engine;   // engine id bit per copy
+    std::vector<int> dep;           // previous copy of the same chain, or -1
     std::vector<hsa_signal_t> sig;
-    State state = WAIT_START;
-    std::chrono::steady_clock::time_point since;
+    std::vector<hipEvent_t> gates;  // copy gates (taken from the pool)
+    std::vector<char> gate_open;
+    size_t next = 0;                // copies issued so far
+    bool start_seen = false;        // the stream reached the handshake
+    State state = ACTIVE;
+    std::chrono::steady_clock::time_point since;  // last issue
     unsigned timeout_ms = 10000;
     bool timed_out = false;
 };
@@ -164,6 +175,7 @@ class ProxyImpl {
     std::deque<ProxyOp *> incoming;
     std::vector<int> free_slots;
     std::vector<hsa_signal_t> free_signals;
+    std::vector<hipEvent_t> free_events;  // pool for copy gates
     bool stop = false;
     std::thread th;
     hoccl_status_t sticky = HOCCL_OK;
@@ -185,28 +197,38 @@ class ProxyImpl {
         }
     }
 
-    bool issue(ProxyOp &op) {
-        for (size_t i = 0; i < op.copies.size(); ++i) {
-            const ProxyCopy &c = op.copies[i];
-            hsa_signal_store_screlease(op.sig[i], 1);
-            const hsa_signal_t *deps = nullptr;
-            uint32_t ndep = 0;
-            if (op.dep[i] >= 0) {
-                deps = &op.sig[(size_t)op.dep[i]];
-                ndep = 1;
-            }
-            hsa_status_t e = hsa_amd_memory_async_copy_on_engine(
-                c.dst, agent, c.src, agent, c.bytes, ndep, deps, op.sig[i],
-                (hsa_amd_sdma_engine_id_t)op.engine[i], true);
-            if (e != HSA_STATUS_SUCCESS) {
-                char buf[160];
-                std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
-                fail(HOCCL_ERR_HIP, buf);
-                // Retire the copies that were never issued so the op completes.
-                for (size_t k = i; k < op.copies.size(); ++k) hsa_signal_store_screlease(op.sig[k], 0);
-                return false;
-            }
+    // Issues copy op.next (its signal was armed at submission, so a later
+    // copy of the same chain waits for it even if issued first).
+    void issue_next(ProxyOp &op) {
+        const size_t i = op.next++;
+        const ProxyCopy &c = op.copies[i];
+        const hsa_signal_t *deps = nullptr;
+        uint32_t ndep = 0;
+        if (op.dep[i] >= 0) {
+            deps = &op.sig[(size_t)op.dep[i]];
+            ndep = 1;
         }
+        hsa_status_t e = hsa_amd_memory_async_copy_on_engine(
+            c.dst, agent, c.src, agent, c.bytes, ndep, deps, op.sig[i],
+            (hsa_amd_sdma_engine_id_t)op.engine[i], true);
+        if (e != HSA_STATUS_SUCCESS) {
+            char buf[160];
+            std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
+            fail(HOCCL_ERR_HIP, buf);
+            // Retire the copies that were never issued so the op completes.
+            for (size_t k = i; k < op.copies.size(); ++k) hsa_signal_store_screlease(op.sig[k], 0);
+            op.next = op.copies.size();
+        }
+    }
+
+    // Whether the copies behind gate g may go: its event has completed (a
+    // failed query opens it and is reported, so the operation still ends).
+    bool gate_open(ProxyOp &op, int g) {
+        if (op.gate_open[(size_t)g]) return true;
+        hipError_t e = hipEventQuery(op.gates[(size_t)g]);
+        if (e == hipErrorNotReady) return false;
+        if (e != hipSuccess) fail(HOCCL_ERR_HIP, "hipEventQuery on a copy gate failed");
+        op.gate_open[(size_t)g] = 1;
         return true;
     }
 
@@ -219,6 +241,7 @@ class ProxyImpl {
     void release(ProxyOp *op) {
         std::lock_guard<std::mutex> lk(mu);
         for (auto &s : op->sig) free_signals.push_back(s);
+        for (auto &e : op->gates) free_events.push_back(e);
         free_slots.push_back(op->slot);
         cv_slot.notify_all();
         delete op;
@@ -249,16 +272,23 @@ class ProxyImpl {
                 ProxyOp *op = active[i];
                 bool retired = false;
                 switch (op->state) {
-                case ProxyOp::WAIT_START:
-                    // The stream has drained everything before the collective.
-                    if (started(*op)) {
-                        issue(*op);
-                        op->state = ProxyOp::COPYING;
+                case ProxyOp::ACTIVE:
+                    // The stream reached the handshake: everything before it,
+                    // including every gate, has completed.
+                    if (!op->start_seen && started(*op)) {
+                        op->start_seen = true;
+                        progress = true;
+                    }
+                    // Issue in order what may go: a gated copy once its gate
+                    // is open, an ungated one once the stream has started.
+                    while (op->next < op->copies.size()) {
+                        const int g = op->copies[op->next].gate;
+                        if (g < 0 ? !op->start_seen : !gate_open(*op, g)) break;
+                        issue_next(*op);
                         op->since = now;
                         progress = true;
                     }
-                    break;
-                case ProxyOp::COPYING:
+                    if (op->next < op->copies.size() || !op->start_seen) break;
                     if (copies_done(*op)) {
                         progress = true;
                         store_flag(finish_flag(op->slot), kFinishValue);
@@ -444,6 +474,7 @@ Proxy::~Proxy() {
         delete op;
     }
     for (auto &s : impl_->free_signals) hsa_signal_destroy(s);
+    for (auto &e : impl_->free_events) (void)hipEventDestroy(e);
     if (impl_->flags) (void)hipHostFree(impl_->flags);
     if (impl_->hs) (void)hipStreamDestroy(impl_->hs);
     if (impl_->ev_fork) (void)hipEventDestroy(impl_->ev_fork);
@@ -577,9 +608,39 @@ EngineSchedule schedule_copies(const ProxyImpl &P, const std::vector<ProxyCopy> 
     return out;
 }
 
+hoccl_status_t Proxy::acquire_events(int n, std::vector<hipEvent_t> &out, std::string &err) {
+    ProxyImpl &P = *impl_;
+    out.clear();
+    {
+        std::lock_guard<std::mutex> lk(P.mu);
+        while ((int)out.size() < n && !P.free_events.empty()) {
+            out.push_back(P.free_events.back());
+            P.free_events.pop_back();
+        }
+    }
+    while ((int)out.size() < n) {
+        hipEvent_t e = nullptr;
+        hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (he != hipSuccess) {
+            err = std::string("hipEventCreateWithFlags: ") + hipGetErrorString(he);
+            release_events(out);
+            return HOCCL_ERR_HIP;
+        }
+        out.push_back(e);
+    }
+    return HOCCL_OK;
+}
+
+void Proxy::release_events(std::vector<hipEvent_t> &events) {
+    std::lock_guard<std::mutex> lk(impl_->mu);
+    for (hipEvent_t e : events) impl_->free_events.push_back(e);
+    events.clear();
+}
+
 hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
                              unsigned timeout_ms, unsigned wait_limit_us, int handshake,
-                             hipStream_t s, int *engines_used, std::string &err) {
+                             hipStream_t s, int *engines_used, std::string &err,
+                             std::vector<hipEvent_t> gates) {
     ProxyImpl &P = *impl_;
     {
         std::lock_guard<std::mutex> lk(P.mu);
@@ -588,30 +649,56 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
             err = P.sticky_msg;
             P.sticky = HOCCL_OK;
             P.sticky_msg.clear();
+            for (hipEvent_t e : gates) P.free_events.push_back(e);  // the lock is held
             return st;
         }
     }
+    for (const ProxyCopy &c : copies)
+        if (c.gate >= (int)gates.size()) {
+            err = "a copy names a gate that was not given";
+            release_events(gates);
+            return HOCCL_ERR_INTERNAL;
+        }
     ProxyOp *op = new ProxyOp();
     op->timeout_ms = timeout_ms ? timeout_ms : 10000;
     {
-        EngineSchedule sch = schedule_copies(P, copies, max_engines);
-        op->copies = std::move(sch.copies);
-        op->engine = std::move(sch.engine);
-        op->dep = std::move(sch.dep);
-        if (engines_used) *engines_used = sch.engines_used;
+        // Each gate's copies are scheduled as a block of their own, the
+        // gates in order and the ungated copies last, so a gate's block goes
+        // out as soon as the gate opens.
+        int used = 0;
+        const int ng = (int)gates.size();
+        for (int k = 0; k <= ng; ++k) {
+            const int g = k < ng ? k : -1;
+            std::vector<ProxyCopy> part;
+            for (const ProxyCopy &c : copies)
+                if (c.gate == g) part.push_back(c);
+            if (part.empty()) continue;
+            EngineSchedule sch = schedule_copies(P, part, max_engines);
+            const int base = (int)op->copies.size();
+            for (size_t i = 0; i < sch.copies.size(); ++i) {
+                op->copies.push_back(sch.copies[i]);
+                op->engine.push_back(sch.engine[i]);
+                op->dep.push_back(sch.dep[i] < 0 ? -1 : base + sch.dep[i]);
+            }
+            used = std::max(used, sch.engines_used);
+        }
+        if (engines_used) *engines_used = used;
     }
+    op->gates = std::move(gates);
+    op->gate_open.assign(op->gates.size(), 0);
     // Signals and a flag slot.
     {
         std::unique_lock<std::mutex> lk(P.mu);
         if (!P.cv_slot.wait_for(lk, std::chrono::milliseconds(op->timeout_ms),
                                 [&] { return !P.free_slots.empty(); })) {
+            for (hipEvent_t e : op->gates) P.free_events.push_back(e);
             delete op;
             err = "no free handshake slot within the proxy timeout";
             return HOCCL_ERR_TIMEOUT;
         }
         op->slot = P.free_slots.back();
         P.free_slots.pop_back();
-        while (op->sig.size() < copies.size() && !P.free_signals.empty()) {
+        while (op->sig.size() < op->copies.size() && !P.free_signals.empty()) {
             op->sig.push_back(P.free_signals.back());
             P.free_signals.pop_back();
         }
@@ -619,10 +706,11 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     auto give_back = [&]() {
         std::lock_guard<std::mutex> lk(P.mu);
         for (auto &x : op->sig) P.free_signals.push_back(x);
+        for (hipEvent_t e : op->gates) P.free_events.push_back(e);
         P.free_slots.push_back(op->slot);
         delete op;
     };
-    while (op->sig.size() < copies.size()) {
+    while (op->sig.size() < op->copies.size()) {
         hsa_signal_t sg;
         if (hsa_signal_create(1, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) {
             err = "hsa_signal_create failed";
@@ -631,6 +719,10 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         }
         op->sig.push_back(sg);
     }
+    // Every copy's signal is armed before any is issued: a copy waits on its
+    // chain predecessor's signal, which must read "pending" until that copy
+    // has been issued and has completed.
+    for (auto &sg : op->sig) hsa_signal_store_screlease(sg, 1);
     // The handshake kernel runs on the caller's stream, or on the private
     // CU-masked stream when asked for (and that stream exists).
     hipStream_t hs = s;

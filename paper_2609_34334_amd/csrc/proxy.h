@@ -16,7 +16,8 @@ struct ProxyCopy {
     void *dst;
     const void *src;
     size_t bytes;
-    int chain;  // copies of one chain run in order; chains are independent
+    int chain;      // copies of one chain run in order; chains are independent
+    int gate = -1;  // index into submit's `gates`, or -1: wait for the stream
 };
 
 class ProxyImpl;
@@ -30,9 +31,20 @@ class Proxy {
 
     int engine_count() const;
 
+    // Events for submit's `gates`, taken from the proxy's pool.  They return
+    // to it when the operation that uses them retires, or by
+    // release_events if the caller does not submit after all.
+    hoccl_status_t acquire_events(int n, std::vector<hipEvent_t> &out, std::string &err);
+    void release_events(std::vector<hipEvent_t> &events);
+
     // Enqueues the handshake on `s` and hands the copies to the proxy
     // thread; returns once enqueued.  Copies run on at most `max_engines`
-    // engines (0 = all), balanced by bytes per engine.
+    // engines (0 = all), balanced by bytes per engine.  A copy with gate
+    // g >= 0 is issued as soon as gates[g] (recorded by the caller on `s`
+    // before the handshake) has completed, which the proxy thread polls;
+    // the others when the stream reaches the handshake.  The handshake
+    // releases the stream once every copy has completed.  The operation
+    // takes the gate events over, also when it fails.
     // The stream side of the start/finish flag handshake (`handshake`, as
     // hoccl_config_t.proxy_handshake): 0, a one-lane kernel on `s`; 1, that
     // kernel on the proxy's private CU-masked stream joined to `s` by
@@ -41,7 +53,8 @@ class Proxy {
     // plus a second).
     hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
                           unsigned timeout_ms, unsigned wait_limit_us, int handshake,
-                          hipStream_t s, int *engines_used, std::string &err);
+                          hipStream_t s, int *engines_used, std::string &err,
+                          std::vector<hipEvent_t> gates = {});
 
     // For a stream that is capturing a graph: records a host node on `s`
     // that, at every replay, issues the copies on their engines and returns

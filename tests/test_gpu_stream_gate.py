@@ -146,6 +146,26 @@ def test_reductions_wait_for_the_gate(algo):
         assert_bitwise(from_dev(outa[r], hc.FP32), refa[r], f"{algo} all-reduce rank {r}")
 
 
+@pytest.mark.parametrize("handshake", [-1, 0])
+def test_grouped_allreduce_on_the_engines_waits_for_the_gate(handshake):
+    """All-reduce in 4 chunk groups on the engine proxy: each group's gather
+    copies run on a library stream that waits for that group's reductions,
+    and the caller's stream joins those streams.  Behind a closed gate none
+    of it may run, and once the gate opens the result is the oracle's."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    hc.set_config(copy_path="engines", allreduce_chunk_groups=4, proxy_handshake=handshake)
+    R, n = 8, 1_000_003
+    x = [W.random_values("bf16", 408, r, n) for r in range(R)]
+    ref = oracle.allreduce_new(x, hc.BF16)
+    send = [to_dev(a, hc.BF16) for a in x]
+    outs = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    gated(lambda s: hc.allreduce(send, outs, stream=s), outs, hc.BF16)
+    assert hc.last_stats()["copy_ops"] > 0
+    for r in range(R):
+        assert_bitwise(from_dev(outs[r], hc.BF16), ref[r], f"grouped all-reduce rank {r}")
+
+
 def test_debug_log_names_the_plan(tmp_path):
     """HOCCL_DEBUG=1 logs each executed plan (checked in a child process)."""
     import subprocess
