@@ -158,7 +158,11 @@ typedef struct {
                                    overlaps the reduction of group g+1 (on
                                    SDMA_ENGINES the proxy issues group g's
                                    copies once an event the stream records
-                                   after its reduction has completed); 0 = 1 */
+                                   after its reduction has completed);
+                                   0 = automatic: 2 on SDMA_ENGINES outside
+                                   graph capture when each rank holds at
+                                   least 32 MiB, else 1 (plan dumps assume
+                                   SDMA_ENGINES)                               */
     hoccl_reduce_algo_t reduce_algo;
     int kernel_timing;          /* 1: record HIP events around every reduce /
                                    copy kernel launch (hoccl_get_kernel_times) */

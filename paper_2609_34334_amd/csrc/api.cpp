@@ -104,7 +104,7 @@ hoccl_config_t default_config() {
     c.sdma_engines = 0;
     c.copy_path = HOCCL_COPY_AUTO;
     c.allgather_direct = 1;
-    c.allreduce_chunk_groups = 1;
+    c.allreduce_chunk_groups = 0;
     c.reduce_algo = HOCCL_REDUCE_RING;
     c.kernel_timing = 0;
     c.proxy_timeout_ms = 10000;
@@ -627,6 +627,10 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     PlanOptions opt = options_from(cfg, in_place);
     const hoccl_copy_path_t path = resolve_path(st, cfg, capturing);
     const int handshake = resolve_handshake(cfg);
+    // Automatic all-reduce groups pay off only where the gather runs on the
+    // engines beside the reduction: on the engine proxy outside capture.
+    if (opt.allreduce_groups == 0 && (path != HOCCL_COPY_SDMA_ENGINES || capturing))
+        opt.allreduce_groups = 1;
     Plan p = build(opt);
     if (size_t c = auto_chunk_bytes(st, cfg, path, p)) {
         opt.chunk_bytes = c;
@@ -803,7 +807,7 @@ PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
     PlanOptions o;
     o.group_partial_bytes = cfg.ring_group_bytes ? cfg.ring_group_bytes : kRingGroupBytesDefault;
     o.allgather_direct = cfg.allgather_direct != 0;
-    o.allreduce_groups = cfg.allreduce_chunk_groups > 0 ? cfg.allreduce_chunk_groups : 1;
+    o.allreduce_groups = cfg.allreduce_chunk_groups;  // 0: automatic
     o.chunk_bytes = cfg.chunk_bytes;
     o.in_place = in_place;
     o.algo = cfg.reduce_algo;

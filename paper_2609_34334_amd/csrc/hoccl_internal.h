@@ -97,7 +97,7 @@ struct Plan {
 
 struct PlanOptions {
     bool allgather_direct = false;
-    int allreduce_groups = 1;
+    int allreduce_groups = 1;  // 0: automatic (plan_allreduce)
     size_t chunk_bytes = 0;
     bool in_place = false;
     hoccl_reduce_algo_t algo = HOCCL_REDUCE_RING;
