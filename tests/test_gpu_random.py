@@ -30,7 +30,7 @@ def draw(i):
                  workgroups_per_step=int(g.choice([0, 0, 1, 7, 300])),
                  threads_per_workgroup=int(g.choice([64, 256, 256, 1024])),
                  ring_group_bytes=int(g.choice([0, 0, 4096])),
-                 allreduce_chunk_groups=int(g.choice([1, 1, 3])),
+                 allreduce_chunk_groups=int(g.choice([0, 1, 3])),
                  allgather_direct=int(g.choice([0, 1])),
                  chunk_bytes=int(g.choice([0, 0, 8192]))),
         seed=int(g.integers(0, 1 << 30)))

@@ -221,3 +221,18 @@ def test_cache_groups_bound_partials_and_keep_bytes():
     with hc.config(ring_group_bytes=16 << 20):
         ar = hc.plan_json(hc.OP_ALLREDUCE, R * n, hc.BF16, R)
     assert ar["ngroups"] == 6
+
+
+def test_automatic_allreduce_groups():
+    """allreduce_chunk_groups 0 (the default) plans two groups once each
+    rank holds at least 32 MiB and one below (plan dumps assume the engine
+    path); an explicit count wins."""
+    assert hc.get_config()["allreduce_chunk_groups"] == 0
+    R = 8
+    below = hc.plan_json(hc.OP_ALLREDUCE, (16 << 20) // 2, hc.BF16, R)
+    at = hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)
+    assert below["ngroups"] == 1 and at["ngroups"] == 2
+    assert [s["group"] for s in at["reduce_steps"]] == [g for g in range(2) for _ in range(R - 1)]
+    assert {c["group"] for c in at["copies"]} == {0, 1}
+    with hc.config(allreduce_chunk_groups=1):
+        assert hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)["ngroups"] == 1
