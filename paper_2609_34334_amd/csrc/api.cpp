@@ -687,11 +687,34 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
         for (const CopyOp &c : p.copies)
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
         int ne = 0;
-        hoccl_status_t r =
-            capturing ? st.proxy->capture(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                          cfg.proxy_wait_limit_us, s, &ne, t_err)
-                      : st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms,
-                                         cfg.proxy_wait_limit_us, handshake, s, &ne, t_err);
+        hoccl_status_t r;
+        if (capturing) {
+            r = st.proxy->capture(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, s,
+                                  &ne, t_err);
+        } else if (handshake == 2 && p.copy_bytes >= ((unsigned long long)1 << 20)) {
+            // The copies may start as soon as everything before them on s
+            // has completed: an event recorded here is their gate, which the
+            // proxy thread polls, so the start of the host-function
+            // handshake (the runtime's callback thread) overlaps the copies
+            // instead of preceding them.  Measured: the pipeline schedule of
+            // 16 MiB messages 6.8 ms against 7.8 ms.  Copies under 1 MiB end
+            // within the callback's start-up time anyway, and the handshake
+            // kernel starts within microseconds, so those go without a gate.
+            std::vector<hipEvent_t> gate;
+            TRY(st.proxy->acquire_events(1, gate, t_err));
+            hipError_t e = hipEventRecord(gate[0], s);
+            if (e != hipSuccess) {
+                st.proxy->release_events(gate);
+                set_err("hipEventRecord: %s", hipGetErrorString(e));
+                return HOCCL_ERR_HIP;
+            }
+            for (ProxyCopy &c : cps) c.gate = 0;
+            r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
+                                 handshake, s, &ne, t_err, std::move(gate));
+        } else {
+            r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
+                                 handshake, s, &ne, t_err);
+        }
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();
     } else {
