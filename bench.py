@@ -961,6 +961,25 @@ def copy_workload(hc, W):
                       "allgather_bytes": sum(t.numel() * 2 for t in ag_out)}))
 
 
+def ar_groups_workload(hc, W):
+    """What the all-reduce overlap trace profiles: the bf16 R=8 bucket
+    all-reduce (25,165,824 elements per rank) in 2 chunk groups on the
+    engine proxy, three calls after one warm-up.  The trace shows group 1's
+    ring-step launches running while the engines copy group 0."""
+    import torch
+    R, n = 8, 25_165_824
+    send = [bf16_dev(a) for a in W.rs_gradients(R, n)]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    hc.set_config(copy_path="engines", allreduce_chunk_groups=2)
+    hc.allreduce(send, recv)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        hc.allreduce(send, recv)
+    torch.cuda.synchronize()
+    print(json.dumps({"ar_groups_workload": "done", "copy_ops": hc.last_stats()["copy_ops"],
+                      "reduce_launches": hc.last_stats()["reduce_launches"]}))
+
+
 def pmc_workload(hc, W):
     """What the counter runs profile: a 1 GiB CU copy of known size (to
     scale FETCH_SIZE / WRITE_SIZE), then five headline reduce-scatters on
@@ -1023,6 +1042,8 @@ def main():
                     help="run only the workload the occupancy counter pass is taken on")
     ap.add_argument("--sweep", action="store_true",
                     help="print algbw against message size per copy path instead")
+    ap.add_argument("--ar-groups-workload", action="store_true",
+                    help="run only the grouped all-reduce the overlap trace profiles")
     ap.add_argument("--copy-workload", action="store_true",
                     help="run only the copy collectives the zero-CU trace is taken on")
     args = ap.parse_args()
@@ -1045,6 +1066,9 @@ def main():
         return
     if args.occupancy_workload:
         occupancy_workload(hc, W)
+        return
+    if args.ar_groups_workload:
+        ar_groups_workload(hc, W)
         return
     if args.copy_workload:
         copy_workload(hc, W)
