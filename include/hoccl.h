@@ -261,7 +261,8 @@ hoccl_status_t hoccl_get_config(hoccl_config_t *cfg);
 hoccl_status_t hoccl_get_last_stats(hoccl_stats_t *stats);
 
 /* With kernel_timing on, every kernel launch of every collective call is
- * bracketed by a pair of timing events on the stream it is launched on.
+ * bracketed by a pair of timing events on the stream it is launched on (at
+ * most 65536 launches between two reads; later ones go untimed).
  * This returns the durations in milliseconds of all launches recorded since
  * the previous read, in launch order, waits for those launches to finish and
  * clears the record.  *n receives the number of launches; at most `cap`

@@ -347,10 +347,15 @@ int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan
     return workgroups_for(st, cfg, passes, threads);
 }
 
+// Launches timed between two reads of hoccl_get_kernel_times; later ones go
+// untimed, so a caller that never reads does not grow the event pool
+// without bound.
+constexpr size_t kMaxTimedLaunches = (size_t)1 << 16;
+
 hoccl_status_t timed_begin(DeviceState &st, const hoccl_config_t &cfg, hipStream_t s,
                            TimingPair **tp) {
     *tp = nullptr;
-    if (!cfg.kernel_timing) return HOCCL_OK;
+    if (!cfg.kernel_timing || st.timing_used >= kMaxTimedLaunches) return HOCCL_OK;
     if (st.timing_used == st.timing_pool.size()) {
         TimingPair p;
         HIP_TRY(hipEventCreate(&p.a));
