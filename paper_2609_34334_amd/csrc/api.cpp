@@ -702,9 +702,10 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
             // proxy thread polls, so the start of the host-function
             // handshake (the runtime's callback thread) overlaps the copies
             // instead of preceding them.  Measured: the pipeline schedule of
-            // 16 MiB messages 6.8 ms against 7.8 ms.  Copies under 1 MiB end
-            // within the callback's start-up time anyway, and the handshake
-            // kernel starts within microseconds, so those go without a gate.
+            // 16 MiB messages 6.8 ms against 7.8 ms.  Copies under 1 MiB go
+            // without a gate: a 4 KiB send/recv gated took the same round
+            // trip (53.6 against 51.6-53.1 us) and 6 us more host time.  So
+            // does the handshake kernel, which starts within microseconds.
             std::vector<hipEvent_t> gate;
             TRY(st.proxy->acquire_events(1, gate, t_err));
             hipError_t e = hipEventRecord(gate[0], s);
