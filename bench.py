@@ -12,9 +12,15 @@ Also printed in the same JSON line:
   * cpu_baseline: the CPU oracle on the same workload, single thread;
   * extra: the other collectives of the hot path on their own workloads
     (all-reduce fp32, FSDP all-gather, PP send/recv, EP all-to-all(v) with a
-    concurrent bf16 GEMM), each with algbw/busbw, %HBM peak and CUs used.
+    concurrent bf16 GEMM), each with algbw/busbw, %HBM peak and CUs used;
+    the direct fold; the reduce-scatter at fixed workgroup budgets and on
+    reserved CUs beside the GEMM; the bucket all-reduce in chunk groups; one
+    rank's ring hop; single messages and small-message round trips.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--quick]
+       python bench.py --sweep            (algbw against message size)
+Profiling workloads (one phase each): --pmc-workload, --occupancy-workload,
+--copy-workload, --ar-groups-workload.
 """
 import argparse
 import json
