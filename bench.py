@@ -446,7 +446,7 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
         r = dict(algbw_GBs=round(S / med / 1e9, 2), busbw_GBs=round(S / med / 1e9 * f, 2),
                  ms=round(med * 1e3, 4), copy_GBs=round(st["copy_bytes"] / med / 1e9, 1),
                  hbm_frac=round(st["hbm_bytes_algorithmic"] / med / 1e9 / HBM_PEAK_GBS, 4),
-                 path_used=["auto", "hip", "engines", "kernel"][st["copy_path_used"]],
+                 path_used=hc.COPY_PATH_NAMES[st["copy_path_used"]],
                  cus_used=st["cus_used_max"], host_enqueue_us=round(st["host_enqueue_us"], 1))
         if gemm is not None:
             (r["gemm_slowdown"], r["gemm_overlap"], r["collective_slowdown"],

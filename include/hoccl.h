@@ -46,9 +46,9 @@
  *   or HSA call returns HOCCL_ERR_HIP; hoccl_last_error_string() describes
  *   it.  Faults of the device work itself surface at the caller's own
  *   synchronisation.  `count == 0` is a successful no-op.  The only error
- *   that outlives its call is the SDMA_ENGINES proxy's watchdog: copies of
+ *   that outlives its call is the SDMA proxy's watchdog: copies of
  *   an earlier call that did not finish within proxy_timeout_ms are reported
- *   once, as HOCCL_ERR_TIMEOUT, by the next SDMA_ENGINES call (which then
+ *   once, as HOCCL_ERR_TIMEOUT, by the next SDMA call (which then
  *   enqueues nothing).
  * Threads.  One host thread at a time may call into the library per device.
  *   Collectives issued on different streams that overlap in time are
@@ -65,7 +65,7 @@
  *   instead.  A call returns HOCCL_ERR_UNSUPPORTED, enqueuing nothing, as
  *   the first call on a device (which creates the library's streams and
  *   probes the engines), when it needs a larger workspace than the library
- *   holds, or when copy_path is SDMA_ENGINES with the handshake kernel
+ *   holds, or when copy_path is SDMA with the handshake kernel
  *   (proxy_handshake 0 or 1).  Make the same call once outside capture
  *   first.  The copy lists of recorded host nodes stay allocated until
  *   hoccl_finalize.  A workspace a graph captured stays
@@ -106,49 +106,55 @@ typedef enum {
 
 typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2 } hoccl_dtype_t;
 
-/* Where pure-copy steps run. */
+/* Where pure-copy steps run.  AUTO, SDMA and KERNEL keep the values 0, 1
+ * and 2; the HIP runtime's own copy is appended as 3. */
 typedef enum {
-    HOCCL_COPY_AUTO = 0,         /* SDMA_ENGINES, the path that keeps copies
-                                    off the compute units; HIP when the
-                                    engines cannot be driven, or while
-                                    capturing under a profiler                */
-    HOCCL_COPY_HIP = 1,          /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
-                                    library's copy streams.  Where the copy
-                                    runs is the HIP runtime's choice: in the
-                                    runtime PyTorch bundles it runs on the
-                                    compute units (it cannot finish while
-                                    every CU is busy), in ROCm 7.2's on one
-                                    SDMA engine.  Graph-capturable            */
-    HOCCL_COPY_SDMA_ENGINES = 2, /* a CPU proxy thread issues each chunk on an
-                                    explicitly chosen SDMA engine (ROCr,
-                                    hsa_amd_memory_async_copy_on_engine) and
-                                    releases the stream by flag handshake
-                                    (proxy_handshake); with chunk_bytes 0 and
-                                    fewer chains than engines it cuts every
-                                    copy into engines/chains equal pieces of
-                                    at least 512 KiB.  Its copies finish
-                                    while every CU is busy                    */
-    HOCCL_COPY_KERNEL = 3        /* CU copy kernel with workgroups_per_step
-                                    workgroups (comparator / fallback)         */
+    HOCCL_COPY_AUTO = 0,   /* SDMA, the path that keeps copies off the compute
+                              units; HIP when the engines cannot be driven,
+                              or while capturing under a profiler           */
+    HOCCL_COPY_SDMA = 1,   /* a CPU proxy thread issues each chunk on an
+                              explicitly chosen SDMA engine (ROCr,
+                              hsa_amd_memory_async_copy_on_engine) and
+                              releases the stream by flag handshake
+                              (proxy_handshake); with chunk_bytes 0 and fewer
+                              chains than engines it cuts every copy into
+                              engines/chains equal pieces of at least
+                              512 KiB.  Its copies finish while every CU is
+                              busy (Zero-SM Point-to-Point Executor)       */
+    HOCCL_COPY_KERNEL = 2, /* CU copy kernel with workgroups_per_step
+                              workgroups (comparator / fallback)           */
+    HOCCL_COPY_HIP = 3     /* hipMemcpyAsync(DeviceToDeviceNoCU) on the
+                              library's copy streams.  Where the copy runs is
+                              the HIP runtime's choice: in the runtime
+                              PyTorch bundles it runs on the compute units
+                              (it cannot finish while every CU is busy), in
+                              ROCm 7.2's on one SDMA engine.
+                              Graph-capturable                             */
 } hoccl_copy_path_t;
 
-/* How reduce-scatter / all-reduce reduce. */
+/* How reduce-scatter / all-reduce reduce.  Every choice folds in the same
+ * order, so the results are identical bit for bit. */
 typedef enum {
-    HOCCL_REDUCE_RING = 0,  /* R-1 ring steps, one kernel launch per step over
-                               all ranks; fp32 partials for bf16               */
-    HOCCL_REDUCE_DIRECT = 1 /* one launch folds all R inputs in the same ring
-                               order (bit-identical result, fewer HBM bytes)   */
+    HOCCL_REDUCE_RING = 0,   /* R-1 ring steps (or fused_hops steps per
+                                launch), one kernel launch per step over all
+                                ranks; fp32 partials for bf16              */
+    HOCCL_REDUCE_DIRECT = 1, /* one launch folds all R inputs in the ring
+                                order (fewer HBM bytes)                    */
+    HOCCL_REDUCE_AUTO = 2    /* DIRECT where the one-GPU fold is faster:
+                                up to direct_max_ranks ranks, whatever the
+                                size; RING otherwise.  The choice made is
+                                reported in hoccl_stats_t.reduce_algo_used */
 } hoccl_reduce_algo_t;
 
+/* The first seven fields are the core configuration; the rest extend it. */
 typedef struct {
     int workgroups_per_step;    /* workgroups per reduce / CU-copy launch;
                                    0 = automatic (fills the chip)              */
     int threads_per_workgroup;  /* 64..1024, multiple of 64; 0 = 256           */
     size_t chunk_bytes;         /* split copies into pieces of this size
                                    (>= 4096); 0 = no split, or the automatic
-                                   split of the AUTO copy path                 */
+                                   split of the SDMA copy path                 */
     int copy_streams;           /* copy streams of the HIP path, 1..16; 0 = 8  */
-    int sdma_engines;           /* engines used by SDMA_ENGINES, 0 = all       */
     hoccl_copy_path_t copy_path;
     int allgather_direct;       /* 1 (default): every rank copies each shard
                                    from its owner, the all-pairs traffic
@@ -156,20 +162,22 @@ typedef struct {
     int allreduce_chunk_groups; /* split each all-reduce ring chunk into this
                                    many groups so the gather of group g
                                    overlaps the reduction of group g+1 (on
-                                   SDMA_ENGINES the proxy issues group g's
+                                   the SDMA path the proxy issues group g's
                                    copies once an event the stream records
                                    after its reduction has completed);
-                                   0 = automatic: 2 on SDMA_ENGINES outside
+                                   0 = automatic: 2 on the SDMA path outside
                                    graph capture when each rank holds at
                                    least 32 MiB, else 1 (plan dumps assume
-                                   SDMA_ENGINES)                               */
+                                   the SDMA path)                              */
+    /* ---- extensions ---- */
+    int sdma_engines;           /* engines the SDMA path may use, 0 = all      */
     hoccl_reduce_algo_t reduce_algo;
     int kernel_timing;          /* 1: record HIP events around every reduce /
                                    copy kernel launch (hoccl_get_kernel_times) */
-    unsigned int proxy_timeout_ms; /* watchdog of the SDMA_ENGINES proxy;
-                                   0 = 10000                                   */
-    int proxy_handshake;        /* the stream side of the SDMA_ENGINES
-                                   start/finish flag handshake:
+    unsigned int proxy_timeout_ms; /* watchdog of the SDMA proxy; 0 = 10000    */
+    int proxy_handshake;        /* the stream side of the SDMA path's
+                                   start/finish flag handshake (Stream
+                                   Manager, CPU-GPU handshake protocol):
                                    -1 (default): 2, or 0 while a ROCm
                                    profiler is loaded;
                                    0: a one-lane kernel on the caller's
@@ -184,9 +192,8 @@ typedef struct {
                                    (hipLaunchHostFunc): no GPU code waits and
                                    no CU is used (4 KiB send/recv: 57 us),
                                    but the HIP runtime's callback thread is
-                                   blocked while the copies run.  A run
-                                   under rocprofv3 hung once, so with a ROCm
-                                   profiler loaded (rocprofiler-sdk
+                                   blocked while the copies run.  With a
+                                   ROCm profiler loaded (rocprofiler-sdk
                                    preloaded, or HSA_TOOLS_LIB set) an
                                    explicit 2 returns HOCCL_ERR_UNSUPPORTED */
     size_t ring_group_bytes;    /* ring reduce-scatter / all-reduce run their
@@ -200,34 +207,41 @@ typedef struct {
     unsigned int proxy_wait_limit_us; /* the handshake kernel stops waiting
                                    after this long, so its dispatch always
                                    ends; the proxy then reports
-                                   HOCCL_ERR_TIMEOUT at the next SDMA_ENGINES
-                                   call.  0 = 2 * proxy_timeout_ms + 1 s       */
+                                   HOCCL_ERR_TIMEOUT at the next SDMA call.
+                                   0 = 2 * proxy_timeout_ms + 1 s              */
 } hoccl_config_t;
 
+/* The first eight fields are the core statistics; the rest extend them. */
 typedef struct {
     int reduce_launches;        /* reduction kernel launches enqueued          */
-    int copy_kernel_launches;   /* CU copy kernel launches enqueued            */
     int copy_ops;               /* copy commands issued to the engine proxy
                                    or the HIP runtime                          */
     int workgroups_per_step;    /* workgroups per launch actually used         */
     int cus_available;          /* compute units of the device                 */
     int cus_used_max;           /* upper bound on CUs occupied by this call:
                                    min(workgroups, CUs) when kernels run; at
-                                   least 1 when the SDMA_ENGINES handshake is
-                                   the one-lane kernel; all CUs when copies go
+                                   least 1 when the SDMA handshake is the
+                                   one-lane kernel; all CUs when copies go
                                    through the HIP runtime (HOCCL_COPY_HIP),
                                    which may run them as a kernel of its own;
-                                   0 for copy-only calls on SDMA_ENGINES with
-                                   the host-function handshake                 */
+                                   0 for copy-only calls on the SDMA path
+                                   with the host-function handshake            */
     hoccl_copy_path_t copy_path_used;
-    hoccl_reduce_algo_t reduce_algo_used;
     unsigned long long hbm_bytes_algorithmic; /* bytes every step must read
                                    and write in HBM, summed over the call      */
-    unsigned long long copy_bytes;             /* bytes moved by copy steps   */
     double host_enqueue_us;     /* host time spent inside the call             */
+    /* ---- extensions ---- */
+    int copy_kernel_launches;   /* CU copy kernel launches enqueued            */
+    hoccl_reduce_algo_t reduce_algo_used; /* RING or DIRECT (never AUTO)       */
+    unsigned long long copy_bytes;             /* bytes moved by copy steps   */
 } hoccl_stats_t;
 
-/* Initialise the library on `device` (the current HIP device if < 0):
+/* ---- set-up and configuration ------------------------------------------
+ * The paper switches a training job between NCCL and its library with one
+ * environment variable (Implementation); here HOCCL_* variables configure
+ * the library the same way.
+ *
+ * Initialise the library on `device` (the current HIP device if < 0):
  * creates the internal copy streams, the event pool and, when the SDMA
  * engines can be driven directly, the proxy thread and its flag pool.
  * Reads HOCCL_* environment variables into the configuration:
@@ -236,10 +250,10 @@ typedef struct {
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
  *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES (the fields of the
  *   same meaning),
- *   HOCCL_COPY_PATH = auto | hip | engines | kernel,
- *   HOCCL_REDUCE_ALGO = ring | direct,
+ *   HOCCL_COPY_PATH = auto | sdma (or engines) | kernel | hip,
+ *   HOCCL_REDUCE_ALGO = ring | direct | auto,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),
- *   HOCCL_SDMA_ENGINE_IDS = "i,j,..." (the SDMA engines the SDMA_ENGINES
+ *   HOCCL_SDMA_ENGINE_IDS = "i,j,..." (the SDMA engines the SDMA
  *   proxy may use, in that order; read when the proxy is created),
  *   HOCCL_PROXY_SCHEDULE = round_robin (ablation: chain c on engine c mod E
  *   in plan order, instead of the byte-balanced, flow-size-interleaved
@@ -257,7 +271,10 @@ hoccl_status_t hoccl_finalize(void);
 hoccl_status_t hoccl_set_config(const hoccl_config_t *cfg);
 hoccl_status_t hoccl_get_config(hoccl_config_t *cfg);
 
-/* Statistics of the most recent collective call on this thread. */
+/* Statistics of the most recent collective call on this thread: launches,
+ * copies, workgroups and CUs, the quantities the paper's communication
+ * benchmark reports per configuration (Evaluation, Communication Benchmark:
+ * bandwidth against the number of SMs a collective may use). */
 hoccl_status_t hoccl_get_last_stats(hoccl_stats_t *stats);
 
 /* With kernel_timing on, every kernel launch of every collective call is
@@ -273,7 +290,9 @@ hoccl_status_t hoccl_get_kernel_times(float *ms, int cap, int *n);
 const char *hoccl_status_string(hoccl_status_t status);
 const char *hoccl_last_error_string(void);
 
-/* Number of SDMA engines the library can drive directly (0 if none). */
+/* Number of SDMA engines the library can drive directly (0 if none): the
+ * copy engines of the Background's DMA Engines section, each executing one
+ * copy at a time. */
 int hoccl_sdma_engine_count(void);
 
 /* ---- collectives --------------------------------------------------------
@@ -287,7 +306,10 @@ int hoccl_sdma_engine_count(void);
  * (ring or direct, any workgroup count, any chunk grouping) follows this
  * order, so results are identical bit for bit. */
 
-/* all-reduce of `count` elements per rank.  The ring splits count into R
+/* all-reduce of `count` elements per rank.  A reduction collective, which
+ * the paper leaves to SM-side execution (Limitations); here the reduction
+ * runs on a chosen number of workgroups and the gather on the SDMA path.
+ * The ring splits count into R
  * chunks of c = ceil(count / R) elements (the last may be short or empty);
  * rank j's reduced chunk j is then forwarded around the ring by copy steps.
  * send[r], recv[r]: count elements each. */
@@ -296,19 +318,25 @@ hoccl_status_t hoccl_allreduce(const void *const *send, void *const *recv,
                                hipStream_t stream);
 
 /* reduce-scatter: send[r] holds R * recvcount elements; rank r receives
- * block r (recvcount elements) of the element-wise sum. */
+ * block r (recvcount elements) of the element-wise sum.  A reduction
+ * collective (Limitations): it runs as reduction kernels only, with no copy
+ * step. */
 hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv,
                                     size_t recvcount, hoccl_dtype_t dtype,
                                     int R, hipStream_t stream);
 
 /* all-gather: send[r] holds sendcount elements; every recv[r] receives the
- * R shards in rank order (R * sendcount elements).  Copy-only: moved by the
- * configured copy path (the SDMA engines by default). */
+ * R shards in rank order (R * sendcount elements).  As a traffic matrix
+ * (Collective Scheduler, traffic matrix abstraction) C[s][d] = sendcount
+ * for every pair: copy-only, moved by the configured copy path (the SDMA
+ * engines by default). */
 hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv,
                                size_t sendcount, hoccl_dtype_t dtype, int R,
                                hipStream_t stream);
 
-/* point-to-point send/recv: rank r sends its count elements to rank
+/* point-to-point send/recv, the primitive of the Zero-SM Point-to-Point
+ * Executor (intra-node communication: the sender's copy engine writes
+ * straight into the receiver's buffer): rank r sends its count elements to rank
  * peers[r] (a host array of R ints; -1 = rank r sends nothing).  A receiver
  * named twice is an argument error; a rank may send to itself (local copy).
  * recv[d] of a rank nobody sends to may be NULL and is left untouched. */
@@ -317,12 +345,16 @@ hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv,
                               hoccl_dtype_t dtype, int R, hipStream_t stream);
 
 /* all-to-all with uniform blocks: block d of send[s] (count elements at
- * offset d * count) lands at block s of recv[d]. */
+ * offset d * count) lands at block s of recv[d].  The traffic matrix
+ * (Collective Scheduler, traffic matrix abstraction) has C[s][d] = count
+ * for every pair. */
 hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv,
                               size_t count, hoccl_dtype_t dtype, int R,
                               hipStream_t stream);
 
-/* all-to-all(v): the traffic matrix C[s][d] = sendcounts[s * R + d]
+/* all-to-all(v): the paper's origin traffic matrix C (Collective
+ * Scheduler, traffic matrix abstraction) given directly:
+ * C[s][d] = sendcounts[s * R + d]
  * elements move from send[s] + sdispls[s * R + d] to
  * recv[d] + rdispls[s * R + d] (all in elements; host arrays of R*R).
  * Destination ranges must not overlap. */
@@ -331,7 +363,8 @@ hoccl_status_t hoccl_alltoallv(const void *const *send,
                                void *const *recv, const size_t *rdispls,
                                hoccl_dtype_t dtype, int R, hipStream_t stream);
 
-/* One ring hop of one rank: out[i] = partial[i] + local[i] for i < count,
+/* One ring hop of one rank (a reduction step, Limitations):
+ * out[i] = partial[i] + local[i] for i < count,
  * in the arithmetic of the ring fold above, with `partial` the earlier
  * ranks' sum (or, on the first hop, the previous rank's own element) and
  * `local` this rank's contribution.  This is the step each GPU runs per hop
@@ -364,12 +397,15 @@ hoccl_status_t hoccl_ring_hop(const void *partial, const void *local, void *out,
                               hipStream_t stream);
 
 /* ---- introspection (tests and tools) ------------------------------------
- * Writes the schedule the planner builds for a collective as JSON into buf
+ * The planner's schedule for a collective: its traffic matrix turned into
+ * copy chains and reduction steps (Collective Scheduler, from C to the
+ * DMA-engine work queues).  Writes it as JSON into buf
  * (NUL-terminated, truncated to len).  op: 0 all-reduce, 1 reduce-scatter,
  * 2 all-gather, 3 send/recv (peers r -> r+1, last rank sends nothing),
  * 4 all-to-all.  Buffers are named symbolically ("send", "recv", "ws" with
  * rank and byte offset), so no device is needed.  Uses the current
- * configuration.  *needed receives the full length including the NUL. */
+ * configuration.  *needed receives the full length including the NUL
+ * (`needed` may be NULL). */
 hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dtype,
                                      int R, char *buf, size_t len,
                                      size_t *needed);
@@ -388,7 +424,8 @@ hoccl_status_t hoccl_debug_schedule_json(int G, const double *C, const int *node
                                          double bw_intra, double bw_inter, char *buf, size_t len,
                                          size_t *needed);
 
-/* Flow-size-aware chunk order on one DMA engine: flows of bytes[i] are cut
+/* Flow-size-aware chunk order on one DMA engine (Collective Scheduler,
+ * flow-size-aware chunk scheduling): flows of bytes[i] are cut
  * into chunk_bytes pieces and order[k] receives the flow of the k-th chunk
  * (at most cap entries); *n receives the total number of chunks. */
 hoccl_status_t hoccl_debug_interleave(int nflows, const double *bytes, double chunk_bytes, int *order,

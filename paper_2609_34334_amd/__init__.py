@@ -26,15 +26,17 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NO_MEMORY, ERR_TIMEOUT, ERR_INTERNAL = range(7)
 INT32, FP32, BF16 = 0, 1, 2
-COPY_AUTO, COPY_HIP, COPY_SDMA_ENGINES, COPY_KERNEL = range(4)
-REDUCE_RING, REDUCE_DIRECT = 0, 1
+COPY_AUTO, COPY_SDMA, COPY_KERNEL, COPY_HIP = range(4)
+REDUCE_RING, REDUCE_DIRECT, REDUCE_AUTO = range(3)
 OP_ALLREDUCE, OP_REDUCE_SCATTER, OP_ALLGATHER, OP_SENDRECV, OP_ALLTOALL = range(5)
 
 _DTYPES = {torch.int32: INT32, torch.float32: FP32, torch.bfloat16: BF16}
 HOP_FIRST, HOP_MIDDLE, HOP_LAST, HOP_ONLY = range(4)
 HOPS = {"first": HOP_FIRST, "middle": HOP_MIDDLE, "last": HOP_LAST, "only": HOP_ONLY}
-COPY_PATHS = {"auto": COPY_AUTO, "hip": COPY_HIP, "engines": COPY_SDMA_ENGINES,
-              "kernel": COPY_KERNEL}
+COPY_PATHS = {"auto": COPY_AUTO, "sdma": COPY_SDMA, "engines": COPY_SDMA,
+              "kernel": COPY_KERNEL, "hip": COPY_HIP}
+COPY_PATH_NAMES = {COPY_AUTO: "auto", COPY_SDMA: "engines", COPY_KERNEL: "kernel", COPY_HIP: "hip"}
+REDUCE_ALGOS = {"ring": REDUCE_RING, "direct": REDUCE_DIRECT, "auto": REDUCE_AUTO}
 
 
 class Config(ctypes.Structure):
@@ -42,10 +44,10 @@ class Config(ctypes.Structure):
                 ("threads_per_workgroup", ctypes.c_int),
                 ("chunk_bytes", ctypes.c_size_t),
                 ("copy_streams", ctypes.c_int),
-                ("sdma_engines", ctypes.c_int),
                 ("copy_path", ctypes.c_int),
                 ("allgather_direct", ctypes.c_int),
                 ("allreduce_chunk_groups", ctypes.c_int),
+                ("sdma_engines", ctypes.c_int),
                 ("reduce_algo", ctypes.c_int),
                 ("kernel_timing", ctypes.c_int),
                 ("proxy_timeout_ms", ctypes.c_uint),
@@ -56,16 +58,16 @@ class Config(ctypes.Structure):
 
 class Stats(ctypes.Structure):
     _fields_ = [("reduce_launches", ctypes.c_int),
-                ("copy_kernel_launches", ctypes.c_int),
                 ("copy_ops", ctypes.c_int),
                 ("workgroups_per_step", ctypes.c_int),
                 ("cus_available", ctypes.c_int),
                 ("cus_used_max", ctypes.c_int),
                 ("copy_path_used", ctypes.c_int),
-                ("reduce_algo_used", ctypes.c_int),
                 ("hbm_bytes_algorithmic", ctypes.c_ulonglong),
-                ("copy_bytes", ctypes.c_ulonglong),
-                ("host_enqueue_us", ctypes.c_double)]
+                ("host_enqueue_us", ctypes.c_double),
+                ("copy_kernel_launches", ctypes.c_int),
+                ("reduce_algo_used", ctypes.c_int),
+                ("copy_bytes", ctypes.c_ulonglong)]
 
 
 _vpp = ctypes.POINTER(ctypes.c_void_p)
@@ -133,14 +135,15 @@ def get_config():
 
 def set_config(**kw):
     """Update configuration fields; copy_path also accepts a name
-    ('auto', 'hip', 'engines', 'kernel') and reduce_algo 'ring'/'direct'."""
+    ('auto', 'sdma' or 'engines', 'kernel', 'hip') and reduce_algo
+    'ring', 'direct' or 'auto'."""
     c = Config()
     _check(_lib.hoccl_get_config(ctypes.byref(c)), "hoccl_get_config")
     for k, v in kw.items():
         if k == "copy_path" and isinstance(v, str):
             v = COPY_PATHS[v]
         if k == "reduce_algo" and isinstance(v, str):
-            v = {"ring": REDUCE_RING, "direct": REDUCE_DIRECT}[v]
+            v = REDUCE_ALGOS[v]
         if not hasattr(c, k):
             raise KeyError(k)
         setattr(c, k, v)

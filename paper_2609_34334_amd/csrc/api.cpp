@@ -105,7 +105,7 @@ hoccl_config_t default_config() {
     c.copy_path = HOCCL_COPY_AUTO;
     c.allgather_direct = 1;
     c.allreduce_chunk_groups = 0;
-    c.reduce_algo = HOCCL_REDUCE_RING;
+    c.reduce_algo = HOCCL_REDUCE_AUTO;
     c.kernel_timing = 0;
     c.proxy_timeout_ms = 10000;
     c.proxy_handshake = -1;
@@ -122,9 +122,9 @@ bool config_valid(const hoccl_config_t &c) {
         return false;
     if (c.copy_streams < 0 || c.copy_streams > 16) return false;
     if (c.sdma_engines < 0 || c.sdma_engines > 32) return false;
-    if ((int)c.copy_path < 0 || (int)c.copy_path > 3) return false;
+    if ((int)c.copy_path < HOCCL_COPY_AUTO || (int)c.copy_path > HOCCL_COPY_HIP) return false;
     if (c.allreduce_chunk_groups < 0 || c.allreduce_chunk_groups > 1024) return false;
-    if ((int)c.reduce_algo < 0 || (int)c.reduce_algo > 1) return false;
+    if ((int)c.reduce_algo < HOCCL_REDUCE_RING || (int)c.reduce_algo > HOCCL_REDUCE_AUTO) return false;
     if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
     if (c.proxy_handshake < -1 || c.proxy_handshake > 2) return false;
     return true;
@@ -154,12 +154,15 @@ void load_config_locked() {
     if (const char *v = std::getenv("HOCCL_RING_GROUP_BYTES")) c.ring_group_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "hip")) c.copy_path = HOCCL_COPY_HIP;
-        else if (!std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA_ENGINES;
+        else if (!std::strcmp(v, "sdma") || !std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA;
         else if (!std::strcmp(v, "kernel")) c.copy_path = HOCCL_COPY_KERNEL;
         else c.copy_path = HOCCL_COPY_AUTO;
     }
-    if (const char *v = std::getenv("HOCCL_REDUCE_ALGO"))
-        c.reduce_algo = std::strcmp(v, "direct") ? HOCCL_REDUCE_RING : HOCCL_REDUCE_DIRECT;
+    if (const char *v = std::getenv("HOCCL_REDUCE_ALGO")) {
+        if (!std::strcmp(v, "ring")) c.reduce_algo = HOCCL_REDUCE_RING;
+        else if (!std::strcmp(v, "direct")) c.reduce_algo = HOCCL_REDUCE_DIRECT;
+        else c.reduce_algo = HOCCL_REDUCE_AUTO;
+    }
     if (!config_valid(c)) c = default_config();
     g_debug = env_long("HOCCL_DEBUG", 0) != 0;
     g_cfg = c;
@@ -588,7 +591,7 @@ int resolve_handshake(const hoccl_config_t &cfg) {
 hoccl_copy_path_t resolve_path(const DeviceState &st, const hoccl_config_t &cfg, bool capturing) {
     if (cfg.copy_path != HOCCL_COPY_AUTO) return cfg.copy_path;
     if (!st.proxy || (capturing && resolve_handshake(cfg) != 2)) return HOCCL_COPY_HIP;
-    return HOCCL_COPY_SDMA_ENGINES;
+    return HOCCL_COPY_SDMA;
 }
 
 // On the engine proxy with no chunk size configured: when there are fewer
@@ -603,7 +606,7 @@ constexpr size_t kMinPieceBytes = (size_t)512 << 10;
 
 size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, hoccl_copy_path_t path,
                         const Plan &p) {
-    if (path != HOCCL_COPY_SDMA_ENGINES || cfg.chunk_bytes != 0 || !st.proxy) return 0;
+    if (path != HOCCL_COPY_SDMA || cfg.chunk_bytes != 0 || !st.proxy) return 0;
     int E = st.proxy->engine_count();
     if (cfg.sdma_engines > 0) E = std::min(E, cfg.sdma_engines);
     if (p.nchains <= 0 || p.nchains >= E) return 0;
@@ -615,76 +618,14 @@ size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, hoccl_
     return c < big ? c : 0;
 }
 
-template <typename Build>
-hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_t s) {
-    auto t0 = std::chrono::steady_clock::now();
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    HIP_TRY(hipStreamIsCapturing(s, &cap));
-    const bool capturing = cap != hipStreamCaptureStatusNone;
-    DeviceState *stp = nullptr;
-    TRY(get_state(&stp, capturing));
-    DeviceState &st = *stp;
-    hoccl_config_t cfg = config();
-    std::memset(&t_stats, 0, sizeof t_stats);
-    // Timing events of a captured call would be recorded only on replay.
-    if (capturing) cfg.kernel_timing = 0;
-    Buffers B = B0;
-    PlanOptions opt = options_from(cfg, in_place);
-    const hoccl_copy_path_t path = resolve_path(st, cfg, capturing);
-    const int handshake = resolve_handshake(cfg);
-    // Automatic all-reduce groups pay off only where the gather runs on the
-    // engines beside the reduction: on the engine proxy outside capture.
-    if (opt.allreduce_groups == 0 && (path != HOCCL_COPY_SDMA_ENGINES || capturing))
-        opt.allreduce_groups = 1;
-    Plan p = build(opt);
-    if (size_t c = auto_chunk_bytes(st, cfg, path, p)) {
-        opt.chunk_bytes = c;
-        p = build(opt);
-    }
-
-    const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
-    const int wg = auto_workgroups(st, cfg, p, threads);
-    if (g_debug)
-        std::fprintf(stderr, "hoccl: device %d stream %p workgroups %d copy_path %d%s plan %s\n",
-                     st.device, (void *)s, wg, (int)path, capturing ? " (captured)" : "",
-                     plan_to_json(p).c_str());
-    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && !st.proxy) {
-        // Asked for explicitly: never fall back silently.
-        set_err("%s", st.proxy_why.c_str());
-        return HOCCL_ERR_UNSUPPORTED;
-    }
-    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && handshake == 2 &&
-        profiler_present()) {
-        set_err("the host-function handshake (proxy_handshake = 2) is refused while a profiler is "
-                "loaded: it blocks the runtime thread the profiler may need");
-        return HOCCL_ERR_UNSUPPORTED;
-    }
-    if (!p.copies.empty() && path == HOCCL_COPY_SDMA_ENGINES && capturing && handshake != 2) {
-        // A replay would run the handshake kernel without the proxy thread
-        // issuing the copies; only the host-function form is recorded as a
-        // node that issues them itself.
-        set_err("the SDMA_ENGINES copy path is captured into a graph only with the host-function "
-                "handshake (proxy_handshake 2 or -1): the handshake kernel waits for copies the "
-                "proxy thread issues at call time");
-        return HOCCL_ERR_UNSUPPORTED;
-    }
-    const bool has_kernels = !p.reduce_steps.empty() || p.has_fold;
-    const bool has_copies = !p.copies.empty();
-
-    if (p.ws_bytes) {
-        TRY(ensure_ws(st, p.ws_bytes, capturing));
-        B.ws = st.ws;
-        // Calls outside capture are chained through ws_event.  A captured
-        // call joins no such chain: the order of its replays against other
-        // users of the workspace is the caller's.
-        if (!capturing && st.ws_last_stream && st.ws_last_stream != s)
-            HIP_TRY(hipStreamWaitEvent(s, st.ws_event, 0));
-    }
-
-    if (has_copies && path == HOCCL_COPY_SDMA_ENGINES && !capturing && p.ngroups > 1 &&
+// Enqueues a plan's reductions and copies on `s` by the chosen copy path.
+hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
+                            const Buffers &B, hipStream_t s, hoccl_copy_path_t path, int handshake,
+                            bool capturing, bool has_copies, int wg, int threads) {
+    if (has_copies && path == HOCCL_COPY_SDMA && !capturing && p.ngroups > 1 &&
         !p.reduce_steps.empty()) {
         TRY(run_engine_groups(st, cfg, p, B, s, wg, threads, handshake));
-    } else if (has_copies && path == HOCCL_COPY_SDMA_ENGINES) {
+    } else if (has_copies && path == HOCCL_COPY_SDMA) {
         // Reductions first (on s), then the proxy takes over the copies.
         TRY(run_reductions(st, cfg, p, B, s, wg, threads, false));
         std::vector<ProxyCopy> cps;
@@ -732,10 +673,92 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
                 TRY(run_copies_hip(st, cfg, p, B, s));
         }
     }
-    if (p.ws_bytes && !capturing) {
-        HIP_TRY(hipEventRecord(st.ws_event, s));
-        st.ws_last_stream = s;
+    return HOCCL_OK;
+}
+
+template <typename Build>
+hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_t s) {
+    auto t0 = std::chrono::steady_clock::now();
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(s, &cap));
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    DeviceState *stp = nullptr;
+    TRY(get_state(&stp, capturing));
+    DeviceState &st = *stp;
+    hoccl_config_t cfg = config();
+    std::memset(&t_stats, 0, sizeof t_stats);
+    // Timing events of a captured call would be recorded only on replay.
+    if (capturing) cfg.kernel_timing = 0;
+    Buffers B = B0;
+    PlanOptions opt = options_from(cfg, in_place);
+    const hoccl_copy_path_t path = resolve_path(st, cfg, capturing);
+    const int handshake = resolve_handshake(cfg);
+    // Automatic all-reduce groups pay off only where the gather runs on the
+    // engines beside the reduction: on the engine proxy outside capture.
+    if (opt.allreduce_groups == 0 && (path != HOCCL_COPY_SDMA || capturing))
+        opt.allreduce_groups = 1;
+    Plan p = build(opt);
+    if (size_t c = auto_chunk_bytes(st, cfg, path, p)) {
+        opt.chunk_bytes = c;
+        p = build(opt);
     }
+
+    const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
+    const int wg = auto_workgroups(st, cfg, p, threads);
+    if (g_debug)
+        std::fprintf(stderr, "hoccl: device %d stream %p workgroups %d copy_path %d%s plan %s\n",
+                     st.device, (void *)s, wg, (int)path, capturing ? " (captured)" : "",
+                     plan_to_json(p).c_str());
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA && !st.proxy) {
+        // Asked for explicitly: never fall back silently.
+        set_err("%s", st.proxy_why.c_str());
+        return HOCCL_ERR_UNSUPPORTED;
+    }
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA && handshake == 2 &&
+        profiler_present()) {
+        set_err("the host-function handshake (proxy_handshake = 2) is refused while a profiler is "
+                "loaded: it blocks the runtime thread the profiler may need");
+        return HOCCL_ERR_UNSUPPORTED;
+    }
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA && capturing && handshake != 2) {
+        // A replay would run the handshake kernel without the proxy thread
+        // issuing the copies; only the host-function form is recorded as a
+        // node that issues them itself.
+        set_err("the SDMA copy path is captured into a graph only with the host-function "
+                "handshake (proxy_handshake 2 or -1): the handshake kernel waits for copies the "
+                "proxy thread issues at call time");
+        return HOCCL_ERR_UNSUPPORTED;
+    }
+    const bool has_kernels = !p.reduce_steps.empty() || p.has_fold;
+    const bool has_copies = !p.copies.empty();
+    // An error the proxy thread stored since the last call (a watchdog
+    // timeout of earlier copies) is reported before anything is enqueued,
+    // so the call that reports it leaves every buffer untouched.
+    if (has_copies && path == HOCCL_COPY_SDMA) TRY(st.proxy->take_error(t_err));
+
+    if (p.ws_bytes) {
+        TRY(ensure_ws(st, p.ws_bytes, capturing));
+        B.ws = st.ws;
+        // Calls outside capture are chained through ws_event.  A captured
+        // call joins no such chain: the order of its replays against other
+        // users of the workspace is the caller's.
+        if (!capturing && st.ws_last_stream && st.ws_last_stream != s)
+            HIP_TRY(hipStreamWaitEvent(s, st.ws_event, 0));
+    }
+    // From here on kernels may be on the stream: whatever happens, the next
+    // workspace user on another stream must wait for them.
+    hoccl_status_t body = enqueue_body(st, cfg, p, B, s, path, handshake, capturing, has_copies, wg,
+                                       threads);
+    if (p.ws_bytes && !capturing) {
+        hipError_t e = hipEventRecord(st.ws_event, s);
+        if (e == hipSuccess) {
+            st.ws_last_stream = s;
+        } else if (body == HOCCL_OK) {
+            set_err("hipEventRecord(ws_event): %s", hipGetErrorString(e));
+            return HOCCL_ERR_HIP;
+        }
+    }
+    TRY(body);
 
     bool cu_work = has_kernels || (has_copies && path == HOCCL_COPY_KERNEL);
     t_stats.workgroups_per_step = cu_work ? wg : 0;
@@ -743,7 +766,7 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     // The engine proxy's handshake kernel waits as one lane on one CU; the
     // host-function form needs none.
     const bool handshake_wave =
-        has_copies && path == HOCCL_COPY_SDMA_ENGINES && handshake != 2;
+        has_copies && path == HOCCL_COPY_SDMA && handshake != 2;
     int cus = cu_work ? std::min(wg, st.num_cus) : 0;
     if (handshake_wave) cus = std::max(cus, 1);
     // The HIP runtime may run its device-to-device copies as a kernel of its

@@ -107,6 +107,13 @@ struct PlanOptions {
     size_t group_partial_bytes = 0;
 };
 
+// HOCCL_REDUCE_AUTO folds directly up to this many ranks.  On one GPU the
+// fold moves (R+1) elements per reduce-scatter output element against the
+// ring's 2(R-1) (plus the fp32 partials of bf16), so it is the faster
+// schedule at every size measured; beyond this rank count the ring is used.
+constexpr int kDirectMaxRanks = 64;
+bool use_direct(hoccl_reduce_algo_t algo, int R);
+
 size_t dtype_size(hoccl_dtype_t dt);
 size_t acc_size(hoccl_dtype_t dt);
 

@@ -26,6 +26,10 @@ size_t acc_size(hoccl_dtype_t) { return 4; }
 
 static inline int mod(int a, int R) { return ((a % R) + R) % R; }
 
+bool use_direct(hoccl_reduce_algo_t algo, int R) {
+    return algo == HOCCL_REDUCE_DIRECT || (algo == HOCCL_REDUCE_AUTO && R <= kDirectMaxRanks);
+}
+
 static BufRef ref(uint8_t kind, int rank, size_t off) {
     BufRef b;
     b.kind = kind;
@@ -170,7 +174,7 @@ Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o
         finish_chains(p);
         return p;
     }
-    if (o.algo == HOCCL_REDUCE_DIRECT) {
+    if (use_direct(o.algo, R)) {
         p.has_fold = true;
         p.fold.c = n;
         p.fold.total = (size_t)R * n;
@@ -209,7 +213,7 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
         size_t b = (size_t)j * c;
         len[(size_t)j] = b >= count ? 0 : std::min(c, count - b);
     }
-    if (o.algo == HOCCL_REDUCE_DIRECT) {
+    if (use_direct(o.algo, R)) {
         p.has_fold = true;
         p.fold.c = c;
         p.fold.total = count;

@@ -485,6 +485,17 @@ Proxy::~Proxy() {
 
 int Proxy::engine_count() const { return (int)impl_->engines.size(); }
 
+hoccl_status_t Proxy::take_error(std::string &err) {
+    std::lock_guard<std::mutex> lk(impl_->mu);
+    hoccl_status_t st = impl_->sticky;
+    if (st != HOCCL_OK) {
+        err = impl_->sticky_msg;
+        impl_->sticky = HOCCL_OK;
+        impl_->sticky_msg.clear();
+    }
+    return st;
+}
+
 // The stream side of the handshake run as a host function: the HIP runtime
 // holds every later operation of the stream until it returns, so the stream
 // waits without any GPU code.  It performs the same four flag steps as the
@@ -642,17 +653,6 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
                              hipStream_t s, int *engines_used, std::string &err,
                              std::vector<hipEvent_t> gates) {
     ProxyImpl &P = *impl_;
-    {
-        std::lock_guard<std::mutex> lk(P.mu);
-        if (P.sticky != HOCCL_OK) {
-            hoccl_status_t st = P.sticky;
-            err = P.sticky_msg;
-            P.sticky = HOCCL_OK;
-            P.sticky_msg.clear();
-            for (hipEvent_t e : gates) P.free_events.push_back(e);  // the lock is held
-            return st;
-        }
-    }
     for (const ProxyCopy &c : copies)
         if (c.gate >= (int)gates.size()) {
             err = "a copy names a gate that was not given";
@@ -801,16 +801,6 @@ hoccl_status_t Proxy::capture(const std::vector<ProxyCopy> &copies, int max_engi
                               unsigned timeout_ms, unsigned wait_limit_us, hipStream_t s,
                               int *engines_used, std::string &err) {
     ProxyImpl &P = *impl_;
-    {
-        std::lock_guard<std::mutex> lk(P.mu);
-        if (P.sticky != HOCCL_OK) {
-            hoccl_status_t st = P.sticky;
-            err = P.sticky_msg;
-            P.sticky = HOCCL_OK;
-            P.sticky_msg.clear();
-            return st;
-        }
-    }
     CapturedOp *op = new CapturedOp();
     op->P = &P;
     {

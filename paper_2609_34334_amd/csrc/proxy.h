@@ -31,6 +31,12 @@ class Proxy {
 
     int engine_count() const;
 
+    // The error the proxy thread stored since the last call (a watchdog
+    // timeout, a failed copy issue), cleared by this call; HOCCL_OK if none.
+    // The executor takes it before it enqueues anything, so a call that
+    // reports it has enqueued nothing.
+    hoccl_status_t take_error(std::string &err);
+
     // Events for submit's `gates`, taken from the proxy's pool.  They return
     // to it when the operation that uses them retires, or by
     // release_events if the caller does not submit after all.

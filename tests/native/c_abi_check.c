@@ -5,6 +5,7 @@
  * bit-for-bit copies; then the documented argument errors.  Exit status 0
  * and the line "c abi ok" mean every check passed. */
 #include <hip/hip_runtime_api.h>
+#include <stddef.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -12,8 +13,41 @@
 
 #include "../../include/hoccl.h"
 
+/* Sizes the Python binding mirrors (tests/test_abi.py checks the same). */
+#define HOCCL_CONFIG_SIZE 72
+#define HOCCL_STATS_SIZE 56
+
 #define R 5
 #define N 1003 /* ragged against R */
+
+/* The boundary's enum values and struct layouts, pinned at compile time:
+ * the copy paths keep AUTO 0, SDMA 1, KERNEL 2 (HIP appended as 3), and
+ * the configuration and statistics keep their core fields first, in order,
+ * with the extensions after them. */
+_Static_assert(HOCCL_OK == 0 && HOCCL_ERR_INVALID_ARG == 1 && HOCCL_ERR_UNSUPPORTED == 2 &&
+               HOCCL_ERR_HIP == 3 && HOCCL_ERR_NO_MEMORY == 4 && HOCCL_ERR_TIMEOUT == 5 &&
+               HOCCL_ERR_INTERNAL == 6, "status values");
+_Static_assert(HOCCL_INT32 == 0 && HOCCL_FP32 == 1 && HOCCL_BF16 == 2, "dtype values");
+_Static_assert(HOCCL_COPY_AUTO == 0 && HOCCL_COPY_SDMA == 1 && HOCCL_COPY_KERNEL == 2 &&
+               HOCCL_COPY_HIP == 3, "copy path values");
+_Static_assert(HOCCL_REDUCE_RING == 0 && HOCCL_REDUCE_DIRECT == 1 && HOCCL_REDUCE_AUTO == 2,
+               "reduction algorithm values");
+_Static_assert(offsetof(hoccl_config_t, workgroups_per_step) == 0 &&
+               offsetof(hoccl_config_t, threads_per_workgroup) == 4 &&
+               offsetof(hoccl_config_t, chunk_bytes) == 8 &&
+               offsetof(hoccl_config_t, copy_streams) == 16 &&
+               offsetof(hoccl_config_t, copy_path) == 20 &&
+               offsetof(hoccl_config_t, allgather_direct) == 24 &&
+               offsetof(hoccl_config_t, allreduce_chunk_groups) == 28, "core configuration layout");
+_Static_assert(offsetof(hoccl_stats_t, reduce_launches) == 0 && offsetof(hoccl_stats_t, copy_ops) == 4 &&
+               offsetof(hoccl_stats_t, workgroups_per_step) == 8 &&
+               offsetof(hoccl_stats_t, cus_available) == 12 &&
+               offsetof(hoccl_stats_t, cus_used_max) == 16 &&
+               offsetof(hoccl_stats_t, copy_path_used) == 20 &&
+               offsetof(hoccl_stats_t, hbm_bytes_algorithmic) == 24 &&
+               offsetof(hoccl_stats_t, host_enqueue_us) == 32, "core statistics layout");
+_Static_assert(sizeof(hoccl_config_t) == HOCCL_CONFIG_SIZE, "configuration size");
+_Static_assert(sizeof(hoccl_stats_t) == HOCCL_STATS_SIZE, "statistics size");
 
 static int failures = 0;
 #define CHECK(cond, ...)                                  \
@@ -93,7 +127,7 @@ int main(void) {
     }
 
     /* all-gather: recv_r[q*N + i] = x_q[i], bitwise, on each copy path */
-    for (int path = HOCCL_COPY_AUTO; path <= HOCCL_COPY_KERNEL; ++path) {
+    for (int path = HOCCL_COPY_AUTO; path <= HOCCL_COPY_HIP; ++path) {
         hoccl_config_t cfg;
         HOCCL_OK_(hoccl_get_config(&cfg));
         cfg.copy_path = (hoccl_copy_path_t)path;
@@ -103,7 +137,7 @@ int main(void) {
             HIP_OK(hipMemcpy(send[r], h, sizeof(int32_t) * N, hipMemcpyHostToDevice));
         }
         hoccl_status_t st2 = hoccl_allgather((const void *const *)send, (void *const *)recv, N, HOCCL_INT32, R, s);
-        if (path == HOCCL_COPY_SDMA_ENGINES && st2 == HOCCL_ERR_UNSUPPORTED) continue;
+        if (path == HOCCL_COPY_SDMA && st2 == HOCCL_ERR_UNSUPPORTED) continue;
         HOCCL_OK_(st2);
         HIP_OK(hipStreamSynchronize(s));
         for (int r = 0; r < R; ++r) {

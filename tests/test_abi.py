@@ -139,7 +139,12 @@ def test_debug_env_logs_plans_without_a_gpu_call():
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
                        cwd=ROOT)
     assert r.returncode == 0, r.stderr
-    assert r.stdout.split() == ["3", "1", "250"], r.stdout
+    assert r.stdout.split() == [str(hc.COPY_KERNEL), str(hc.REDUCE_DIRECT), "250"], r.stdout
+    env.update(HOCCL_COPY_PATH="sdma", HOCCL_REDUCE_ALGO="auto")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                       cwd=ROOT)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == [str(hc.COPY_SDMA), str(hc.REDUCE_AUTO), "250"], r.stdout
 
 
 
@@ -169,3 +174,48 @@ def test_ring_hop_rejects_bad_arguments_before_the_device():
     assert L.hoccl_ring_hop(a, b, a + 8, 4, hc.BF16, hc.HOP_MIDDLE, None) == hc.ERR_INVALID_ARG
     # last hop: bf16 out aliasing the fp32 partial is a different element size
     assert L.hoccl_ring_hop(a, b, a, 4, hc.BF16, hc.HOP_LAST, None) == hc.ERR_INVALID_ARG
+
+
+def _compile_and_run(tmp_path, name, body):
+    import subprocess
+    src = tmp_path / f"{name}.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "hoccl.h"\nint main(void){\n'
+                   + body + "return 0;}\n")
+    exe = tmp_path / name
+    subprocess.run(["gcc", "-std=c11", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
+                    "-I/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    return subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()
+
+
+@pytest.mark.parametrize("cls,ctype", [(hc.Config, "hoccl_config_t"), (hc.Stats, "hoccl_stats_t")])
+def test_binding_structs_match_header_layout(tmp_path, cls, ctype):
+    """The ctypes mirrors of the configuration and statistics structs have
+    the header's field offsets and size (a C compiler says what they are)."""
+    body = "".join(f'printf("%zu\\n", offsetof({ctype}, {f}));' for f, _ in cls._fields_)
+    body += f'printf("%zu\\n", sizeof({ctype}));'
+    got = [int(v) for v in _compile_and_run(tmp_path, ctype, body)]
+    want = [getattr(cls, f).offset for f, _ in cls._fields_] + [ctypes.sizeof(cls)]
+    assert got == want
+
+
+def test_enum_values_match_binding(tmp_path):
+    """Copy paths keep AUTO 0, SDMA 1, KERNEL 2 with HIP appended as 3; the
+    binding's constants equal the header's."""
+    names = ["HOCCL_COPY_AUTO", "HOCCL_COPY_SDMA", "HOCCL_COPY_KERNEL", "HOCCL_COPY_HIP",
+             "HOCCL_REDUCE_RING", "HOCCL_REDUCE_DIRECT", "HOCCL_REDUCE_AUTO",
+             "HOCCL_INT32", "HOCCL_FP32", "HOCCL_BF16"]
+    got = [int(v) for v in _compile_and_run(tmp_path, "enums",
+                                            "".join(f'printf("%d\\n", (int){n});' for n in names))]
+    assert got == [0, 1, 2, 3, 0, 1, 2, 0, 1, 2]
+    assert [hc.COPY_AUTO, hc.COPY_SDMA, hc.COPY_KERNEL, hc.COPY_HIP] == [0, 1, 2, 3]
+    assert [hc.REDUCE_RING, hc.REDUCE_DIRECT, hc.REDUCE_AUTO] == [0, 1, 2]
+
+
+def test_c_abi_check_compiles_with_its_layout_pins():
+    """tests/native/c_abi_check.c pins enum values and struct layouts with
+    static assertions; it must compile against the header (it runs on the
+    GPU)."""
+    import subprocess
+    subprocess.run(["gcc", "-std=c11", "-fsyntax-only", "-D__HIP_PLATFORM_AMD__",
+                    "-I" + os.path.join(ROOT, "include"), "-I/opt/rocm/include",
+                    os.path.join(ROOT, "tests", "native", "c_abi_check.c")], check=True)

@@ -72,6 +72,28 @@ def test_ring_in_cache_groups(dt, R):
                 assert_bitwise(gota[r], refa[r], f"grouped AR budget={budget} r={r}")
 
 
+@pytest.mark.parametrize("R", [2, 5, 8, 16])
+def test_auto_reduction_folds_and_matches_the_oracle(R):
+    """The default reduction (AUTO) folds directly on one GPU, reports that
+    choice, and gives the oracle's bits for reduce-scatter and all-reduce,
+    ragged, on the default copy path."""
+    hc.set_config(reduce_algo="auto", copy_path="auto")
+    for dt in DTS:
+        n = R * 37 + 3
+        x = [W.random_values(NAME[dt], 720 + R, r, R * n) for r in range(R)]
+        got = run_rs(x, dt, lead=1)
+        assert hc.last_stats()["reduce_algo_used"] == hc.REDUCE_DIRECT
+        ref = oracle.reduce_scatter_new(x, dt)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"AUTO RS {NAME[dt]} R={R} r={r}")
+        xa = [W.random_values(NAME[dt], 730 + R, r, 4099) for r in range(R)]
+        gota = run_ar(xa, dt, lead=2)
+        assert hc.last_stats()["reduce_algo_used"] == hc.REDUCE_DIRECT
+        refa = oracle.allreduce_new(xa, dt)
+        for r in range(R):
+            assert_bitwise(gota[r], refa[r], f"AUTO AR {NAME[dt]} R={R} r={r}")
+
+
 @pytest.mark.parametrize("algo", ["ring", "direct"])
 @pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
 @pytest.mark.parametrize("R", [1, 2, 3, 4, 8])
@@ -285,8 +307,8 @@ def test_copy_paths_report_their_cus():
     R, n = 8, 1 << 16
     x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
     ncu = torch.cuda.get_device_properties(0).multi_processor_count
-    for path, hs, cus, used in [("auto", -1, 0, hc.COPY_SDMA_ENGINES), ("engines", -1, 0, hc.COPY_SDMA_ENGINES),
-                                ("engines", 0, 1, hc.COPY_SDMA_ENGINES), ("hip", -1, ncu, hc.COPY_HIP)]:
+    for path, hs, cus, used in [("auto", -1, 0, hc.COPY_SDMA), ("engines", -1, 0, hc.COPY_SDMA),
+                                ("engines", 0, 1, hc.COPY_SDMA), ("hip", -1, ncu, hc.COPY_HIP)]:
         hc.set_config(copy_path=path, proxy_handshake=hs)
         hc.allgather(x)
         s = hc.last_stats()
@@ -416,6 +438,39 @@ def test_proxy_watchdog_reports_timeout_then_recovers():
     hc.allgather(x, recv)
     torch.cuda.synchronize()
     assert torch.equal(recv[3][5 * n:6 * n], x[5])
+
+
+def test_stored_timeout_reported_before_anything_is_enqueued():
+    """Failure handling forced from the host: a 1 ms watchdog expires on an
+    all-gather's copies.  The next engine call, a ring all-reduce that would
+    reduce on the CUs before handing its gather to the proxy, reports the
+    timeout and enqueues nothing: its outputs keep their contents.  Then the
+    same all-reduce runs and matches the oracle."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    R, n = 8, 1 << 24
+    x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    hc.set_config(copy_path="engines", proxy_timeout_ms=1, reduce_algo="ring")
+    hc.allgather(x, recv)
+    torch.cuda.synchronize()
+    m = 300_007
+    xa = [W.random_values("fp32", 97, r, m) for r in range(R)]
+    send = [to_dev(a, hc.FP32) for a in xa]
+    outs = [torch.full((m,), 7.0, device="cuda") for _ in range(R)]
+    torch.cuda.synchronize()
+    with pytest.raises(hc.HocclError) as ei:
+        hc.allreduce(send, outs)
+    assert ei.value.status == hc.ERR_TIMEOUT
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert bool((outs[r] == 7.0).all()), f"rank {r}'s output changed under a reported error"
+    hc.set_config(proxy_timeout_ms=0)
+    hc.allreduce(send, outs)
+    torch.cuda.synchronize()
+    ref = oracle.allreduce_new(xa, hc.FP32)
+    for r in (0, R - 1):
+        assert_bitwise(from_dev(outs[r], hc.FP32), ref[r], f"all-reduce after the error, rank {r}")
 
 
 def test_finalize_and_reinit():

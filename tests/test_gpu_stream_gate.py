@@ -181,16 +181,18 @@ def test_debug_log_names_the_plan(tmp_path):
     assert "hoccl: device 0" in r.stderr and "plan {" in r.stderr, r.stderr[-2000:]
 
 
-def test_many_engine_operations_in_flight():
-    """300 engine-proxy send/recv operations queued behind a closed gate
-    (more than the old pool of 64 handshake slots), each copying buffer k
-    into buffer k+1: when the gate opens they must run in stream order, so
-    every buffer ends up holding buffer 0's bits and none keeps its
-    canary."""
+@pytest.mark.parametrize("K,n", [(300, 2048), (24, (1 << 19) + 3)], ids=["4KiB", "1MiB"])
+def test_many_engine_operations_in_flight(K, n):
+    """Engine-proxy send/recv operations queued behind a closed gate, each
+    copying buffer k into buffer k+1: when the gate opens they must run in
+    stream order, so every buffer ends up holding buffer 0's bits and none
+    keeps its canary.  300 messages of 4 KiB (more than the old pool of 64
+    handshake slots) take the ungated form; 24 of just over 1 MiB take the
+    form whose copies start on an event the proxy polls, so each message's
+    copies must wait for the previous message's handshake."""
     if hc.sdma_engine_count() == 0:
         pytest.skip("engine proxy unavailable")
     hc.set_config(copy_path="engines")
-    K, n = 300, 2048
     bufs = [torch.full((n,), 0x7A5A, dtype=torch.int16, device="cuda").view(torch.bfloat16)
             for _ in range(K + 1)]
     first = to_dev(W.random_bits(405, 0, n, 2), hc.BF16)

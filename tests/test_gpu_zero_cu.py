@@ -114,7 +114,7 @@ def test_copy_collectives_finish_while_every_cu_is_busy(path):
     for name, run, outs, ref in _copy_workloads():
         done_ms, round_ms = finish_time_beside_spin(run)
         s = hc.last_stats()
-        assert s["copy_path_used"] == hc.COPY_SDMA_ENGINES and s["cus_used_max"] == 0, (name, s)
+        assert s["copy_path_used"] == hc.COPY_SDMA and s["cus_used_max"] == 0, (name, s)
         assert done_ms < round_ms - 10, (
             f"{path} {name}: finished {done_ms:.1f} ms after the spin began, not before its "
             f"first round ended ({round_ms:.0f} ms): its copies needed a CU")
@@ -145,12 +145,12 @@ def test_graph_replay_on_auto_finishes_while_every_cu_is_busy():
     coll_s = o["streams"][1]
     run(coll_s)                                # eager first: library state
     torch.cuda.synchronize()
-    assert hc.last_stats()["copy_path_used"] == hc.COPY_SDMA_ENGINES
+    assert hc.last_stats()["copy_path_used"] == hc.COPY_SDMA
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=coll_s):
         run(coll_s)
     torch.cuda.synchronize()
-    assert hc.last_stats()["copy_path_used"] == hc.COPY_SDMA_ENGINES
+    assert hc.last_stats()["copy_path_used"] == hc.COPY_SDMA
     for t in outs:
         t.zero_()
     torch.cuda.synchronize()
