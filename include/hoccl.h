@@ -325,6 +325,26 @@ hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv,
                                     size_t recvcount, hoccl_dtype_t dtype,
                                     int R, hipStream_t stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * operation, arguments and results as hoccl_reduce_scatter, bit for bit,
+ * but the call allocates nothing and creates no stream or event.  Where the
+ * ring keeps fp32 partials (bf16 over more than two ranks; int32 / fp32 in
+ * place) they live in a static device array of 128 MiB that every device
+ * the library runs on holds from initialisation until the process ends.  A
+ * call that needs more (R * recvcount * 4 bytes beyond 128 MiB) returns
+ * HOCCL_ERR_INVALID_ARG and enqueues nothing; the reduction the
+ * configuration picks decides whether any is needed (the direct fold needs
+ * none).  The library must already be initialised on the current device
+ * (hoccl_init, or any earlier call), else HOCCL_ERR_UNSUPPORTED.  Kernel
+ * timing is off for these calls and a one-rank copy runs as a CU copy
+ * kernel.  Every such call on a device shares that device's array: calls
+ * whose executions overlap on one GPU (on different streams, or in graph
+ * replays) race and give wrong results, so the caller orders them. */
+hoccl_status_t hoccl_reduce_scatter_noalloc(const void *const *send, void *const *recv,
+                                            size_t recvcount, hoccl_dtype_t dtype, int R,
+                                            hipStream_t stream);
+
 /* all-gather: send[r] holds sendcount elements; every recv[r] receives the
  * R shards in rank order (R * sendcount elements).  As a traffic matrix
  * (Collective Scheduler, traffic matrix abstraction) C[s][d] = sendcount

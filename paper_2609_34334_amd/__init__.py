@@ -83,6 +83,7 @@ _SIGS = {
     "hoccl_get_kernel_times": [ctypes.POINTER(ctypes.c_float), _i, ctypes.POINTER(_i)],
     "hoccl_allreduce": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
     "hoccl_reduce_scatter": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
+    "hoccl_reduce_scatter_noalloc": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
     "hoccl_allgather": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
     "hoccl_sendrecv": [_vpp, _vpp, ctypes.POINTER(_i), _sz, _i, _i, ctypes.c_void_p],
     "hoccl_alltoall": [_vpp, _vpp, _sz, _i, _i, ctypes.c_void_p],
@@ -302,6 +303,23 @@ def reduce_scatter(send, recv=None, stream=None):
         raise ValueError("buffer sizes do not match")
     _check(_lib.hoccl_reduce_scatter(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
            "hoccl_reduce_scatter")
+    return recv
+
+
+@_on_send_device
+def reduce_scatter_noalloc(send, recv, stream=None):
+    """reduce_scatter through the entry point that allocates nothing: the
+    ring's partials live in the library's static device scratch.  `recv`
+    must be given; the library must be initialised on the device."""
+    R = len(send)
+    if send[0].numel() % R:
+        raise ValueError("send buffers must hold R * recvcount elements")
+    n = send[0].numel() // R
+    dt = _dtype_of(list(send) + list(recv))
+    if any(t.numel() != R * n for t in send) or any(t.numel() != n for t in recv):
+        raise ValueError("buffer sizes do not match")
+    _check(_lib.hoccl_reduce_scatter_noalloc(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
+           "hoccl_reduce_scatter_noalloc")
     return recv
 
 

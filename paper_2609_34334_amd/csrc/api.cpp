@@ -62,6 +62,8 @@ struct DeviceState {
     size_t timing_used = 0;
     Proxy *proxy = nullptr;
     std::string proxy_why;  // why the proxy could not be created
+    void *scratch = nullptr;  // this device's address of the static scratch
+    std::string scratch_why;  // why it has none
 };
 
 std::mutex g_mu;
@@ -236,13 +238,22 @@ hoccl_status_t create_state(int device, DeviceState **out) {
         set_err("hipEventCreateWithFlags: %s", hipGetErrorString(e));
         return fail(HOCCL_ERR_HIP);
     }
+    // The static scratch of the entry point that allocates nothing: this
+    // device's address of it, taken once here with the device current.
+    // A failure leaves only that entry point unusable.
+    if ((e = scratch_address(&st->scratch)) != hipSuccess) {
+        (void)hipGetLastError();  // handled: do not leave it for the next caller
+        st->scratch = nullptr;
+        st->scratch_why = std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e);
+    }
     st->proxy = Proxy::create(device, &st->proxy_why);  // null when the engines cannot be driven
     *out = st;
     return HOCCL_OK;
 }
 
-// `capturing`: the caller's stream is capturing a graph.  Creating the state
-// then would synchronise the device and allocate, so it is refused.
+// `capturing`: the caller's stream is capturing a graph, or the caller must
+// not allocate.  Creating the state then would synchronise the device and
+// allocate, so it is refused.
 hoccl_status_t get_state(DeviceState **out, bool capturing = false) {
     int dev = 0;
     HIP_TRY(hipGetDevice(&dev));
@@ -255,7 +266,8 @@ hoccl_status_t get_state(DeviceState **out, bool capturing = false) {
     }
     if (capturing) {
         set_err("the library is not initialised on device %d and cannot be during stream "
-                "capture: call hoccl_init (or any collective) outside capture first", dev);
+                "capture or in a call that allocates nothing: call hoccl_init (or any "
+                "collective) first", dev);
         return HOCCL_ERR_UNSUPPORTED;
     }
     DeviceState *st = nullptr;
@@ -676,19 +688,26 @@ hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Pl
     return HOCCL_OK;
 }
 
+// `noalloc`: the call allocates nothing (hoccl_reduce_scatter_noalloc): the
+// library must already be initialised on the device, kernel timing is off,
+// copies run as CU copy kernels, and the ring's partials live in the static
+// scratch instead of the workspace.
 template <typename Build>
-hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_t s) {
+hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_t s,
+                       bool noalloc = false) {
     auto t0 = std::chrono::steady_clock::now();
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     HIP_TRY(hipStreamIsCapturing(s, &cap));
     const bool capturing = cap != hipStreamCaptureStatusNone;
     DeviceState *stp = nullptr;
-    TRY(get_state(&stp, capturing));
+    TRY(get_state(&stp, capturing || noalloc));
     DeviceState &st = *stp;
     hoccl_config_t cfg = config();
     std::memset(&t_stats, 0, sizeof t_stats);
-    // Timing events of a captured call would be recorded only on replay.
-    if (capturing) cfg.kernel_timing = 0;
+    // Timing events of a captured call would be recorded only on replay; a
+    // call that allocates nothing creates none.
+    if (capturing || noalloc) cfg.kernel_timing = 0;
+    if (noalloc) cfg.copy_path = HOCCL_COPY_KERNEL;
     Buffers B = B0;
     PlanOptions opt = options_from(cfg, in_place);
     const hoccl_copy_path_t path = resolve_path(st, cfg, capturing);
@@ -736,7 +755,18 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     // so the call that reports it leaves every buffer untouched.
     if (has_copies && path == HOCCL_COPY_SDMA) TRY(st.proxy->take_error(t_err));
 
-    if (p.ws_bytes) {
+    if (p.ws_bytes && noalloc) {
+        if (p.ws_bytes > kScratchBytes) {
+            set_err("this call needs %zu bytes of scratch for its partials; the static scratch of "
+                    "the call that allocates nothing holds %zu", p.ws_bytes, kScratchBytes);
+            return HOCCL_ERR_INVALID_ARG;
+        }
+        if (!st.scratch) {
+            set_err("%s", st.scratch_why.c_str());
+            return HOCCL_ERR_UNSUPPORTED;
+        }
+        B.ws = st.scratch;
+    } else if (p.ws_bytes) {
         TRY(ensure_ws(st, p.ws_bytes, capturing));
         B.ws = st.ws;
         // Calls outside capture are chained through ws_event.  A captured
@@ -749,7 +779,7 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     // workspace user on another stream must wait for them.
     hoccl_status_t body = enqueue_body(st, cfg, p, B, s, path, handshake, capturing, has_copies, wg,
                                        threads);
-    if (p.ws_bytes && !capturing) {
+    if (p.ws_bytes && !capturing && !noalloc) {
         hipError_t e = hipEventRecord(st.ws_event, s);
         if (e == hipSuccess) {
             st.ws_last_stream = s;
@@ -870,6 +900,29 @@ PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
 }  // namespace hoccl
 
 using namespace hoccl;
+
+static hoccl_status_t reduce_scatter_impl(const void *const *send, void *const *recv, size_t n,
+                                          hoccl_dtype_t dt, int R, hipStream_t stream, bool noalloc) {
+    TRY(check_common(send, recv, dt, R));
+    if (n == 0) return HOCCL_OK;
+    TRY(check_ptrs(send, R, "send"));
+    TRY(check_ptrs((const void *const *)recv, R, "recv"));
+    size_t es = dtype_size(dt);
+    if (size_overflows(n, es * (size_t)R)) return HOCCL_ERR_INVALID_ARG;
+    size_t ob = n * es, ib = (size_t)R * n * es;
+    std::vector<Range> outs, ins;
+    bool in_place = true;
+    for (int r = 0; r < R; ++r) {
+        outs.push_back({(uintptr_t)recv[r], (uintptr_t)recv[r] + ob, r, true});
+        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + ib, r, false});
+        in_place &= ((const char *)recv[r] == (const char *)send[r] + (size_t)r * ob);
+    }
+    TRY(check_overlaps(outs, ins, [ob](const Range &o, const Range &i) {
+        return o.who == i.who && o.lo == i.lo + (uintptr_t)o.who * ob;
+    }));
+    return execute([&](const PlanOptions &o) { return plan_reduce_scatter(n, dt, R, o); }, in_place,
+                   Buffers{send, recv, nullptr}, stream, noalloc);
+}
 
 extern "C" {
 
@@ -1051,25 +1104,12 @@ hoccl_status_t hoccl_allreduce(const void *const *send, void *const *recv, size_
 
 hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv, size_t n,
                                     hoccl_dtype_t dt, int R, hipStream_t stream) {
-    TRY(check_common(send, recv, dt, R));
-    if (n == 0) return HOCCL_OK;
-    TRY(check_ptrs(send, R, "send"));
-    TRY(check_ptrs((const void *const *)recv, R, "recv"));
-    size_t es = dtype_size(dt);
-    if (size_overflows(n, es * (size_t)R)) return HOCCL_ERR_INVALID_ARG;
-    size_t ob = n * es, ib = (size_t)R * n * es;
-    std::vector<Range> outs, ins;
-    bool in_place = true;
-    for (int r = 0; r < R; ++r) {
-        outs.push_back({(uintptr_t)recv[r], (uintptr_t)recv[r] + ob, r, true});
-        ins.push_back({(uintptr_t)send[r], (uintptr_t)send[r] + ib, r, false});
-        in_place &= ((const char *)recv[r] == (const char *)send[r] + (size_t)r * ob);
-    }
-    TRY(check_overlaps(outs, ins, [ob](const Range &o, const Range &i) {
-        return o.who == i.who && o.lo == i.lo + (uintptr_t)o.who * ob;
-    }));
-    return execute([&](const PlanOptions &o) { return plan_reduce_scatter(n, dt, R, o); }, in_place,
-                   Buffers{send, recv, nullptr}, stream);
+    return reduce_scatter_impl(send, recv, n, dt, R, stream, false);
+}
+
+hoccl_status_t hoccl_reduce_scatter_noalloc(const void *const *send, void *const *recv, size_t n,
+                                            hoccl_dtype_t dt, int R, hipStream_t stream) {
+    return reduce_scatter_impl(send, recv, n, dt, R, stream, true);
 }
 
 hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv, size_t n,

@@ -208,4 +208,9 @@ size_t fold_elems_per_thread(hoccl_dtype_t dt);
 size_t copy_bytes_per_thread();
 hipError_t launch_handshake(const HandshakeArgs &a, hipStream_t s);
 
+// The static device scratch of hoccl_reduce_scatter_noalloc (scratch.hip):
+// its size, and this device's address of it (call with the device current).
+constexpr size_t kScratchBytes = (size_t)128 << 20;
+hipError_t scratch_address(void **out);
+
 }  // namespace hoccl
