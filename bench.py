@@ -477,7 +477,8 @@ def bench_allreduce(hc, W, reps, gemm):
     # (each call queued behind a spin), with the cache warm and flushed.
     dev = {}
     for name, kw in (("kernel", {"copy_path": "kernel"}), ("hip", {"copy_path": "hip"}),
-                     ("engines", {"copy_path": "engines"}), ("direct_fold", {"reduce_algo": "direct"})):
+                     ("engines", {"copy_path": "engines"}), ("direct_fold", {"reduce_algo": "direct"}),
+                     ("auto", {"reduce_algo": "auto", "copy_path": "auto"})):
         with hc.config(**kw):
             warm, _ = queued_time(lambda: hc.allreduce(send, recv), reps, flush=False)
             cold, _ = queued_time(lambda: hc.allreduce(send, recv), reps, flush=True)
@@ -677,6 +678,52 @@ def bench_rs_variants(hc, reps):
     out["workload"] = ("ring reduce-scatter, 25,165,824 elements per rank: fp32 and int32 at R=8; "
                        "bf16 at other R (the headline is bf16 at R=8)")
     return out
+
+
+def bench_fused_hops(hc, send_np, steps, warmup):
+    """The headline ring reduce-scatter with k ring hops folded per launch
+    (fused_hops = k; k = 7 folds a whole chunk in one launch): algorithmic
+    bytes against time.  Per point: HIP events on the launching stream over
+    `steps` back-to-back calls, as for the headline, and per-launch kernel
+    times from the library's kernel timing."""
+    import torch
+    R = len(send_np)
+    n = send_np[0].size // R
+    send = [bf16_dev(a) for a in send_np]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    stream = torch.cuda.current_stream()
+    out = {}
+    for k in (1, 2, 4, 7):
+        with hc.config(reduce_algo="ring", fused_hops=k, kernel_timing=0):
+            def step():
+                hc.reduce_scatter(send, recv, stream=stream)
+            for _ in range(warmup):
+                step()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(steps):
+                step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            st = hc.last_stats()
+            t = e0.elapsed_time(e1) / 1e3 / steps
+            hc.set_config(kernel_timing=1)
+            hc.kernel_times()
+            for _ in range(10):
+                step()
+            kt = hc.kernel_times()
+            hc.set_config(kernel_timing=0)
+        b = st["hbm_bytes_algorithmic"]
+        L = st["reduce_launches"]
+        out[f"k{k}"] = dict(hops_per_launch=k, launches=L, bytes_per_op=b,
+                            bytes_per_element=round(b / (R * n), 3), us=round(t * 1e6, 2),
+                            algbw_GBs=round(R * n * 2 / t / 1e9, 1), achieved_GBs=round(b / t / 1e9, 1),
+                            frac=round(b / t / 1e9 / HBM_PEAK_GBS, 4),
+                            launch_us=[round(statistics.mean(kt[i::L]) * 1e3, 2) for i in range(L)])
+    return dict(workload="ring reduce-scatter bf16 R=8, 25,165,824 elements per rank, k ring hops "
+                         "folded per launch (bit-identical to k = 1)", **out)
 
 
 def bench_rs_graph(hc, send_np, steps):
@@ -1134,6 +1181,11 @@ def main():
             extra["reduce_scatter_variants"] = bench_rs_variants(hc, 10)
         except Exception as e:
             extra["reduce_scatter_variants"] = {"error": repr(e)}
+        log("reduce-scatter with fused ring hops")
+        try:
+            extra["reduce_scatter_fused_hops"] = bench_fused_hops(hc, rs["x"], args.steps, args.warmup)
+        except Exception as e:
+            extra["reduce_scatter_fused_hops"] = {"error": repr(e)}
         log("reduce-scatter in a graph")
         try:
             extra["reduce_scatter_graph"] = bench_rs_graph(hc, rs["x"], args.steps)

@@ -209,6 +209,15 @@ typedef struct {
                                    ends; the proxy then reports
                                    HOCCL_ERR_TIMEOUT at the next SDMA call.
                                    0 = 2 * proxy_timeout_ms + 1 s              */
+    int fused_hops;             /* ring reduce-scatter / all-reduce: ring hops
+                                   folded per reduction launch, 0..64 (0 and
+                                   1: one hop per launch; at most 8 per
+                                   launch are used).  A fused launch adds its
+                                   hops' contributions to the partial in
+                                   registers, in the ring's order (same
+                                   bits), and reads and writes the partial
+                                   once instead of once per hop; R-1 hops
+                                   fold the whole chunk in one launch      */
 } hoccl_config_t;
 
 /* The first eight fields are the core statistics; the rest extend them. */
@@ -248,8 +257,8 @@ typedef struct {
  *   HOCCL_WG_PER_STEP, HOCCL_THREADS_PER_WG, HOCCL_CHUNK_BYTES,
  *   HOCCL_COPY_STREAMS, HOCCL_SDMA_ENGINES, HOCCL_AG_DIRECT,
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
- *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES (the fields of the
- *   same meaning),
+ *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES, HOCCL_FUSED_HOPS
+ *   (the fields of the same meaning),
  *   HOCCL_COPY_PATH = auto | sdma (or engines) | kernel | hip,
  *   HOCCL_REDUCE_ALGO = ring | direct | auto,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),

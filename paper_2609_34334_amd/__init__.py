@@ -53,7 +53,8 @@ class Config(ctypes.Structure):
                 ("proxy_timeout_ms", ctypes.c_uint),
                 ("proxy_handshake", ctypes.c_int),
                 ("ring_group_bytes", ctypes.c_size_t),
-                ("proxy_wait_limit_us", ctypes.c_uint)]
+                ("proxy_wait_limit_us", ctypes.c_uint),
+                ("fused_hops", ctypes.c_int)]
 
 
 class Stats(ctypes.Structure):

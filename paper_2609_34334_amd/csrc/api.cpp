@@ -113,6 +113,7 @@ hoccl_config_t default_config() {
     c.proxy_handshake = -1;
     c.ring_group_bytes = 0;
     c.proxy_wait_limit_us = 0;
+    c.fused_hops = 1;
     return c;
 }
 
@@ -129,6 +130,7 @@ bool config_valid(const hoccl_config_t &c) {
     if ((int)c.reduce_algo < HOCCL_REDUCE_RING || (int)c.reduce_algo > HOCCL_REDUCE_AUTO) return false;
     if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
     if (c.proxy_handshake < -1 || c.proxy_handshake > 2) return false;
+    if (c.fused_hops < 0 || c.fused_hops > kMaxRanks) return false;
     return true;
 }
 
@@ -153,6 +155,7 @@ void load_config_locked() {
     c.kernel_timing = (int)env_long("HOCCL_KERNEL_TIMING", c.kernel_timing);
     c.proxy_handshake = (int)env_long("HOCCL_PROXY_HANDSHAKE", c.proxy_handshake);
     c.proxy_wait_limit_us = (unsigned)env_long("HOCCL_PROXY_WAIT_LIMIT_US", c.proxy_wait_limit_us);
+    c.fused_hops = (int)env_long("HOCCL_FUSED_HOPS", c.fused_hops);
     if (const char *v = std::getenv("HOCCL_RING_GROUP_BYTES")) c.ring_group_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "hip")) c.copy_path = HOCCL_COPY_HIP;
@@ -354,7 +357,7 @@ int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan
     for (const ReduceStep &s : p.reduce_steps) {
         unsigned long long n = 0;
         for (const ReduceSeg &g : s.segs) n += g.n;
-        need(n, reduce_step_elems_per_thread(p.dtype, s.phase));
+        need(n, s.hops > 1 ? multihop_elems_per_thread(p.dtype) : reduce_step_elems_per_thread(p.dtype, s.phase));
     }
     if (p.has_fold) need(p.fold.total, fold_elems_per_thread(p.dtype));
     if (cfg.copy_path == HOCCL_COPY_KERNEL)
@@ -394,7 +397,29 @@ hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const 
                               bool record_groups, const std::vector<hipEvent_t> *gates = nullptr) {
     for (size_t i = 0; i < p.reduce_steps.size(); ++i) {
         const ReduceStep &step = p.reduce_steps[i];
-        for (size_t b = 0; b < step.segs.size(); b += kMaxReduceSegs) {
+        // A fused step: every segment's partial plus its contributions in
+        // order, up to kMaxMultiSegs segments per launch.
+        for (size_t b = 0; step.hops > 1 && b < step.segs.size(); b += kMaxMultiSegs) {
+            MultiArgs a;
+            std::memset(&a, 0, sizeof a);
+            int ns = (int)std::min<size_t>(kMaxMultiSegs, step.segs.size() - b);
+            for (int k = 0; k < ns; ++k) {
+                const ReduceSeg &g = step.segs[b + (size_t)k];
+                a.seg[k].in0 = resolve(g.in0, B);
+                a.seg[k].loc[0] = resolve(g.in1, B);
+                for (size_t m = 0; m < g.more.size(); ++m) a.seg[k].loc[m + 1] = resolve(g.more[m], B);
+                a.seg[k].nloc = 1 + (int)g.more.size();
+                a.seg[k].out = resolve(g.out, B);
+                a.seg[k].n = g.n;
+            }
+            a.nseg = ns;
+            TimingPair *tp;
+            TRY(timed_begin(st, cfg, s, &tp));
+            HIP_TRY(launch_multihop(p.dtype, step.phase, a, wg, threads, s));
+            TRY(timed_end(tp, s));
+            t_stats.reduce_launches++;
+        }
+        for (size_t b = 0; step.hops == 1 && b < step.segs.size(); b += kMaxReduceSegs) {
             ReduceArgs a;
             std::memset(&a, 0, sizeof a);
             int ns = (int)std::min<size_t>(kMaxReduceSegs, step.segs.size() - b);
@@ -893,6 +918,7 @@ PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
     o.chunk_bytes = cfg.chunk_bytes;
     o.in_place = in_place;
     o.algo = cfg.reduce_algo;
+    o.fused_hops = cfg.fused_hops;
     return o;
 }
 

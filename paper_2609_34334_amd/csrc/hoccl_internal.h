@@ -43,17 +43,25 @@ enum Phase : int {
 
 struct ReduceSeg {
     BufRef in0, in1, out;
+    std::vector<BufRef> more;  // further contributions, added after in1 in order
     size_t n = 0;  // elements
 };
 
 // One ring step: every rank adds its contribution to the partial it
-// received; one kernel launch covers all ranks' segments of the step.
+// received; one kernel launch covers all ranks' segments of the step.  A
+// fused step folds `hops` consecutive ring hops in one launch: each segment
+// adds in1 and then the `more` contributions to its partial, which stays in
+// registers between the adds.
 struct ReduceStep {
     Phase phase = PH_MIDDLE;
     int group = 0;
-    int step = 0;
+    int step = 0;   // the first ring hop the launch performs
+    int hops = 1;
     std::vector<ReduceSeg> segs;
 };
+
+// Ring hops one fused launch may fold (contributions per segment).
+constexpr int kMaxHops = 8;
 
 // Direct reduction: one launch folds all R inputs of every chunk in the ring
 // order.  Chunk j spans elements [j*c, min(total, (j+1)*c)) of the inputs;
@@ -105,6 +113,8 @@ struct PlanOptions {
     // at most this many bytes (0: one group), so that they stay in the
     // last-level cache from one step to the next.
     size_t group_partial_bytes = 0;
+    // Ring hops per reduction launch (0 or 1: one; at most kMaxHops).
+    int fused_hops = 1;
 };
 
 // HOCCL_REDUCE_AUTO folds directly up to this many ranks.  On one GPU the
@@ -160,6 +170,23 @@ struct ReduceArgsT {
 };
 using ReduceArgs = ReduceArgsT<kMaxReduceSegs>;
 
+// A fused step's segment: the partial (or first operand) in0, then nloc
+// contributions loc[0..nloc) added in order, into out.
+struct MSegArg {
+    const void *in0;
+    const void *loc[kMaxHops];
+    void *out;
+    uint64_t n;
+    int nloc;
+};
+constexpr int kMaxMultiSegs = 32;  // 32 segments: 3.1 KiB of arguments
+template <int CAP>
+struct MultiArgsT {
+    MSegArg seg[CAP];
+    int nseg;
+};
+using MultiArgs = MultiArgsT<kMaxMultiSegs>;
+
 struct CSegArg {
     const void *src;
     void *dst;
@@ -199,12 +226,15 @@ hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, i
                               int threads, hipStream_t s);
 hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
                        hipStream_t s);
+hipError_t launch_multihop(hoccl_dtype_t dt, Phase ph, const MultiArgs &a, int wg, int threads,
+                           hipStream_t s);
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s);
 
 // Work one thread does in one pass of each kernel's main loop (elements of
 // the collective's dtype, or bytes for the copy kernel).
 size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph);
 size_t fold_elems_per_thread(hoccl_dtype_t dt);
+size_t multihop_elems_per_thread(hoccl_dtype_t dt);
 size_t copy_bytes_per_thread();
 hipError_t launch_handshake(const HandshakeArgs &a, hipStream_t s);
 

@@ -228,6 +228,126 @@ __global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgsT<CAP>) {
     });
 }
 
+// ---- fused ring hops ---------------------------------------------------------------
+// One launch folds several consecutive ring hops of every segment: the
+// partial (or, on the ring's first hop, the previous rank's own element) is
+// loaded once, the nloc contributions are added to it in the ring's order
+// while it stays in registers, and the result is stored once.  The adds are
+// the ring's adds in the ring's order, so the bits are the ring's; only the
+// partial's round trips through memory between the fused hops are gone.
+// nloc is the same for every lane, so the guards on the unrolled
+// contribution loop are uniform branches.
+template <class T0, class T1, class TO, int VE, int U, int NT, int MAXL>
+__device__ __forceinline__ void multihop_segment(const MSegArg &s, int lb, int nb) {
+    constexpr bool NT0 = NT & 1, NT1 = NT & 2, NTO = NT & 4;
+    using S0 = typename T0::S;
+    using S1 = typename T1::S;
+    using SO = typename TO::S;
+    using A = typename T1::A;
+    using P0 = Pack<S0, VE>;
+    using P1 = Pack<S1, VE>;
+    using PO = Pack<SO, VE>;
+    const S0 *in0 = (const S0 *)s.in0;
+    SO *out = (SO *)s.out;
+    const int nl = s.nloc;
+    const uint64_t n = s.n;
+    const S1 *loc[MAXL];
+#pragma unroll
+    for (int m = 0; m < MAXL; ++m) loc[m] = m < nl ? (const S1 *)s.loc[m] : (const S1 *)s.loc[0];
+
+    // Elements before the first contribution reaches 16-byte alignment; the
+    // vector body needs every operand 16-byte aligned at the same element.
+    uint64_t h = ((16u - ((uintptr_t)loc[0] & 15u)) & 15u) / sizeof(S1);
+    if (h > n) h = n;
+    uintptr_t mis = (uintptr_t)(in0 + h) | (uintptr_t)(out + h);
+#pragma unroll
+    for (int m = 0; m < MAXL; ++m) mis |= (uintptr_t)(loc[m] + h);
+    if (mis & 15u) h = n;
+    const uint64_t nv = (n - h) / VE;
+    const uint64_t tail = h + nv * VE;
+
+    const uint64_t bd = blockDim.x;
+    const uint64_t t = (uint64_t)lb * bd + threadIdx.x;
+    const uint64_t stride = (uint64_t)nb * bd;
+    auto scalar = [&](uint64_t k) {
+        A acc = T0::widen(in0[k]);
+#pragma unroll
+        for (int m = 0; m < MAXL; ++m)
+            if (m < nl) acc = acc + T1::widen(loc[m][k]);
+        out[k] = TO::narrow(acc);
+    };
+    for (uint64_t k = t; k < h; k += stride) scalar(k);
+    for (uint64_t k = tail + t; k < n; k += stride) scalar(k);
+
+    const P0 *v0 = (const P0 *)(in0 + h);
+    const P1 *vl[MAXL];
+#pragma unroll
+    for (int m = 0; m < MAXL; ++m) vl[m] = (const P1 *)(loc[m] + h);
+    PO *vo = (PO *)(out + h);
+    auto one = [&](uint64_t i) {
+        P0 a = ldp<NT0>(v0 + i);
+        P1 b[MAXL];
+#pragma unroll
+        for (int m = 0; m < MAXL; ++m)
+            if (m < nl) b[m] = ldp<NT1>(vl[m] + i);
+        A acc[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) acc[e] = T0::widen(a.v[e]);
+#pragma unroll
+        for (int m = 0; m < MAXL; ++m)
+            if (m < nl)
+#pragma unroll
+                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T1::widen(b[m].v[e]);
+        PO y;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) y.v[e] = TO::narrow(acc[e]);
+        stp<NTO>(vo + i, y);
+    };
+    // Main loop: U vectors of every operand per thread, all in range, every
+    // load issued before the adds consume them.
+    uint64_t base = (uint64_t)lb * bd * U + threadIdx.x;
+    for (; base + (uint64_t)(U - 1) * bd < nv; base += stride * U) {
+        P0 a[U];
+        P1 b[U][MAXL];
+#pragma unroll
+        for (int u = 0; u < U; ++u) a[u] = ldp<NT0>(v0 + base + (uint64_t)u * bd);
+#pragma unroll
+        for (int m = 0; m < MAXL; ++m)
+            if (m < nl)
+#pragma unroll
+                for (int u = 0; u < U; ++u) b[u][m] = ldp<NT1>(vl[m] + base + (uint64_t)u * bd);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            A acc[VE];
+#pragma unroll
+            for (int e = 0; e < VE; ++e) acc[e] = T0::widen(a[u].v[e]);
+#pragma unroll
+            for (int m = 0; m < MAXL; ++m)
+                if (m < nl)
+#pragma unroll
+                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T1::widen(b[u][m].v[e]);
+            PO y;
+#pragma unroll
+            for (int e = 0; e < VE; ++e) y.v[e] = TO::narrow(acc[e]);
+            stp<NTO>(vo + base + (uint64_t)u * bd, y);
+        }
+    }
+    // At most one partial iteration is left for this thread.
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        uint64_t i = base + (uint64_t)u * bd;
+        if (i < nv) one(i);
+    }
+}
+
+template <class T0, class T1, class TO, int VE, int U, int NT, int MAXL, int CAP>
+__global__ void __launch_bounds__(1024) multihop_kernel(MultiArgsT<CAP>) {
+    const MultiArgsT<CAP> &a = kernargs<MultiArgsT<CAP>>();
+    for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
+        multihop_segment<T0, T1, TO, VE, U, NT, MAXL>(a.seg[seg], lb, nb);
+    });
+}
+
 // ---- direct fold ------------------------------------------------------------------
 // Chunk j reads x[(j+1)%R], x[(j+2)%R], ..., x[j] at the chunk's elements and
 // adds them left to right; loads are issued in batches of KB ranks so several
@@ -433,6 +553,13 @@ static ReduceArgsT<CAP> fit(const ReduceArgs &a) {
     return b;
 }
 template <int CAP>
+static MultiArgsT<CAP> fit(const MultiArgs &a) {
+    MultiArgsT<CAP> b{};
+    for (int k = 0; k < a.nseg; ++k) b.seg[k] = a.seg[k];
+    b.nseg = a.nseg;
+    return b;
+}
+template <int CAP>
 static CopyArgsT<CAP> fit(const CopyArgs &a) {
     CopyArgsT<CAP> b{};
     for (int k = 0; k < a.nseg; ++k) b.seg[k] = a.seg[k];
@@ -510,6 +637,61 @@ hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, i
     }
     return hipErrorInvalidValue;
 }
+
+// Fused ring hops.  Every lane moves 4 elements of every operand (8 bytes of
+// bf16, 16 of fp32 / int32), and keeps U such vectors of each operand in
+// flight, U chosen per bound on the contributions so that the registers
+// they need stay within the 128 VGPRs a 1024-thread launch bound allows
+// without spilling: bf16 2 whatever the bound; 32-bit types 4, 2 and 1 for
+// at most 2, 4 and 8 contributions.
+template <class T0, class T1, class TO, int NT, int MAXL>
+static hipError_t launch_mh_l(const MultiArgs &a, int wg, int threads, hipStream_t s) {
+    constexpr int U = sizeof(typename T1::S) == 2 ? 2 : (MAXL <= 2 ? 4 : (MAXL <= 4 ? 2 : 1));
+    if (a.nseg <= kSmallSegs)
+        return launch((const void *)multihop_kernel<T0, T1, TO, 4, U, NT, MAXL, kSmallSegs>,
+                      fit<kSmallSegs>(a), wg, threads, s);
+    return launch((const void *)multihop_kernel<T0, T1, TO, 4, U, NT, MAXL, kMaxMultiSegs>, a, wg, threads,
+                  s);
+}
+
+template <class T0, class T1, class TO, int NT>
+static hipError_t launch_mh(const MultiArgs &a, int wg, int threads, hipStream_t s) {
+    int nl = 0;
+    for (int k = 0; k < a.nseg; ++k) nl = a.seg[k].nloc > nl ? a.seg[k].nloc : nl;
+    if (nl <= 2) return launch_mh_l<T0, T1, TO, NT, 2>(a, wg, threads, s);
+    if (nl <= 4) return launch_mh_l<T0, T1, TO, NT, 4>(a, wg, threads, s);
+    return launch_mh_l<T0, T1, TO, NT, kMaxHops>(a, wg, threads, s);
+}
+
+hipError_t launch_multihop(hoccl_dtype_t dt, Phase ph, const MultiArgs &a, int wg, int threads,
+                           hipStream_t s) {
+    if (dt == HOCCL_BF16) {
+        switch (ph) {
+        case PH_FIRST: return launch_mh<TBF16, TBF16, TF32, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_mh<TF32, TBF16, TF32, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_mh<TF32, TBF16, TBF16, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_mh<TBF16, TBF16, TBF16, kNtOnly>(a, wg, threads, s);
+        }
+    } else if (dt == HOCCL_FP32) {
+        switch (ph) {
+        case PH_FIRST: return launch_mh<TF32, TF32, TF32, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_mh<TF32, TF32, TF32, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_mh<TF32, TF32, TF32, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_mh<TF32, TF32, TF32, kNtOnly>(a, wg, threads, s);
+        }
+    } else if (dt == HOCCL_INT32) {
+        switch (ph) {
+        case PH_FIRST: return launch_mh<TI32, TI32, TI32, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_mh<TI32, TI32, TI32, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_mh<TI32, TI32, TI32, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_mh<TI32, TI32, TI32, kNtOnly>(a, wg, threads, s);
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+// Grid sizing for fused launches assumes 2 vectors of 4 elements per pass.
+size_t multihop_elems_per_thread(hoccl_dtype_t) { return 8; }
 
 // Elements one thread covers in one pass of each kernel's main loop; the
 // executor sizes automatic launches to about one pass per thread.

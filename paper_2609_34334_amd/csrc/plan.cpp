@@ -113,17 +113,29 @@ static void finish_chains(Plan &p) {
 // partial of element e lives at workspace element e (a mirror of the input
 // index space) so it keeps the inputs' vector alignment.  Rank j's result
 // goes to recv[j] at element out_base(j) + (e - j * stride).
+//
+// With H hops per launch, one launch performs ring hops s0 .. s0+H-1 for
+// every chunk: chunk j's operands in fold order are x[j+1], x[j+2], ...,
+// x[j] (rank indices mod R); hop s adds operand s+1 (rank j+s+2), the
+// addition rank j+s+2 performs in the ring.  So a fused launch reads the
+// partial once (on the first hop: x[j+1] itself), adds its H operands in
+// that order and writes once.  H = 1 is the ring step itself; H >= R-1 folds
+// every operand in one launch.
 static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
                         const std::vector<size_t> &chunk_len, size_t g0, size_t glen,
-                        int group, bool out_at_chunk) {
+                        int group, bool out_at_chunk, int H) {
     size_t es = dtype_size(dt), as = acc_size(dt);
-    for (int s = 0; s <= R - 2; ++s) {
+    for (int s0 = 0; s0 <= R - 2; s0 += H) {
+        const int s1 = std::min(s0 + H, R - 1);  // hops s0 .. s1-1
+        const bool first = s0 == 0, last = s1 == R - 1;
         ReduceStep st;
         st.group = group;
-        st.step = s;
-        st.phase = (R == 2) ? PH_ONLY : (s == 0 ? PH_FIRST : (s == R - 2 ? PH_LAST : PH_MIDDLE));
+        st.step = s0;
+        st.hops = s1 - s0;
+        st.phase = first ? (last ? PH_ONLY : PH_FIRST) : (last ? PH_LAST : PH_MIDDLE);
         for (int r = 0; r < R; ++r) {
-            int j = mod(r - s - 2, R);
+            // The rank performing hop s0 of chunk j is r = j + s0 + 2.
+            int j = mod(r - s0 - 2, R);
             size_t L = chunk_len[(size_t)j];
             if (g0 >= L) continue;
             size_t n = std::min(glen, L - g0);
@@ -131,21 +143,27 @@ static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
             ReduceSeg sg;
             sg.n = n;
             sg.in1 = ref(BUF_SEND, r, e * es);
-            if (s == 0)
+            for (int h = s0 + 1; h < s1; ++h) sg.more.push_back(ref(BUF_SEND, mod(j + h + 2, R), e * es));
+            if (first)
                 sg.in0 = ref(BUF_SEND, mod(r - 1, R), e * es);
             else
                 sg.in0 = ref(BUF_WS, 0, e * as);
-            if (s == R - 2) {
+            if (last) {
                 size_t oe = out_at_chunk ? g0 : e;
                 sg.out = ref(BUF_RECV, j, oe * es);
             } else {
                 sg.out = ref(BUF_WS, 0, e * as);
             }
-            p.hbm_bytes += seg_bytes(dt, st.phase, n);
-            st.segs.push_back(sg);
+            p.hbm_bytes += seg_bytes(dt, st.phase, n) + (unsigned long long)n * es * sg.more.size();
+            st.segs.push_back(std::move(sg));
         }
         if (!st.segs.empty()) p.reduce_steps.push_back(std::move(st));
     }
+}
+
+// Hops per ring launch from the option (0 and 1: one), at most kMaxHops.
+static int hops_per_launch(const PlanOptions &o) {
+    return std::max(1, std::min(o.fused_hops, kMaxHops));
 }
 
 // Groups a ring reduction over chunks of c elements is split into so that
@@ -187,8 +205,10 @@ Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o
     const int G = cache_groups(R, n, dt, o.group_partial_bytes);
     const size_t gl = (n + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;
-    for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, n, len, (size_t)g * gl, gl, g, true);
-    p.ws_bytes = (R > 2) ? (size_t)R * n * acc_size(dt) : 0;
+    const int H = hops_per_launch(o);
+    for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, n, len, (size_t)g * gl, gl, g, true, H);
+    // Partials cross launches only when the hops take more than one.
+    p.ws_bytes = (R - 1 > H) ? (size_t)R * n * acc_size(dt) : 0;
     return p;
 }
 
@@ -232,7 +252,8 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
     if ((size_t)G > c) G = (int)c;
     size_t cg = (c + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;
-    for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, c, len, (size_t)g * cg, cg, g, false);
+    const int H = hops_per_launch(o);
+    for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, c, len, (size_t)g * cg, cg, g, false, H);
     // Gather phase: chunk j (group g) travels j -> j+1 -> ... -> j-1.
     int maxp = 1;
     for (int g = 0; g < G; ++g)
@@ -259,7 +280,7 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
                          o.allgather_direct ? 0 : s, o.chunk_bytes, maxp);
             }
         }
-    p.ws_bytes = (R > 2) ? (size_t)R * c * acc_size(dt) : 0;
+    p.ws_bytes = (R - 1 > H) ? (size_t)R * c * acc_size(dt) : 0;
     finish_chains(p);
     return p;
 }
@@ -399,7 +420,7 @@ std::string plan_to_json(const Plan &p) {
         const auto &s = p.reduce_steps[i];
         if (i) os << ",";
         os << "{\"phase\":\"" << phases[s.phase] << "\",\"group\":" << s.group
-           << ",\"step\":" << s.step << ",\"segs\":[";
+           << ",\"step\":" << s.step << ",\"hops\":" << s.hops << ",\"segs\":[";
         for (size_t k = 0; k < s.segs.size(); ++k) {
             const auto &g = s.segs[k];
             if (k) os << ",";
@@ -407,7 +428,12 @@ std::string plan_to_json(const Plan &p) {
             put_ref(os, g.in0);
             os << ",\"in1\":";
             put_ref(os, g.in1);
-            os << ",\"out\":";
+            os << ",\"more\":[";
+            for (size_t m = 0; m < g.more.size(); ++m) {
+                if (m) os << ",";
+                put_ref(os, g.more[m]);
+            }
+            os << "],\"out\":";
             put_ref(os, g.out);
             os << ",\"n\":" << g.n << "}";
         }

@@ -57,7 +57,16 @@ void replay(const Plan &p, const Bufs &B) {
         size_t eo = (st.phase == PH_LAST || st.phase == PH_ONLY) ? es : as;
         for (const ReduceSeg &g : st.segs) {
             char *in0 = at(g.in0, B), *in1 = at(g.in1, B), *out = at(g.out, B);
-            for (size_t i = 0; i < g.n; ++i) mix(out + i * eo, in0 + i * e0, in1 + i * es, eo, e0, es);
+            std::vector<char *> more;
+            for (const BufRef &m : g.more) more.push_back(at(m, B));
+            for (size_t i = 0; i < g.n; ++i) {
+                // the partial is read first; a fused step's further
+                // contributions are read before the output is written
+                char acc[8] = {0};
+                mix(acc, in0 + i * e0, in1 + i * es, eo, e0, es);
+                for (char *m : more) mix(acc, acc, m + i * es, eo, eo, es);
+                std::memcpy(out + i * eo, acc, eo);
+            }
         }
     }
     if (p.has_fold) {
@@ -139,6 +148,14 @@ int main() {
                                     run(plan_allgather(n, dt, R, o), R, n * es, (size_t)R * n * es, ip ? 1 : 0);
                                 }
                                 run(plan_reduce_scatter(n, dt, R, o), R, (size_t)R * n * es, n * es, ip ? 2 : 0);
+                                if (algo == 0)
+                                    for (int hops : {3, 64}) {  // fused ring hops
+                                        PlanOptions f = o;
+                                        f.fused_hops = hops;
+                                        run(plan_allreduce(n, dt, R, f), R, n * es, n * es, ip ? 3 : 0);
+                                        run(plan_reduce_scatter(n, dt, R, f), R, (size_t)R * n * es, n * es,
+                                            ip ? 2 : 0);
+                                    }
                                 if (ip) continue;
                                 std::vector<int> shift((size_t)R), rev((size_t)R);
                                 for (int r = 0; r < R; ++r) {

@@ -19,10 +19,14 @@ def _defaults():
     hc.set_config(**saved)
 
 
-@pytest.mark.parametrize("algo", ["ring", "direct"])
+@pytest.mark.parametrize("algo", ["ring", "direct", "fused2", "fused4", "fused7"])
 def test_reduce_scatter_gradient_bucket(algo):
-    """bf16, R=8, 25,165,824 elements per rank: every output element."""
-    hc.set_config(reduce_algo=algo)
+    """bf16, R=8, 25,165,824 elements per rank: every output element; the
+    ring also with 2, 4 and 7 hops fused per launch."""
+    if algo.startswith("fused"):
+        hc.set_config(reduce_algo="ring", fused_hops=int(algo[5:]))
+    else:
+        hc.set_config(reduce_algo=algo)
     R, n_in = 8, 25_165_824
     x = W.rs_gradients(R, n_in)
     ref = oracle.reduce_scatter_new(x, hc.BF16)
@@ -46,7 +50,7 @@ def test_allreduce_fp32_R4(path, algo):
         assert_bitwise(from_dev(recv[r], hc.FP32), ref[r], f"rank {r}")
 
 
-@pytest.mark.parametrize("path", ["hip", "engines"])
+@pytest.mark.parametrize("path", ["hip", "engines", "kernel"])
 def test_allgather_fsdp_block(path):
     """201,326,592 bf16 parameters over R=8: each rank's output is compared
     with the concatenation of the shards (the oracle's definition)."""

@@ -94,6 +94,41 @@ def test_auto_reduction_folds_and_matches_the_oracle(R):
             assert_bitwise(gota[r], refa[r], f"AUTO AR {NAME[dt]} R={R} r={r}")
 
 
+@pytest.mark.parametrize("hops", [2, 3, 4, 7, 64])
+@pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
+@pytest.mark.parametrize("R", [3, 4, 8, 13])
+def test_fused_ring_hops(hops, dt, R):
+    """The ring with several hops folded per launch gives the oracle's bits
+    (the ring's order), ragged, with misaligned outputs and with inputs
+    misaligned against each other, and takes ceil((R-1)/k) launches of at
+    most 8 hops each."""
+    hc.set_config(reduce_algo="ring", fused_hops=hops, copy_path="hip")
+    k = min(hops, 8)
+    for n in [1, 7, R * 37 + 3, 65536 + 5]:
+        x = [W.random_values(NAME[dt], 740 + R + hops, r, R * n) for r in range(R)]
+        ref = oracle.reduce_scatter_new(x, dt)
+        got = run_rs(x, dt, lead=3)
+        assert hc.last_stats()["reduce_launches"] == -(-(R - 1) // k)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"fused RS k={hops} n={n} r={r}")
+        xa = [W.random_values(NAME[dt], 750 + R + hops, r, n) for r in range(R)]
+        refa = oracle.allreduce_new(xa, dt)
+        gota = run_ar(xa, dt, lead=1)
+        for r in range(R):
+            assert_bitwise(gota[r], refa[r], f"fused AR k={hops} n={n} r={r}")
+    # inputs at different offsets from 16-byte alignment (every operand of
+    # a launch must then take the element-wise path)
+    n = 4099
+    x = [W.random_values(NAME[dt], 760 + R, r, R * n) for r in range(R)]
+    ref = oracle.reduce_scatter_new(x, dt)
+    bufs = [to_dev(np.concatenate([np.zeros(r % 3, x[r].dtype), x[r]]), dt) for r in range(R)]
+    send = [bufs[r][r % 3:] for r in range(R)]
+    out = hc.reduce_scatter(send)
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(out[r], dt), ref[r], f"fused RS misaligned inputs k={hops} r={r}")
+
+
 @pytest.mark.parametrize("algo", ["ring", "direct"])
 @pytest.mark.parametrize("dt", DTS, ids=lambda d: NAME[d])
 @pytest.mark.parametrize("R", [1, 2, 3, 4, 8])

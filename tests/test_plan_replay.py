@@ -54,12 +54,14 @@ def replay(plan, send, recv):
         out_acc = ph in ("first", "middle")
         for g in st["segs"]:
             n = g["n"]
-            a = widen(region(g["in0"], n * (4 if in0_acc else es)).copy(), dt, in0_acc)
-            b = widen(region(g["in1"], n * es).copy(), dt, False)
-            if dt == hc.INT32:
-                r = (a.astype(np.uint64) + b.astype(np.uint64)) & 0xFFFFFFFF
-            else:
-                r = a + b
+            r = widen(region(g["in0"], n * (4 if in0_acc else es)).copy(), dt, in0_acc)
+            # a fused step adds in1 and then its further contributions in order
+            for ref in [g["in1"]] + g["more"]:
+                b = widen(region(ref, n * es).copy(), dt, False)
+                if dt == hc.INT32:
+                    r = (r.astype(np.uint64) + b.astype(np.uint64)) & 0xFFFFFFFF
+                else:
+                    r = r + b
             region(g["out"], n * (4 if out_acc else es))[:] = narrow(r, dt, out_acc)
     f = plan["fold"]
     if f is not None:
@@ -100,6 +102,10 @@ CONFIGS = [
     dict(reduce_algo="direct"),
     dict(ring_group_bytes=1000),                      # many cache groups, ragged last group
     dict(ring_group_bytes=4096, allreduce_chunk_groups=2, chunk_bytes=4096),
+    dict(fused_hops=2),                               # fused ring hops, a one-hop remainder at R=4, 8
+    dict(fused_hops=3, ring_group_bytes=1000, allreduce_chunk_groups=2),
+    dict(fused_hops=64),                              # every hop in one launch (capped at 8 per launch)
+    dict(reduce_algo="auto"),
 ]
 
 
@@ -236,3 +242,19 @@ def test_automatic_allreduce_groups():
     assert {c["group"] for c in at["copies"]} == {0, 1}
     with hc.config(allreduce_chunk_groups=1):
         assert hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)["ngroups"] == 1
+
+
+@pytest.mark.parametrize("hops,per_element,launches", [(1, 66, 7), (2, 42, 4), (4, 26, 2), (7, 18, 1)])
+def test_fused_hops_bytes_and_launches(hops, per_element, launches):
+    """bf16 at R = 8, bytes per element of each chunk, worked out by hand:
+    one hop per launch 8 + 5*10 + 8 = 66; two, hops [0,2) [2,4) [4,6) [6,7):
+    (3*2 + 4) + 2*(4 + 2*2 + 4) + (4 + 2 + 2) = 42; four, [0,4) [4,7):
+    (5*2 + 4) + (4 + 3*2 + 2) = 26; seven: 8*2 + 2 = 18, the direct fold's
+    bytes, with no partial in memory at all."""
+    n = 3_145_728
+    with hc.config(fused_hops=hops):
+        plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, 8)
+    assert plan["hbm_bytes"] == 8 * n * per_element
+    assert len(plan["reduce_steps"]) == launches
+    assert [s["hops"] for s in plan["reduce_steps"]] == [min(hops, 7 - k * hops) for k in range(launches)]
+    assert plan["ws_bytes"] == (0 if hops >= 7 else 8 * n * 4)
