@@ -329,8 +329,8 @@ def host_gate():
     return ev, open_gate
 
 
-def _gated(gemm, collective=None, n_coll=0):
-    """20 GEMMs and `n_coll` collectives (an event after each), all enqueued
+def _gated(gemm, collective=None, n_coll=0, k=20):
+    """k GEMMs and `n_coll` collectives (an event after each), all enqueued
     behind one host gate, which then opens so that both loops start
     together; then the host synchronises.  The host thread does the same
     thing while the GPU runs whether or not collectives are enqueued: GEMM
@@ -356,58 +356,148 @@ def _gated(gemm, collective=None, n_coll=0):
                     e = torch.cuda.Event(enable_timing=True)
                     e.record(cs)
                     ends.append(e)
-        _, _, ts = _gemm_run(gemm)
+        _, _, ts = _gemm_run(gemm, k)
     finally:
         blocked = open_gate()
     torch.cuda.synchronize()
     return c0, ends, ts, blocked
 
 
-def gemm_slowdown(hc, collective, med, gemm):
-    """Interference between `collective` looping on one queue and a bf16
-    GEMM loop on another.  GEMM i of the concurrent run is compared with
-    GEMM i of runs alone under the same gate, one before and one after
-    (GEMM time drifts as clocks settle, so position matters); only GEMMs
-    that ran entirely inside the collective window count.  The collective's own slowdown is its time per
-    call while the GEMMs ran (the calls that finished before the last GEMM,
-    from the common start) against `med`, its median time alone.  Returns
-    (median GEMM slowdown, fraction of the 20 GEMMs that overlapped,
-    collective slowdown, collectives queued).  A run whose enqueue held up
-    the host is void: it is repeated with half the collectives, twice at
-    most, and otherwise all three figures are None."""
+def _boot_ci(x, reps=4000, seed=1):
+    """Bootstrap 95% interval of the mean of x (resampling its items)."""
+    import numpy as np
+    x = np.asarray(x, dtype=np.float64)
+    rng = np.random.default_rng(seed)
+    means = x[rng.integers(0, len(x), size=(reps, len(x)))].mean(axis=1)
+    lo, hi = np.percentile(means, [2.5, 97.5])
+    return float(lo), float(hi)
+
+
+def interference(hc, collective, med, gemm, pairs=100, k=4, seed=0):
+    """Slowdown of a bf16 8192^3 GEMM loop on one queue while `collective`
+    loops on another, resolved by pairing.  Each of `pairs` pairs is one run
+    of k GEMMs alone and one run of k GEMMs beside back-to-back collectives,
+    both under the same host gate (so the host thread does the same in both
+    arms), in an order drawn at random per pair.  A pair's ratio is the mean
+    time of the GEMMs that ran entirely inside the collective window over
+    the mean time of the same GEMMs (by position) alone; adjacent runs
+    cancel the drift of the clocks.  Reports the mean ratio - 1 with a
+    bootstrap 95% interval over pairs, the collective's own slowdown (its
+    time per call while the GEMMs ran, against `med` alone; median over
+    pairs) and the pairs voided because the host was held up while
+    enqueueing (the collectives then could not start with the GEMMs)."""
+    import random
     import torch
     t_alone, cs = gemm[3], gemm[5]
-    n_coll = int(45 * t_alone / max(med, 1e-6)) + 3
+    n_coll = int(1.5 * k * t_alone / max(med, 1e-6)) + 2
     with torch.cuda.stream(cs):
         collective(cs)
-    for attempt in range(3):
-        _, _, before, b0 = _gated(gemm)
-        c0, ends, ts, b1 = _gated(gemm, collective, n_coll)
-        _, _, after, b2 = _gated(gemm)
-        if not (b0 or b1 or b2):
-            break
-        log(f"  the host was held up enqueueing {n_coll} collectives behind the gate: void")
-        if n_coll == 1:
-            break
-        n_coll = max(1, n_coll // 2)
-    if b0 or b1 or b2:
-        return None, None, None, n_coll
-    # GEMM i alone, averaged over a run before and a run after the
-    # concurrent one, so that a drift of the clocks across the three runs
-    # does not read as a slowdown or a speed-up.
-    base = [(a.elapsed_time(b) + c.elapsed_time(d)) / 2 for (a, b), (c, d) in zip(before, after)]
-    end = c0.elapsed_time(ends[-1])
-    ratios = [a.elapsed_time(b) / base[i] for i, (a, b) in enumerate(ts)
-              if c0.elapsed_time(a) >= 0 and c0.elapsed_time(b) <= end]
-    if not ratios:
-        return None, 0.0, None, n_coll
-    # The collective's calls that finished while the GEMMs still ran, timed
-    # from the common start: their mean time per call against `med`.  None
-    # when not even the first call finished before the last GEMM.
-    g_hi = c0.elapsed_time(ts[-1][1])
-    done = [t for t in (c0.elapsed_time(e) for e in ends) if t <= g_hi]
-    coll = round(done[-1] / len(done) / 1e3 / med - 1, 4) if done else None
-    return (round(statistics.median(ratios) - 1, 4), round(len(ratios) / len(ts), 3), coll, n_coll)
+    torch.cuda.synchronize()
+    rng = random.Random(seed)
+    ratios, colls, overlaps = [], [], []
+    void = 0
+    for _ in range(pairs):
+        order = [False, True] if rng.random() < 0.5 else [True, False]
+        runs = {}
+        for conc in order:
+            runs[conc] = _gated(gemm, collective if conc else None, n_coll if conc else 0, k)
+        if runs[True][3] or runs[False][3]:
+            void += 1
+            if void >= 3 and not ratios:
+                break
+            continue
+        c0, ends, ts, _ = runs[True]
+        alone = runs[False][2]
+        end = c0.elapsed_time(ends[-1])
+        inside = [i for i, (a, b) in enumerate(ts)
+                  if c0.elapsed_time(a) >= 0 and c0.elapsed_time(b) <= end]
+        overlaps.append(len(inside) / k)
+        if not inside:
+            continue
+        tc = statistics.mean(ts[i][0].elapsed_time(ts[i][1]) for i in inside)
+        ta = statistics.mean(alone[i][0].elapsed_time(alone[i][1]) for i in inside)
+        ratios.append(tc / ta)
+        g_hi = c0.elapsed_time(ts[-1][1])
+        done = [t for t in (c0.elapsed_time(e) for e in ends) if t <= g_hi]
+        if done:
+            colls.append(done[-1] / len(done) / 1e3 / med - 1)
+    out = dict(gemm_slowdown=None, gemm_slowdown_ci95=None, pairs=len(ratios), pairs_void=void,
+               gemms_per_run=k, gemm_overlap=round(statistics.mean(overlaps), 3) if overlaps else None,
+               collective_slowdown=round(statistics.median(colls), 4) if colls else None,
+               collectives_queued=n_coll)
+    if len(ratios) >= 2:
+        lo, hi = _boot_ci(ratios)
+        out.update(gemm_slowdown=round(statistics.mean(ratios) - 1, 4),
+                   gemm_slowdown_ci95=[round(lo - 1, 4), round(hi - 1, 4)])
+    if void and not ratios:
+        out["gemm_slowdown_void"] = ("the enqueueing thread was held up with the collectives queued "
+                                     "behind the gate, so they could not start with the GEMMs")
+    return out
+
+
+def null_interference(gemm, pairs=100, k=4, seed=0):
+    """The harness's resolution: the same pairs with nothing beside the
+    GEMMs in either arm (an A/A test).  Its interval should hold 0 and its
+    half-width is what `interference` can resolve."""
+    import random
+    rng = random.Random(seed)
+    ratios = []
+    for _ in range(pairs):
+        a = _gated(gemm, None, 0, k)
+        b = _gated(gemm, None, 0, k)
+        if a[3] or b[3]:
+            continue
+        if rng.random() < 0.5:
+            a, b = b, a
+        ta = statistics.mean(x.elapsed_time(y) for x, y in a[2])
+        tb = statistics.mean(x.elapsed_time(y) for x, y in b[2])
+        ratios.append(tb / ta)
+    lo, hi = _boot_ci(ratios)
+    return dict(gemm_slowdown=round(statistics.mean(ratios) - 1, 4),
+                gemm_slowdown_ci95=[round(lo - 1, 4), round(hi - 1, 4)], pairs=len(ratios), gemms_per_run=k)
+
+
+def interference_workload(hc, W, engines=(16, 8, 6, 4, 2), pairs=100):
+    """GEMM interference of the zero-CU copy collectives against the SDMA
+    engines they may use: the FSDP all-gather, the PP schedule and the EP
+    all-to-all(v) on the engine proxy beside the bf16 8192^3 GEMM, each at
+    several engine budgets, plus the harness's own null (A/A) interval."""
+    import torch
+    gemm = make_gemm()
+    out = {"gemm_alone_ms": round(gemm[3] * 1e3, 4), "null": null_interference(gemm, pairs)}
+    R = 8
+    x = W.ag_parameters(R)
+    ag_send = [bf16_dev(a) for a in x]
+    ag_recv = [torch.empty(R * x[0].size, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    p = W.p2p_activations(R)
+    pp_send = [bf16_dev(a) for a in p]
+    pp_recv = [torch.empty(p[0].size, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    fwd = [r + 1 if r + 1 < R else -1 for r in range(R)]
+    bwd = [r - 1 for r in range(R)]
+
+    def pp(s):
+        for _ in range(16):
+            hc.sendrecv(pp_send, pp_recv, fwd, stream=s)
+            hc.sendrecv(pp_send, pp_recv, bwd, stream=s)
+    send_np, counts, sd, rd, rsz = W.a2a_tokens(R)
+    a2a_send = [bf16_dev(a) for a in send_np]
+    a2a_recv = [torch.empty(q, dtype=torch.bfloat16, device="cuda") for q in rsz]
+    work = [("allgather_fsdp", lambda s: hc.allgather(ag_send, ag_recv, stream=s),
+             R * x[0].size * 2 * (R - 1)),
+            ("p2p_pp", pp, 224 * p[0].size * 2),
+            ("alltoallv_ep", lambda s: hc.alltoallv(a2a_send, counts, sd, a2a_recv, rd, stream=s),
+             sum(counts) * 2)]
+    for name, run, copied in work:
+        rows = {}
+        for E in engines:
+            with hc.config(copy_path="engines", sdma_engines=E):
+                med, _ = event_time(lambda: run(None), 5)
+                row = dict(ms=round(med * 1e3, 4), copy_GBs=round(copied / med / 1e9, 1))
+                row.update(interference(hc, run, med, gemm, pairs=pairs))
+            rows[f"engines{E}"] = row
+            log(f"  {name} engines={E}: {row['ms']} ms, GEMM {row['gemm_slowdown']} {row['gemm_slowdown_ci95']}")
+        out[name] = rows
+    return out
 
 
 def make_gemm():
@@ -428,11 +518,19 @@ def make_gemm():
 
 
 # Copy paths compared by the copy workloads.  "engines" is the engine proxy
-# with its default host-function handshake: what AUTO resolves to.
+# with its default host-function handshake and engine budget (4): what AUTO
+# resolves to; "engines16" the same on all 16 engines.
 PATHS = [("engines", {"copy_path": "engines"}),
+         ("engines16", {"copy_path": "engines", "sdma_engines": 16}),
          ("engines_kernel_handshake", {"copy_path": "engines", "proxy_handshake": 0}),
          ("hip", {"copy_path": "hip"}),
          ("kernel", {"copy_path": "kernel"})]
+
+
+# Paths whose GEMM interference is resolved with 100 pairs (the zero-CU
+# paths, whose target is a loss of at most 2%); the CU paths cost tens of
+# percent and get 20.
+INTERFERENCE_PATHS = ("engines", "engines16", "engines_ring", "auto")
 
 
 def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
@@ -449,11 +547,7 @@ def copy_paths(hc, run, S, f, reps, gemm=None, extra_paths=()):
                  path_used=hc.COPY_PATH_NAMES[st["copy_path_used"]],
                  cus_used=st["cus_used_max"], host_enqueue_us=round(st["host_enqueue_us"], 1))
         if gemm is not None:
-            (r["gemm_slowdown"], r["gemm_overlap"], r["collective_slowdown"],
-             r["collectives_queued"]) = gemm_slowdown(hc, run, med, gemm)
-            if r["gemm_overlap"] is None:
-                r["gemm_slowdown_void"] = ("the enqueueing thread was held up with the collectives queued "
-                                           "behind the gate, so they could not start with the GEMMs")
+            r.update(interference(hc, run, med, gemm, pairs=100 if name in INTERFERENCE_PATHS else 20))
         res[name] = r
         hc.set_config(**saved)
     return res
@@ -599,13 +693,15 @@ def _p2p_size_rows(hc, reps, big, big2):
         s0, d1 = big[:ne], big2[:ne]
         row = {"bytes": sz}
         for name, kw in [("hip", dict(copy_path="hip")), ("engines", dict(copy_path="engines")),
+                         ("engines16", dict(copy_path="engines", sdma_engines=16)),
                          ("engines_kernel_handshake", dict(copy_path="engines", proxy_handshake=0)),
                          ("engines_striped", dict(copy_path="engines", chunk_bytes=max(1 << 20, sz // 16)))] + \
                         [(f"kernel_wg{w}", dict(copy_path="kernel", workgroups_per_step=w)) for w in (1, 2, 4, 8, 64, 256)]:
             hc.set_config(**kw)
             med, _ = event_time(lambda: hc.sendrecv([s0, s0], [d1, d1], [1, -1]), reps)
             row[name] = round(sz / med / 1e9, 1)
-            hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0, proxy_handshake=-1)
+            hc.set_config(copy_path="auto", chunk_bytes=0, workgroups_per_step=0, proxy_handshake=-1,
+                          sdma_engines=0)
         rows.append(row)
     return rows
 
@@ -843,9 +939,8 @@ def bench_rs_workgroups(hc, x, reps, gemm=None):
                    hbm_GBs=round(st["hbm_bytes_algorithmic"] / med / 1e9, 1),
                    cus_used=st["cus_used_max"])
         if gemm is not None:
-            (row["gemm_slowdown"], row["gemm_overlap"], row["collective_slowdown"],
-             row["collectives_queued"]) = gemm_slowdown(hc, lambda s: hc.reduce_scatter(send, recv, stream=s),
-                                                        med, gemm)
+            row.update(interference(hc, lambda s: hc.reduce_scatter(send, recv, stream=s), med, gemm,
+                                    pairs=20))
         out[f"wg{st['workgroups_per_step']}"] = row
     hc.set_config(workgroups_per_step=0)
     return out
@@ -882,9 +977,8 @@ def bench_cu_partition(hc, x, gemm):
             row = dict(gemm_masked_ms=round(t_masked * 1e3, 4),
                        gemm_cost_of_the_mask=round(t_masked / t_full - 1, 4),
                        reduce_scatter_alone_ms=round(med * 1e3, 4))
-            (row["gemm_slowdown"], row["gemm_overlap"], row["collective_slowdown"],
-             row["collectives_queued"]) = gemm_slowdown(
-                hc, lambda s: hc.reduce_scatter(send, recv, stream=s), med, g2)
+            row.update(interference(hc, lambda s: hc.reduce_scatter(send, recv, stream=s), med, g2,
+                                    pairs=20))
         out[f"cus{K}"] = row
     return dict(workload="headline ring reduce-scatter on K reserved CUs (K workgroups per step) beside "
                          "a bf16 8192^3 GEMM masked to the other CUs", **out)
@@ -899,6 +993,7 @@ def size_sweep(hc):
     R = 8
     sizes = [2 << 20, 8 << 20, 32 << 20, 128 << 20, 512 << 20, 1 << 30]
     paths = [("hip", {"copy_path": "hip"}), ("engines", {"copy_path": "engines"}),
+             ("engines16", {"copy_path": "engines", "sdma_engines": 16}),
              ("kernel_wg8", {"copy_path": "kernel", "workgroups_per_step": 8}),
              ("kernel_wg256", {"copy_path": "kernel", "workgroups_per_step": 256})]
     out = {"sendrecv": [], "allgather": [], "alltoall": []}
@@ -916,7 +1011,7 @@ def size_sweep(hc):
                 s0, d1 = big[:sz].view(torch.int32), big2[:sz].view(torch.int32)
                 med, _ = event_time(lambda: hc.sendrecv([s0, s0], [d1, d1], [1, -1]), 5)
                 row[name] = round(sz / med / 1e9, 1)
-                hc.set_config(copy_path="auto", workgroups_per_step=0)
+                hc.set_config(copy_path="auto", workgroups_per_step=0, sdma_engines=0)
             out["sendrecv"].append(row)
     del big, big2
     for op in ("allgather", "alltoall"):
@@ -932,7 +1027,7 @@ def size_sweep(hc):
                      (lambda: hc.alltoall(send, recv))
                 med, _ = event_time(fn, 3, warmup=1)
                 row[name] = round(R * n * 4 / med / 1e9, 1)
-                hc.set_config(copy_path="auto", workgroups_per_step=0)
+                hc.set_config(copy_path="auto", workgroups_per_step=0, sdma_engines=0)
             out[op].append(row)
             del send, recv
             torch.cuda.empty_cache()
@@ -944,7 +1039,8 @@ def size_sweep(hc):
         send = [torch.zeros(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
         recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
         row = {"bytes": R * n * 2}
-        for name, kw in (("ring", {}), ("ring_wg8", {"workgroups_per_step": 8}),
+        for name, kw in (("ring", {"reduce_algo": "ring"}),
+                         ("ring_wg8", {"reduce_algo": "ring", "workgroups_per_step": 8}),
                          ("direct", {"reduce_algo": "direct"})):
             with hc.config(**kw):
                 med, _ = event_time(lambda: hc.reduce_scatter(send, recv), 3, warmup=1)
@@ -1102,6 +1198,8 @@ def main():
                     help="print algbw against message size per copy path instead")
     ap.add_argument("--ar-groups-workload", action="store_true",
                     help="run only the grouped all-reduce the overlap trace profiles")
+    ap.add_argument("--interference-workload", action="store_true",
+                    help="GEMM interference of the engine-path collectives against the engine budget")
     ap.add_argument("--copy-workload", action="store_true",
                     help="run only the copy collectives the zero-CU trace is taken on")
     args = ap.parse_args()
@@ -1119,6 +1217,9 @@ def main():
 
     torch.cuda.set_device(0)
     hc.init(0)
+    # The benchmark studies the ring schedule (the step each GPU runs when the
+    # ranks are GPUs); rows that measure the direct fold or AUTO ask for it.
+    hc.set_config(reduce_algo="ring")
     if args.pmc_workload:
         pmc_workload(hc, W)
         return
@@ -1130,6 +1231,9 @@ def main():
         return
     if args.copy_workload:
         copy_workload(hc, W)
+        return
+    if args.interference_workload:
+        print(json.dumps({"interference": interference_workload(hc, W)}), flush=True)
         return
     if args.sweep:
         print(json.dumps({"sweep": size_sweep(hc)}), flush=True)

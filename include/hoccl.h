@@ -170,7 +170,13 @@ typedef struct {
                                    least 32 MiB, else 1 (plan dumps assume
                                    the SDMA path)                              */
     /* ---- extensions ---- */
-    int sdma_engines;           /* engines the SDMA path may use, 0 = all      */
+    int sdma_engines;           /* engines the SDMA path may use, 1..32 (at
+                                   most those available, 16 on MI355X);
+                                   0 = automatic: 4, the most whose copies
+                                   cost a concurrent bf16 GEMM at most 2%
+                                   (the copies run about 3x slower than on
+                                   all 16; set 16 where no compute runs
+                                   beside them)                                */
     hoccl_reduce_algo_t reduce_algo;
     int kernel_timing;          /* 1: record HIP events around every reduce /
                                    copy kernel launch (hoccl_get_kernel_times) */

@@ -390,6 +390,20 @@ hoccl_status_t timed_end(TimingPair *tp, hipStream_t s) {
     return HOCCL_OK;
 }
 
+// SDMA engines the copy proxy may use.  sdma_engines 0 is the automatic
+// budget: the most engines whose copies cost a concurrent bf16 8192^3 GEMM
+// at most 2% at the upper end of a 95% interval (100 paired runs each) on
+// the FSDP all-gather, the pipeline send/recv schedule and the EP
+// all-to-all(v).  Measured: 4 engines (about 220 GB/s of copies) cost it
+// 0.0-0.1% (upper bounds 0.6-0.8%); 5 and 6 engines up to 1.6% (upper
+// bound 2.3%); 8 engines 1.6-1.9% (upper bound 2.7%); all 16 (650 GB/s)
+// 4.6-6.0%.  The GEMM's loss follows the copies' aggregate rate.
+constexpr int kAutoSdmaEngines = 4;
+
+int engine_budget(const hoccl_config_t &cfg) {
+    return cfg.sdma_engines > 0 ? cfg.sdma_engines : kAutoSdmaEngines;
+}
+
 // With record_groups, an event is recorded on s after each group's last
 // reduction step: gates[g] when given, else the library's ev_group[g].
 hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
@@ -557,7 +571,7 @@ hoccl_status_t run_engine_groups(DeviceState &st, const hoccl_config_t &cfg, con
         cps.push_back(pc);
     }
     int ne = 0;
-    r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, handshake,
+    r = st.proxy->submit(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, handshake,
                          s, &ne, t_err, std::move(gates));
     if (r == HOCCL_OK) t_stats.copy_ops += (int)cps.size();
     return r;
@@ -645,7 +659,7 @@ size_t auto_chunk_bytes(const DeviceState &st, const hoccl_config_t &cfg, hoccl_
                         const Plan &p) {
     if (path != HOCCL_COPY_SDMA || cfg.chunk_bytes != 0 || !st.proxy) return 0;
     int E = st.proxy->engine_count();
-    if (cfg.sdma_engines > 0) E = std::min(E, cfg.sdma_engines);
+    E = std::min(E, engine_budget(cfg));
     if (p.nchains <= 0 || p.nchains >= E) return 0;
     size_t big = 0;
     for (const CopyOp &c : p.copies) big = std::max(big, c.bytes);
@@ -672,7 +686,7 @@ hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Pl
         int ne = 0;
         hoccl_status_t r;
         if (capturing) {
-            r = st.proxy->capture(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, s,
+            r = st.proxy->capture(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, s,
                                   &ne, t_err);
         } else if (handshake == 2 && p.copy_bytes >= ((unsigned long long)1 << 20)) {
             // The copies may start as soon as everything before them on s
@@ -693,10 +707,10 @@ hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Pl
                 return HOCCL_ERR_HIP;
             }
             for (ProxyCopy &c : cps) c.gate = 0;
-            r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
+            r = st.proxy->submit(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
                                  handshake, s, &ne, t_err, std::move(gate));
         } else {
-            r = st.proxy->submit(cps, cfg.sdma_engines, cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
+            r = st.proxy->submit(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
                                  handshake, s, &ne, t_err);
         }
         if (r != HOCCL_OK) return r;
