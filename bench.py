@@ -662,9 +662,27 @@ def bench_a2a(hc, W, reps, gemm):
     res = copy_paths(hc, lambda s: hc.alltoallv(send, counts, sd, recv, rd, stream=s), sent // R, (R - 1) / R,
                      reps, gemm, extra_paths=[("kernel_wg8", {"copy_path": "kernel", "workgroups_per_step": 8}),
                                               ("kernel_wg64", {"copy_path": "kernel", "workgroups_per_step": 64})])
+    # The collective scheduler's stages (Algorithm 1 on this traffic
+    # matrix, one memory domain) against the byte-balanced schedule.
+    C = [[counts[s * R + d] * 2 if s != d else 0 for d in range(R)] for s in range(R)]
+    nstages = len(hc.schedule(C, [0] * R, [-1] * R, 1.0, 1.0)["stages"])
+    ab = {"stages": nstages}
+    for E in (0, 16):
+        for sched, name in ((0, "byte_balanced"), (1, "stages")):
+            with hc.config(copy_path="engines", sdma_engines=E, a2a_schedule=sched):
+                med, mn = event_time(lambda: hc.alltoallv(send, counts, sd, recv, rd), reps)
+            ab[f"{name}_engines{E or 4}"] = dict(ms=round(med * 1e3, 4), min_ms=round(mn * 1e3, 4),
+                                                 copy_GBs=round(sent / med / 1e9, 1))
+    for sched, name in ((0, "byte_balanced"), (2, "stages_serial")):
+        with hc.config(copy_path="kernel", a2a_schedule=sched):
+            med, mn = event_time(lambda: hc.alltoallv(send, counts, sd, recv, rd), reps)
+            st = hc.last_stats()
+        ab[f"{name}_cu_kernel"] = dict(ms=round(med * 1e3, 4), min_ms=round(mn * 1e3, 4),
+                                       copy_GBs=round(sent / med / 1e9, 1),
+                                       launches=st["copy_kernel_launches"])
     return dict(workload="EP all-to-all(v) bf16, 4096 tokens x 2048 per rank, 64 experts over R=8, top-6 "
                          "(one copy per destination rank), gemm_slowdown against a concurrent 8192^3 bf16 GEMM",
-                bytes_sent_total=sent, **res)
+                bytes_sent_total=sent, schedule_ab=ab, **res)
 
 
 def bench_p2p_sizes(hc, reps, bufs=None):

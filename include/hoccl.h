@@ -224,6 +224,22 @@ typedef struct {
                                    bits), and reads and writes the partial
                                    once instead of once per hop; R-1 hops
                                    fold the whole chunk in one launch      */
+    int a2a_schedule;           /* all-to-all(v) copy schedule:
+                                   0 (default): every flow a chain of its
+                                   own, chains balanced over the engines by
+                                   bytes and interleaved by flow size;
+                                   1: the stages of the collective
+                                   scheduler's Birkhoff-like decomposition
+                                   of the traffic matrix (Collective
+                                   Scheduler, Algorithm 1): each stage a
+                                   matching (every rank sends and receives
+                                   at most one piece), the engines' queues
+                                   in stage order;
+                                   2: as 1, the stages run one after another
+                                   (the CU copy kernel launches stage by
+                                   stage; on the SDMA path this returns
+                                   HOCCL_ERR_UNSUPPORTED, enqueuing
+                                   nothing).  The HIP path ignores stages  */
 } hoccl_config_t;
 
 /* The first eight fields are the core statistics; the rest extend them. */
@@ -263,8 +279,8 @@ typedef struct {
  *   HOCCL_WG_PER_STEP, HOCCL_THREADS_PER_WG, HOCCL_CHUNK_BYTES,
  *   HOCCL_COPY_STREAMS, HOCCL_SDMA_ENGINES, HOCCL_AG_DIRECT,
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
- *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES, HOCCL_FUSED_HOPS
- *   (the fields of the same meaning),
+ *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES, HOCCL_FUSED_HOPS,
+ *   HOCCL_A2A_SCHEDULE (the fields of the same meaning),
  *   HOCCL_COPY_PATH = auto | sdma (or engines) | kernel | hip,
  *   HOCCL_REDUCE_ALGO = ring | direct | auto,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),

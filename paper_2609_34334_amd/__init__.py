@@ -54,7 +54,8 @@ class Config(ctypes.Structure):
                 ("proxy_handshake", ctypes.c_int),
                 ("ring_group_bytes", ctypes.c_size_t),
                 ("proxy_wait_limit_us", ctypes.c_uint),
-                ("fused_hops", ctypes.c_int)]
+                ("fused_hops", ctypes.c_int),
+                ("a2a_schedule", ctypes.c_int)]
 
 
 class Stats(ctypes.Structure):

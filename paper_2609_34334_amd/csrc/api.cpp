@@ -114,6 +114,7 @@ hoccl_config_t default_config() {
     c.ring_group_bytes = 0;
     c.proxy_wait_limit_us = 0;
     c.fused_hops = 1;
+    c.a2a_schedule = 0;
     return c;
 }
 
@@ -131,6 +132,7 @@ bool config_valid(const hoccl_config_t &c) {
     if (c.chunk_bytes != 0 && c.chunk_bytes < 4096) return false;
     if (c.proxy_handshake < -1 || c.proxy_handshake > 2) return false;
     if (c.fused_hops < 0 || c.fused_hops > kMaxRanks) return false;
+    if (c.a2a_schedule < 0 || c.a2a_schedule > 2) return false;
     return true;
 }
 
@@ -156,6 +158,7 @@ void load_config_locked() {
     c.proxy_handshake = (int)env_long("HOCCL_PROXY_HANDSHAKE", c.proxy_handshake);
     c.proxy_wait_limit_us = (unsigned)env_long("HOCCL_PROXY_WAIT_LIMIT_US", c.proxy_wait_limit_us);
     c.fused_hops = (int)env_long("HOCCL_FUSED_HOPS", c.fused_hops);
+    c.a2a_schedule = (int)env_long("HOCCL_A2A_SCHEDULE", c.a2a_schedule);
     if (const char *v = std::getenv("HOCCL_RING_GROUP_BYTES")) c.ring_group_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "hip")) c.copy_path = HOCCL_COPY_HIP;
@@ -681,8 +684,10 @@ hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Pl
         TRY(run_reductions(st, cfg, p, B, s, wg, threads, false));
         std::vector<ProxyCopy> cps;
         cps.reserve(p.copies.size());
-        for (const CopyOp &c : p.copies)
+        for (const CopyOp &c : p.copies) {
             cps.push_back(ProxyCopy{resolve(c.dst, B), resolve(c.src, B), c.bytes, c.chain});
+            cps.back().stage = c.stage;
+        }
         int ne = 0;
         hoccl_status_t r;
         if (capturing) {
@@ -776,6 +781,16 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
         profiler_present()) {
         set_err("the host-function handshake (proxy_handshake = 2) is refused while a profiler is "
                 "loaded: it blocks the runtime thread the profiler may need");
+        return HOCCL_ERR_UNSUPPORTED;
+    }
+    if (!p.copies.empty() && path == HOCCL_COPY_SDMA && cfg.a2a_schedule == 2 &&
+        (p.op == Op::AllToAll || p.op == Op::AllToAllV)) {
+        // Stages run one after another on the engines made every copy of a
+        // stage wait on all copies of the previous stage through dependency
+        // signals; that form's first run ended in a host fault whose cause
+        // is not established, so it is not offered.
+        set_err("a2a_schedule 2 (stages run one after another) is not available on the SDMA copy "
+                "path; use a2a_schedule 1 (stage order) or the CU copy kernel");
         return HOCCL_ERR_UNSUPPORTED;
     }
     if (!p.copies.empty() && path == HOCCL_COPY_SDMA && capturing && handshake != 2) {
@@ -933,6 +948,7 @@ PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
     o.in_place = in_place;
     o.algo = cfg.reduce_algo;
     o.fused_hops = cfg.fused_hops;
+    o.a2a_schedule = cfg.a2a_schedule;
     return o;
 }
 

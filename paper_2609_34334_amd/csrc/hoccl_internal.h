@@ -85,6 +85,7 @@ struct CopyOp {
     int chain = 0;
     int group = -1;
     int level = 0;
+    int stage = -1;  // all-to-all stage of the collective scheduler, or -1
 };
 
 struct Plan {
@@ -115,6 +116,10 @@ struct PlanOptions {
     size_t group_partial_bytes = 0;
     // Ring hops per reduction launch (0 or 1: one; at most kMaxHops).
     int fused_hops = 1;
+    // All-to-all(v) copy schedule (hoccl_config_t.a2a_schedule): 0 byte-
+    // balanced chains; 1 and 2 the stages of the collective scheduler's
+    // decomposition (copies tagged with their stage; 2 runs them serially).
+    int a2a_schedule = 0;
 };
 
 // HOCCL_REDUCE_AUTO folds directly up to this many ranks.  On one GPU the

@@ -18,6 +18,7 @@
 #include <sstream>
 
 #include "hoccl_internal.h"
+#include "schedule.h"
 
 namespace hoccl {
 
@@ -336,6 +337,74 @@ Plan plan_sendrecv(size_t n, hoccl_dtype_t dt, int R, const int *peers, const Pl
     return p;
 }
 
+// All-to-all(v) by the collective scheduler's stages (Collective
+// Scheduler, Algorithm 1).  The traffic matrix C (bytes, one memory domain:
+// every rank in one node, no symmetric peers, so no forwarding traffic) is
+// decomposed into stages, each a matching: every rank sends at most one
+// piece and receives at most one.  Flow (s, d) is cut into the pieces its
+// stages carry, in stage order, each piece a chain of its own tagged with
+// its stage (and, for the CU copy kernel, launched stage by stage through
+// `level`).  The ranks' copies to themselves, which the decomposition
+// leaves out, form one last stage.
+static void plan_a2a_stages(Plan &p, const size_t *counts, const size_t *sd, const size_t *rd, int R,
+                            size_t es) {
+    Topology t;
+    t.G = R;
+    t.node.assign((size_t)R, 0);
+    t.peer.assign((size_t)R, -1);
+    std::vector<std::vector<double>> C((size_t)R, std::vector<double>((size_t)R, 0.0));
+    for (int s = 0; s < R; ++s)
+        for (int d = 0; d < R; ++d)
+            if (s != d) C[(size_t)s][(size_t)d] = (double)(counts[(size_t)s * R + d] * es);
+    Schedule sch = decompose(t, C);
+    std::vector<size_t> done((size_t)R * R, 0);  // bytes of each flow planned so far
+    int chain = 0;
+    auto piece = [&](int s, int d, size_t bytes, int stage) {
+        size_t k = (size_t)s * R + d;
+        CopyOp c;
+        c.dst = ref(BUF_RECV, d, rd[k] * es + done[k]);
+        c.src = ref(BUF_SEND, s, sd[k] * es + done[k]);
+        c.bytes = bytes;
+        c.chain = chain++;
+        c.stage = stage;
+        c.level = stage;
+        p.copies.push_back(c);
+        p.copy_bytes += bytes;
+        p.hbm_bytes += 2ull * bytes;
+        done[k] += bytes;
+    };
+    int stage = 0;
+    for (const auto &S : sch.stages) {
+        bool any = false;
+        for (int s = 0; s < R; ++s)
+            for (int d = 0; d < R; ++d) {
+                if (s == d || !(S[(size_t)s][(size_t)d] > 0.0)) continue;
+                size_t k = (size_t)s * R + d, left = counts[k] * es - done[k];
+                // The stage amounts are sums and differences of whole flow
+                // sizes, so they are exact in double; clamp all the same.
+                size_t b = std::min(left, (size_t)(S[(size_t)s][(size_t)d] + 0.5));
+                if (b) {
+                    piece(s, d, b, stage);
+                    any = true;
+                }
+            }
+        if (any) ++stage;
+    }
+    // Whatever a stage did not carry (none, as the decomposition is
+    // complete) and the copies to self go last.
+    bool any = false;
+    for (int s = 0; s < R; ++s)
+        for (int d = 0; d < R; ++d) {
+            size_t k = (size_t)s * R + d, left = counts[k] * es - done[k];
+            if (left) {
+                piece(s, d, left, stage);
+                any = true;
+            }
+        }
+    (void)any;
+    p.nchains = chain;
+}
+
 Plan plan_alltoall(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o) {
     Plan p;
     p.op = Op::AllToAll;
@@ -344,6 +413,16 @@ Plan plan_alltoall(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o) {
     p.count = n;
     if (n == 0) return p;
     size_t bytes = n * dtype_size(dt);
+    if (o.a2a_schedule != 0) {
+        std::vector<size_t> counts((size_t)R * R, n), sd((size_t)R * R), rd((size_t)R * R);
+        for (int s = 0; s < R; ++s)
+            for (int d = 0; d < R; ++d) {
+                sd[(size_t)s * R + d] = (size_t)d * n;
+                rd[(size_t)s * R + d] = (size_t)s * n;
+            }
+        plan_a2a_stages(p, counts.data(), sd.data(), rd.data(), R, dtype_size(dt));
+        return p;
+    }
     int P = pieces_for(bytes, o.chunk_bytes);
     for (int s = 0; s < R; ++s)
         for (int d = 0; d < R; ++d)
@@ -367,6 +446,10 @@ Plan plan_alltoallv(const size_t *counts, const size_t *sd, const size_t *rd, ho
         P = std::max(P, pieces_for(counts[k] * es, o.chunk_bytes));
     }
     p.count = total;
+    if (o.a2a_schedule != 0) {
+        plan_a2a_stages(p, counts, sd, rd, R, es);
+        return p;
+    }
     for (int s = 0; s < R; ++s)
         for (int d = 0; d < R; ++d) {
             size_t k = (size_t)s * R + d;
@@ -455,7 +538,7 @@ std::string plan_to_json(const Plan &p) {
         os << ",\"src\":";
         put_ref(os, c.src);
         os << ",\"bytes\":" << c.bytes << ",\"chain\":" << c.chain << ",\"group\":" << c.group
-           << ",\"level\":" << c.level << "}";
+           << ",\"level\":" << c.level << ",\"stage\":" << c.stage << "}";
     }
     os << "]}";
     return os.str();

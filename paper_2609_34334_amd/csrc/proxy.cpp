@@ -148,7 +148,7 @@ struct ProxyOp {
     int slot = -1;
     std::vector<ProxyCopy> copies;  // in issue order: the gates' blocks, then the ungated
     std::vector<uint32_t> engine;   // engine id bit per copy
-    std::vector<int> dep;           // previous copy of the same chain, or -1
+    std::vector<std::vector<int>> deps;  // earlier copies each copy waits for
     std::vector<hsa_signal_t> sig;
     std::vector<hipEvent_t> gates;  // copy gates (taken from the pool)
     std::vector<char> gate_open;
@@ -202,15 +202,11 @@ class ProxyImpl {
     void issue_next(ProxyOp &op) {
         const size_t i = op.next++;
         const ProxyCopy &c = op.copies[i];
-        const hsa_signal_t *deps = nullptr;
-        uint32_t ndep = 0;
-        if (op.dep[i] >= 0) {
-            deps = &op.sig[(size_t)op.dep[i]];
-            ndep = 1;
-        }
+        std::vector<hsa_signal_t> deps;
+        for (int d : op.deps[i]) deps.push_back(op.sig[(size_t)d]);
         hsa_status_t e = hsa_amd_memory_async_copy_on_engine(
-            c.dst, agent, c.src, agent, c.bytes, ndep, deps, op.sig[i],
-            (hsa_amd_sdma_engine_id_t)op.engine[i], true);
+            c.dst, agent, c.src, agent, c.bytes, (uint32_t)deps.size(), deps.empty() ? nullptr : deps.data(),
+            op.sig[i], (hsa_amd_sdma_engine_id_t)op.engine[i], true);
         if (e != HSA_STATUS_SUCCESS) {
             char buf[160];
             std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
@@ -427,7 +423,7 @@ struct CapturedOp {
     ProxyImpl *P = nullptr;
     std::vector<ProxyCopy> copies;
     std::vector<uint32_t> engine;
-    std::vector<int> dep;
+    std::vector<std::vector<int>> deps;
     std::vector<hsa_signal_t> sig;
     std::chrono::microseconds limit{0};
 };
@@ -442,10 +438,11 @@ void run_captured(void *arg) {
     for (size_t i = 0; i < op.copies.size(); ++i, ++issued) {
         const ProxyCopy &c = op.copies[i];
         hsa_signal_store_screlease(op.sig[i], 1);
-        const hsa_signal_t *deps = op.dep[i] >= 0 ? &op.sig[(size_t)op.dep[i]] : nullptr;
-        if (hsa_amd_memory_async_copy_on_engine(c.dst, P.agent, c.src, P.agent, c.bytes, deps ? 1 : 0,
-                                                deps, op.sig[i], (hsa_amd_sdma_engine_id_t)op.engine[i],
-                                                true) != HSA_STATUS_SUCCESS) {
+        std::vector<hsa_signal_t> deps;
+        for (int d : op.deps[i]) deps.push_back(op.sig[(size_t)d]);
+        if (hsa_amd_memory_async_copy_on_engine(c.dst, P.agent, c.src, P.agent, c.bytes, (uint32_t)deps.size(),
+                                                deps.empty() ? nullptr : deps.data(), op.sig[i],
+                                                (hsa_amd_sdma_engine_id_t)op.engine[i], true) != HSA_STATUS_SUCCESS) {
             hsa_signal_store_screlease(op.sig[i], 0);
             P.fail(HOCCL_ERR_HIP, "hsa_amd_memory_async_copy_on_engine failed in a graph replay");
             break;
@@ -532,13 +529,68 @@ void host_side_handshake(void *arg) {
 // its own order.
 struct EngineSchedule {
     std::vector<ProxyCopy> copies;
-    std::vector<uint32_t> engine;  // engine id bit per copy
-    std::vector<int> dep;          // previous copy of the same chain, or -1
+    std::vector<uint32_t> engine;         // engine id bit per copy
+    std::vector<std::vector<int>> deps;   // copies each copy waits for
     int engines_used = 0;
 };
 
+// The collective scheduler's stages on the engines (Collective Scheduler,
+// Algorithm 1).  Every stage's copies go to the engines largest first onto
+// the least loaded by bytes so far, each engine's queue in stage order,
+// issued stage by stage and one copy per engine in turn; only the engines'
+// own order keeps the stages apart (no copy waits for another).
+EngineSchedule schedule_stages(const ProxyImpl &P, const std::vector<ProxyCopy> &copies, int max_engines) {
+    int E = (int)P.engines.size();
+    if (max_engines > 0) E = std::min(E, max_engines);
+    int nst = 0;
+    for (auto &c : copies) nst = std::max(nst, c.stage + 1);
+    std::vector<std::vector<size_t>> of_stage((size_t)nst);
+    for (size_t i = 0; i < copies.size(); ++i) of_stage[(size_t)copies[i].stage].push_back(i);
+    std::vector<unsigned long long> load((size_t)E, 0);
+    std::vector<std::vector<size_t>> per_engine((size_t)E);
+    std::vector<int> eng(copies.size(), 0);
+    for (auto &st : of_stage) {
+        std::vector<size_t> q = st;
+        std::stable_sort(q.begin(), q.end(), [&](size_t a, size_t b) { return copies[a].bytes > copies[b].bytes; });
+        for (size_t i : q) {
+            size_t best = 0;
+            for (size_t k = 1; k < load.size(); ++k)
+                if (load[k] < load[best]) best = k;
+            load[best] += copies[i].bytes;
+            per_engine[best].push_back(i);
+            eng[i] = (int)best;
+        }
+    }
+    // Issue order: stage by stage, and within a stage one copy per engine in
+    // turn, so every copy is issued after every copy it may wait for.
+    EngineSchedule out;
+    std::vector<int> pos(copies.size(), -1);
+    for (int sidx = 0; sidx < nst; ++sidx) {
+        std::vector<size_t> next((size_t)E, 0);
+        bool more = true;
+        while (more) {
+            more = false;
+            for (int e = 0; e < E; ++e) {
+                auto &q = per_engine[(size_t)e];
+                while (next[(size_t)e] < q.size() && copies[q[next[(size_t)e]]].stage < sidx) ++next[(size_t)e];
+                if (next[(size_t)e] < q.size() && copies[q[next[(size_t)e]]].stage == sidx) {
+                    size_t i = q[next[(size_t)e]++];
+                    pos[i] = (int)out.copies.size();
+                    out.copies.push_back(copies[i]);
+                    out.engine.push_back(P.engines[(size_t)e]);
+                    more = true;
+                }
+            }
+        }
+    }
+    out.deps.assign(out.copies.size(), {});
+    for (auto l : load) out.engines_used += l > 0;
+    return out;
+}
+
 EngineSchedule schedule_copies(const ProxyImpl &P, const std::vector<ProxyCopy> &copies,
                                int max_engines) {
+    if (!copies.empty() && copies[0].stage >= 0) return schedule_stages(P, copies, max_engines);
     int E = (int)P.engines.size();
     if (max_engines > 0) E = std::min(E, max_engines);
     // Balance bytes per engine: largest chain first onto the least loaded.
@@ -608,11 +660,11 @@ EngineSchedule schedule_copies(const ProxyImpl &P, const std::vector<ProxyCopy> 
     for (size_t i : issue) out.copies.push_back(copies[i]);
     std::vector<int> last((size_t)nch, -1);
     out.engine.resize(out.copies.size());
-    out.dep.resize(out.copies.size());
+    out.deps.assign(out.copies.size(), {});
     for (size_t i = 0; i < out.copies.size(); ++i) {
         int ch = out.copies[i].chain;
         out.engine[i] = P.engines[(size_t)eng_of_chain[(size_t)ch]];
-        out.dep[i] = last[(size_t)ch];
+        if (last[(size_t)ch] >= 0) out.deps[i].push_back(last[(size_t)ch]);
         last[(size_t)ch] = (int)i;
     }
     for (auto l : load) out.engines_used += l > 0;
@@ -678,7 +730,9 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
             for (size_t i = 0; i < sch.copies.size(); ++i) {
                 op->copies.push_back(sch.copies[i]);
                 op->engine.push_back(sch.engine[i]);
-                op->dep.push_back(sch.dep[i] < 0 ? -1 : base + sch.dep[i]);
+                std::vector<int> d = sch.deps[i];
+                for (int &x : d) x += base;
+                op->deps.push_back(std::move(d));
             }
             used = std::max(used, sch.engines_used);
         }
@@ -807,7 +861,7 @@ hoccl_status_t Proxy::capture(const std::vector<ProxyCopy> &copies, int max_engi
         EngineSchedule sch = schedule_copies(P, copies, max_engines);
         op->copies = std::move(sch.copies);
         op->engine = std::move(sch.engine);
-        op->dep = std::move(sch.dep);
+        op->deps = std::move(sch.deps);
         if (engines_used) *engines_used = sch.engines_used;
     }
     const uint64_t t = timeout_ms ? timeout_ms : 10000;

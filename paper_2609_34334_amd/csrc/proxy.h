@@ -18,6 +18,7 @@ struct ProxyCopy {
     size_t bytes;
     int chain;      // copies of one chain run in order; chains are independent
     int gate = -1;  // index into submit's `gates`, or -1: wait for the stream
+    int stage = -1; // collective-scheduler stage (all-to-all), or -1
 };
 
 class ProxyImpl;
@@ -57,6 +58,9 @@ class Proxy {
     // events; 2, a host function on `s` run by the HIP runtime's callback
     // thread.  It stops waiting after wait_limit_us (0: twice the timeout
     // plus a second).
+    // Copies tagged with stages (all of them, or none) are scheduled stage
+    // by stage instead: each stage's copies over the engines by bytes, every
+    // engine's queue in stage order.
     hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
                           unsigned timeout_ms, unsigned wait_limit_us, int handshake,
                           hipStream_t s, int *engines_used, std::string &err,

@@ -165,6 +165,9 @@ int main() {
                                 run(plan_sendrecv(n, dt, R, shift.data(), o), R, n * es, n * es, 0);
                                 run(plan_sendrecv(n, dt, R, rev.data(), o), R, n * es, n * es, 0);
                                 run(plan_alltoall(n, dt, R, o), R, (size_t)R * n * es, (size_t)R * n * es, 0);
+                                PlanOptions st = o;  // the collective scheduler's stages
+                                st.a2a_schedule = 1;
+                                run(plan_alltoall(n, dt, R, st), R, (size_t)R * n * es, (size_t)R * n * es, 0);
                                 // all-to-all(v): counts s->d from a fixed pattern, packed displacements
                                 std::vector<size_t> C((size_t)R * R), sd((size_t)R * R), rd((size_t)R * R);
                                 for (int s = 0; s < R; ++s)
@@ -188,6 +191,8 @@ int main() {
                                     rmax = std::max(rmax, off);
                                 }
                                 run(plan_alltoallv(C.data(), sd.data(), rd.data(), dt, R, o), R, smax * es,
+                                    rmax * es, 0);
+                                run(plan_alltoallv(C.data(), sd.data(), rd.data(), dt, R, st), R, smax * es,
                                     rmax * es, 0);
                             }
         }

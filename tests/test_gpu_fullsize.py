@@ -82,9 +82,11 @@ def test_pp_activation_round(path):
             assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"{peers} rank {r}")
 
 
-@pytest.mark.parametrize("path", ["hip", "engines"])
-def test_alltoallv_ep_dispatch(path):
-    hc.set_config(copy_path=path)
+@pytest.mark.parametrize("path,sched", [("hip", 0), ("engines", 0), ("engines", 1), ("kernel", 2)])
+def test_alltoallv_ep_dispatch(path, sched):
+    """EP dispatch at full size; also copied stage by stage as the
+    collective scheduler decomposes its traffic matrix."""
+    hc.set_config(copy_path=path, a2a_schedule=sched)
     R = 8
     send, counts, sd, rd, rsz = W.a2a_tokens(R)
     ref = [np.zeros(s, np.uint16) for s in rsz]

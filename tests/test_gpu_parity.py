@@ -16,6 +16,11 @@ from gpu_util import (ES, NAME, TORCH, assert_bitwise, check_canaries, from_dev,
 pytestmark = pytest.mark.gpu
 
 DTS = [hc.INT32, hc.FP32, hc.BF16]
+# Stages run one after another on the SDMA engines (every copy of a stage
+# waiting on all copies of the previous one through dependency signals)
+# ended its first GPU run in a host segmentation fault whose cause is not
+# established; the library refuses that form and its cases stay off.
+SERIAL_STAGES_OFF = "a2a_schedule 2 on the SDMA engines is refused (host fault of unknown cause)"
 PATHS = ["hip", "engines", "kernel"]
 
 
@@ -316,9 +321,15 @@ def test_sendrecv_and_alltoall(path, chunk):
             assert_bitwise(from_dev(got[r], hc.FP32), ref[r], f"A2A n={n} r={r}")
 
 
+@pytest.mark.parametrize("sched", [0, 1, 2])
 @pytest.mark.parametrize("path", PATHS)
-def test_alltoallv_routing(path):
-    hc.set_config(copy_path=path)
+def test_alltoallv_routing(path, sched):
+    """EP routing (one copy per destination rank), with the byte-balanced
+    schedule and with the collective scheduler's stages (in order, and run
+    one after another)."""
+    if path == "engines" and sched == 2:
+        pytest.skip(SERIAL_STAGES_OFF)
+    hc.set_config(copy_path=path, a2a_schedule=sched)
     R = 8
     send, counts, sd, rd, rsz = W.a2a_tokens(R=R, tokens=512, hidden=256)
     ref = [np.zeros(s, np.uint16) for s in rsz]
@@ -328,6 +339,42 @@ def test_alltoallv_routing(path):
     torch.cuda.synchronize()
     for r in range(R):
         assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"A2Av r={r}")
+
+
+@pytest.mark.parametrize("sched", [1, 2])
+@pytest.mark.parametrize("path", PATHS)
+def test_alltoall_by_stages(path, sched):
+    """Uniform all-to-all through the scheduler's stages, ragged and odd
+    rank counts, every element against the oracle."""
+    if path == "engines" and sched == 2:
+        pytest.skip(SERIAL_STAGES_OFF)
+    hc.set_config(copy_path=path, a2a_schedule=sched)
+    for R, n in ((3, 7), (5, 4099), (8, 65537)):
+        xs = [W.random_bits(83 + R, r, R * n, 2) for r in range(R)]
+        ref = [np.zeros_like(a) for a in xs]
+        oracle.alltoall(xs, ref, n, hc.BF16)
+        got = hc.alltoall([to_dev(a, hc.BF16) for a in xs])
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(got[r], hc.BF16), ref[r], f"A2A stages R={R} n={n} r={r}")
+
+
+def test_serial_stages_refused_on_the_engines():
+    """a2a_schedule 2 on the SDMA path is refused before anything is
+    enqueued (its outputs keep their contents); stage order (1) runs."""
+    R = 4
+    xs = [W.random_bits(88, r, R * 100, 2) for r in range(R)]
+    send = [to_dev(a, hc.BF16) for a in xs]
+    out = [torch.full((R * 100,), 0x5A, dtype=torch.int16, device="cuda").view(torch.bfloat16) for _ in range(R)]
+    torch.cuda.synchronize()
+    for path in ("engines", "auto"):
+        hc.set_config(copy_path=path, a2a_schedule=2)
+        with pytest.raises(hc.HocclError) as ei:
+            hc.alltoall(send, out)
+        assert ei.value.status == hc.ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert (out[r].view(torch.int16) == 0x5A).all()
 
 
 def test_copy_paths_report_their_cus():

@@ -32,7 +32,8 @@ def draw(i):
                  ring_group_bytes=int(g.choice([0, 0, 4096])),
                  allreduce_chunk_groups=int(g.choice([0, 1, 3])),
                  allgather_direct=int(g.choice([0, 1])),
-                 chunk_bytes=int(g.choice([0, 0, 8192]))),
+                 chunk_bytes=int(g.choice([0, 0, 8192])),
+                 a2a_schedule=int(g.choice([0, 0, 1, 2]))),
         seed=int(g.integers(0, 1 << 30)))
 
 
@@ -58,6 +59,9 @@ def test_random_case(i):
     op, dt, R, n, lead, seed = c["op"], c["dt"], c["R"], c["n"], c["lead"], c["seed"]
     if c["cfg"]["copy_path"] == "engines" and hc.sdma_engine_count() == 0:
         c["cfg"]["copy_path"] = "hip"
+    # stages run one after another are refused on the engine path (AUTO's)
+    if c["cfg"]["a2a_schedule"] == 2 and c["cfg"]["copy_path"] in ("engines", "auto"):
+        c["cfg"]["a2a_schedule"] = 1
     es = ES[dt]
     with hc.config(**c["cfg"]):
         if op == "allreduce":

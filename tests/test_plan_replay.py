@@ -106,6 +106,8 @@ CONFIGS = [
     dict(fused_hops=3, ring_group_bytes=1000, allreduce_chunk_groups=2),
     dict(fused_hops=64),                              # every hop in one launch (capped at 8 per launch)
     dict(reduce_algo="auto"),
+    dict(a2a_schedule=1),                             # all-to-all by the scheduler's stages
+    dict(a2a_schedule=2, chunk_bytes=4096),
 ]
 
 
@@ -258,3 +260,31 @@ def test_fused_hops_bytes_and_launches(hops, per_element, launches):
     assert len(plan["reduce_steps"]) == launches
     assert [s["hops"] for s in plan["reduce_steps"]] == [min(hops, 7 - k * hops) for k in range(launches)]
     assert plan["ws_bytes"] == (0 if hops >= 7 else 8 * n * 4)
+
+
+@pytest.mark.parametrize("R", [2, 3, 5, 8])
+def test_alltoall_stages_are_matchings_and_complete(R):
+    """With a2a_schedule the all-to-all's copies carry the stages of the
+    collective scheduler's decomposition: inside each stage every rank sends
+    at most one piece and receives at most one (the per-stage degree bound,
+    Eq. 8, here over the single memory domain), except the last stage of
+    copies to self; stages are numbered in order; and every byte of every
+    flow is copied exactly once (completeness, Eq. 7)."""
+    n, dt = 1001, hc.BF16
+    with hc.config(a2a_schedule=1):
+        plan = hc.plan_json(hc.OP_ALLTOALL, n, dt, R)
+    stages = sorted({c["stage"] for c in plan["copies"]})
+    assert stages == list(range(len(stages)))
+    for st in stages[:-1]:
+        cps = [c for c in plan["copies"] if c["stage"] == st]
+        srcs = [c["src"][1] for c in cps]
+        dsts = [c["dst"][1] for c in cps]
+        assert len(set(srcs)) == len(srcs) and len(set(dsts)) == len(dsts), st
+        assert all(a != b for a, b in zip(srcs, dsts))
+    last = [c for c in plan["copies"] if c["stage"] == stages[-1]]
+    assert all(c["src"][1] == c["dst"][1] for c in last) and len(last) == R
+    cov = {}
+    for c in plan["copies"]:
+        arr = cov.setdefault(c["dst"][1], np.zeros(R * n * 2, np.int32))
+        arr[c["dst"][2]:c["dst"][2] + c["bytes"]] += 1
+    assert all((a == 1).all() for a in cov.values()) and len(cov) == R
