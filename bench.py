@@ -915,6 +915,128 @@ def copy_ceiling(hc):
     return 2 * (1 << 31) / t / 1e9
 
 
+def bench_callback_thread(hc, reps=5):
+    """What the host-function handshake does to other host callbacks.  An
+    all-gather on the engine proxy (AUTO: host-function handshake) is
+    enqueued on stream 1, then a host function on stream 2, which has no
+    other work, and a host function on stream 1 after the all-gather.  The
+    host functions record when they run (host clock).  If stream 2's
+    callback runs only once the all-gather's handshake has returned, the
+    two share the HIP runtime's callback thread.  Control: the same stream-2
+    callback with stream 1 idle.  All times in us from stream 2's enqueue."""
+    import ctypes
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")    # the HIP runtime torch has loaded
+    CB = ctypes.CFUNCTYPE(None, ctypes.c_void_p)
+    hip.hipLaunchHostFunc.argtypes = [ctypes.c_void_p, CB, ctypes.c_void_p]
+    stamps = {}
+
+    def mk(key):
+        return CB(lambda _arg: stamps.__setitem__(key, time.perf_counter()))
+    cb2, cb1 = mk("other_stream"), mk("after_allgather")
+    R, n = 8, 1 << 23                         # 16 MiB shards: 56 copies of 16 MiB
+    send = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    rows = {"busy": [], "idle": []}
+    hc.allgather(send, recv, stream=s1)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        for case in ("busy", "idle"):
+            stamps.clear()
+            if case == "busy":
+                hc.allgather(send, recv, stream=s1)
+                assert hip.hipLaunchHostFunc(ctypes.c_void_p(s1.cuda_stream), cb1, None) == 0
+            t0 = time.perf_counter()
+            assert hip.hipLaunchHostFunc(ctypes.c_void_p(s2.cuda_stream), cb2, None) == 0
+            # Poll with sleeps (which release the interpreter lock the
+            # callbacks need) rather than block in a synchronisation.
+            while not (s1.query() and s2.query()) and time.perf_counter() - t0 < 10:
+                time.sleep(20e-6)
+            torch.cuda.synchronize()
+            rows[case].append({k: round((v - t0) * 1e6, 1) for k, v in stamps.items()})
+    # Does the proxy's polling of copy gates (hipEventQuery) need that
+    # thread?  A ring all-reduce whose gather copies the proxy starts on gate
+    # events, with the handshake kernel (no host function of its own), on
+    # stream 2 while a host function on stream 1 holds the callback thread
+    # for 5 ms (sleeping: no engine and no CU is used); its device time
+    # against the same all-reduce alone.
+    hold = CB(lambda _arg: time.sleep(0.005))
+    ar_send = [torch.randn(1 << 23, device="cuda").to(torch.bfloat16) for _ in range(R)]
+    ar_recv = [torch.empty_like(t) for t in ar_send]
+    gate_rows = {"busy": [], "idle": []}
+
+    def ar():
+        with hc.config(reduce_algo="ring", allreduce_chunk_groups=2, proxy_handshake=0):
+            hc.allreduce(ar_send, ar_recv, stream=s2)
+    ar()
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        for case in ("busy", "idle"):
+            if case == "busy":
+                assert hip.hipLaunchHostFunc(ctypes.c_void_p(s1.cuda_stream), hold, None) == 0
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s2)
+            ar()
+            e1.record(s2)
+            t0 = time.perf_counter()
+            while not (s1.query() and s2.query()) and time.perf_counter() - t0 < 10:
+                time.sleep(20e-6)
+            torch.cuda.synchronize()
+            gate_rows[case].append(round(e0.elapsed_time(e1) * 1e3, 1))
+    # Do ROCr's asynchronous signal handlers (hsa_amd_signal_async_handler,
+    # which is how a tool completes a copy it traces) run on that thread
+    # too?  A handler registered on a fresh signal, the signal set while a
+    # host function holds the callback thread for 5 ms: when does it fire?
+    hsa = ctypes.CDLL("libhsa-runtime64.so.1")
+
+    class Sig(ctypes.Structure):
+        _fields_ = [("handle", ctypes.c_uint64)]
+    HANDLER = ctypes.CFUNCTYPE(ctypes.c_bool, ctypes.c_int64, ctypes.c_void_p)
+    hsa.hsa_signal_create.argtypes = [ctypes.c_int64, ctypes.c_uint32, ctypes.c_void_p, ctypes.POINTER(Sig)]
+    hsa.hsa_amd_signal_async_handler.argtypes = [Sig, ctypes.c_int, ctypes.c_int64, HANDLER, ctypes.c_void_p]
+    hsa.hsa_signal_store_screlease.argtypes = [Sig, ctypes.c_int64]
+    hsa.hsa_signal_destroy.argtypes = [Sig]
+    fired = {}
+    handler = HANDLER(lambda _v, _a: (fired.__setitem__("t", time.perf_counter()), False)[1])
+    began = {}
+    hold2 = CB(lambda _arg: (began.__setitem__("t", time.perf_counter()), time.sleep(0.005)))
+    hsa_rows = {"busy": [], "idle": []}
+    for _ in range(reps):
+        for case in ("busy", "idle"):
+            sig = Sig()
+            assert hsa.hsa_signal_create(1, 0, None, ctypes.byref(sig)) == 0
+            fired.clear()
+            began.clear()
+            assert hsa.hsa_amd_signal_async_handler(sig, 0, 0, handler, None) == 0  # EQ 0
+            if case == "busy":
+                assert hip.hipLaunchHostFunc(ctypes.c_void_p(s1.cuda_stream), hold2, None) == 0
+                t0 = time.perf_counter()
+                while "t" not in began and time.perf_counter() - t0 < 10:
+                    time.sleep(20e-6)
+            t_set = time.perf_counter()
+            hsa.hsa_signal_store_screlease(sig, 0)
+            while "t" not in fired and time.perf_counter() - t_set < 10:
+                time.sleep(20e-6)
+            while not s1.query() and time.perf_counter() - t_set < 10:
+                time.sleep(20e-6)
+            torch.cuda.synchronize()
+            hsa_rows[case].append(round((fired.get("t", float("nan")) - t_set) * 1e6, 1))
+            hsa.hsa_signal_destroy(sig)
+    med = lambda xs: round(statistics.median(xs), 1)
+    busy_other = med([r["other_stream"] for r in rows["busy"]])
+    busy_end = med([r["after_allgather"] for r in rows["busy"]])
+    return dict(workload="host function on an idle stream while an engine-path all-gather (8 x 16 MiB "
+                         "shards, host-function handshake) runs on another",
+                other_stream_callback_us=busy_other, allgather_done_callback_us=busy_end,
+                idle_control_callback_us=med([r["other_stream"] for r in rows["idle"]]),
+                other_waited_for_allgather=bool(busy_other >= 0.5 * busy_end), runs=rows,
+                gated_allreduce_us=dict(beside_held_callback_thread=med(gate_rows["busy"]),
+                                        alone=med(gate_rows["idle"]), runs=gate_rows),
+                hsa_async_handler_us=dict(beside_5ms_host_function=med(hsa_rows["busy"]),
+                                          alone=med(hsa_rows["idle"]), runs=hsa_rows))
+
+
 def bench_small_message(hc, reps):
     """Latency of one 4 KiB send/recv (rank 0 -> 1) through each copy path:
     the engine proxy's flag handshake (host function, and the one-lane
@@ -1321,6 +1443,11 @@ def main():
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 11)
         extra["small_message_latency"] = bench_small_message(hc, 30)
+        log("host callbacks beside the host-function handshake")
+        try:
+            extra["callback_thread"] = bench_callback_thread(hc)
+        except Exception as e:
+            extra["callback_thread"] = {"error": repr(e)}
 
     ceiling = round(copy_ceiling(hc), 1)
     st = rs["stats"]
