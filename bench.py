@@ -184,6 +184,8 @@ def direct_reduce_scatter(hc, send_np, steps, warmup):
                                 "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                                 "traffic": measured_traffic(FOLD_TRAFFIC_SUMMARY),
+                                "traffic_dram_destined": measured_traffic(
+                                    FOLD_TRAFFIC_SUMMARY, key="dram_destined_bytes_per_launch"),
                                 "avg_launch_us": round(launch * 1e6, 2),
                                 "bytes_per_launch": st["hbm_bytes_algorithmic"]})
 
@@ -623,8 +625,57 @@ def bench_allgather(hc, W, reps, gemm):
                                   ("kernel_wg8", {"copy_path": "kernel", "workgroups_per_step": 8}),
                                   ("kernel_wg64", {"copy_path": "kernel", "workgroups_per_step": 64})])
     hc.set_config(allgather_direct=1)
+    # Roofline of the engine path: HBM bytes (each copied byte read once and
+    # written once) against the 8 TB/s peak, and its copy rate against what
+    # the 16 engines move on one large striped message (512 MiB, each engine
+    # copying one 32 MiB piece), this path's own ceiling.
+    with hc.config(copy_path="engines", sdma_engines=16):
+        src = torch.empty(1 << 28, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        med, _ = event_time(lambda: hc.sendrecv([src, src], [dst, dst], [1, -1]), 5)
+        del src, dst
+    ceiling = (1 << 29) / med / 1e9
+    roof = {}
+    for name in ("engines", "engines16"):
+        r = res[name]
+        copied = total * 2 * R                     # out-of-place: every rank's 8 shards
+        achieved = 2 * copied / (r["ms"] / 1e3) / 1e9
+        roof[name] = {"bound": "hbm", "kernel": "SDMA engine copies (no kernel)", "achieved": round(achieved, 1),
+                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                      "copy_GBs": round(copied / (r["ms"] / 1e3) / 1e9, 1),
+                      "engine_ceiling_copy_GBs": round(ceiling, 1),
+                      "frac_of_engine_ceiling": round(copied / (r["ms"] / 1e3) / 1e9 / ceiling, 4),
+                      "bytes_per_op": 2 * copied}
     return dict(workload="FSDP all-gather bf16 R=8, 25,165,824-element shards (one GPT-6.7B block, "
-                         "201,326,592 params), out-of-place", **res)
+                         "201,326,592 params), out-of-place", roofline=roof,
+                cpu_baseline=allgather_cpu_baseline(x), **res)
+
+
+def allgather_cpu_baseline(x, budget_s=10.0):
+    """The oracle all-gather (single-threaded C, bit copies) on the FSDP
+    workload, repeated for about budget_s seconds on one pinned host core."""
+    import numpy as np
+    import oracle
+    R, n = len(x), x[0].size
+    out = [np.empty(R * n, np.uint16) for _ in range(R)]
+    saved = os.sched_getaffinity(0)
+    core = min(saved)
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            oracle.allgather(x, out, n, oracle.BF16)
+            reps += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+        sec = (time.perf_counter() - t0) / reps
+    finally:
+        os.sched_setaffinity(0, saved)
+    S = R * n * 2
+    return {"value": round(S / sec / 1e9, 4), "unit": "GB/s (algbw)", "cores": 1, "kind": "oracle",
+            "sample": f"the full FSDP all-gather, {reps} repetitions, {sec:.2f} s each, pinned to host "
+                      f"core {core}", "ms": round(sec * 1e3, 1)}
 
 
 def bench_p2p(hc, W, reps, gemm):
@@ -1210,9 +1261,29 @@ def kernel_source_hash():
     return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
-def measured_traffic(summary=TRAFFIC_SUMMARY):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, or
-    None when it is missing or the kernels changed since."""
+CEILINGS_SUMMARY = os.path.join(ROOT, "profiles", "stream_ceilings_kernel_durations.txt")
+TRAFFIC_NOTE = ("FETCH_SIZE + WRITE_SIZE: bytes crossing the L2-to-fabric boundary, scaled by a 1 GiB copy; "
+                "an upper bound on HBM bytes, since no counter separates what the 256 MB Infinity Cache "
+                "behind that boundary serves (the DRAM-destined request counters read the same)")
+
+
+def stream_ceilings():
+    """Kernel-time streaming ceilings (GB/s moved) at the 2 GiB operand size
+    from the committed profile summary, or None."""
+    if not os.path.exists(CEILINGS_SUMMARY):
+        return None
+    for line in open(CEILINGS_SUMMARY):
+        if line.startswith("| 2048 MiB |"):
+            cells = [c.strip().split()[0] for c in line.strip().strip("|").split("|")[1:]]
+            return dict(zip(("read", "write", "copy", "two_reads_one_write", "in_place_rmw"),
+                            (float(c) for c in cells)))
+    return None
+
+
+def measured_traffic(summary=TRAFFIC_SUMMARY, key="traffic_bytes_per_launch"):
+    """Bytes per launch from a committed rocprofv3 counter summary (`key`:
+    FETCH_SIZE + WRITE_SIZE by default), or None when it is missing or the
+    kernels changed since."""
     if not os.path.exists(summary):
         return None
     kv = {}
@@ -1223,7 +1294,7 @@ def measured_traffic(summary=TRAFFIC_SUMMARY):
     if kv.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     try:
-        return int(float(kv["traffic_bytes_per_launch"]))
+        return int(float(kv[key]))
     except (KeyError, ValueError):
         return None
 
@@ -1277,7 +1348,8 @@ def ar_groups_workload(hc, W):
 def pmc_workload(hc, W):
     """What the counter runs profile: a 1 GiB CU copy of known size (to
     scale FETCH_SIZE / WRITE_SIZE), then five headline reduce-scatters on
-    the ring and five with the direct fold."""
+    the ring, five with the direct fold, and five each with 2 and 4 ring
+    hops fused per launch."""
     import torch
     src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
@@ -1293,8 +1365,53 @@ def pmc_workload(hc, W):
     with hc.config(reduce_algo="direct"):
         for _ in range(5):
             hc.reduce_scatter(send, recv)
+    for k in (2, 4):
+        with hc.config(reduce_algo="ring", fused_hops=k):
+            for _ in range(5):
+                hc.reduce_scatter(send, recv)
     torch.cuda.synchronize()
     print(json.dumps({"pmc_workload": "done", "kernel_source_sha256_16": kernel_source_hash()}))
+
+
+def ceilings_workload(hc, sizes=(64 << 20, 128 << 20, 256 << 20, 2 << 30), reps=50):
+    """The memory system's streaming ceilings (hoccl_debug_stream_ceiling):
+    read only, write only, copy, two reads and a write (fp32 add) and an
+    in-place fp32 read-modify-write, per operand size: 64, 128 and 256 MiB,
+    which the 256 MB Infinity Cache holds once warm, and 2 GiB, which it
+    cannot.  Each: 3 warm-up launches, then `reps` back-to-back launches
+    between two events (per-launch time includes the launch gap; the
+    rocprofv3 trace of this workload gives kernel time alone).  GB/s of
+    bytes moved (read + written)."""
+    import torch
+    big = max(sizes)
+    A = torch.zeros(big, dtype=torch.uint8, device="cuda")
+    B = torch.zeros(big, dtype=torch.uint8, device="cuda")
+    C = torch.zeros(big, dtype=torch.uint8, device="cuda")
+    out = {}
+    for size in sizes:
+        row = {}
+        for mode in ("read", "write", "copy", "add", "rmw"):
+            a = A[:size] if mode in ("read", "copy", "add") else None
+            b = B[:size] if mode == "add" else None
+            c = C[:size]
+
+            def fn():
+                hc.stream_ceiling(mode, a, b, c, nbytes=size)
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / 1e3 / reps
+            moved = hc.last_stats()["hbm_bytes_algorithmic"]
+            row[mode] = dict(us=round(t * 1e6, 2), GBs=round(moved / t / 1e9, 1))
+        out[f"{size >> 20}MiB"] = row
+        log(f"  ceilings {size >> 20} MiB: " + ", ".join(f"{m} {v['GBs']}" for m, v in row.items()))
+    return out
 
 
 def occupancy_workload(hc, W):
@@ -1340,6 +1457,8 @@ def main():
                     help="run only the grouped all-reduce the overlap trace profiles")
     ap.add_argument("--interference-workload", action="store_true",
                     help="GEMM interference of the engine-path collectives against the engine budget")
+    ap.add_argument("--ceilings-workload", action="store_true",
+                    help="the memory system's streaming ceilings (read, write, copy, 2R+1W, RMW)")
     ap.add_argument("--copy-workload", action="store_true",
                     help="run only the copy collectives the zero-CU trace is taken on")
     args = ap.parse_args()
@@ -1371,6 +1490,9 @@ def main():
         return
     if args.copy_workload:
         copy_workload(hc, W)
+        return
+    if args.ceilings_workload:
+        print(json.dumps({"ceilings": ceilings_workload(hc)}), flush=True)
         return
     if args.interference_workload:
         print(json.dumps({"interference": interference_workload(hc, W)}), flush=True)
@@ -1478,6 +1600,9 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "reduce_step_kernel (ring step, all 8 ranks per launch)",
                      "achieved": round(rs["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(rs["achieved"] / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+                     "traffic_dram_destined": measured_traffic(key="dram_destined_bytes_per_launch"),
+                     "traffic_counts": TRAFFIC_NOTE,
+                     "stream_ceilings_2GiB_GBs": stream_ceilings(),
                      "avg_launch_us": round(rs["avg_launch_us"], 2),
                      "bytes_per_launch": rs["bytes_per_op"] // rs["launches"],
                      "launches_per_step": rs["launches"],

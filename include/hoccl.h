@@ -482,6 +482,18 @@ hoccl_status_t hoccl_debug_schedule_json(int G, const double *C, const int *node
 hoccl_status_t hoccl_debug_interleave(int nflows, const double *bytes, double chunk_bytes, int *order,
                                       size_t cap, size_t *n);
 
+/* Streaming ceilings of the memory system, the rates the collectives'
+ * kernels are read against (the paper reports bandwidth against what the
+ * hardware moves, Evaluation, Communication Benchmark).  One launch over
+ * `bytes` bytes per operand: mode 0 reads a; 1 writes c; 2 copies a to c;
+ * 3 writes c = a + b (fp32); 4 adds 1 to c in place (fp32).  Device
+ * pointers, 16-byte aligned, `bytes` a multiple of 16; mode 0 needs c as a
+ * 4-byte sink it never writes in practice.  Launch shape from
+ * workgroups_per_step and threads_per_workgroup (automatic: about 4
+ * vectors per thread).  Statistics report the bytes moved. */
+hoccl_status_t hoccl_debug_stream_ceiling(int mode, const void *a, const void *b, void *c, size_t bytes,
+                                          hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

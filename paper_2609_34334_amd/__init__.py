@@ -97,6 +97,8 @@ _SIGS = {
                                   ctypes.c_char_p, _sz, _szp],
     "hoccl_debug_interleave": [_i, ctypes.POINTER(ctypes.c_double), ctypes.c_double,
                                ctypes.POINTER(_i), _sz, _szp],
+    "hoccl_debug_stream_ceiling": [_i, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _sz,
+                                   ctypes.c_void_p],
 }
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -377,6 +379,23 @@ def alltoallv(send, counts, sdispls, recv, rdispls, stream=None):
     _check(_lib.hoccl_alltoallv(_ptrs(send), S(*counts), S(*sdispls), _ptrs(recv), S(*rdispls),
                                 dt, R, _stream(stream)), "hoccl_alltoallv")
     return recv
+
+
+CEILING_MODES = {"read": 0, "write": 1, "copy": 2, "add": 3, "rmw": 4}
+
+
+def stream_ceiling(mode, a=None, b=None, c=None, nbytes=None, stream=None):
+    """One launch of a streaming-ceiling kernel (hoccl_debug_stream_ceiling):
+    'read' a, 'write' c, 'copy' a -> c, 'add' c = a + b (fp32), 'rmw' c += 1
+    (fp32).  nbytes defaults to the size of the first tensor given."""
+    m = CEILING_MODES[mode] if isinstance(mode, str) else int(mode)
+    ts = [t for t in (a, b, c) if t is not None]
+    if nbytes is None:
+        nbytes = ts[0].numel() * ts[0].element_size()
+    ptr = lambda t: None if t is None else t.data_ptr()
+    with torch.cuda.device(ts[0].device):
+        _check(_lib.hoccl_debug_stream_ceiling(m, ptr(a), ptr(b), ptr(c), nbytes, _stream(stream)),
+               "hoccl_debug_stream_ceiling")
 
 
 def ring_hop(partial, local, out=None, hop="middle", stream=None):

@@ -30,6 +30,7 @@
 #include <string>
 #include <vector>
 
+#include "ceilings.h"
 #include "hoccl_internal.h"
 #include "proxy.h"
 #include "schedule.h"
@@ -1345,6 +1346,37 @@ hoccl_status_t hoccl_debug_schedule_json(int G, const double *C, const int *node
         std::memcpy(buf, js.data(), k);
         buf[k] = 0;
     }
+    return HOCCL_OK;
+}
+
+hoccl_status_t hoccl_debug_stream_ceiling(int mode, const void *a, const void *b, void *c, size_t bytes,
+                                          hipStream_t stream) {
+    if (mode < 0 || mode > 4) {
+        set_err("unknown mode %d", mode);
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if (bytes == 0) return HOCCL_OK;
+    const bool need_a = mode == 0 || mode == 2 || mode == 3, need_b = mode == 3, need_c = true;
+    if ((need_a && !a) || (need_b && !b) || (need_c && !c)) {
+        set_err("a pointer the mode needs is NULL");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if (bytes % 16 || ((uintptr_t)a | (uintptr_t)b | (uintptr_t)c) % 16) {
+        set_err("bytes and every pointer must be multiples of 16");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    DeviceState *st = nullptr;
+    TRY(get_state(&st));
+    hoccl_config_t cfg = config();
+    const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
+    const int wg = workgroups_for(*st, cfg, (bytes / 16 + 3) / 4, threads);
+    std::memset(&t_stats, 0, sizeof t_stats);
+    HIP_TRY(launch_stream_ceiling(mode, a, b, c, bytes, wg, threads, stream));
+    t_stats.workgroups_per_step = wg;
+    t_stats.cus_available = st->num_cus;
+    t_stats.cus_used_max = std::min(wg, st->num_cus);
+    static const unsigned long long per_byte[] = {1, 1, 2, 3, 2};
+    t_stats.hbm_bytes_algorithmic = per_byte[mode] * (unsigned long long)bytes;
     return HOCCL_OK;
 }
 

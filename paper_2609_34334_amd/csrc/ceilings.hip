@@ -1,0 +1,140 @@
+// Streaming ceilings of the GPU's memory system: the reference rates the
+// collectives' kernels are read against (read only, write only, copy, two
+// reads and a write, an in-place read-modify-write).  They are measurement
+// tools, not steps of a collective, and live apart from kernels.hip so that
+// the collectives' kernel source (and the counter figures keyed to it)
+// does not change with them.
+//
+// Every kernel moves 16-byte vectors in a grid-stride loop with 4 vectors
+// in flight per thread, like the collectives' kernels.  Buffers are 16-byte
+// aligned and their length a multiple of 16 bytes (checked by the caller).
+#include <hip/hip_runtime.h>
+
+#include "ceilings.h"
+
+namespace hoccl {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kU = 4;
+
+// Reads every vector (non-temporal) and folds it into a per-thread value
+// that is stored only if it matches a key the data never produces, so the
+// loads cannot be dropped and nothing is written in practice.
+__global__ void __launch_bounds__(1024) read_kernel(const u32x4 *a, uint64_t nv, uint32_t key,
+                                                     uint32_t *sink) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x * kU + threadIdx.x;
+    u32x4 acc = {0, 0, 0, 0};
+    for (; i + (uint64_t)(kU - 1) * blockDim.x < nv; i += stride * kU) {
+        u32x4 v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(a + i + (uint64_t)u * blockDim.x);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) acc ^= v[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+        if (i + (uint64_t)u * blockDim.x < nv) acc ^= a[i + (uint64_t)u * blockDim.x];
+    const uint32_t x = acc.x ^ acc.y ^ acc.z ^ acc.w;
+    if (x == key) sink[0] = x;
+}
+
+__global__ void __launch_bounds__(1024) write_kernel(u32x4 *c, uint64_t nv, uint32_t value) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    const u32x4 v = {value, value, value, value};
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) c[i] = v;
+}
+
+__global__ void __launch_bounds__(1024) copy_stream_kernel(const u32x4 *a, u32x4 *c, uint64_t nv) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x * kU + threadIdx.x;
+    for (; i + (uint64_t)(kU - 1) * blockDim.x < nv; i += stride * kU) {
+        u32x4 v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(a + i + (uint64_t)u * blockDim.x);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) c[i + (uint64_t)u * blockDim.x] = v[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+        if (i + (uint64_t)u * blockDim.x < nv) c[i + (uint64_t)u * blockDim.x] = a[i + (uint64_t)u * blockDim.x];
+}
+
+// c = a + b in fp32: two streams read, one written.
+__global__ void __launch_bounds__(1024) add_kernel(const f32x4 *a, const f32x4 *b, f32x4 *c, uint64_t nv) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x * kU + threadIdx.x;
+    for (; i + (uint64_t)(kU - 1) * blockDim.x < nv; i += stride * kU) {
+        f32x4 x[kU], y[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            x[u] = __builtin_nontemporal_load(a + i + (uint64_t)u * blockDim.x);
+            y[u] = __builtin_nontemporal_load(b + i + (uint64_t)u * blockDim.x);
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) c[i + (uint64_t)u * blockDim.x] = x[u] + y[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t k = i + (uint64_t)u * blockDim.x;
+        if (k < nv) c[k] = a[k] + b[k];
+    }
+}
+
+// a += 1 in fp32, in place: the access pattern of a partial updated by a
+// ring step, without the second operand.
+__global__ void __launch_bounds__(1024) rmw_kernel(f32x4 *a, uint64_t nv) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x * kU + threadIdx.x;
+    for (; i + (uint64_t)(kU - 1) * blockDim.x < nv; i += stride * kU) {
+        f32x4 x[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) x[u] = a[i + (uint64_t)u * blockDim.x];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) a[i + (uint64_t)u * blockDim.x] = x[u] + 1.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t k = i + (uint64_t)u * blockDim.x;
+        if (k < nv) a[k] = a[k] + 1.0f;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_stream_ceiling(int mode, const void *a, const void *b, void *c, size_t bytes, int wg,
+                                 int threads, hipStream_t s) {
+    uint64_t nv = bytes / 16;
+    uint32_t key = 0x9e3779b9u, value = 0x3f800000u;
+    const void *kernel = nullptr;
+    void *args[4] = {};
+    switch (mode) {
+    case 0:
+        kernel = (const void *)read_kernel;
+        args[0] = &a; args[1] = &nv; args[2] = &key; args[3] = &c;
+        break;
+    case 1:
+        kernel = (const void *)write_kernel;
+        args[0] = &c; args[1] = &nv; args[2] = &value;
+        break;
+    case 2:
+        kernel = (const void *)copy_stream_kernel;
+        args[0] = &a; args[1] = &c; args[2] = &nv;
+        break;
+    case 3:
+        kernel = (const void *)add_kernel;
+        args[0] = &a; args[1] = &b; args[2] = &c; args[3] = &nv;
+        break;
+    case 4:
+        kernel = (const void *)rmw_kernel;
+        args[0] = &c; args[1] = &nv;
+        break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipLaunchKernel(kernel, dim3((unsigned)wg), dim3((unsigned)threads), args, 0, s);
+}
+
+}  // namespace hoccl

@@ -219,3 +219,13 @@ def test_c_abi_check_compiles_with_its_layout_pins():
     subprocess.run(["gcc", "-std=c11", "-fsyntax-only", "-D__HIP_PLATFORM_AMD__",
                     "-I" + os.path.join(ROOT, "include"), "-I/opt/rocm/include",
                     os.path.join(ROOT, "tests", "native", "c_abi_check.c")], check=True)
+
+
+def test_stream_ceiling_rejects_bad_arguments_without_a_device():
+    L = hc.lib()
+    V = ctypes.c_void_p
+    assert L.hoccl_debug_stream_ceiling(9, V(0x1000), None, V(0x2000), 64, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_debug_stream_ceiling(2, V(0x1000), None, V(0x2008), 64, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_debug_stream_ceiling(2, V(0x1000), None, V(0x2000), 60, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_debug_stream_ceiling(3, V(0x1000), None, V(0x2000), 64, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_debug_stream_ceiling(1, None, None, V(0x2000), 0, None) == hc.OK
