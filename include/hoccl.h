@@ -447,6 +447,31 @@ hoccl_status_t hoccl_ring_hop(const void *partial, const void *local, void *out,
                               size_t count, hoccl_dtype_t dtype, hoccl_hop_t hop,
                               hipStream_t stream);
 
+/* ---- several processes on one device ------------------------------------
+ * The paper's runtime IPC-handle exchange (Zero-SM Point-to-Point Executor,
+ * intra-node communication): a process exports the allocation holding one
+ * of its device buffers, another process on the same device opens it and
+ * can then pass the buffer to the collectives above as one of its R
+ * pointers.  The handles travel out of band (the PyTorch backend uses the
+ * c10d store).  The exporter must not free the allocation while an
+ * importer has it open.
+ *
+ * Export the allocation that contains device pointer `ptr`: `handle`
+ * receives 64 bytes, *offset ptr's byte offset in the allocation and
+ * *alloc_bytes its size.  HOCCL_ERR_INVALID_ARG if ptr is not device memory
+ * of an allocation; HOCCL_ERR_UNSUPPORTED for allocations of 2 GiB or more,
+ * which are not shared. */
+hoccl_status_t hoccl_ipc_export(const void *ptr, void *handle, size_t *offset, size_t *alloc_bytes);
+
+/* Open a handle another process exported (each handle is opened once and
+ * cached: later calls with the same handle reuse the mapping) and return
+ * in *ptr the device address of byte `offset` of that allocation.
+ * Allocations of 2 GiB or more are refused (HOCCL_ERR_UNSUPPORTED). */
+hoccl_status_t hoccl_ipc_open(const void *handle, size_t offset, size_t alloc_bytes, void **ptr);
+
+/* Close every handle this process opened. */
+hoccl_status_t hoccl_ipc_close_all(void);
+
 /* ---- introspection (tests and tools) ------------------------------------
  * The planner's schedule for a collective: its traffic matrix turned into
  * copy chains and reduction steps (Collective Scheduler, from C to the

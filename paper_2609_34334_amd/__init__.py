@@ -99,6 +99,9 @@ _SIGS = {
                                ctypes.POINTER(_i), _sz, _szp],
     "hoccl_debug_stream_ceiling": [_i, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, _sz,
                                    ctypes.c_void_p],
+    "hoccl_ipc_export": [ctypes.c_void_p, ctypes.c_void_p, _szp, _szp],
+    "hoccl_ipc_open": [ctypes.c_void_p, _sz, _sz, ctypes.POINTER(ctypes.c_void_p)],
+    "hoccl_ipc_close_all": [],
 }
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -379,6 +382,32 @@ def alltoallv(send, counts, sdispls, recv, rdispls, stream=None):
     _check(_lib.hoccl_alltoallv(_ptrs(send), S(*counts), S(*sdispls), _ptrs(recv), S(*rdispls),
                                 dt, R, _stream(stream)), "hoccl_alltoallv")
     return recv
+
+
+IPC_HANDLE_BYTES = 64
+
+
+def ipc_export(t):
+    """(handle bytes, byte offset, allocation bytes) of the allocation that
+    holds tensor `t`'s data (hoccl_ipc_export)."""
+    h = ctypes.create_string_buffer(IPC_HANDLE_BYTES)
+    off, size = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    with torch.cuda.device(t.device):
+        _check(_lib.hoccl_ipc_export(t.data_ptr(), h, ctypes.byref(off), ctypes.byref(size)),
+               "hoccl_ipc_export")
+    return h.raw, off.value, size.value
+
+
+def ipc_open(handle, offset, alloc_bytes):
+    """Device address, in this process, of byte `offset` of an allocation
+    another process exported (hoccl_ipc_open; cached per handle)."""
+    p = ctypes.c_void_p()
+    _check(_lib.hoccl_ipc_open(handle, offset, alloc_bytes, ctypes.byref(p)), "hoccl_ipc_open")
+    return p.value
+
+
+def ipc_close_all():
+    _check(_lib.hoccl_ipc_close_all(), "hoccl_ipc_close_all")
 
 
 CEILING_MODES = {"read": 0, "write": 1, "copy": 2, "add": 3, "rmw": 4}

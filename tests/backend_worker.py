@@ -1,0 +1,90 @@
+"""One rank of the multi-process test of the "hoccl" torch.distributed
+backend (tests/test_gpu_backend.py launches WORLD_SIZE of these with
+torchrun, all on GPU 0, with HOCCL_BACKEND=1).  Every rank generates every
+rank's seeded inputs, so it can compute the oracle's result itself and
+compare its own output with it bit for bit: all_reduce, reduce_scatter_tensor,
+reduce_scatter (list), all_gather_into_tensor, all_gather (list),
+all_to_all_single with uneven splits, send/recv around the ring, barrier.
+Prints "rank r: backend ok" when everything matched."""
+import os
+import sys
+from datetime import timedelta
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, os.path.dirname(HERE))
+sys.path.insert(0, HERE)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+import torch.distributed as dist  # noqa: E402
+
+import oracle  # noqa: E402
+import paper_2609_34334_amd as hc  # noqa: E402
+import workloads as W  # noqa: E402
+from gpu_util import NAME, assert_bitwise, from_dev, to_dev  # noqa: E402
+from paper_2609_34334_amd import distributed as hdist  # noqa: E402
+
+
+def main():
+    rank, R = int(os.environ["RANK"]), int(os.environ["WORLD_SIZE"])
+    torch.cuda.set_device(0)
+    # HOCCL_BACKEND=1 selects hoccl; every store wait ends within 60 s
+    hdist.init_process_group(backend="nccl", timeout=timedelta(seconds=60))
+    assert dist.get_backend() == hdist.BACKEND, dist.get_backend()
+    print(f"rank {rank}: {dist.get_backend()} over {R} ranks", flush=True)
+    for dt in (hc.INT32, hc.FP32, hc.BF16):
+        for n in (1, 4099, 3 * 65536 + 7):
+            xs = [W.random_values(NAME[dt], 900 + n, r, n) for r in range(R)]
+            t = to_dev(xs[rank], dt)
+            dist.all_reduce(t)
+            assert_bitwise(from_dev(t, dt), oracle.allreduce_new(xs, dt)[rank], f"all_reduce {NAME[dt]} n={n}")
+            xr = [W.random_values(NAME[dt], 910 + n, r, R * n) for r in range(R)]
+            ref = oracle.reduce_scatter_new(xr, dt)[rank]
+            out = torch.empty(n, dtype=t.dtype, device="cuda")
+            dist.reduce_scatter_tensor(out, to_dev(xr[rank], dt))
+            assert_bitwise(from_dev(out, dt), ref, f"reduce_scatter_tensor {NAME[dt]} n={n}")
+            out2 = torch.empty(n, dtype=t.dtype, device="cuda")
+            dist.reduce_scatter(out2, list(to_dev(xr[rank], dt).chunk(R)))
+            assert_bitwise(from_dev(out2, dt), ref, f"reduce_scatter {NAME[dt]} n={n}")
+            xg = [W.random_values(NAME[dt], 920 + n, r, n) for r in range(R)]
+            refg = oracle.allgather_new(xg, dt)[rank]
+            g = torch.empty(R * n, dtype=t.dtype, device="cuda")
+            dist.all_gather_into_tensor(g, to_dev(xg[rank], dt))
+            assert_bitwise(from_dev(g, dt), refg, f"all_gather_into_tensor {NAME[dt]} n={n}")
+            parts = [torch.empty(n, dtype=t.dtype, device="cuda") for _ in range(R)]
+            dist.all_gather(parts, to_dev(xg[rank], dt))
+            assert_bitwise(from_dev(torch.cat(parts), dt), refg, f"all_gather {NAME[dt]} n={n}")
+    # all_to_all_single, uneven rows: rank s sends C[s][d] rows of 96 bf16 to d
+    rng = np.random.default_rng(77)
+    C = rng.integers(0, 9, size=(R, R))
+    row = 96
+    xs = [W.random_bits(930, s, int(C[s].sum()) * row, 2) for s in range(R)]
+    counts = [int(C[s][d]) * row for s in range(R) for d in range(R)]
+    sd = [int(C[s][:d].sum()) * row for s in range(R) for d in range(R)]
+    rd = [int(C[:s, d].sum()) * row for s in range(R) for d in range(R)]
+    ref = [np.zeros(int(C[:, d].sum()) * row, np.uint16) for d in range(R)]
+    oracle.alltoallv(xs, counts, sd, ref, rd, hc.BF16)
+    inp = to_dev(xs[rank], hc.BF16).view(-1, row)
+    out = torch.empty(int(C[:, rank].sum()), row, dtype=torch.bfloat16, device="cuda")
+    dist.all_to_all_single(out, inp, output_split_sizes=[int(c) for c in C[:, rank]],
+                           input_split_sizes=[int(c) for c in C[rank]])
+    assert_bitwise(from_dev(out.reshape(-1), hc.BF16), ref[rank], "all_to_all_single")
+    # send/recv around the ring, three rounds (even ranks send first)
+    for k in range(3):
+        mine = W.random_bits(940 + k, rank, 70_001, 2)
+        prev = W.random_bits(940 + k, (rank - 1) % R, 70_001, 2)
+        src, got = to_dev(mine, hc.BF16), torch.empty(70_001, dtype=torch.bfloat16, device="cuda")
+        if rank % 2 == 0:
+            dist.send(src, (rank + 1) % R)
+            dist.recv(got, (rank - 1) % R)
+        else:
+            dist.recv(got, (rank - 1) % R)
+            dist.send(src, (rank + 1) % R)
+        assert_bitwise(from_dev(got, hc.BF16), prev, f"recv round {k}")
+    dist.barrier()
+    hdist.destroy_process_group()
+    print(f"rank {rank}: backend ok", flush=True)
+
+
+if __name__ == "__main__":
+    main()

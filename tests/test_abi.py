@@ -229,3 +229,32 @@ def test_stream_ceiling_rejects_bad_arguments_without_a_device():
     assert L.hoccl_debug_stream_ceiling(2, V(0x1000), None, V(0x2000), 60, None) == hc.ERR_INVALID_ARG
     assert L.hoccl_debug_stream_ceiling(3, V(0x1000), None, V(0x2000), 64, None) == hc.ERR_INVALID_ARG
     assert L.hoccl_debug_stream_ceiling(1, None, None, V(0x2000), 0, None) == hc.OK
+
+
+def test_backend_switch_and_registration():
+    """HOCCL_BACKEND selects the backend init_process_group uses; the
+    backend registers once under its name."""
+    import torch.distributed as dist
+    from paper_2609_34334_amd import distributed as hdist
+    old = os.environ.pop("HOCCL_BACKEND", None)
+    try:
+        assert hdist.selected_backend("nccl") == "nccl"
+        os.environ["HOCCL_BACKEND"] = "0"
+        assert hdist.selected_backend("gloo") == "gloo"
+        os.environ["HOCCL_BACKEND"] = "1"
+        assert hdist.selected_backend("nccl") == "hoccl"
+    finally:
+        os.environ.pop("HOCCL_BACKEND", None)
+        if old is not None:
+            os.environ["HOCCL_BACKEND"] = old
+    hdist.register()
+    hdist.register()
+    assert dist.Backend.HOCCL == "hoccl"
+
+
+def test_ipc_export_rejects_host_memory():
+    import ctypes as C
+    buf = C.create_string_buffer(64)
+    off, size = C.c_size_t(0), C.c_size_t(0)
+    host = (C.c_char * 256)()
+    assert hc.lib().hoccl_ipc_export(C.addressof(host), buf, C.byref(off), C.byref(size)) != hc.OK
