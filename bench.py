@@ -15,12 +15,15 @@ Also printed in the same JSON line:
     concurrent bf16 GEMM), each with algbw/busbw, %HBM peak and CUs used;
     the direct fold; the reduce-scatter at fixed workgroup budgets and on
     reserved CUs beside the GEMM; the bucket all-reduce in chunk groups; one
-    rank's ring hop; single messages and small-message round trips.
+    rank's ring hop; single messages and small-message round trips; the
+    engines right after a large device-memory free, static against
+    balanced issue.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--quick]
        python bench.py --sweep            (algbw against message size)
 Profiling workloads (one phase each): --pmc-workload, --occupancy-workload,
---copy-workload, --ar-groups-workload.
+--copy-workload, --ar-groups-workload, --interference-workload,
+--ceilings-workload, --after-free-workload.
 """
 import argparse
 import json
@@ -966,6 +969,141 @@ def copy_ceiling(hc):
     return 2 * (1 << 31) / t / 1e9
 
 
+def bench_after_free(hc, W):
+    """The SDMA engines right after a large device-memory free, the
+    caching-allocator case: torch's empty_cache (or any hipFree of a large
+    allocation) hands memory back, and while the driver releases it one
+    engine runs at about half rate.  Per workload on all 16 engines: every
+    copy issued at once on its scheduled engine (proxy_slice_bytes =
+    SIZE_MAX) against the default balanced issue, settled (1.5 s after the
+    last free) and in the first milliseconds after freeing 2 GiB.  Then each
+    of four engines alone, settled and right after a free: which engine the
+    release slows."""
+    import numpy as np
+    import torch
+    MiB = 1 << 20
+    SMAX = (1 << 64) - 1
+    R = 8
+
+    def one(fn):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / 1e3
+
+    def free_2gib():
+        F = [torch.empty(64 * MiB, dtype=torch.uint8, device="cuda") for _ in range(32)]
+        torch.cuda.synchronize()
+        time.sleep(0.3)
+        del F
+        torch.cuda.empty_cache()
+
+    def measure(fn, per_rank, **cfg):
+        with hc.config(proxy_timeout_ms=3000, **cfg):
+            time.sleep(1.5)
+            for _ in range(2):
+                one(fn)
+            steady = statistics.median(one(fn) for _ in range(7))
+            free_2gib()
+            after = statistics.median(one(fn) for _ in range(3))
+        return dict(ms=round(steady * 1e3, 4), after_free_ms=round(after * 1e3, 4),
+                    GBs_per_rank=round(per_rank / steady / 1e9, 1),
+                    after_free_GBs_per_rank=round(per_rank / after / 1e9, 1))
+
+    out = {}
+    n = (1 << 30) // 4 // R
+    x = W.ag_parameters(R)
+    for name in ("allgather_1GiB", "alltoall_1GiB", "allgather_fsdp"):
+        if name == "allgather_1GiB":
+            send = [torch.full((n,), r, dtype=torch.int32, device="cuda") for r in range(R)]
+            recv = [torch.empty(R * n, dtype=torch.int32, device="cuda") for _ in range(R)]
+            fn, per_rank = (lambda: hc.allgather(send, recv)), R * n * 4
+        elif name == "alltoall_1GiB":
+            send = [torch.full((R * n,), r, dtype=torch.int32, device="cuda") for r in range(R)]
+            recv = [torch.empty(R * n, dtype=torch.int32, device="cuda") for _ in range(R)]
+            fn, per_rank = (lambda: hc.alltoall(send, recv)), R * n * 4
+        else:
+            send = [bf16_dev(a) for a in x]
+            recv = [torch.empty(R * x[0].size, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+            fn, per_rank = (lambda: hc.allgather(send, recv)), R * x[0].size * 2
+        row = {}
+        for mode, sl in (("static", SMAX), ("balanced", 0)):
+            row[mode] = measure(fn, per_rank, copy_path="engines", sdma_engines=16, proxy_slice_bytes=sl)
+        log(f"  after free, {name}: static {row['static']['ms']} / {row['static']['after_free_ms']} ms, "
+            f"balanced {row['balanced']['ms']} / {row['balanced']['after_free_ms']} ms")
+        out[name] = row
+        del send, recv
+        torch.cuda.empty_cache()
+    # Which engine: each alone (the proxy restricted to it), 256 MiB copies.
+    saved = hc.get_config()
+    src = torch.empty(64 * MiB, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    engines = {}
+    try:
+        for eng in (0, 1, 5, 14):
+            os.environ["HOCCL_SDMA_ENGINE_IDS"] = str(eng)
+            hc.finalize()
+            hc.init(0)
+            r = measure(lambda: hc.sendrecv([src, src], [None, dst], [1, -1]), 256 * MiB,
+                        copy_path="engines", sdma_engines=1)
+            engines[str(eng)] = dict(GBs=r["GBs_per_rank"], after_free_GBs=r["after_free_GBs_per_rank"])
+    finally:
+        os.environ.pop("HOCCL_SDMA_ENGINE_IDS", None)
+        hc.finalize()
+        hc.init(0)
+        hc.set_config(**saved)
+    out["single_engine_256MiB"] = engines
+    # What one engine command costs: 64 MiB on one engine as N commands,
+    # every copy issued at once (no balanced issue, no gaps).
+    cost = {}
+    with hc.config(copy_path="engines", sdma_engines=1, proxy_slice_bytes=SMAX):
+        for nc in (1, 4, 16, 64):
+            with hc.config(chunk_bytes=(64 * MiB) // nc):
+                f = lambda: hc.sendrecv([src[:16 * MiB], src[:16 * MiB]], [None, dst[:16 * MiB]], [1, -1])
+                for _ in range(2):
+                    one(f)
+                cost[str(nc)] = round(statistics.median(one(f) for _ in range(9)) * 1e6, 1)
+    out["one_engine_64MiB_us_by_commands"] = cost
+    del src, dst
+    torch.cuda.empty_cache()
+    time.sleep(1.5)
+    # The default engine budget (4 engines, which the release never slows):
+    # what balanced issue costs or gains where no engine is slow, settled.
+    dflt = {}
+    send_np, counts, sd, rd, rsz = W.a2a_tokens(R)
+    ep_s = [bf16_dev(a) for a in send_np]
+    ep_r = [torch.zeros(q, dtype=torch.bfloat16, device="cuda") for q in rsz]
+    pp_s = [torch.full((2048 * 4096,), r, dtype=torch.int32, device="cuda") for r in range(R)]
+    pp_r = [torch.zeros(2048 * 4096, dtype=torch.int32, device="cuda") for _ in range(R)]
+    fwd = [r + 1 if r + 1 < R else -1 for r in range(R)]
+    fs = [bf16_dev(a) for a in x]
+    fr = [torch.empty(R * x[0].size, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    for name, fn in (("sendrecv_32MiB", lambda: hc.sendrecv([pp_s[0], pp_s[0]], [None, pp_r[1]], [1, -1])),
+                     ("pp_round_7x32MiB", lambda: hc.sendrecv(pp_s, pp_r, fwd)),
+                     ("ep_alltoallv", lambda: hc.alltoallv(ep_s, counts, sd, ep_r, rd)),
+                     ("allgather_fsdp", lambda: hc.allgather(fs, fr))):
+        row = {}
+        for mode, sl in (("static", SMAX), ("balanced", 0)):
+            with hc.config(copy_path="engines", sdma_engines=0, proxy_slice_bytes=sl):
+                for _ in range(2):
+                    one(fn)
+                row[mode + "_ms"] = round(statistics.median(one(fn) for _ in range(11)) * 1e3, 4)
+        dflt[name] = row
+    out["default_budget_settled"] = dflt
+    del ep_s, ep_r, pp_s, pp_r, fs, fr
+    torch.cuda.empty_cache()
+    time.sleep(1.5)
+    out["workload"] = ("R=8 on all 16 SDMA engines: all-gather and all-to-all with 1 GiB per rank (int32), "
+                       "the FSDP all-gather (bf16, 25,165,824-element shards); settled, then right after "
+                       "freeing 2 GiB (the median of the first 3 calls); GB/s = bytes each rank receives "
+                       "over time.  default_budget_settled: the automatic 4 engines, a 32 MiB send/recv, one "
+                       "pipeline round of seven 32 MiB messages, the EP all-to-all(v), the FSDP all-gather")
+    return out
+
+
 def bench_callback_thread(hc, reps=5):
     """What the host-function handshake does to other host callbacks.  An
     all-gather on the engine proxy (AUTO: host-function handshake) is
@@ -1461,6 +1599,8 @@ def main():
                     help="the memory system's streaming ceilings (read, write, copy, 2R+1W, RMW)")
     ap.add_argument("--copy-workload", action="store_true",
                     help="run only the copy collectives the zero-CU trace is taken on")
+    ap.add_argument("--after-free-workload", action="store_true",
+                    help="the SDMA engines right after a large device-memory free, static against balanced")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -1499,6 +1639,9 @@ def main():
         return
     if args.sweep:
         print(json.dumps({"sweep": size_sweep(hc)}), flush=True)
+        return
+    if args.after_free_workload:
+        print(json.dumps({"sdma_after_free": bench_after_free(hc, W)}), flush=True)
         return
     log("reduce-scatter headline")
     rs = bench_reduce_scatter(hc, W, args.steps, args.warmup)
@@ -1570,6 +1713,12 @@ def main():
             extra["callback_thread"] = bench_callback_thread(hc)
         except Exception as e:
             extra["callback_thread"] = {"error": repr(e)}
+        # Last: its 2 GiB frees slow one engine for a while after each.
+        log("SDMA engines after a large free")
+        try:
+            extra["sdma_after_free"] = bench_after_free(hc, W)
+        except Exception as e:
+            extra["sdma_after_free"] = {"error": repr(e)}
 
     ceiling = round(copy_ceiling(hc), 1)
     st = rs["stats"]

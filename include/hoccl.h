@@ -46,8 +46,8 @@
  *   or HSA call returns HOCCL_ERR_HIP; hoccl_last_error_string() describes
  *   it.  Faults of the device work itself surface at the caller's own
  *   synchronisation.  `count == 0` is a successful no-op.  The only error
- *   that outlives its call is the SDMA proxy's watchdog: copies of
- *   an earlier call that did not finish within proxy_timeout_ms are reported
+ *   that outlives its call is the SDMA proxy's watchdog: copies of an
+ *   earlier call that made no progress for proxy_timeout_ms are reported
  *   once, as HOCCL_ERR_TIMEOUT, by the next SDMA call (which then
  *   enqueues nothing).
  * Threads.  One host thread at a time may call into the library per device.
@@ -180,7 +180,10 @@ typedef struct {
     hoccl_reduce_algo_t reduce_algo;
     int kernel_timing;          /* 1: record HIP events around every reduce /
                                    copy kernel launch (hoccl_get_kernel_times) */
-    unsigned int proxy_timeout_ms; /* watchdog of the SDMA proxy; 0 = 10000    */
+    unsigned int proxy_timeout_ms; /* watchdog of the SDMA proxy: an operation
+                                   whose copies make no progress (none
+                                   issued, none completed) for this long is
+                                   reported; 0 = 10000                      */
     int proxy_handshake;        /* the stream side of the SDMA path's
                                    start/finish flag handshake (Stream
                                    Manager, CPU-GPU handshake protocol):
@@ -240,6 +243,28 @@ typedef struct {
                                    stage; on the SDMA path this returns
                                    HOCCL_ERR_UNSUPPORTED, enqueuing
                                    nothing).  The HIP path ignores stages  */
+    size_t proxy_slice_bytes;   /* how the SDMA proxy hands an operation's
+                                   copies to its engines when no copy waits
+                                   for another (send/recv, direct all-gather,
+                                   all-to-all(v)): the scheduled copies are
+                                   cut into pieces of the bytes still to be
+                                   cut over twice the engine count (whole
+                                   copies while much remains, this many
+                                   bytes at least: a multiple of 4096,
+                                   >= 64 KiB) that the engines pull in
+                                   order, an engine taking the next piece
+                                   when it has none in flight or when the
+                                   piece fits within twice this many bytes
+                                   with those it has.  An engine slowed by
+                                   other work then takes fewer pieces
+                                   instead of holding back the operation
+                                   (flow-size-aware chunk scheduling).
+                                   0 = automatic (4 MiB); SIZE_MAX = every
+                                   copy issued at once on its scheduled
+                                   engine.  Copies that wait for others (the
+                                   ring all-gather, the reduce-scatter /
+                                   all-reduce gathers) and graph captures
+                                   are always issued at once               */
 } hoccl_config_t;
 
 /* The first eight fields are the core statistics; the rest extend them. */
@@ -280,7 +305,8 @@ typedef struct {
  *   HOCCL_COPY_STREAMS, HOCCL_SDMA_ENGINES, HOCCL_AG_DIRECT,
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
  *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES, HOCCL_FUSED_HOPS,
- *   HOCCL_A2A_SCHEDULE (the fields of the same meaning),
+ *   HOCCL_A2A_SCHEDULE, HOCCL_PROXY_SLICE_BYTES (the fields of the same
+ *   meaning),
  *   HOCCL_COPY_PATH = auto | sdma (or engines) | kernel | hip,
  *   HOCCL_REDUCE_ALGO = ring | direct | auto,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),

@@ -55,7 +55,8 @@ class Config(ctypes.Structure):
                 ("ring_group_bytes", ctypes.c_size_t),
                 ("proxy_wait_limit_us", ctypes.c_uint),
                 ("fused_hops", ctypes.c_int),
-                ("a2a_schedule", ctypes.c_int)]
+                ("a2a_schedule", ctypes.c_int),
+                ("proxy_slice_bytes", ctypes.c_size_t)]
 
 
 class Stats(ctypes.Structure):

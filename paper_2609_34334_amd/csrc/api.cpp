@@ -116,6 +116,7 @@ hoccl_config_t default_config() {
     c.proxy_wait_limit_us = 0;
     c.fused_hops = 1;
     c.a2a_schedule = 0;
+    c.proxy_slice_bytes = 0;
     return c;
 }
 
@@ -134,6 +135,9 @@ bool config_valid(const hoccl_config_t &c) {
     if (c.proxy_handshake < -1 || c.proxy_handshake > 2) return false;
     if (c.fused_hops < 0 || c.fused_hops > kMaxRanks) return false;
     if (c.a2a_schedule < 0 || c.a2a_schedule > 2) return false;
+    if (c.proxy_slice_bytes != 0 && c.proxy_slice_bytes != SIZE_MAX &&
+        (c.proxy_slice_bytes < ((size_t)64 << 10) || c.proxy_slice_bytes % 4096 != 0))
+        return false;
     return true;
 }
 
@@ -161,6 +165,7 @@ void load_config_locked() {
     c.fused_hops = (int)env_long("HOCCL_FUSED_HOPS", c.fused_hops);
     c.a2a_schedule = (int)env_long("HOCCL_A2A_SCHEDULE", c.a2a_schedule);
     if (const char *v = std::getenv("HOCCL_RING_GROUP_BYTES")) c.ring_group_bytes = std::strtoull(v, nullptr, 0);
+    if (const char *v = std::getenv("HOCCL_PROXY_SLICE_BYTES")) c.proxy_slice_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
         if (!std::strcmp(v, "hip")) c.copy_path = HOCCL_COPY_HIP;
         else if (!std::strcmp(v, "sdma") || !std::strcmp(v, "engines")) c.copy_path = HOCCL_COPY_SDMA;
@@ -408,6 +413,20 @@ int engine_budget(const hoccl_config_t &cfg) {
     return cfg.sdma_engines > 0 ? cfg.sdma_engines : kAutoSdmaEngines;
 }
 
+// Smallest piece of the proxy's balanced issue (0 asks the proxy to issue
+// every copy at once).  Freeing a large device allocation slows one SDMA
+// engine to about half its rate for tens of ms per GiB freed; with every
+// copy issued at once, an all-gather on all 16 engines then waits for that
+// engine (443 instead of 700 GB/s).  Pieces pulled by free engines give the
+// slowed engine only what it can finish; an engine command costs about
+// 7 us to start, so the pieces stay whole copies while much remains.
+constexpr size_t kProxySliceBytes = (size_t)4 << 20;
+
+size_t proxy_slice(const hoccl_config_t &cfg) {
+    if (cfg.proxy_slice_bytes == SIZE_MAX) return 0;
+    return cfg.proxy_slice_bytes ? cfg.proxy_slice_bytes : kProxySliceBytes;
+}
+
 // With record_groups, an event is recorded on s after each group's last
 // reduction step: gates[g] when given, else the library's ev_group[g].
 hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const Plan &p,
@@ -575,8 +594,8 @@ hoccl_status_t run_engine_groups(DeviceState &st, const hoccl_config_t &cfg, con
         cps.push_back(pc);
     }
     int ne = 0;
-    r = st.proxy->submit(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us, handshake,
-                         s, &ne, t_err, std::move(gates));
+    r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg), cfg.proxy_timeout_ms,
+                         cfg.proxy_wait_limit_us, handshake, s, &ne, t_err, std::move(gates));
     if (r == HOCCL_OK) t_stats.copy_ops += (int)cps.size();
     return r;
 }
@@ -713,11 +732,11 @@ hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Pl
                 return HOCCL_ERR_HIP;
             }
             for (ProxyCopy &c : cps) c.gate = 0;
-            r = st.proxy->submit(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
-                                 handshake, s, &ne, t_err, std::move(gate));
+            r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg), cfg.proxy_timeout_ms,
+                                 cfg.proxy_wait_limit_us, handshake, s, &ne, t_err, std::move(gate));
         } else {
-            r = st.proxy->submit(cps, engine_budget(cfg), cfg.proxy_timeout_ms, cfg.proxy_wait_limit_us,
-                                 handshake, s, &ne, t_err);
+            r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg), cfg.proxy_timeout_ms,
+                                 cfg.proxy_wait_limit_us, handshake, s, &ne, t_err);
         }
         if (r != HOCCL_OK) return r;
         t_stats.copy_ops += (int)cps.size();

@@ -158,6 +158,15 @@ struct ProxyOp {
     std::chrono::steady_clock::time_point since;  // last issue
     unsigned timeout_ms = 10000;
     bool timed_out = false;
+    bool copy_failed = false;
+    size_t ended = 0;               // copies seen ended so far
+    // Balanced issue (Proxy::submit) over the engines of the budget: the
+    // scheduled copies are cut into pieces as engines take them; `pieces`
+    // and `sig` grow with every piece issued.
+    bool balanced = false;
+    BalancedIssue bal;
+    std::vector<uint32_t> slot_engine;  // engine id bit per engine slot
+    std::vector<ProxyCopy> pieces;
 };
 
 struct CapturedOp;
@@ -197,24 +206,78 @@ class ProxyImpl {
         }
     }
 
-    // Issues copy op.next (its signal was armed at submission, so a later
-    // copy of the same chain waits for it even if issued first).
-    void issue_next(ProxyOp &op) {
-        const size_t i = op.next++;
+    // Issues copy i on `engine` behind the copies it depends on (their
+    // signals were armed at submission, so a copy waits for a predecessor
+    // even if issued first).  A failure is stored and false returned.
+    bool issue_copy(ProxyOp &op, size_t i, uint32_t engine) {
         const ProxyCopy &c = op.copies[i];
         std::vector<hsa_signal_t> deps;
         for (int d : op.deps[i]) deps.push_back(op.sig[(size_t)d]);
         hsa_status_t e = hsa_amd_memory_async_copy_on_engine(
             c.dst, agent, c.src, agent, c.bytes, (uint32_t)deps.size(), deps.empty() ? nullptr : deps.data(),
-            op.sig[i], (hsa_amd_sdma_engine_id_t)op.engine[i], true);
-        if (e != HSA_STATUS_SUCCESS) {
-            char buf[160];
-            std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
-            fail(HOCCL_ERR_HIP, buf);
+            op.sig[i], (hsa_amd_sdma_engine_id_t)engine, true);
+        if (e == HSA_STATUS_SUCCESS) return true;
+        char buf[160];
+        std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
+        fail(HOCCL_ERR_HIP, buf);
+        return false;
+    }
+
+    // Issues copy op.next on its scheduled engine.
+    void issue_next(ProxyOp &op) {
+        const size_t i = op.next++;
+        if (!issue_copy(op, i, op.engine[i])) {
             // Retire the copies that were never issued so the op completes.
             for (size_t k = i; k < op.copies.size(); ++k) hsa_signal_store_screlease(op.sig[k], 0);
             op.next = op.copies.size();
         }
+    }
+
+    // A completion signal for a new piece, from the pool or created; armed
+    // (value 1) before the piece is issued.
+    bool piece_signal(hsa_signal_t &sg) {
+        {
+            std::lock_guard<std::mutex> lk(mu);
+            if (!free_signals.empty()) {
+                sg = free_signals.back();
+                free_signals.pop_back();
+                hsa_signal_store_screlease(sg, 1);
+                return true;
+            }
+        }
+        if (hsa_signal_create(1, 0, nullptr, &sg) == HSA_STATUS_SUCCESS) return true;
+        fail(HOCCL_ERR_HIP, "hsa_signal_create failed");
+        return false;
+    }
+
+    // Issues a piece of the operation's copy pc.copy on `engine`.
+    bool issue_piece(ProxyOp &op, const Piece &pc, uint32_t engine) {
+        hsa_signal_t sg;
+        if (!piece_signal(sg)) return false;
+        ProxyCopy c = op.copies[(size_t)pc.copy];
+        c.dst = (char *)c.dst + pc.offset;
+        c.src = (const char *)c.src + pc.offset;
+        c.bytes = pc.bytes;
+        op.pieces.push_back(c);
+        op.sig.push_back(sg);
+        const hsa_status_t e = hsa_amd_memory_async_copy_on_engine(c.dst, agent, c.src, agent, c.bytes, 0, nullptr,
+                                                                   sg, (hsa_amd_sdma_engine_id_t)engine, true);
+        if (e == HSA_STATUS_SUCCESS) return true;
+        hsa_signal_store_screlease(sg, 0);  // never issued: counts as ended
+        char buf[160];
+        std::snprintf(buf, sizeof buf, "hsa_amd_memory_async_copy_on_engine failed (%d)", (int)e);
+        fail(HOCCL_ERR_HIP, buf);
+        return false;
+    }
+
+    // One pass of balanced issue.  After a failed issue nothing more is
+    // issued, and the operation completes once the issued pieces have.
+    bool issue_balanced(ProxyOp &op) {
+        const double now_us =
+            std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now().time_since_epoch()).count();
+        return op.bal.pass(
+            now_us, [&](int i) { return copy_ended(op, (size_t)i); },
+            [&](int e, const Piece &pc) { return issue_piece(op, pc, op.slot_engine[(size_t)e]); });
     }
 
     // Whether the copies behind gate g may go: its event has completed (a
@@ -228,10 +291,42 @@ class ProxyImpl {
         return true;
     }
 
-    bool copies_done(const ProxyOp &op) {
-        for (const hsa_signal_t &s : op.sig)
-            if (hsa_signal_load_scacquire(s) != 0) return false;
-        return true;
+    // A copy's completion signal drops from 1 to 0 when it completes; ROCr
+    // sets it negative when the copy fails.  A failed copy counts as ended
+    // (so the operation still completes) and is reported once.
+    bool copy_ended(ProxyOp &op, size_t i) {
+        const hsa_signal_value_t v = hsa_signal_load_scacquire(op.sig[i]);
+        if (v < 0 && !op.copy_failed) {
+            op.copy_failed = true;
+            char buf[160];
+            std::snprintf(buf, sizeof buf, "an SDMA copy of %zu bytes reported an error (%lld)",
+                          (op.balanced ? op.pieces[i] : op.copies[i]).bytes, (long long)v);
+            fail(HOCCL_ERR_HIP, buf);
+        }
+        return v <= 0;
+    }
+
+    size_t copies_ended(ProxyOp &op) {
+        size_t n = 0;
+        for (size_t i = 0; i < op.sig.size(); ++i) n += copy_ended(op, i);
+        return n;
+    }
+
+    void report_timeout(ProxyOp &op) {
+        size_t ended = 0;
+        for (size_t i = 0; i < op.sig.size(); ++i) ended += hsa_signal_load_scacquire(op.sig[i]) <= 0;
+        char buf[200];
+        if (op.balanced)
+            std::snprintf(buf, sizeof buf,
+                          "SDMA copies did not complete within the proxy timeout (balanced issue of %zu copies: "
+                          "%zu pieces issued, %zu ended%s)",
+                          op.copies.size(), op.bal.issued(), ended, op.bal.all_issued() ? "" : ", more to issue");
+        else
+            std::snprintf(buf, sizeof buf,
+                          "SDMA copies did not complete within the proxy timeout (%zu of %zu copies issued, "
+                          "%zu ended)",
+                          op.next, op.copies.size(), ended);
+        fail(HOCCL_ERR_TIMEOUT, buf);
     }
 
     void release(ProxyOp *op) {
@@ -275,25 +370,52 @@ class ProxyImpl {
                         op->start_seen = true;
                         progress = true;
                     }
-                    // Issue in order what may go: a gated copy once its gate
-                    // is open, an ungated one once the stream has started.
-                    while (op->next < op->copies.size()) {
-                        const int g = op->copies[op->next].gate;
-                        if (g < 0 ? !op->start_seen : !gate_open(*op, g)) break;
-                        issue_next(*op);
-                        op->since = now;
-                        progress = true;
+                    if (op->balanced) {
+                        // All copies share one gate (or none: the stream's start).
+                        const int g = op->copies[0].gate;
+                        const bool may_go = g < 0 ? op->start_seen : gate_open(*op, g);
+                        if (may_go && !op->bal.all_issued()) {
+                            if (issue_balanced(*op)) {
+                                op->since = now;
+                                progress = true;
+                            } else if (!op->timed_out && now - op->since >
+                                                             std::chrono::milliseconds(op->timeout_ms)) {
+                                // Copies in flight that never complete hold back the rest.
+                                op->timed_out = true;
+                                report_timeout(*op);
+                            }
+                        }
+                        if (!op->bal.all_issued() || !op->start_seen) break;
+                    } else {
+                        // Issue in order what may go: a gated copy once its
+                        // gate is open, an ungated one once the stream has
+                        // started.
+                        while (op->next < op->copies.size()) {
+                            const int g = op->copies[op->next].gate;
+                            if (g < 0 ? !op->start_seen : !gate_open(*op, g)) break;
+                            issue_next(*op);
+                            op->since = now;
+                            progress = true;
+                        }
+                        if (op->next < op->copies.size() || !op->start_seen) break;
                     }
-                    if (op->next < op->copies.size() || !op->start_seen) break;
-                    if (copies_done(*op)) {
-                        progress = true;
-                        store_flag(finish_flag(op->slot), kFinishValue);
-                        op->state = ProxyOp::WAIT_ACK;
-                        op->since = now;
-                    } else if (!op->timed_out &&
-                               now - op->since > std::chrono::milliseconds(op->timeout_ms)) {
-                        op->timed_out = true;
-                        fail(HOCCL_ERR_TIMEOUT, "SDMA copies did not complete within the proxy timeout");
+                    {
+                        // The watchdog runs on progress: a copy issued or
+                        // completed restarts it.
+                        const size_t ended = copies_ended(*op);
+                        if (ended == op->sig.size()) {
+                            progress = true;
+                            store_flag(finish_flag(op->slot), kFinishValue);
+                            op->state = ProxyOp::WAIT_ACK;
+                            op->since = now;
+                        } else if (ended > op->ended) {
+                            op->ended = ended;
+                            op->since = now;
+                        } else if (!op->timed_out &&
+                                   now - op->since > std::chrono::milliseconds(op->timeout_ms)) {
+                            op->timed_out = true;
+                            report_timeout(*op);
+                        }
                     }
                     break;
                 case ProxyOp::WAIT_ACK:
@@ -700,19 +822,38 @@ void Proxy::release_events(std::vector<hipEvent_t> &events) {
     events.clear();
 }
 
-hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engines,
+// Whether an operation's copies may be issued balanced: one gate for all,
+// and no copy waits for another (every chain a single copy, or stage-tagged
+// copies, which the stage schedule never makes wait).
+bool balance_eligible(const std::vector<ProxyCopy> &copies) {
+    if (copies.empty()) return false;
+    std::vector<int> chains;
+    chains.reserve(copies.size());
+    for (const ProxyCopy &c : copies) {
+        if (c.gate != copies[0].gate) return false;
+        chains.push_back(c.chain);
+    }
+    if (copies[0].stage >= 0) return true;
+    std::sort(chains.begin(), chains.end());
+    return std::adjacent_find(chains.begin(), chains.end()) == chains.end();
+}
+
+hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies_in, int max_engines, size_t slice_bytes,
                              unsigned timeout_ms, unsigned wait_limit_us, int handshake,
                              hipStream_t s, int *engines_used, std::string &err,
                              std::vector<hipEvent_t> gates) {
     ProxyImpl &P = *impl_;
-    for (const ProxyCopy &c : copies)
+    for (const ProxyCopy &c : copies_in)
         if (c.gate >= (int)gates.size()) {
             err = "a copy names a gate that was not given";
             release_events(gates);
             return HOCCL_ERR_INTERNAL;
         }
+    const std::vector<ProxyCopy> &copies = copies_in;
+    const bool balanced = slice_bytes > 0 && balance_eligible(copies);
     ProxyOp *op = new ProxyOp();
     op->timeout_ms = timeout_ms ? timeout_ms : 10000;
+    op->since = std::chrono::steady_clock::now();
     {
         // Each gate's copies are scheduled as a block of their own, the
         // gates in order and the ungated copies last, so a gate's block goes
@@ -738,8 +879,22 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         }
         if (engines_used) *engines_used = used;
     }
+    if (balanced) {
+        // The schedule's issue order (byte-balanced, flow-size interleaved,
+        // or stage by stage) is the order in which the engines of the
+        // budget take pieces of the copies.
+        int E = (int)P.engines.size();
+        if (max_engines > 0) E = std::min(E, max_engines);
+        std::vector<size_t> bytes;
+        for (const ProxyCopy &c : op->copies) bytes.push_back(c.bytes);
+        op->balanced = true;
+        op->slot_engine.assign(P.engines.begin(), P.engines.begin() + E);
+        op->bal = BalancedIssue(E, slice_bytes, 2 * slice_bytes, bytes);
+        if (engines_used) *engines_used = std::min(E, (int)op->copies.size());
+    }
     op->gates = std::move(gates);
     op->gate_open.assign(op->gates.size(), 0);
+    const size_t sig_wanted = op->balanced ? 0 : op->copies.size();
     // Signals and a flag slot.
     {
         std::unique_lock<std::mutex> lk(P.mu);
@@ -752,7 +907,7 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         }
         op->slot = P.free_slots.back();
         P.free_slots.pop_back();
-        while (op->sig.size() < op->copies.size() && !P.free_signals.empty()) {
+        while (op->sig.size() < sig_wanted && !P.free_signals.empty()) {
             op->sig.push_back(P.free_signals.back());
             P.free_signals.pop_back();
         }
@@ -764,7 +919,7 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
         P.free_slots.push_back(op->slot);
         delete op;
     };
-    while (op->sig.size() < op->copies.size()) {
+    while (op->sig.size() < sig_wanted) {
         hsa_signal_t sg;
         if (hsa_signal_create(1, 0, nullptr, &sg) != HSA_STATUS_SUCCESS) {
             err = "hsa_signal_create failed";
@@ -775,7 +930,8 @@ hoccl_status_t Proxy::submit(const std::vector<ProxyCopy> &copies, int max_engin
     }
     // Every copy's signal is armed before any is issued: a copy waits on its
     // chain predecessor's signal, which must read "pending" until that copy
-    // has been issued and has completed.
+    // has been issued and has completed.  (Balanced pieces take and arm
+    // their signals as they are issued.)
     for (auto &sg : op->sig) hsa_signal_store_screlease(sg, 1);
     // The handshake kernel runs on the caller's stream, or on the private
     // CU-masked stream when asked for (and that stream exists).

@@ -61,7 +61,15 @@ class Proxy {
     // Copies tagged with stages (all of them, or none) are scheduled stage
     // by stage instead: each stage's copies over the engines by bytes, every
     // engine's queue in stage order.
-    hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines,
+    // With slice_bytes > 0, an operation whose copies wait for no other copy
+    // and share one gate is issued balanced: the scheduled copies, in their
+    // issue order, are cut into guided pieces (the bytes still to be cut
+    // over twice the engine count, at least slice_bytes) that the engines
+    // pull in order, an engine taking a piece when it has none in flight or
+    // when the piece fits within 2 * slice_bytes with those it has.
+    // Otherwise (and with slice_bytes 0) every copy is issued at once on its
+    // scheduled engine.
+    hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines, size_t slice_bytes,
                           unsigned timeout_ms, unsigned wait_limit_us, int handshake,
                           hipStream_t s, int *engines_used, std::string &err,
                           std::vector<hipEvent_t> gates = {});

@@ -280,4 +280,97 @@ std::string schedule_to_json(const Schedule &s) {
     return os.str();
 }
 
+BalancedIssue::BalancedIssue(int engines, size_t min_piece, size_t window, const std::vector<size_t> &copy_bytes)
+    : min_piece_(std::max<size_t>(min_piece, 4096)), window_(window), copy_bytes_(copy_bytes),
+      inflight_((size_t)std::max(engines, 1)), inflight_bytes_((size_t)std::max(engines, 1), 0),
+      rate_((size_t)std::max(engines, 1), 0.0), last_done_us_((size_t)std::max(engines, 1), 0.0) {
+    for (size_t b : copy_bytes) unissued_ += b;
+    total_ = unissued_;
+    took_.assign(inflight_.size(), 0);
+    while (cur_ < copy_bytes_.size() && copy_bytes_[cur_] == 0) ++cur_;
+}
+
+size_t BalancedIssue::next_bytes(size_t e) const {
+    const size_t r = copy_bytes_[cur_] - off_;
+    const double E = (double)inflight_.size();
+    if (!took_[e] && (double)r * E <= (double)total_) return r;
+    size_t g = (size_t)std::ceil((double)unissued_ / E);
+    g = std::max(min_piece_, (g + 4095) & ~(size_t)4095);
+    return r <= g || r - g < min_piece_ / 2 ? r : g;
+}
+
+void BalancedIssue::advance(size_t b) {
+    unissued_ -= b;
+    off_ += b;
+    if (off_ == copy_bytes_[cur_]) {
+        off_ = 0;
+        ++cur_;
+        while (cur_ < copy_bytes_.size() && copy_bytes_[cur_] == 0) ++cur_;
+    }
+}
+
+// The engine's oldest piece has completed (seen at now_us): it started when
+// it was issued or when the engine's previous piece completed, whichever
+// was later; its bytes over that time update the engine's rate (mean of the
+// new and the old estimate).
+void BalancedIssue::retire(size_t e, double now_us) {
+    std::deque<int> &f = inflight_[e];
+    const int i = f.front();
+    const double start = std::max(issued_us_[(size_t)i], last_done_us_[e]);
+    const double busy = now_us - start;
+    if (busy > 0) {
+        const double r = (double)piece_bytes_[(size_t)i] / busy;
+        rate_[e] = rate_[e] > 0 ? 0.5 * (rate_[e] + r) : r;
+    }
+    last_done_us_[e] = now_us;
+    inflight_bytes_[e] -= piece_bytes_[(size_t)i];
+    inflight_total_ -= piece_bytes_[(size_t)i];
+    f.pop_front();
+}
+
+// Time until engine e has run what it holds, at rate r.  The oldest piece
+// has been running since it was issued or since the previous completion;
+// once it is overdue, the time it has overrun counts as still to come, so
+// an engine that stopped completing looks ever busier instead of idle.
+double BalancedIssue::drain_us(size_t e, double now_us, double r) const {
+    const std::deque<int> &f = inflight_[e];
+    if (f.empty()) return 0.0;
+    const int i = f.front();
+    const double start = std::max(issued_us_[(size_t)i], last_done_us_[e]);
+    const double expect = (double)piece_bytes_[(size_t)i] / r, ran = now_us - start;
+    double t = ran < expect ? expect - ran : ran - expect;
+    t += (double)(inflight_bytes_[e] - piece_bytes_[(size_t)i]) / r;
+    return t;
+}
+
+// Whether engine e should take a piece of b bytes: it would finish it
+// before the projected end of the operation (what all engines hold plus
+// every unissued byte, over the sum of their rates), or within 15% (and
+// 20 us) of the earliest finish any engine could give it.  Engines not yet
+// measured are taken at the mean of the measured ones; before any
+// measurement every engine qualifies.
+bool BalancedIssue::earliest(size_t e, size_t b, double now_us) const {
+    double sum = 0;
+    int known = 0;
+    for (double r : rate_)
+        if (r > 0) {
+            sum += r;
+            ++known;
+        }
+    if (known == 0) return true;
+    const double mean = sum / known;
+    double total_rate = 0, held = 0, best = 1e300;
+    for (size_t k = 0; k < inflight_.size(); ++k) {
+        const double r = rate_[k] > 0 ? rate_[k] : mean;
+        const double d = drain_us(k, now_us, r);
+        total_rate += r;
+        held += d * r;
+        best = std::min(best, d + (double)b / r);
+    }
+    const double r = rate_[e] > 0 ? rate_[e] : mean;
+    const double mine = drain_us(e, now_us, r) + (double)b / r;
+    const double end = (held + (double)unissued_) / total_rate;
+    return mine <= end || mine <= 1.15 * best + 20.0;
+}
+
 }  // namespace hoccl

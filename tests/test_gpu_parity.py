@@ -499,15 +499,26 @@ def test_engine_proxy_handshakes(handshake):
             assert_bitwise(from_dev(out[r], hc.FP32), ref[r], f"handshake={handshake} direct={direct} r={r}")
 
 
-def test_proxy_watchdog_reports_timeout_then_recovers():
-    """Failure handling forced from the host: a 1 ms watchdog on copies that
-    take several ms.  The copies still complete (results are right), the
-    next call reports HOCCL_ERR_TIMEOUT once, and the call after that works."""
-    R, n = 8, 1 << 24
+def watchdog_allgather(slice_bytes):
+    """An all-gather whose copies make no progress for longer than a 1 ms
+    watchdog: 128 MiB shards on one engine, about 2 ms per copy."""
+    R, n = 8, 1 << 26
     x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
     recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
-    hc.set_config(copy_path="engines", proxy_timeout_ms=1)
+    hc.set_config(copy_path="engines", sdma_engines=1, proxy_timeout_ms=1, proxy_slice_bytes=slice_bytes)
     hc.allgather(x, recv)
+    return R, n, x, recv
+
+
+@pytest.mark.parametrize("slice_bytes", [0, (1 << 64) - 1])
+def test_proxy_watchdog_reports_timeout_then_recovers(slice_bytes):
+    """Failure handling forced from the host: a 1 ms watchdog on copies that
+    each take about 2 ms, with balanced issue and with every copy issued at
+    once.  The copies still complete (results are right), the next call
+    reports HOCCL_ERR_TIMEOUT once, and the call after that works."""
+    if hc.sdma_engine_count() == 0:
+        pytest.skip("engine proxy unavailable")
+    R, n, x, recv = watchdog_allgather(slice_bytes)
     torch.cuda.synchronize()
     for r in (0, R - 1):
         for s in range(R):
@@ -530,11 +541,8 @@ def test_stored_timeout_reported_before_anything_is_enqueued():
     same all-reduce runs and matches the oracle."""
     if hc.sdma_engine_count() == 0:
         pytest.skip("engine proxy unavailable")
-    R, n = 8, 1 << 24
-    x = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(R)]
-    recv = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
-    hc.set_config(copy_path="engines", proxy_timeout_ms=1, reduce_algo="ring")
-    hc.allgather(x, recv)
+    R = watchdog_allgather(0)[0]
+    hc.set_config(reduce_algo="ring")
     torch.cuda.synchronize()
     m = 300_007
     xa = [W.random_values("fp32", 97, r, m) for r in range(R)]

@@ -1,7 +1,8 @@
 """Randomised GPU parity: 160 seeded cases, each drawing a collective, dtype,
 rank count (up to 64), ragged count, misaligned buffer offset, copy path,
-reduction algorithm, launch shape and group options, run through the C ABI
-and compared bit for bit with the oracle."""
+reduction algorithm, launch shape, group options and the engine proxy's
+issue mode, run through the C ABI and compared bit for bit with the
+oracle."""
 import numpy as np
 import pytest
 import torch
@@ -21,7 +22,7 @@ def draw(i):
     g = np.random.default_rng([9001, i])
     R = int(g.choice([1, 2, 3, 4, 5, 7, 8, 13, 64], p=[.04, .12, .12, .14, .08, .1, .25, .08, .07]))
     n = int(g.integers(1, 40_000 if R <= 8 else 600))
-    return dict(
+    c = dict(
         op=str(g.choice(["allreduce", "reduce_scatter", "allgather", "sendrecv", "alltoall", "alltoallv"])),
         dt=[hc.INT32, hc.FP32, hc.BF16][int(g.integers(0, 3))], R=R, n=n,
         lead=int(g.choice([0, 1, 3, 8])),
@@ -35,6 +36,10 @@ def draw(i):
                  chunk_bytes=int(g.choice([0, 0, 8192])),
                  a2a_schedule=int(g.choice([0, 0, 1, 2]))),
         seed=int(g.integers(0, 1 << 30)))
+    # Drawn last so the earlier fields keep their values: the engine
+    # proxy's balanced issue (automatic, 64 KiB pieces) or all at once.
+    c["cfg"]["proxy_slice_bytes"] = int(g.choice([0, 0, 64 << 10, (1 << 64) - 1]))
+    return c
 
 
 def dev_views(arrays, dt, lead):

@@ -1,8 +1,9 @@
 """The host code under AddressSanitizer and UBSan (CPU only): the planner and
 the collective scheduler replay every plan shape on exactly-sized host
-buffers, and the C oracle runs every function the same way.  A read or write
+buffers, the C oracle runs every function the same way, and the engine
+proxy's balanced issue runs against simulated engines.  A read or write
 outside a documented buffer, or undefined behaviour such as signed overflow,
-fails the run.  The two drivers are built separately and share nothing."""
+fails the run.  The oracle's driver shares nothing with the other two."""
 import os
 import shutil
 import subprocess
@@ -43,3 +44,14 @@ def test_oracle_under_sanitizers(tmp_path):
            os.path.join(HERE, "native", "oracle_bounds.c"), "-o", exe]
     out = _run(cmd, tmp_path, exe)
     assert "oracle cases run: 672" in out, out
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
+def test_proxy_balanced_issue_simulation(tmp_path):
+    """The SDMA proxy's balanced issue against simulated engines (one at
+    half rate, all equal, all work on one engine, a failed issue)."""
+    exe = str(tmp_path / "balance_sim")
+    cmd = ["g++", "-std=c++17", *SAN, os.path.join(HERE, "native", "balance_sim.cpp"),
+           os.path.join(CSRC, "schedule.cpp"), "-o", exe]
+    out = _run(cmd, tmp_path, exe)
+    assert "balance cases: 133" in out, out
