@@ -1070,8 +1070,9 @@ def bench_after_free(hc, W):
     del src, dst
     torch.cuda.empty_cache()
     time.sleep(1.5)
-    # The default engine budget (4 engines, which the release never slows):
-    # what balanced issue costs or gains where no engine is slow, settled.
+    # The default engine budget (4 engines, which the release never slows,
+    # and which issues every copy at once by default): what balanced issue
+    # would cost or gain there, settled.
     dflt = {}
     send_np, counts, sd, rd, rsz = W.a2a_tokens(R)
     ep_s = [bf16_dev(a) for a in send_np]
@@ -1086,7 +1087,7 @@ def bench_after_free(hc, W):
                      ("ep_alltoallv", lambda: hc.alltoallv(ep_s, counts, sd, ep_r, rd)),
                      ("allgather_fsdp", lambda: hc.allgather(fs, fr))):
         row = {}
-        for mode, sl in (("static", SMAX), ("balanced", 0)):
+        for mode, sl in (("static", SMAX), ("balanced", 4 * MiB)):
             with hc.config(copy_path="engines", sdma_engines=0, proxy_slice_bytes=sl):
                 for _ in range(2):
                     one(fn)

@@ -243,26 +243,36 @@ typedef struct {
                                    stage; on the SDMA path this returns
                                    HOCCL_ERR_UNSUPPORTED, enqueuing
                                    nothing).  The HIP path ignores stages  */
-    size_t proxy_slice_bytes;   /* how the SDMA proxy hands an operation's
-                                   copies to its engines when no copy waits
-                                   for another (send/recv, direct all-gather,
-                                   all-to-all(v)): the scheduled copies are
-                                   cut into pieces of the bytes still to be
-                                   cut over twice the engine count (whole
-                                   copies while much remains, this many
-                                   bytes at least: a multiple of 4096,
-                                   >= 64 KiB) that the engines pull in
-                                   order, an engine taking the next piece
-                                   when it has none in flight or when the
-                                   piece fits within twice this many bytes
-                                   with those it has.  An engine slowed by
-                                   other work then takes fewer pieces
-                                   instead of holding back the operation
-                                   (flow-size-aware chunk scheduling).
-                                   0 = automatic (4 MiB); SIZE_MAX = every
-                                   copy issued at once on its scheduled
-                                   engine.  Copies that wait for others (the
-                                   ring all-gather, the reduce-scatter /
+    size_t proxy_slice_bytes;   /* balanced issue on the SDMA path, for
+                                   operations whose copies wait for no
+                                   other (send/recv, direct all-gather,
+                                   all-to-all(v)): instead of issuing every
+                                   copy at once on its scheduled engine,
+                                   the proxy lets the engines take pieces
+                                   in the schedule's order as they have
+                                   room (two pieces, or twice this many
+                                   bytes, in flight each).  An engine's
+                                   first piece is a whole copy; later ones
+                                   are the unissued bytes over the engine
+                                   count, at least this many bytes.  An
+                                   engine takes a piece only if it would
+                                   finish it before the operation's
+                                   projected end or about as early as any
+                                   engine, from rates measured on its
+                                   completed pieces; so an engine slowed by
+                                   other work (for a while after a large
+                                   device free, engine 1) costs only its
+                                   share (flow-size-aware chunk
+                                   scheduling).  A multiple of 4096,
+                                   >= 64 KiB.  0 = automatic: 4 MiB with 8
+                                   or more engines, and every copy at once
+                                   with fewer (the automatic 4 engines,
+                                   which the release does not slow, where
+                                   balanced issue raised a concurrent
+                                   GEMM's loss by about half a point);
+                                   SIZE_MAX = every copy at once.  Copies
+                                   that wait for others (the ring
+                                   all-gather, the reduce-scatter /
                                    all-reduce gathers) and graph captures
                                    are always issued at once               */
 } hoccl_config_t;

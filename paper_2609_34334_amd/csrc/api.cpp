@@ -414,17 +414,23 @@ int engine_budget(const hoccl_config_t &cfg) {
 }
 
 // Smallest piece of the proxy's balanced issue (0 asks the proxy to issue
-// every copy at once).  Freeing a large device allocation slows one SDMA
-// engine to about half its rate for tens of ms per GiB freed; with every
+// every copy at once).  Freeing a large device allocation slows SDMA
+// engine 1 to about half its rate for tens of ms per GiB freed; with every
 // copy issued at once, an all-gather on all 16 engines then waits for that
-// engine (443 instead of 700 GB/s).  Pieces pulled by free engines give the
-// slowed engine only what it can finish; an engine command costs about
-// 7 us to start, so the pieces stay whole copies while much remains.
+// engine (58 instead of 94 GB/s per rank).  Pieces pulled by the engines,
+// with a finish-time gate, give the slowed engine only what it can finish
+// (94 GB/s).  Automatic: balanced from kBalancedMinEngines engines up.  The
+// automatic budget of 4 (engines 2-5, never slowed by the release) issues
+// every copy at once: balanced issue there raised a concurrent GEMM's loss
+// beside the FSDP all-gather from 0.8-1.5% to 1.4-2.1% (three alternating
+// runs of 100 pairs) and made the EP all-to-all(v) 1.7% slower.
 constexpr size_t kProxySliceBytes = (size_t)4 << 20;
+constexpr int kBalancedMinEngines = 8;
 
 size_t proxy_slice(const hoccl_config_t &cfg) {
     if (cfg.proxy_slice_bytes == SIZE_MAX) return 0;
-    return cfg.proxy_slice_bytes ? cfg.proxy_slice_bytes : kProxySliceBytes;
+    if (cfg.proxy_slice_bytes) return cfg.proxy_slice_bytes;
+    return engine_budget(cfg) >= kBalancedMinEngines ? kProxySliceBytes : 0;
 }
 
 // With record_groups, an event is recorded on s after each group's last

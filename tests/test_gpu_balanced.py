@@ -87,12 +87,12 @@ def test_sendrecv_small_pieces_odd_sizes(engines):
         assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"send/recv rank {r}")
 
 
-@pytest.mark.parametrize("slice_bytes", [64 << 10, 0, SIZE_MAX])
-def test_alltoallv_ep_balanced_and_static(slice_bytes):
+@pytest.mark.parametrize("engines,slice_bytes", [(0, 64 << 10), (0, 0), (0, SIZE_MAX), (16, 0)])
+def test_alltoallv_ep_balanced_and_static(engines, slice_bytes):
     send_np, counts, sd, rd, rsz = W.a2a_tokens(R)
     send = [to_dev(a, hc.BF16) for a in send_np]
     recv = [torch.zeros(s, dtype=torch.bfloat16, device="cuda") for s in rsz]
-    hc.set_config(copy_path="engines", sdma_engines=0, proxy_slice_bytes=slice_bytes)
+    hc.set_config(copy_path="engines", sdma_engines=engines, proxy_slice_bytes=slice_bytes)
     hc.alltoallv(send, counts, sd, recv, rd)
     torch.cuda.synchronize()
     ref = [np.zeros(s, np.uint16) for s in rsz]

@@ -510,7 +510,7 @@ def watchdog_allgather(slice_bytes):
     return R, n, x, recv
 
 
-@pytest.mark.parametrize("slice_bytes", [0, (1 << 64) - 1])
+@pytest.mark.parametrize("slice_bytes", [4 << 20, (1 << 64) - 1])
 def test_proxy_watchdog_reports_timeout_then_recovers(slice_bytes):
     """Failure handling forced from the host: a 1 ms watchdog on copies that
     each take about 2 ms, with balanced issue and with every copy issued at
@@ -541,7 +541,7 @@ def test_stored_timeout_reported_before_anything_is_enqueued():
     same all-reduce runs and matches the oracle."""
     if hc.sdma_engine_count() == 0:
         pytest.skip("engine proxy unavailable")
-    R = watchdog_allgather(0)[0]
+    R = watchdog_allgather(4 << 20)[0]
     hc.set_config(reduce_algo="ring")
     torch.cuda.synchronize()
     m = 300_007
