@@ -975,7 +975,8 @@ def bench_after_free(hc, W):
     allocation) hands memory back, and while the driver releases it one
     engine runs at about half rate.  Per workload on all 16 engines: every
     copy issued at once on its scheduled engine (proxy_slice_bytes =
-    SIZE_MAX) against the default balanced issue, settled (1.5 s after the
+    SIZE_MAX) against balanced issue with 4 MiB pieces (what the automatic
+    setting picks for these sizes on 16 engines), settled (1.5 s after the
     last free) and in the first milliseconds after freeing 2 GiB.  Then each
     of four engines alone, settled and right after a free: which engine the
     release slows."""
@@ -1030,7 +1031,7 @@ def bench_after_free(hc, W):
             recv = [torch.empty(R * x[0].size, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
             fn, per_rank = (lambda: hc.allgather(send, recv)), R * x[0].size * 2
         row = {}
-        for mode, sl in (("static", SMAX), ("balanced", 0)):
+        for mode, sl in (("static", SMAX), ("balanced", 4 * MiB)):
             row[mode] = measure(fn, per_rank, copy_path="engines", sdma_engines=16, proxy_slice_bytes=sl)
         log(f"  after free, {name}: static {row['static']['ms']} / {row['static']['after_free_ms']} ms, "
             f"balanced {row['balanced']['ms']} / {row['balanced']['after_free_ms']} ms")

@@ -265,11 +265,14 @@ typedef struct {
                                    share (flow-size-aware chunk
                                    scheduling).  A multiple of 4096,
                                    >= 64 KiB.  0 = automatic: 4 MiB with 8
-                                   or more engines, and every copy at once
-                                   with fewer (the automatic 4 engines,
+                                   or more engines for operations of at
+                                   least 64 MiB per engine, every copy at
+                                   once otherwise (the automatic 4 engines,
                                    which the release does not slow, where
                                    balanced issue raised a concurrent
-                                   GEMM's loss by about half a point);
+                                   GEMM's loss by about half a point, and
+                                   smaller operations, where it cost more
+                                   than a slowed engine could);
                                    SIZE_MAX = every copy at once.  Copies
                                    that wait for others (the ring
                                    all-gather, the reduce-scatter /

@@ -419,18 +419,25 @@ int engine_budget(const hoccl_config_t &cfg) {
 // copy issued at once, an all-gather on all 16 engines then waits for that
 // engine (58 instead of 94 GB/s per rank).  Pieces pulled by the engines,
 // with a finish-time gate, give the slowed engine only what it can finish
-// (94 GB/s).  Automatic: balanced from kBalancedMinEngines engines up.  The
+// (94 GB/s).  Automatic: balanced from kBalancedMinEngines engines up, for
+// operations that move at least kBalancedMinBytesPerEngine per engine.  The
 // automatic budget of 4 (engines 2-5, never slowed by the release) issues
 // every copy at once: balanced issue there raised a concurrent GEMM's loss
 // beside the FSDP all-gather from 0.8-1.5% to 1.4-2.1% (three alternating
-// runs of 100 pairs) and made the EP all-to-all(v) 1.7% slower.
+// runs of 100 pairs) and made the EP all-to-all(v) 1.7% slower.  Below
+// 64 MiB per engine it cost more than a slowed engine could: a 32 MiB
+// message on 16 engines took 123-146 us against 113-131.
 constexpr size_t kProxySliceBytes = (size_t)4 << 20;
 constexpr int kBalancedMinEngines = 8;
+constexpr unsigned long long kBalancedMinBytesPerEngine = 64ull << 20;
 
-size_t proxy_slice(const hoccl_config_t &cfg) {
+size_t proxy_slice(const hoccl_config_t &cfg, unsigned long long copy_bytes) {
     if (cfg.proxy_slice_bytes == SIZE_MAX) return 0;
     if (cfg.proxy_slice_bytes) return cfg.proxy_slice_bytes;
-    return engine_budget(cfg) >= kBalancedMinEngines ? kProxySliceBytes : 0;
+    const int E = engine_budget(cfg);
+    return E >= kBalancedMinEngines && copy_bytes >= (unsigned long long)E * kBalancedMinBytesPerEngine
+               ? kProxySliceBytes
+               : 0;
 }
 
 // With record_groups, an event is recorded on s after each group's last
@@ -600,7 +607,7 @@ hoccl_status_t run_engine_groups(DeviceState &st, const hoccl_config_t &cfg, con
         cps.push_back(pc);
     }
     int ne = 0;
-    r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg), cfg.proxy_timeout_ms,
+    r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg, p.copy_bytes), cfg.proxy_timeout_ms,
                          cfg.proxy_wait_limit_us, handshake, s, &ne, t_err, std::move(gates));
     if (r == HOCCL_OK) t_stats.copy_ops += (int)cps.size();
     return r;
@@ -738,10 +745,10 @@ hoccl_status_t enqueue_body(DeviceState &st, const hoccl_config_t &cfg, const Pl
                 return HOCCL_ERR_HIP;
             }
             for (ProxyCopy &c : cps) c.gate = 0;
-            r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg), cfg.proxy_timeout_ms,
+            r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg, p.copy_bytes), cfg.proxy_timeout_ms,
                                  cfg.proxy_wait_limit_us, handshake, s, &ne, t_err, std::move(gate));
         } else {
-            r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg), cfg.proxy_timeout_ms,
+            r = st.proxy->submit(cps, engine_budget(cfg), proxy_slice(cfg, p.copy_bytes), cfg.proxy_timeout_ms,
                                  cfg.proxy_wait_limit_us, handshake, s, &ne, t_err);
         }
         if (r != HOCCL_OK) return r;

@@ -345,8 +345,8 @@ double BalancedIssue::drain_us(size_t e, double now_us, double r) const {
 
 // Whether engine e should take a piece of b bytes: it would finish it
 // before the projected end of the operation (what all engines hold plus
-// every unissued byte, over the sum of their rates), or within 15% (and
-// 20 us) of the earliest finish any engine could give it.  Engines not yet
+// every unissued byte, over the sum of their rates), or within 5% (and
+// 10 us) of the earliest finish any engine could give it.  Engines not yet
 // measured are taken at the mean of the measured ones; before any
 // measurement every engine qualifies.
 bool BalancedIssue::earliest(size_t e, size_t b, double now_us) const {
@@ -370,7 +370,7 @@ bool BalancedIssue::earliest(size_t e, size_t b, double now_us) const {
     const double r = rate_[e] > 0 ? rate_[e] : mean;
     const double mine = drain_us(e, now_us, r) + (double)b / r;
     const double end = (held + (double)unissued_) / total_rate;
-    return mine <= end || mine <= 1.15 * best + 20.0;
+    return mine <= end || mine <= 1.05 * best + 10.0;
 }
 
 }  // namespace hoccl

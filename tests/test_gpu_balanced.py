@@ -38,7 +38,7 @@ def free_2gib():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("slice_bytes", [0, SIZE_MAX])
+@pytest.mark.parametrize("slice_bytes", [0, 4 << 20, SIZE_MAX])
 def test_allgather_16_engines_after_free(slice_bytes):
     n = (16 << 20) // 4                      # 16 MiB shards: 64 copies of 16 MiB
     x = [W.random_bits(700, r, n, 4).view(np.int32) for r in range(R)]
@@ -59,7 +59,7 @@ def test_alltoall_16_engines_after_free():
     x = [W.random_bits(701, r, R * n, 4).view(np.int32) for r in range(R)]
     send = [to_dev(a, hc.INT32) for a in x]
     recv = [torch.full((R * n,), -7, dtype=torch.int32, device="cuda") for _ in range(R)]
-    hc.set_config(copy_path="engines", sdma_engines=16)
+    hc.set_config(copy_path="engines", sdma_engines=16, proxy_slice_bytes=4 << 20)
     free_2gib()
     hc.alltoall(send, recv)
     torch.cuda.synchronize()
