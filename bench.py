@@ -1228,11 +1228,14 @@ def bench_callback_thread(hc, reps=5):
                                           alone=med(hsa_rows["idle"]), runs=hsa_rows))
 
 
-def bench_small_message(hc, reps):
+def bench_small_message(hc, reps, gemm=None):
     """Latency of one 4 KiB send/recv (rank 0 -> 1) through each copy path:
     the engine proxy's flag handshake (host function, and the one-lane
     kernel), the HIP runtime's copy, and the CU copy kernel; plus the host
-    time of the call."""
+    time of the call.  With `gemm`: the slowdown of the bf16 GEMM beside a
+    loop of 40 such messages on the engines, per handshake form (why AUTO
+    keeps the host function, whose copies need no CU, although the kernel
+    form's round trip is shorter)."""
     import torch
     src = torch.zeros(2048, dtype=torch.bfloat16, device="cuda")
     dst = torch.empty_like(src)
@@ -1249,6 +1252,16 @@ def bench_small_message(hc, reps):
         out[name] = dict(device_us=round(med * 1e6, 2), device_min_us=round(mn * 1e6, 2),
                          host_call_us=round(statistics.median(host) * 1e6, 2))
     hc.set_config(copy_path="auto", proxy_handshake=-1)
+    if gemm is not None:
+        loop = {}
+        for name, hs in (("host_function", 2), ("kernel", 0)):
+            with hc.config(copy_path="engines", proxy_handshake=hs):
+                run = lambda st: [hc.sendrecv([src, src], [dst, dst], [1, -1], stream=st) for _ in range(40)]
+                med, _ = event_time(lambda: run(None), 3)
+                row = interference(hc, run, med, gemm, pairs=60)
+            loop[name] = dict(ms_per_40=round(med * 1e3, 3), gemm_slowdown=row["gemm_slowdown"],
+                              gemm_slowdown_ci95=row["gemm_slowdown_ci95"])
+        out["loop_of_40_beside_gemm"] = loop
     return dict(workload="one 4 KiB message rank 0 -> 1 (stream-manager round trip)", **out)
 
 
@@ -1709,7 +1722,7 @@ def main():
             extra["ring_hop_one_rank"] = {"error": repr(e)}
         log("p2p sizes")
         extra["p2p_single_message"] = bench_p2p_sizes(hc, 11)
-        extra["small_message_latency"] = bench_small_message(hc, 30)
+        extra["small_message_latency"] = bench_small_message(hc, 30, gemm)
         log("host callbacks beside the host-function handshake")
         try:
             extra["callback_thread"] = bench_callback_thread(hc)
