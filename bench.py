@@ -812,6 +812,47 @@ def bench_ring_hop(hc, x, reps):
                          "bf16 local block, fp32 partial (hoccl_ring_hop)", **out)
 
 
+def bench_rs_launch_shapes(hc, x, steps=20):
+    """The headline ring reduce-scatter at other launch shapes and ring-group
+    sizes than the automatic ones: workgroups per launch x threads per
+    workgroup, and the fp32 partials' group budget.  Per point the best of
+    3 runs of `steps` back-to-back reduce-scatters (HIP events, current
+    stream), in microseconds per reduce-scatter."""
+    import torch
+    R = len(x)
+    n = x[0].size // R
+    send = [bf16_dev(a) for a in x]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+
+    def run():
+        for _ in range(5):
+            hc.reduce_scatter(send, recv)
+        torch.cuda.synchronize()
+        best = None
+        for _ in range(3):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(steps):
+                hc.reduce_scatter(send, recv)
+            b.record()
+            b.synchronize()
+            t = a.elapsed_time(b) / steps * 1e3
+            best = t if best is None else min(best, t)
+        return round(best, 2)
+    shapes, groups = {}, {}
+    for w in (0, 1024, 4096, 8192):
+        for t in (256, 512, 1024):
+            with hc.config(reduce_algo="ring", workgroups_per_step=w, threads_per_workgroup=t):
+                shapes[f"{'auto' if w == 0 else w}x{t}"] = run()
+    for g, name in ((0, "default"), ((1 << 64) - 1, "one_group"), (32 << 20, "32MiB"), (64 << 20, "64MiB"),
+                    (128 << 20, "128MiB")):
+        with hc.config(reduce_algo="ring", ring_group_bytes=g):
+            groups[name] = run()
+    return dict(workload="the headline ring reduce-scatter (bf16, R=8, 25,165,824 elements per rank), "
+                         "us per reduce-scatter", workgroups_x_threads=shapes, ring_group_bytes=groups)
+
+
 def bench_rs_variants(hc, reps):
     """The ring reduce-scatter beyond the headline: the same 25,165,824
     elements per rank in fp32 and int32 (12 bytes per element per step), and
@@ -1705,6 +1746,11 @@ def main():
             extra["reduce_scatter_variants"] = bench_rs_variants(hc, 10)
         except Exception as e:
             extra["reduce_scatter_variants"] = {"error": repr(e)}
+        log("reduce-scatter launch shapes")
+        try:
+            extra["reduce_scatter_launch_shapes"] = bench_rs_launch_shapes(hc, rs["x"])
+        except Exception as e:
+            extra["reduce_scatter_launch_shapes"] = {"error": repr(e)}
         log("reduce-scatter with fused ring hops")
         try:
             extra["reduce_scatter_fused_hops"] = bench_fused_hops(hc, rs["x"], args.steps, args.warmup)
