@@ -167,8 +167,11 @@ typedef struct {
                                    after its reduction has completed);
                                    0 = automatic: 2 on the SDMA path outside
                                    graph capture when each rank holds at
-                                   least 32 MiB, else 1 (plan dumps assume
-                                   the SDMA path)                              */
+                                   least 32 MiB and the engine budget is 8
+                                   or more (with fewer engines the gather
+                                   dwarfs the reduction it would overlap),
+                                   else 1 (plan dumps assume the SDMA
+                                   path)                                       */
     /* ---- extensions ---- */
     int sdma_engines;           /* engines the SDMA path may use, 1..32 (at
                                    most those available, 16 on MI355X);

@@ -972,11 +972,19 @@ bool size_overflows(size_t a, size_t b) {
 // group.
 constexpr size_t kRingGroupBytesDefault = (size_t)256 << 20;
 
+// Automatic all-reduce chunk groups need enough engines: the overlap of a
+// group's gather with the next group's reduction pays only while the
+// gather is not far longer than the reduction.  bf16, R = 8, 48 MiB per
+// rank, one group against two: 4 engines 1.91 / 1.98 ms, 8 engines 1.30 /
+// 1.26, 12 engines 1.01 / 0.96, 16 engines 0.88 / 0.81.
+constexpr int kAutoGroupsMinEngines = 8;
+
 PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
     PlanOptions o;
     o.group_partial_bytes = cfg.ring_group_bytes ? cfg.ring_group_bytes : kRingGroupBytesDefault;
     o.allgather_direct = cfg.allgather_direct != 0;
     o.allreduce_groups = cfg.allreduce_chunk_groups;  // 0: automatic
+    if (o.allreduce_groups == 0 && engine_budget(cfg) < kAutoGroupsMinEngines) o.allreduce_groups = 1;
     o.chunk_bytes = cfg.chunk_bytes;
     o.in_place = in_place;
     o.algo = cfg.reduce_algo;

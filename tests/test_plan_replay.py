@@ -233,17 +233,26 @@ def test_cache_groups_bound_partials_and_keep_bytes():
 
 def test_automatic_allreduce_groups():
     """allreduce_chunk_groups 0 (the default) plans two groups once each
-    rank holds at least 32 MiB and one below (plan dumps assume the engine
-    path); an explicit count wins."""
+    rank holds at least 32 MiB and one below, on an engine budget of 8 or
+    more; on the automatic budget of 4 it plans one (plan dumps assume the
+    engine path); an explicit count wins."""
     assert hc.get_config()["allreduce_chunk_groups"] == 0
     R = 8
-    below = hc.plan_json(hc.OP_ALLREDUCE, (16 << 20) // 2, hc.BF16, R)
-    at = hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)
-    assert below["ngroups"] == 1 and at["ngroups"] == 2
-    assert [s["group"] for s in at["reduce_steps"]] == [g for g in range(2) for _ in range(R - 1)]
-    assert {c["group"] for c in at["copies"]} == {0, 1}
-    with hc.config(allreduce_chunk_groups=1):
+    at_default = hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)
+    assert at_default["ngroups"] == 1
+    for engines in (8, 16):
+        with hc.config(sdma_engines=engines):
+            below = hc.plan_json(hc.OP_ALLREDUCE, (16 << 20) // 2, hc.BF16, R)
+            at = hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)
+        assert below["ngroups"] == 1 and at["ngroups"] == 2
+        assert [s["group"] for s in at["reduce_steps"]] == [g for g in range(2) for _ in range(R - 1)]
+        assert {c["group"] for c in at["copies"]} == {0, 1}
+    with hc.config(sdma_engines=7):
         assert hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)["ngroups"] == 1
+    with hc.config(allreduce_chunk_groups=1, sdma_engines=16):
+        assert hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)["ngroups"] == 1
+    with hc.config(allreduce_chunk_groups=2):
+        assert hc.plan_json(hc.OP_ALLREDUCE, (32 << 20) // 2, hc.BF16, R)["ngroups"] == 2
 
 
 @pytest.mark.parametrize("hops,per_element,launches", [(1, 66, 7), (2, 42, 4), (4, 26, 2), (7, 18, 1)])
