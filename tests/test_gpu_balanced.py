@@ -108,3 +108,29 @@ def test_slice_bytes_validation():
     hc.set_config(proxy_slice_bytes=64 << 10)
     hc.set_config(proxy_slice_bytes=SIZE_MAX)
     hc.set_config(proxy_slice_bytes=0)
+
+
+def test_pipeline_schedule_queued_ahead_balanced():
+    """The pipeline schedule's 32 rounds (16 microbatches, forward then
+    backward, 7 messages of 16 MiB each) enqueued ahead on one stream, on
+    16 engines with 4 MiB pieces: every round's copies go out by balanced
+    issue as its gate opens, each round into buffers of its own, and every
+    message matches the oracle."""
+    n = 2048 * 4096
+    mbs = 16
+    xs = [[W.random_bits(710 + mb, r, n, 2) for r in range(R)] for mb in range(mbs)]
+    send = [[to_dev(a, hc.BF16) for a in x] for x in xs]
+    fwd = [r + 1 if r + 1 < R else -1 for r in range(R)]
+    bwd = [r - 1 for r in range(R)]
+    rounds = [(mb, peers) for mb in range(mbs) for peers in (fwd, bwd)]
+    recv = [[torch.full((n,), 0x7A5A, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+             for _ in range(R)] for _ in rounds]
+    hc.set_config(copy_path="engines", sdma_engines=16, proxy_slice_bytes=4 << 20)
+    for i, (mb, peers) in enumerate(rounds):
+        hc.sendrecv(send[mb], recv[i], peers)
+    torch.cuda.synchronize()
+    for i, (mb, peers) in enumerate(rounds):
+        ref = [np.full(n, 0x7A5A, np.uint16) for _ in range(R)]
+        oracle.sendrecv(xs[mb], ref, peers, n, hc.BF16)
+        for r in range(R):
+            assert_bitwise(from_dev(recv[i][r], hc.BF16), ref[r], f"round {i} rank {r}")
