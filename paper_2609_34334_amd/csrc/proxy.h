@@ -62,11 +62,14 @@ class Proxy {
     // by stage instead: each stage's copies over the engines by bytes, every
     // engine's queue in stage order.
     // With slice_bytes > 0, an operation whose copies wait for no other copy
-    // and share one gate is issued balanced: the scheduled copies, in their
-    // issue order, are cut into guided pieces (the bytes still to be cut
-    // over twice the engine count, at least slice_bytes) that the engines
-    // pull in order, an engine taking a piece when it has none in flight or
-    // when the piece fits within 2 * slice_bytes with those it has.
+    // and share one gate is issued balanced (BalancedIssue): the scheduled
+    // copies, in their issue order, are cut into guided pieces as the
+    // engines take them (an engine's first piece whole where it fits its
+    // share; then the unissued bytes over the engine count, at least
+    // slice_bytes).  An engine takes a piece while it holds fewer than two
+    // or the piece fits within 2 * slice_bytes with those it holds, and only
+    // if, at the engines' measured rates, it would finish the piece before
+    // the operation's projected end or about as early as any engine could.
     // Otherwise (and with slice_bytes 0) every copy is issued at once on its
     // scheduled engine.
     hoccl_status_t submit(const std::vector<ProxyCopy> &copies, int max_engines, size_t slice_bytes,

@@ -22,14 +22,22 @@ Point-to-point: the receiver publishes its buffer's handle; the sender opens
 it, copies straight into it through the library (the engine proxy by
 default) and publishes completion, which the receiver waits for.
 
+Broadcast is a one-row all-to-all(v): the root's buffer is copied into every
+other rank's.
+
 Every call synchronises the calling rank's current stream before it
 publishes (its inputs are complete and its outputs free) and returns once
-the operation has completed: the returned work is already done.  Reductions
-are sums.  Buffers must be contiguous CUDA tensors of int32, float32 or
-bfloat16 on the shared GPU, in allocations below 2 GiB (larger ones are not
+the operation has completed: the returned work is already done, and its
+future holds the output tensors (as DistributedDataParallel's reducer
+expects).  Reductions are sums of int32, float32 or bfloat16.  The copy
+collectives (broadcast, all-gather, all-to-all, send/recv) move bytes, so
+they take any dtype; the library copies them in 4- or 2-byte units, and a
+copy whose byte counts are odd is refused.  Buffers must be contiguous CUDA
+tensors on the shared GPU, in allocations below 2 GiB (larger ones are not
 shared), and must not be freed (``torch.cuda.empty_cache``) while the group
 lives.  ``destroy_process_group`` closes the opened handles before any rank
-may free its memory.
+may free its memory.  With these, torch.nn.parallel.DistributedDataParallel
+runs over the backend (parameter and buffer broadcast, gradient buckets).
 
 Use::
 
@@ -109,21 +117,43 @@ class _Done(dist._Work):
         return self._fut
 
 
-def _dtype(t):
-    if t.dtype not in _DTYPES:
-        raise TypeError(f"hoccl: unsupported dtype {t.dtype}")
+def _check_buffer(t):
     if t.device.type != "cuda" or not t.is_contiguous():
         raise ValueError("hoccl: buffers must be contiguous CUDA tensors")
+
+
+def _dtype(t):
+    """The library dtype of a reduction's buffer."""
+    if t.dtype not in _DTYPES:
+        raise TypeError(f"hoccl: reductions take int32, float32 or bfloat16, not {t.dtype}")
+    _check_buffer(t)
     return _DTYPES[t.dtype]
 
 
+def _nbytes(t):
+    _check_buffer(t)
+    return t.numel() * t.element_size()
+
+
+def _unit(byte_counts):
+    """(library dtype, unit bytes) of a copy: copies move bits, so the dtype
+    only sets the unit, the largest of 4 and 2 bytes that divides every
+    count and offset."""
+    for size, dt in ((4, INT32), (2, BF16)):
+        if all(b % size == 0 for b in byte_counts):
+            return dt, size
+    raise ValueError(f"hoccl: copies move 2-byte units; byte counts {sorted(set(byte_counts))[:8]} are odd")
+
+
 def _export(t):
+    if t.numel() == 0:
+        return None                           # no allocation to share; nothing is copied
     h, off, size = ipc_export(t)
     return {"h": h.hex(), "o": off, "n": size, "dev": t.device.index}
 
 
 def _open(d):
-    return ipc_open(bytes.fromhex(d["h"]), d["o"], d["n"])
+    return None if d is None else ipc_open(bytes.fromhex(d["h"]), d["o"], d["n"])
 
 
 def _ptrs(vals):
@@ -158,9 +188,10 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     # ---- the collective protocol ----------------------------------------------
 
-    def _call(self, desc, run):
+    def _call(self, desc, run, result=None):
         """Publish this rank's `desc`; rank 0 gathers every rank's and runs
-        `run(descs)`; every rank waits for completion."""
+        `run(descs)`; every rank waits for completion.  The work's future
+        holds `result` (the output tensors)."""
         k = self._seq
         self._seq += 1
         torch.cuda.current_stream().synchronize()
@@ -182,7 +213,7 @@ class HocclProcessGroup(dist.ProcessGroup):
                 self._store.delete_key(key)
         if status != "ok":
             raise RuntimeError(status)
-        return _Done()
+        return _Done(result)
 
     def _resolve(self, descs, field, mine):
         """Device pointers of every rank's `field`: rank 0's own, the others
@@ -202,7 +233,30 @@ class HocclProcessGroup(dist.ProcessGroup):
                 raise ValueError("hoccl: all_reduce tensors differ between ranks")
             p = _ptrs(self._resolve(descs, "t", t.data_ptr()))
             _check(lib().hoccl_allreduce(p, p, t.numel(), dt, self._n, _stream()), "hoccl_allreduce")
-        return self._call(desc, run)
+        return self._call(desc, run, [t])
+
+    def broadcast(self, tensors, opts=None):
+        """The root's tensor into every rank's: an all-to-all(v) whose only
+        nonzero row is the root's, every copy reading the root's whole
+        buffer."""
+        (t,) = tensors
+        root = getattr(opts, "rootRank", 0)
+        if not 0 <= root < self._n:
+            raise ValueError(f"hoccl: broadcast root {root} outside 0..{self._n - 1}")
+        nb = _nbytes(t)
+        desc = {"t": _export(t), "bytes": nb, "type": str(t.dtype), "dev": t.device.index}
+
+        def run(descs):
+            R = self._n
+            if any(d["bytes"] != nb or d["type"] != str(t.dtype) for d in descs):
+                raise ValueError("hoccl: broadcast tensors differ between ranks")
+            dt, u = _unit([nb])
+            p = _ptrs(self._resolve(descs, "t", t.data_ptr()))
+            S = ctypes.c_size_t * (R * R)
+            counts = S(*[nb // u if s == root and d != root else 0 for s in range(R) for d in range(R)])
+            zero = S()
+            _check(lib().hoccl_alltoallv(p, counts, zero, p, zero, dt, R, _stream()), "hoccl_alltoallv")
+        return self._call(desc, run, [t])
 
     def _reduce_scatter_base(self, output, input, opts=None):
         _sum_only(opts)
@@ -219,7 +273,7 @@ class HocclProcessGroup(dist.ProcessGroup):
             r = _ptrs(self._resolve(descs, "out", output.data_ptr()))
             _check(lib().hoccl_reduce_scatter(s, r, output.numel(), dt, self._n, _stream()),
                    "hoccl_reduce_scatter")
-        return self._call(desc, run)
+        return self._call(desc, run, [output])
 
     def reduce_scatter(self, output_tensors, input_tensors, opts=None):
         (out,) = output_tensors
@@ -228,19 +282,20 @@ class HocclProcessGroup(dist.ProcessGroup):
         return self._reduce_scatter_base(out, flat, opts)
 
     def _allgather_base(self, output, input, opts=None):
-        dt = _dtype(input)
-        if _dtype(output) != dt or output.numel() != self._n * input.numel():
+        nb = _nbytes(input)
+        if output.dtype != input.dtype or _nbytes(output) != self._n * nb:
             raise ValueError("hoccl: all_gather needs an output of world_size times the input")
-        desc = {"in": _export(input), "out": _export(output), "numel": input.numel(), "dt": dt,
+        desc = {"in": _export(input), "out": _export(output), "bytes": nb, "type": str(input.dtype),
                 "dev": input.device.index}
 
         def run(descs):
-            if any(d["numel"] != input.numel() or d["dt"] != dt for d in descs):
+            if any(d["bytes"] != nb or d["type"] != str(input.dtype) for d in descs):
                 raise ValueError("hoccl: all_gather tensors differ between ranks")
+            dt, u = _unit([nb])
             s = _ptrs(self._resolve(descs, "in", input.data_ptr()))
             r = _ptrs(self._resolve(descs, "out", output.data_ptr()))
-            _check(lib().hoccl_allgather(s, r, input.numel(), dt, self._n, _stream()), "hoccl_allgather")
-        return self._call(desc, run)
+            _check(lib().hoccl_allgather(s, r, nb // u, dt, self._n, _stream()), "hoccl_allgather")
+        return self._call(desc, run, [output])
 
     def allgather(self, output_tensors, input_tensors, opts=None):
         (outs,) = output_tensors
@@ -249,45 +304,50 @@ class HocclProcessGroup(dist.ProcessGroup):
         w = self._allgather_base(flat, inp.reshape(-1) if inp.is_contiguous() else inp.contiguous(), opts)
         for r, o in enumerate(outs):
             o.copy_(flat[r * inp.numel():(r + 1) * inp.numel()].view_as(o))
-        return w
+        return _Done([outs])
 
     def alltoall_base(self, output, input, output_split_sizes, input_split_sizes, opts=None):
-        dt = _dtype(input)
-        if _dtype(output) != dt:
+        if output.dtype != input.dtype:
             raise ValueError("hoccl: all_to_all tensors differ in dtype")
+        _check_buffer(input)
+        _check_buffer(output)
+        es = input.element_size()
         row_in = input.numel() // max(1, input.size(0)) if input.dim() else 1
         row_out = output.numel() // max(1, output.size(0)) if output.dim() else 1
         if row_in != row_out:
             raise ValueError("hoccl: all_to_all rows differ in size")
         split_in = list(input_split_sizes) or [input.size(0) // self._n] * self._n
         split_out = list(output_split_sizes) or [output.size(0) // self._n] * self._n
-        desc = {"in": _export(input), "out": _export(output), "dt": dt, "dev": input.device.index,
-                "sin": [s * row_in for s in split_in], "sout": [s * row_out for s in split_out]}
+        desc = {"in": _export(input), "out": _export(output), "type": str(input.dtype),
+                "dev": input.device.index,
+                "sin": [s * row_in * es for s in split_in], "sout": [s * row_out * es for s in split_out]}
 
         def run(descs):
             R = self._n
-            if any(d["dt"] != dt for d in descs):
+            if any(d["type"] != str(input.dtype) for d in descs):
                 raise ValueError("hoccl: all_to_all dtypes differ between ranks")
-            counts, sd, rd = [], [], []
+            counts, sd, rd = [], [], []           # in bytes until the unit is known
             for s in range(R):
                 off = 0
                 for d in range(R):
                     c = descs[s]["sin"][d]
                     if descs[d]["sout"][s] != c:
-                        raise ValueError(f"hoccl: rank {s} sends {c} elements to rank {d}, which expects "
-                                         f"{descs[d]['sout'][s]}")
+                        raise ValueError(f"hoccl: rank {s} sends {c // es} elements to rank {d}, which "
+                                         f"expects {descs[d]['sout'][s] // es}")
                     counts.append(c)
                     sd.append(off)
                     off += c
             for s in range(R):
                 for d in range(R):
                     rd.append(sum(descs[d]["sout"][:s]))
+            dt, u = _unit(counts + sd + rd)
             S = ctypes.c_size_t * (R * R)
+            units = lambda v: S(*[b // u for b in v])
             sp = _ptrs(self._resolve(descs, "in", input.data_ptr()))
             rp = _ptrs(self._resolve(descs, "out", output.data_ptr()))
-            _check(lib().hoccl_alltoallv(sp, S(*counts), S(*sd), rp, S(*rd), dt, R, _stream()),
+            _check(lib().hoccl_alltoallv(sp, units(counts), units(sd), rp, units(rd), dt, R, _stream()),
                    "hoccl_alltoallv")
-        return self._call(desc, run)
+        return self._call(desc, run, [output])
 
     def barrier(self, opts=None):
         return self._call({}, lambda descs: None)
@@ -301,17 +361,19 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     def send(self, tensors, dst, tag=0):
         (t,) = tensors
-        dt = _dtype(t)
+        nb = _nbytes(t)
         key = self._p2p_key(self._r, dst)
         torch.cuda.current_stream().synchronize()
         d = json.loads(self._store.get(key + "/recv"))          # the receiver's buffer
         status = "ok"
         try:
-            if d["numel"] != t.numel() or d["dt"] != dt:
-                raise ValueError(f"hoccl: send of {t.numel()} elements to a receive of {d['numel']}")
+            if d["bytes"] != nb or d["type"] != str(t.dtype):
+                raise ValueError(f"hoccl: send of {nb} bytes of {t.dtype} to a receive of "
+                                 f"{d['bytes']} bytes of {d['type']}")
+            dt, u = _unit([nb])
             dst_ptr = _open(d["t"])
             _check(lib().hoccl_sendrecv(_ptrs([t.data_ptr(), None]), _ptrs([None, dst_ptr]),
-                                        (ctypes.c_int * 2)(1, -1), t.numel(), dt, 2, _stream()),
+                                        (ctypes.c_int * 2)(1, -1), nb // u, dt, 2, _stream()),
                    "hoccl_sendrecv")
             torch.cuda.current_stream().synchronize()
         except Exception as e:
@@ -319,20 +381,20 @@ class HocclProcessGroup(dist.ProcessGroup):
         self._store.set(key + "/done", status)
         if status != "ok":
             raise RuntimeError(status)
-        return _Done()
+        return _Done([t])
 
     def recv(self, tensors, src, tag=0):
         (t,) = tensors
-        dt = _dtype(t)
+        nb = _nbytes(t)
         key = self._p2p_key(src, self._r)
         torch.cuda.current_stream().synchronize()
-        self._store.set(key + "/recv", json.dumps({"t": _export(t), "numel": t.numel(), "dt": dt}))
+        self._store.set(key + "/recv", json.dumps({"t": _export(t), "bytes": nb, "type": str(t.dtype)}))
         status = self._store.get(key + "/done").decode()
         self._store.delete_key(key + "/recv")
         self._store.delete_key(key + "/done")
         if status != "ok":
             raise RuntimeError(status)
-        return _Done()
+        return _Done([t])
 
     # ---- teardown ----------------------------------------------------------------------
 

@@ -4,7 +4,10 @@ torchrun, all on GPU 0, with HOCCL_BACKEND=1).  Every rank generates every
 rank's seeded inputs, so it can compute the oracle's result itself and
 compare its own output with it bit for bit: all_reduce, reduce_scatter_tensor,
 reduce_scatter (list), all_gather_into_tensor, all_gather (list),
-all_to_all_single with uneven splits, send/recv around the ring, barrier.
+all_to_all_single with uneven splits, send/recv around the ring, broadcast
+from every root, barrier.  The copy collectives also run on dtypes the
+library has no arithmetic for (int64, uint8, float16), whose bytes they
+move in 4- or 2-byte units; an odd byte count is refused on every rank.
 Prints "rank r: backend ok" when everything matched."""
 import os
 import sys
@@ -23,6 +26,19 @@ import paper_2609_34334_amd as hc  # noqa: E402
 import workloads as W  # noqa: E402
 from gpu_util import NAME, assert_bitwise, from_dev, to_dev  # noqa: E402
 from paper_2609_34334_amd import distributed as hdist  # noqa: E402
+
+
+def byte_tensor(seed, rank, n, dtype):
+    """n seeded elements of `dtype` on the GPU, arbitrary bit patterns."""
+    nbytes = n * torch.empty(0, dtype=dtype).element_size()
+    raw = W.random_bits(seed, rank, (nbytes + 1) // 2, 2).view(np.uint8)[:nbytes]
+    return torch.from_numpy(raw.copy()).view(dtype).to("cuda") if nbytes else torch.empty(0, dtype=dtype, device="cuda")
+
+
+def assert_same_bytes(got, want, what):
+    a = got.cpu().reshape(-1).view(torch.uint8).numpy()
+    b = want.cpu().reshape(-1).view(torch.uint8).numpy()
+    assert a.shape == b.shape and np.array_equal(a, b), (what, np.flatnonzero(a != b)[:8])
 
 
 def main():
@@ -81,6 +97,39 @@ def main():
             dist.recv(got, (rank - 1) % R)
             dist.send(src, (rank + 1) % R)
         assert_bitwise(from_dev(got, hc.BF16), prev, f"recv round {k}")
+    # broadcast from every root; dtypes beyond the library's move as bytes
+    for root in range(R):
+        for k, (dtype, n) in enumerate(((torch.float32, 4099), (torch.bfloat16, 3 * 65536 + 7),
+                                        (torch.int32, 1), (torch.int64, 33), (torch.uint8, 1000),
+                                        (torch.float16, 77), (torch.float32, 0))):
+            want = byte_tensor(950 + k, root, n, dtype)
+            t = want.clone() if rank == root else torch.full_like(want, 7)
+            dist.broadcast(t, root)
+            assert_same_bytes(t, want, f"broadcast {dtype} n={n} root={root}")
+    # all_gather_into_tensor, all_to_all_single and send/recv of int64 and uint8
+    for k, (dtype, n) in enumerate(((torch.int64, 1001), (torch.uint8, 6))):
+        xs = [byte_tensor(960 + k, r, n, dtype) for r in range(R)]
+        g = torch.empty(R * n, dtype=dtype, device="cuda")
+        dist.all_gather_into_tensor(g, xs[rank])
+        assert_same_bytes(g, torch.cat(xs), f"all_gather_into_tensor {dtype}")
+        ys = [byte_tensor(970 + k, r, R * n, dtype) for r in range(R)]
+        out = torch.empty(R * n, dtype=dtype, device="cuda")
+        dist.all_to_all_single(out, ys[rank])
+        assert_same_bytes(out, torch.cat([ys[s][rank * n:(rank + 1) * n] for s in range(R)]),
+                          f"all_to_all_single {dtype}")
+        got = torch.empty(n, dtype=dtype, device="cuda")
+        if rank % 2 == 0:
+            dist.send(xs[rank], (rank + 1) % R)
+            dist.recv(got, (rank - 1) % R)
+        else:
+            dist.recv(got, (rank - 1) % R)
+            dist.send(xs[rank], (rank + 1) % R)
+        assert_same_bytes(got, xs[(rank - 1) % R], f"recv {dtype}")
+    try:                                    # 3 bytes: no 2-byte unit divides them
+        dist.broadcast(torch.zeros(3, dtype=torch.uint8, device="cuda"), 0)
+        raise AssertionError("an odd-sized broadcast was accepted")
+    except RuntimeError as e:
+        assert "odd" in str(e), e
     dist.barrier()
     hdist.destroy_process_group()
     print(f"rank {rank}: backend ok", flush=True)

@@ -252,6 +252,21 @@ def test_backend_switch_and_registration():
     assert dist.Backend.HOCCL == "hoccl"
 
 
+def test_backend_copy_units():
+    """The backend's copy collectives move any dtype as bytes: 4-byte units
+    where every count and offset allows, else 2-byte units; odd byte counts
+    are refused.  Reductions keep to the library's three dtypes."""
+    import torch
+    from paper_2609_34334_amd import distributed as hdist
+    assert hdist._unit([8, 4, 0]) == (hc.INT32, 4)
+    assert hdist._unit([8, 6]) == (hc.BF16, 2)
+    assert hdist._unit([]) == (hc.INT32, 4)
+    with pytest.raises(ValueError, match="odd"):
+        hdist._unit([4, 3])
+    with pytest.raises(TypeError, match="int32, float32 or bfloat16"):
+        hdist._dtype(torch.zeros(2, dtype=torch.int64))
+
+
 def test_ipc_export_rejects_host_memory():
     import ctypes as C
     buf = C.create_string_buffer(64)

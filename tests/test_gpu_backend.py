@@ -1,7 +1,8 @@
 """The "hoccl" torch.distributed backend across processes sharing the one
-GPU: four ranks launched by torchrun (HOCCL_BACKEND=1 turns the requested
-backend into hoccl), every collective's output compared with the oracle by
-each rank (tests/backend_worker.py)."""
+GPU: ranks launched by torchrun (HOCCL_BACKEND=1 turns the requested
+backend into hoccl).  Every collective's output compared with the oracle by
+each rank (tests/backend_worker.py), and DistributedDataParallel training
+over the backend (tests/ddp_worker.py)."""
 import os
 import signal
 import socket
@@ -21,12 +22,11 @@ def free_port():
         return s.getsockname()[1]
 
 
-@pytest.mark.parametrize("ranks", [2, 4])
-def test_backend_across_processes_on_one_gpu(ranks):
+def run_ranks(worker, ranks, done):
     env = dict(os.environ, HOCCL_BACKEND="1", MASTER_ADDR="127.0.0.1", OMP_NUM_THREADS="1")
     cmd = [sys.executable, "-m", "torch.distributed.run", "--nnodes=1", f"--nproc-per-node={ranks}",
            "--master-addr=127.0.0.1", f"--master-port={free_port()}",
-           os.path.join(ROOT, "tests", "backend_worker.py")]
+           os.path.join(ROOT, "tests", worker)]
     print("launching", " ".join(cmd[3:]), flush=True)
     p = subprocess.Popen(cmd, env=env, cwd=ROOT, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
                          start_new_session=True)
@@ -37,4 +37,14 @@ def test_backend_across_processes_on_one_gpu(ranks):
         out, err = p.communicate()
         raise AssertionError(("timed out", out[-3000:], err[-3000:]))
     assert p.returncode == 0, (out[-3000:], err[-4000:])
-    assert out.count("backend ok") == ranks, out[-3000:]
+    assert out.count(done) == ranks, out[-3000:]
+
+
+@pytest.mark.parametrize("ranks", [2, 4])
+def test_backend_across_processes_on_one_gpu(ranks):
+    run_ranks("backend_worker.py", ranks, "backend ok")
+
+
+@pytest.mark.parametrize("ranks", [2, 4])
+def test_ddp_over_the_backend(ranks):
+    run_ranks("ddp_worker.py", ranks, "ddp ok")
