@@ -255,9 +255,11 @@ typedef struct {
                                    in the schedule's order as they have
                                    room (two pieces, or twice this many
                                    bytes, in flight each).  An engine's
-                                   first piece is a whole copy; later ones
-                                   are the unissued bytes over the engine
-                                   count, at least this many bytes.  An
+                                   first piece is a whole copy if that is
+                                   no more than its share of the total;
+                                   later ones are the unissued bytes over
+                                   the engine count, at least this many
+                                   bytes.  An
                                    engine takes a piece only if it would
                                    finish it before the operation's
                                    projected end or about as early as any

@@ -29,7 +29,10 @@ Every call synchronises the calling rank's current stream before it
 publishes (its inputs are complete and its outputs free) and returns once
 the operation has completed: the returned work is already done, and its
 future holds the output tensors (as DistributedDataParallel's reducer
-expects).  Reductions are sums of int32, float32 or bfloat16.  The copy
+expects).  Reductions are sums of int32, float32 or bfloat16, or averages
+of float32 or bfloat16 (FSDP's gradient reduce-scatter): the sum, rounded
+once to the dtype, then divided by the world size in that dtype on the
+caller's stream (exact when the world size is a power of two).  The copy
 collectives (broadcast, all-gather, all-to-all, send/recv) move bytes, so
 they take any dtype; the library copies them in 4- or 2-byte units, and a
 copy whose byte counts are odd is refused.  Buffers must be contiguous CUDA
@@ -37,7 +40,11 @@ tensors on the shared GPU, in allocations below 2 GiB (larger ones are not
 shared), and must not be freed (``torch.cuda.empty_cache``) while the group
 lives.  ``destroy_process_group`` closes the opened handles before any rank
 may free its memory.  With these, torch.nn.parallel.DistributedDataParallel
-runs over the backend (parameter and buffer broadcast, gradient buckets).
+(parameter and buffer broadcast, gradient buckets) and FSDP2's fully_shard
+(parameter all-gathers, averaging gradient reduce-scatters) run over the
+backend.  torch's functional collectives (DTensor redistribution such as
+``full_tensor()``) call a process group's C++ backend directly, which a
+process group written in Python does not have: they are not supported.
 
 Use::
 
@@ -164,10 +171,16 @@ def _stream():
     return _VP(torch.cuda.current_stream().cuda_stream)
 
 
-def _sum_only(opts):
+def _average(opts, t):
+    """Whether the reduction is an average: SUM, or AVG (FSDP's gradient
+    reduce-scatter) of float32 or bfloat16, which is the library's sum
+    divided by the world size afterwards."""
     op = getattr(opts, "reduceOp", dist.ReduceOp.SUM)
-    if op != dist.ReduceOp.SUM:
-        raise ValueError("hoccl: only sum reductions")
+    if op == dist.ReduceOp.SUM:
+        return False
+    if op == dist.ReduceOp.AVG and t.dtype in (torch.float32, torch.bfloat16):
+        return True
+    raise ValueError(f"hoccl: only sums, and averages of float32 or bfloat16 ({op} on {t.dtype})")
 
 
 class HocclProcessGroup(dist.ProcessGroup):
@@ -182,9 +195,25 @@ class HocclProcessGroup(dist.ProcessGroup):
         self._seq = 0
         self._p2p = {}
         self._closed = False
+        self._name, self._desc = "", ""
 
     def getBackendName(self):
         return BACKEND
+
+    # torch keeps a group's name in its C++ backends, which a process group
+    # written in Python has none of; these keep it here (DeviceMesh, and so
+    # FSDP2, looks groups up by name).
+    def getGroupName(self):
+        return self._name
+
+    def setGroupName(self, name):
+        self._name = name
+
+    def getGroupDesc(self):
+        return self._desc
+
+    def setGroupDesc(self, desc):
+        self._desc = desc
 
     # ---- the collective protocol ----------------------------------------------
 
@@ -223,8 +252,8 @@ class HocclProcessGroup(dist.ProcessGroup):
     # ---- collectives ---------------------------------------------------------------
 
     def allreduce(self, tensors, opts=None):
-        _sum_only(opts)
         (t,) = tensors
+        avg = _average(opts, t)
         dt = _dtype(t)
         desc = {"t": _export(t), "numel": t.numel(), "dt": dt, "dev": t.device.index}
 
@@ -233,7 +262,10 @@ class HocclProcessGroup(dist.ProcessGroup):
                 raise ValueError("hoccl: all_reduce tensors differ between ranks")
             p = _ptrs(self._resolve(descs, "t", t.data_ptr()))
             _check(lib().hoccl_allreduce(p, p, t.numel(), dt, self._n, _stream()), "hoccl_allreduce")
-        return self._call(desc, run, [t])
+        w = self._call(desc, run, [t])
+        if avg:
+            t.div_(self._n)
+        return w
 
     def broadcast(self, tensors, opts=None):
         """The root's tensor into every rank's: an all-to-all(v) whose only
@@ -259,7 +291,7 @@ class HocclProcessGroup(dist.ProcessGroup):
         return self._call(desc, run, [t])
 
     def _reduce_scatter_base(self, output, input, opts=None):
-        _sum_only(opts)
+        avg = _average(opts, input)
         dt = _dtype(input)
         if _dtype(output) != dt or input.numel() != self._n * output.numel():
             raise ValueError("hoccl: reduce_scatter needs an input of world_size times the output")
@@ -273,7 +305,10 @@ class HocclProcessGroup(dist.ProcessGroup):
             r = _ptrs(self._resolve(descs, "out", output.data_ptr()))
             _check(lib().hoccl_reduce_scatter(s, r, output.numel(), dt, self._n, _stream()),
                    "hoccl_reduce_scatter")
-        return self._call(desc, run, [output])
+        w = self._call(desc, run, [output])
+        if avg:
+            output.div_(self._n)
+        return w
 
     def reduce_scatter(self, output_tensors, input_tensors, opts=None):
         (out,) = output_tensors

@@ -267,6 +267,37 @@ def test_backend_copy_units():
         hdist._dtype(torch.zeros(2, dtype=torch.int64))
 
 
+def test_backend_reduction_ops():
+    """Sums of every library dtype; averages (FSDP2's reduce-scatter) of
+    float32 and bfloat16 only; nothing else."""
+    import torch
+    import torch.distributed as dist
+    from paper_2609_34334_amd import distributed as hdist
+
+    def opts(op):
+        o = dist.AllreduceOptions()
+        o.reduceOp = op
+        return o
+    assert hdist._average(None, torch.zeros(1)) is False
+    assert hdist._average(opts(dist.ReduceOp.SUM), torch.zeros(1, dtype=torch.int32)) is False
+    assert hdist._average(opts(dist.ReduceOp.AVG), torch.zeros(1)) is True
+    assert hdist._average(opts(dist.ReduceOp.AVG), torch.zeros(1, dtype=torch.bfloat16)) is True
+    for op, dt in ((dist.ReduceOp.AVG, torch.int32), (dist.ReduceOp.MAX, torch.float32),
+                   (dist.ReduceOp.PRODUCT, torch.bfloat16)):
+        with pytest.raises(ValueError, match="only sums"):
+            hdist._average(opts(op), torch.zeros(1, dtype=dt))
+
+
+def test_backend_group_name():
+    """DeviceMesh finds a group by the name torch sets on it."""
+    import torch.distributed as dist
+    from paper_2609_34334_amd import distributed as hdist
+    g = hdist.HocclProcessGroup(dist.HashStore(), 0, 2, None)
+    g._set_group_name("7")
+    g._set_group_desc("mesh_default")
+    assert (g.group_name, g.group_desc) == ("7", "mesh_default")
+
+
 def test_ipc_export_rejects_host_memory():
     import ctypes as C
     buf = C.create_string_buffer(64)
