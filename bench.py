@@ -23,7 +23,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--quick]
        python bench.py --sweep            (algbw against message size)
 Profiling workloads (one phase each): --pmc-workload, --occupancy-workload,
 --copy-workload, --ar-groups-workload, --interference-workload,
---ceilings-workload, --after-free-workload.
+--ceilings-workload, --after-free-workload, --backend-workload (the
+torch.distributed backend's per-call time over rank processes).
 """
 import argparse
 import json
@@ -1659,7 +1660,81 @@ def occupancy_workload(hc, W):
                       "kernel_source_sha256_16": kernel_source_hash()}))
 
 
+def backend_rank():
+    """One rank of --backend-workload (started by torchrun with
+    HOCCL_BACKEND=1): per-call host time of the torch.distributed backend,
+    rank 0 printing one JSON line."""
+    from datetime import timedelta
+
+    import torch
+    import torch.distributed as dist
+
+    from paper_2609_34334_amd import distributed as hdist
+    rank, R = int(os.environ["RANK"]), int(os.environ["WORLD_SIZE"])
+    torch.cuda.set_device(0)
+    hdist.init_process_group(backend="nccl", timeout=timedelta(seconds=60))
+    reps, out = 50, {"ranks": R}
+
+    def per_call(fn):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return round((time.perf_counter() - t0) / reps * 1e6, 1)
+    for n in (1024, 1 << 20, 16 << 20):
+        t = torch.ones(n, device="cuda")
+        out[f"all_reduce_fp32_{n * 4 >> 10}KiB_us"] = per_call(lambda: dist.all_reduce(t))
+    g = torch.empty(R << 20, dtype=torch.bfloat16, device="cuda")
+    x = torch.ones(1 << 20, dtype=torch.bfloat16, device="cuda")
+    out["all_gather_bf16_2MiB_shard_us"] = per_call(lambda: dist.all_gather_into_tensor(g, x))
+    b = torch.ones(1 << 20, device="cuda")
+    out["broadcast_fp32_4MiB_us"] = per_call(lambda: dist.broadcast(b, 0))
+    out["barrier_us"] = per_call(lambda: dist.barrier())
+    m = torch.ones(1024, device="cuda")
+
+    def ping():
+        if rank == 0:
+            dist.send(m, 1)
+            dist.recv(m, 1)
+        elif rank == 1:
+            dist.recv(m, 0)
+            dist.send(m, 0)
+    out["send_recv_4KiB_round_trip_us"] = per_call(ping)
+    dist.barrier()
+    hdist.destroy_process_group()
+    if rank == 0:
+        print(json.dumps(out), flush=True)
+
+
+def bench_backend(ranks=(2, 4)):
+    """Per-call time of the torch.distributed backend with R processes
+    sharing the GPU: torchrun starts this file with --backend-rank."""
+    import socket
+    import subprocess
+    res = {}
+    for R in ranks:
+        with socket.socket() as so:
+            so.bind(("127.0.0.1", 0))
+            port = so.getsockname()[1]
+        env = dict(os.environ, HOCCL_BACKEND="1", OMP_NUM_THREADS="1")
+        cmd = [sys.executable, "-m", "torch.distributed.run", "--nnodes=1", f"--nproc-per-node={R}",
+               "--master-addr=127.0.0.1", f"--master-port={port}", os.path.abspath(__file__),
+               "--backend-rank"]
+        r = subprocess.run(cmd, env=env, capture_output=True, text=True, timeout=300)
+        lines = [l for l in r.stdout.splitlines() if l.startswith("{")]
+        res[f"R{R}"] = json.loads(lines[-1]) if r.returncode == 0 and lines else {
+            "error": (r.stderr or r.stdout)[-800:]}
+        log(f"backend R={R}: {res[f'R{R}']}")
+    return res
+
+
 def main():
+    if "--backend-rank" in sys.argv:
+        backend_rank()
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
@@ -1682,12 +1757,18 @@ def main():
                     help="run only the copy collectives the zero-CU trace is taken on")
     ap.add_argument("--after-free-workload", action="store_true",
                     help="the SDMA engines right after a large device-memory free, static against balanced")
+    ap.add_argument("--backend-workload", action="store_true",
+                    help="per-call time of the torch.distributed backend, 2 and 4 rank processes")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the R virtual ranks of every collective live in "
               "that GPU's HBM; run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.backend_workload:
+        print(json.dumps({"backend": bench_backend()}), flush=True)
+        return
 
     import numpy as np
     import torch

@@ -516,6 +516,50 @@ hoccl_status_t hoccl_ipc_open(const void *handle, size_t offset, size_t alloc_by
 /* Close every handle this process opened. */
 hoccl_status_t hoccl_ipc_close_all(void);
 
+/* Cross-process mailboxes: the paper's CPU-based cross-process
+ * synchronisation (Zero-SM Point-to-Point Executor, intra-node), by which
+ * processes that share buffers tell each other that inputs are ready and
+ * operations have completed.  A mailbox is a POSIX shared-memory object of
+ * `slots` slots, each a 32-bit sequence number plus up to `slot_bytes` of
+ * payload.  Host memory only: no device is touched, and these calls work
+ * without a GPU.
+ *
+ * Protocol: a writer posts a payload into a slot with a sequence number;
+ * a reader waits until the slot's number has reached the one it expects
+ * (numbers compare modulo 2^32, so a slot's numbers should only grow), then
+ * reads the payload.  The payload written before the number is visible to
+ * any reader that has seen the number.  A slot's writer must not post again
+ * until every reader of the previous payload is done with it; the caller's
+ * protocol orders that (the PyTorch backend lets a rank post call k + 1
+ * only after it has seen call k complete).  Every slot starts at 0.
+ *
+ * hoccl_mailbox_create makes the object `name` ("/name", as shm_open) and
+ * maps it; it fails if the name exists.  hoccl_mailbox_open maps an
+ * existing one and takes its geometry from it.  hoccl_mailbox_unlink
+ * removes the name (mappings stay valid, so once every process has opened
+ * it nothing is left behind when they exit).  hoccl_mailbox_close unmaps
+ * and frees the handle.  The handle is owned by the caller; one handle may
+ * be used from several threads, but not to post into one slot at once.
+ *
+ * hoccl_mailbox_wait polls briefly, then sleeps on the slot (a futex on
+ * the shared word); it returns HOCCL_ERR_TIMEOUT after timeout_ms.
+ * hoccl_mailbox_read copies the payload into buf (cap bytes) and stores its
+ * length in *len; HOCCL_ERR_INVALID_ARG if it does not fit.  Bad names,
+ * slots or sizes are HOCCL_ERR_INVALID_ARG; hoccl_last_error_string() says
+ * which. */
+typedef struct hoccl_mailbox hoccl_mailbox_t;
+hoccl_status_t hoccl_mailbox_create(const char *name, unsigned slots, size_t slot_bytes,
+                                    hoccl_mailbox_t **box);
+hoccl_status_t hoccl_mailbox_open(const char *name, hoccl_mailbox_t **box);
+hoccl_status_t hoccl_mailbox_unlink(const char *name);
+hoccl_status_t hoccl_mailbox_close(hoccl_mailbox_t *box);
+hoccl_status_t hoccl_mailbox_post(hoccl_mailbox_t *box, unsigned slot, unsigned seq,
+                                  const void *data, size_t len);
+hoccl_status_t hoccl_mailbox_wait(hoccl_mailbox_t *box, unsigned slot, unsigned seq,
+                                  unsigned timeout_ms);
+hoccl_status_t hoccl_mailbox_read(hoccl_mailbox_t *box, unsigned slot, void *buf, size_t cap,
+                                  size_t *len);
+
 /* ---- introspection (tests and tools) ------------------------------------
  * The planner's schedule for a collective: its traffic matrix turned into
  * copy chains and reduction steps (Collective Scheduler, from C to the

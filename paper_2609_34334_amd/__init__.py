@@ -103,6 +103,13 @@ _SIGS = {
     "hoccl_ipc_export": [ctypes.c_void_p, ctypes.c_void_p, _szp, _szp],
     "hoccl_ipc_open": [ctypes.c_void_p, _sz, _sz, ctypes.POINTER(ctypes.c_void_p)],
     "hoccl_ipc_close_all": [],
+    "hoccl_mailbox_create": [ctypes.c_char_p, ctypes.c_uint, _sz, _vpp],
+    "hoccl_mailbox_open": [ctypes.c_char_p, _vpp],
+    "hoccl_mailbox_unlink": [ctypes.c_char_p],
+    "hoccl_mailbox_close": [ctypes.c_void_p],
+    "hoccl_mailbox_post": [ctypes.c_void_p, ctypes.c_uint, ctypes.c_uint, ctypes.c_char_p, _sz],
+    "hoccl_mailbox_wait": [ctypes.c_void_p, ctypes.c_uint, ctypes.c_uint, ctypes.c_uint],
+    "hoccl_mailbox_read": [ctypes.c_void_p, ctypes.c_uint, ctypes.c_char_p, _sz, _szp],
 }
 for _name, _args in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -409,6 +416,45 @@ def ipc_open(handle, offset, alloc_bytes):
 
 def ipc_close_all():
     _check(_lib.hoccl_ipc_close_all(), "hoccl_ipc_close_all")
+
+
+class Mailbox:
+    """A cross-process mailbox (hoccl_mailbox_*): numbered slots of a
+    sequence number and a payload in POSIX shared memory.  Given `slots`, it
+    creates the object `name`; otherwise it opens an existing one."""
+
+    def __init__(self, name, slots=None, slot_bytes=None):
+        self._h = ctypes.c_void_p()
+        self.name = name
+        if slots is None:
+            _check(_lib.hoccl_mailbox_open(name.encode(), ctypes.byref(self._h)), "hoccl_mailbox_open")
+        else:
+            _check(_lib.hoccl_mailbox_create(name.encode(), slots, slot_bytes, ctypes.byref(self._h)),
+                   "hoccl_mailbox_create")
+        self._buf = ctypes.create_string_buffer(slot_bytes or (1 << 20))
+        self._len = ctypes.c_size_t(0)
+
+    @staticmethod
+    def unlink(name):
+        _check(_lib.hoccl_mailbox_unlink(name.encode()), "hoccl_mailbox_unlink")
+
+    def post(self, slot, seq, data=b""):
+        _check(_lib.hoccl_mailbox_post(self._h, slot, seq & 0xFFFFFFFF, data, len(data)),
+               "hoccl_mailbox_post")
+
+    def wait(self, slot, seq, timeout_ms):
+        _check(_lib.hoccl_mailbox_wait(self._h, slot, seq & 0xFFFFFFFF, int(timeout_ms)),
+               "hoccl_mailbox_wait")
+
+    def read(self, slot):
+        _check(_lib.hoccl_mailbox_read(self._h, slot, self._buf, len(self._buf), ctypes.byref(self._len)),
+               "hoccl_mailbox_read")
+        return self._buf.raw[:self._len.value]
+
+    def close(self):
+        if self._h:
+            _lib.hoccl_mailbox_close(self._h)
+            self._h = ctypes.c_void_p()
 
 
 CEILING_MODES = {"read": 0, "write": 1, "copy": 2, "add": 3, "rmw": 4}

@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhoccl.so")
 SOURCES = ["api.cpp", "plan.cpp", "proxy.cpp", "schedule.cpp", "kernels.hip", "handshake.hip",
-           "scratch.hip", "ceilings.hip", "ipc.cpp"]
+           "scratch.hip", "ceilings.hip", "ipc.cpp", "mailbox.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # The packed-fp32 feature is switched off for device code: the library
 # writes plain scalar float arithmetic and never wants v_pk_*_f32.

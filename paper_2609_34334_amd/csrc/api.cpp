@@ -31,6 +31,7 @@
 #include <vector>
 
 #include "ceilings.h"
+#include "errors.h"
 #include "hoccl_internal.h"
 #include "proxy.h"
 #include "schedule.h"
@@ -994,6 +995,9 @@ PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
 }
 
 }  // namespace
+
+void set_error_message(const char *msg) { t_err = msg; }
+
 }  // namespace hoccl
 
 using namespace hoccl;

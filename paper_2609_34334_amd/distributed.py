@@ -9,18 +9,27 @@ collective over R device pointers in one process, so each call goes like the
 paper's intra-node path (Zero-SM Point-to-Point Executor):
 
 * runtime IPC-handle exchange: every rank exports the allocations that hold
-  its buffers (``hoccl_ipc_export``) and publishes the handles in the c10d
-  store under the call's sequence number;
-* rank 0 opens the other ranks' handles (``hoccl_ipc_open``, cached per
-  allocation), runs the collective through the C ABI on its current stream
-  over all ranks' buffers, waits for it and publishes completion;
-* CPU-based cross-process synchronisation: every rank waits for that
-  completion key in the store before the call returns, so its later work
-  sees the results.
+  its buffers (``hoccl_ipc_export``) and posts the handles, with the call's
+  sequence number, into its slot of the group's shared-memory mailbox
+  (``hoccl_mailbox_*``);
+* rank 0 waits for every rank's slot, opens the other ranks' handles
+  (``hoccl_ipc_open``, cached per allocation), runs the collective through
+  the C ABI on its current stream over all ranks' buffers, waits for it and
+  posts the status into the mailbox's status slot;
+* CPU-based cross-process synchronisation: every rank waits for that status
+  before the call returns, so its later work sees the results.  The
+  mailbox is the paper's shared-memory semaphores: a waiter polls briefly,
+  then sleeps on a futex.
 
-Point-to-point: the receiver publishes its buffer's handle; the sender opens
-it, copies straight into it through the library (the engine proxy by
-default) and publishes completion, which the receiver waits for.
+Point-to-point: the receiver posts its buffer's handle into the mailbox
+slot of the (sender, receiver) pair; the sender opens it, copies straight
+into it through the library (the engine proxy by default) and posts
+completion, which the receiver waits for.
+
+The c10d store is used once, when the group is created: rank 0 creates the
+mailboxes and publishes their names, every rank opens them, and once all
+have, rank 0 removes the names (the mappings stay, and nothing is left in
+/dev/shm when the processes exit).
 
 Broadcast is a one-row all-to-all(v): the root's buffer is copied into every
 other rank's.
@@ -56,17 +65,20 @@ Use::
 import ctypes
 import json
 import os
+import secrets
 from datetime import timedelta
 
 import torch
 import torch.distributed as dist
 
-from . import (BF16, FP32, INT32, _check, _DTYPES, ipc_close_all, ipc_export, ipc_open, lib)
+from . import (BF16, FP32, INT32, Mailbox, _check, _DTYPES, ipc_close_all, ipc_export, ipc_open, lib)
 
 BACKEND = "hoccl"
 ENV = "HOCCL_BACKEND"
 _VP = ctypes.c_void_p
 _GROUPS = []
+COLL_SLOT_BYTES = 64 << 10    # one rank's call description (handles, split sizes)
+P2P_SLOT_BYTES = 2 << 10      # a receive buffer's handle, or a completion status
 
 
 def selected_backend(requested):
@@ -196,6 +208,29 @@ class HocclProcessGroup(dist.ProcessGroup):
         self._p2p = {}
         self._closed = False
         self._name, self._desc = "", ""
+        t = timeout.total_seconds() if isinstance(timeout, timedelta) else timeout
+        self._timeout_ms = int(1000 * t) if t else 30 * 60 * 1000
+        self._open_mailboxes()
+
+    def _open_mailboxes(self):
+        """Rank 0 creates the collective mailbox (a slot per rank plus the
+        status slot) and the point-to-point one (two slots per ordered pair);
+        every rank opens them; rank 0 removes the names once all have."""
+        if self._r == 0:
+            base = f"/hoccl-{os.getpid()}-{secrets.token_hex(6)}"
+            self._coll = Mailbox(base + "-c", self._n + 1, COLL_SLOT_BYTES)
+            self._pp = Mailbox(base + "-p", 2 * self._n * self._n, P2P_SLOT_BYTES)
+            self._store.set("mailbox", base)
+        else:
+            base = self._store.get("mailbox").decode()
+            self._coll = Mailbox(base + "-c")
+            self._pp = Mailbox(base + "-p")
+        if self._store.add("mailbox-opened", 1) == self._n:
+            self._store.set("mailbox-all", "1")
+        self._store.get("mailbox-all")
+        if self._r == 0:
+            Mailbox.unlink(base + "-c")
+            Mailbox.unlink(base + "-p")
 
     def getBackendName(self):
         return BACKEND
@@ -218,16 +253,22 @@ class HocclProcessGroup(dist.ProcessGroup):
     # ---- the collective protocol ----------------------------------------------
 
     def _call(self, desc, run, result=None):
-        """Publish this rank's `desc`; rank 0 gathers every rank's and runs
+        """Post this rank's `desc`; rank 0 gathers every rank's and runs
         `run(descs)`; every rank waits for completion.  The work's future
-        holds `result` (the output tensors)."""
-        k = self._seq
+        holds `result` (the output tensors).  A rank posts call k + 1 only
+        after it has seen call k's status, so rank 0 has read every slot
+        before it is written again."""
         self._seq += 1
+        k, R, box = self._seq, self._n, self._coll
         torch.cuda.current_stream().synchronize()
-        self._store.set(f"c{k}/{self._r}", json.dumps(desc))
-        if self._r == 0:
+        if self._r != 0:
+            box.post(self._r, k, json.dumps(desc).encode())
+        else:
             try:
-                descs = [json.loads(self._store.get(f"c{k}/{r}")) for r in range(self._n)]
+                descs = [desc]
+                for r in range(1, R):
+                    box.wait(r, k, self._timeout_ms)
+                    descs.append(json.loads(box.read(r)))
                 if len({d["dev"] for d in descs if "dev" in d}) > 1:
                     raise ValueError("hoccl: all ranks must use the same GPU")
                 run(descs)
@@ -235,11 +276,9 @@ class HocclProcessGroup(dist.ProcessGroup):
                 status = "ok"
             except Exception as e:  # every rank must learn of it, not only rank 0
                 status = f"error: {e}"
-            self._store.set(f"c{k}/done", status)
-        status = self._store.get(f"c{k}/done").decode()
-        if self._store.add(f"c{k}/ack", 1) == self._n:     # the last reader cleans up
-            for key in [f"c{k}/{r}" for r in range(self._n)] + [f"c{k}/done", f"c{k}/ack"]:
-                self._store.delete_key(key)
+            box.post(R, k, status.encode()[:COLL_SLOT_BYTES])
+        box.wait(R, k, self._timeout_ms)
+        status = box.read(R).decode(errors="replace")
         if status != "ok":
             raise RuntimeError(status)
         return _Done(result)
@@ -389,17 +428,21 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     # ---- point to point ----------------------------------------------------------------
 
-    def _p2p_key(self, src, dst):
-        n = self._p2p.get((src, dst), 0)
-        self._p2p[(src, dst)] = n + 1
-        return f"p{src}-{dst}/{n}"
+    def _p2p_slot(self, src, dst):
+        """(slot of the receiver's buffer, slot of the completion, message
+        number) of the next message from src to dst."""
+        n = self._p2p.get((src, dst), 0) + 1
+        self._p2p[(src, dst)] = n
+        base = 2 * (src * self._n + dst)
+        return base, base + 1, n
 
     def send(self, tensors, dst, tag=0):
         (t,) = tensors
         nb = _nbytes(t)
-        key = self._p2p_key(self._r, dst)
+        want, done, n = self._p2p_slot(self._r, dst)
         torch.cuda.current_stream().synchronize()
-        d = json.loads(self._store.get(key + "/recv"))          # the receiver's buffer
+        self._pp.wait(want, n, self._timeout_ms)
+        d = json.loads(self._pp.read(want))                    # the receiver's buffer
         status = "ok"
         try:
             if d["bytes"] != nb or d["type"] != str(t.dtype):
@@ -413,7 +456,7 @@ class HocclProcessGroup(dist.ProcessGroup):
             torch.cuda.current_stream().synchronize()
         except Exception as e:
             status = f"error: {e}"
-        self._store.set(key + "/done", status)
+        self._pp.post(done, n, status.encode()[:P2P_SLOT_BYTES])
         if status != "ok":
             raise RuntimeError(status)
         return _Done([t])
@@ -421,12 +464,11 @@ class HocclProcessGroup(dist.ProcessGroup):
     def recv(self, tensors, src, tag=0):
         (t,) = tensors
         nb = _nbytes(t)
-        key = self._p2p_key(src, self._r)
+        want, done, n = self._p2p_slot(src, self._r)
         torch.cuda.current_stream().synchronize()
-        self._store.set(key + "/recv", json.dumps({"t": _export(t), "bytes": nb, "type": str(t.dtype)}))
-        status = self._store.get(key + "/done").decode()
-        self._store.delete_key(key + "/recv")
-        self._store.delete_key(key + "/done")
+        self._pp.post(want, n, json.dumps({"t": _export(t), "bytes": nb, "type": str(t.dtype)}).encode())
+        self._pp.wait(done, n, self._timeout_ms)
+        status = self._pp.read(done).decode(errors="replace")
         if status != "ok":
             raise RuntimeError(status)
         return _Done([t])
@@ -442,6 +484,8 @@ class HocclProcessGroup(dist.ProcessGroup):
         self.barrier()
         ipc_close_all()
         self.barrier()
+        self._coll.close()
+        self._pp.close()
         self._closed = True
         if self in _GROUPS:
             _GROUPS.remove(self)

@@ -292,10 +292,12 @@ def test_backend_group_name():
     """DeviceMesh finds a group by the name torch sets on it."""
     import torch.distributed as dist
     from paper_2609_34334_amd import distributed as hdist
-    g = hdist.HocclProcessGroup(dist.HashStore(), 0, 2, None)
+    g = hdist.HocclProcessGroup(dist.HashStore(), 0, 1, None)
     g._set_group_name("7")
     g._set_group_desc("mesh_default")
     assert (g.group_name, g.group_desc) == ("7", "mesh_default")
+    g._coll.close()
+    g._pp.close()
 
 
 def test_ipc_export_rejects_host_memory():

@@ -1,7 +1,8 @@
 """The host code under AddressSanitizer and UBSan (CPU only): the planner and
 the collective scheduler replay every plan shape on exactly-sized host
 buffers, the C oracle runs every function the same way, and the engine
-proxy's balanced issue runs against simulated engines.  A read or write
+proxy's balanced issue runs against simulated engines, and two processes
+ping-pong through the cross-process mailbox.  A read or write
 outside a documented buffer, or undefined behaviour such as signed overflow,
 fails the run.  The oracle's driver shares nothing with the other two."""
 import os
@@ -55,3 +56,14 @@ def test_proxy_balanced_issue_simulation(tmp_path):
            os.path.join(CSRC, "schedule.cpp"), "-o", exe]
     out = _run(cmd, tmp_path, exe)
     assert "balance cases: 133" in out, out
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
+def test_mailbox_across_a_fork(tmp_path):
+    """The cross-process mailbox between a parent and a forked child."""
+    exe = str(tmp_path / "mailbox_check")
+    cmd = ["g++", "-std=c++17", *SAN, "-I/opt/rocm/include", "-D__HIP_PLATFORM_AMD__",
+           os.path.join(HERE, "native", "mailbox_check.cpp"), os.path.join(CSRC, "mailbox.cpp"),
+           "-o", exe]
+    out = _run(cmd, tmp_path, exe)
+    assert "mailbox cases: 1512" in out, out
