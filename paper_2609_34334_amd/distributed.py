@@ -51,9 +51,9 @@ lives.  ``destroy_process_group`` closes the opened handles before any rank
 may free its memory.  With these, torch.nn.parallel.DistributedDataParallel
 (parameter and buffer broadcast, gradient buckets) and FSDP2's fully_shard
 (parameter all-gathers, averaging gradient reduce-scatters) run over the
-backend.  torch's functional collectives (DTensor redistribution such as
-``full_tensor()``) call a process group's C++ backend directly, which a
-process group written in Python does not have: they are not supported.
+backend, and so do torch's functional collectives (all_gather_tensor,
+reduce_scatter_tensor, all_reduce(_coalesced), all_to_all_single,
+broadcast), which DTensor redistribution such as ``full_tensor()`` uses.
 
 Use::
 
@@ -306,6 +306,11 @@ class HocclProcessGroup(dist.ProcessGroup):
             t.div_(self._n)
         return w
 
+    def allreduce_coalesced(self, tensors, opts=None):
+        for t in tensors:
+            self.allreduce([t], opts)
+        return _Done(list(tensors))
+
     def broadcast(self, tensors, opts=None):
         """The root's tensor into every rank's: an all-to-all(v) whose only
         nonzero row is the root's, every copy reading the root's whole
@@ -349,6 +354,13 @@ class HocclProcessGroup(dist.ProcessGroup):
             output.div_(self._n)
         return w
 
+    def reduce_scatter_tensor_coalesced(self, outputs, inputs, opts=None):
+        """One reduce-scatter per pair (torch's functional reduce_scatter_tensor
+        arrives here)."""
+        for o, i in zip(outputs, inputs):
+            self._reduce_scatter_base(o, i, opts)
+        return _Done(list(outputs))
+
     def reduce_scatter(self, output_tensors, input_tensors, opts=None):
         (out,) = output_tensors
         (ins,) = input_tensors
@@ -370,6 +382,13 @@ class HocclProcessGroup(dist.ProcessGroup):
             r = _ptrs(self._resolve(descs, "out", output.data_ptr()))
             _check(lib().hoccl_allgather(s, r, nb // u, dt, self._n, _stream()), "hoccl_allgather")
         return self._call(desc, run, [output])
+
+    def allgather_into_tensor_coalesced(self, outputs, inputs, opts=None):
+        """One all-gather per pair (torch's functional all_gather_tensor, and
+        so DTensor's full_tensor(), arrives here)."""
+        for o, i in zip(outputs, inputs):
+            self._allgather_base(o, i, opts)
+        return _Done(list(outputs))
 
     def allgather(self, output_tensors, input_tensors, opts=None):
         (outs,) = output_tensors

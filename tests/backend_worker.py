@@ -5,7 +5,8 @@ rank's seeded inputs, so it can compute the oracle's result itself and
 compare its own output with it bit for bit: all_reduce, reduce_scatter_tensor,
 reduce_scatter (list), all_gather_into_tensor, all_gather (list),
 all_to_all_single with uneven splits, send/recv around the ring, broadcast
-from every root, barrier.  The copy collectives also run on dtypes the
+from every root, barrier, and torch's functional collectives (all_reduce,
+reduce_scatter_tensor, all_gather_tensor, all_to_all_single, broadcast).  The copy collectives also run on dtypes the
 library has no arithmetic for (int64, uint8, float16), whose bytes they
 move in 4- or 2-byte units; an odd byte count is refused on every rank.
 Prints "rank r: backend ok" when everything matched."""
@@ -125,6 +126,26 @@ def main():
             dist.recv(got, (rank - 1) % R)
             dist.send(xs[rank], (rank + 1) % R)
         assert_same_bytes(got, xs[(rank - 1) % R], f"recv {dtype}")
+    # torch's functional collectives (what DTensor uses) reach the backend too
+    import torch.distributed._functional_collectives as funcol
+    grp = dist.group.WORLD
+    done = lambda x: x.wait() if hasattr(x, "wait") else x
+    for dt in (hc.INT32, hc.FP32, hc.BF16):
+        n = 4099
+        xs = [W.random_values(NAME[dt], 980, r, n) for r in range(R)]
+        got = done(funcol.all_reduce(to_dev(xs[rank], dt), "sum", grp))
+        assert_bitwise(from_dev(got, dt), oracle.allreduce_new(xs, dt)[rank], f"funcol all_reduce {NAME[dt]}")
+        xr = [W.random_values(NAME[dt], 981, r, R * n) for r in range(R)]
+        got = done(funcol.reduce_scatter_tensor(to_dev(xr[rank], dt), "sum", 0, grp))
+        assert_bitwise(from_dev(got, dt), oracle.reduce_scatter_new(xr, dt)[rank],
+                       f"funcol reduce_scatter_tensor {NAME[dt]}")
+        got = done(funcol.all_gather_tensor(to_dev(xs[rank], dt), 0, grp))
+        assert_bitwise(from_dev(got, dt), oracle.allgather_new(xs, dt)[rank], f"funcol all_gather {NAME[dt]}")
+        got = done(funcol.all_to_all_single(to_dev(xr[rank], dt), None, None, grp))
+        want = np.concatenate([xr[s][rank * n:(rank + 1) * n] for s in range(R)])
+        assert_bitwise(from_dev(got, dt), want, f"funcol all_to_all_single {NAME[dt]}")
+        got = done(funcol.broadcast(to_dev(xs[rank], dt), R - 1, grp))
+        assert_bitwise(from_dev(got, dt), xs[R - 1], f"funcol broadcast {NAME[dt]}")
     try:                                    # 3 bytes: no 2-byte unit divides them
         dist.broadcast(torch.zeros(3, dtype=torch.uint8, device="cuda"), 0)
         raise AssertionError("an odd-sized broadcast was accepted")

@@ -10,7 +10,8 @@ With argument "bf16" the parameters are gathered and the gradients reduced
 in bfloat16 (MixedPrecisionPolicy), otherwise in float32.
 
 Three SGD steps on per-rank seeded batches.  After each backward the
-gathered gradients are compared with the average over ranks of the local
+gradients, gathered with DTensor.full_tensor() (torch's functional
+all-gather, which reaches the backend too), are compared with the average over ranks of the local
 gradients, which every rank computes itself on a plain copy of the model
 (in the parameter dtype, as FSDP computes them): within the recursive
 summation bound of a fold over the ranks in float32, plus the final
@@ -56,21 +57,6 @@ def batch(rank, step):
     return torch.randn(BATCH, WIDTH, generator=g).cuda(), torch.randint(0, OUT, (BATCH,), generator=g).cuda()
 
 
-@torch.no_grad()
-def gathered(d, R):
-    """The full tensor of a dim-0 sharded DTensor, through the backend's
-    all_gather_into_tensor (torch's functional collectives, which
-    DTensor.full_tensor uses, need a C++ backend)."""
-    local = d.to_local()
-    rows = d.shape[0]
-    per = -(-rows // R)                               # fully_shard's chunks: ceil(rows / R) each
-    pad = torch.zeros((per,) + tuple(d.shape[1:]), dtype=local.dtype, device="cuda")
-    pad[:local.shape[0]] = local
-    out = torch.empty((R * per,) + tuple(d.shape[1:]), dtype=local.dtype, device="cuda")
-    dist.all_gather_into_tensor(out, pad)
-    return out[:rows]
-
-
 def main():
     rank, R = int(os.environ["RANK"]), int(os.environ["WORLD_SIZE"])
     low = len(sys.argv) > 1 and sys.argv[1] == "bf16"
@@ -101,7 +87,7 @@ def main():
         F.cross_entropy(model(x).float(), y).backward()
         grads = {}
         for n, p in model.named_parameters():
-            full = gathered(p.grad, R)
+            full = p.grad.full_tensor()           # torch's functional all-gather, over the backend
             g = full.double()
             exact = sum(t[n].double() for t in local) / R
             bound = (gamma + ulp) * sum(t[n].double().abs() for t in local) / R + 1e-30
@@ -113,7 +99,7 @@ def main():
             for n, p in plain.named_parameters():
                 p.add_(grads[n], alpha=-0.05)
         for n, p in model.named_parameters():
-            full = gathered(p, R)
+            full = p.full_tensor()
             ref = dict(plain.named_parameters())[n]
             assert torch.allclose(full, ref, rtol=2 ** -22, atol=1e-9), \
                 f"step {step}: {n} parameters off by {float((full - ref).abs().max())}"
