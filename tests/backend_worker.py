@@ -6,7 +6,8 @@ compare its own output with it bit for bit: all_reduce, reduce_scatter_tensor,
 reduce_scatter (list), all_gather_into_tensor, all_gather (list),
 all_to_all_single with uneven splits, send/recv around the ring, broadcast
 from every root, barrier, and torch's functional collectives (all_reduce,
-reduce_scatter_tensor, all_gather_tensor, all_to_all_single, broadcast).  The copy collectives also run on dtypes the
+reduce_scatter_tensor, all_gather_tensor, all_to_all_single, broadcast);
+an all-reduce and an all-gather in a subgroup of the odd ranks.  The copy collectives also run on dtypes the
 library has no arithmetic for (int64, uint8, float16), whose bytes they
 move in 4- or 2-byte units; an odd byte count is refused on every rank.
 Prints "rank r: backend ok" when everything matched."""
@@ -146,6 +147,21 @@ def main():
         assert_bitwise(from_dev(got, dt), want, f"funcol all_to_all_single {NAME[dt]}")
         got = done(funcol.broadcast(to_dev(xs[rank], dt), R - 1, grp))
         assert_bitwise(from_dev(got, dt), xs[R - 1], f"funcol broadcast {NAME[dt]}")
+    # a subgroup of the odd ranks (every rank creates it; only members call)
+    odd = list(range(1, R, 2))
+    sub = dist.new_group(odd)
+    if rank in odd:
+        n = 1000
+        xs = [W.random_values("fp32", 990, r, n) for r in odd]
+        t = to_dev(xs[odd.index(rank)], hc.FP32)
+        dist.all_reduce(t, group=sub)
+        assert_bitwise(from_dev(t, hc.FP32), oracle.allreduce_new(xs, hc.FP32)[odd.index(rank)],
+                       "subgroup all_reduce")
+        g = torch.empty(len(odd) * n, dtype=torch.float32, device="cuda")
+        dist.all_gather_into_tensor(g, t, group=sub)
+        assert_bitwise(from_dev(g, hc.FP32), np.concatenate([from_dev(t, hc.FP32)] * len(odd)),
+                       "subgroup all_gather")
+    dist.barrier()
     try:                                    # 3 bytes: no 2-byte unit divides them
         dist.broadcast(torch.zeros(3, dtype=torch.uint8, device="cuda"), 0)
         raise AssertionError("an odd-sized broadcast was accepted")
