@@ -218,11 +218,17 @@ class HocclProcessGroup(dist.ProcessGroup):
         every rank opens them; rank 0 removes the names once all have."""
         if self._r == 0:
             base = f"/hoccl-{os.getpid()}-{secrets.token_hex(6)}"
-            self._coll = Mailbox(base + "-c", self._n + 1, COLL_SLOT_BYTES)
-            self._pp = Mailbox(base + "-p", 2 * self._n * self._n, P2P_SLOT_BYTES)
+            try:
+                self._coll = Mailbox(base + "-c", self._n + 1, COLL_SLOT_BYTES)
+                self._pp = Mailbox(base + "-p", 2 * self._n * self._n, P2P_SLOT_BYTES)
+            except Exception as e:             # the other ranks wait for the name
+                self._store.set("mailbox", f"error: {e}")
+                raise
             self._store.set("mailbox", base)
         else:
             base = self._store.get("mailbox").decode()
+            if base.startswith("error: "):
+                raise RuntimeError(f"hoccl: rank 0 could not create the group's mailboxes ({base[7:]})")
             self._coll = Mailbox(base + "-c")
             self._pp = Mailbox(base + "-p")
         if self._store.add("mailbox-opened", 1) == self._n:
