@@ -18,6 +18,7 @@
 #include <sys/syscall.h>
 #include <unistd.h>
 
+#include <algorithm>
 #include <cerrno>
 #include <chrono>
 #include <climits>
@@ -181,19 +182,24 @@ hoccl_status_t hoccl_mailbox_wait(hoccl_mailbox_t *box, unsigned slot, unsigned 
         if (seq_reached(__atomic_load_n(&s->seq, __ATOMIC_ACQUIRE), seq)) return HOCCL_OK;
         __builtin_ia32_pause();
     }
-    const auto deadline = std::chrono::steady_clock::now() + std::chrono::milliseconds(timeout_ms);
+    using clock = std::chrono::steady_clock;
+    const auto deadline = clock::now() + std::chrono::milliseconds(timeout_ms);
     for (;;) {
+        const auto left = std::chrono::duration_cast<std::chrono::nanoseconds>(deadline - clock::now());
+        if (left.count() <= 0)
+            return fail(HOCCL_ERR_TIMEOUT, "mailbox_wait: slot %u did not reach %u within %u ms",
+                        slot, seq, timeout_ms);
+        // Sleep at most 10 ms at a time, so the deadline is re-checked even
+        // if a wake-up were missed.
+        const long ns = std::min<long>(left.count(), 10L * 1000 * 1000);
         __atomic_fetch_add(&s->waiters, 1u, __ATOMIC_SEQ_CST);
         const uint32_t now = __atomic_load_n(&s->seq, __ATOMIC_SEQ_CST);
         if (!seq_reached(now, seq)) {
-            struct timespec ts = {0, 10 * 1000 * 1000};  // re-check at least every 10 ms
+            struct timespec ts = {0, ns};
             futex(&s->seq, FUTEX_WAIT, now, &ts);
         }
         __atomic_fetch_sub(&s->waiters, 1u, __ATOMIC_SEQ_CST);
         if (seq_reached(__atomic_load_n(&s->seq, __ATOMIC_ACQUIRE), seq)) return HOCCL_OK;
-        if (std::chrono::steady_clock::now() > deadline)
-            return fail(HOCCL_ERR_TIMEOUT, "mailbox_wait: slot %u did not reach %u within %u ms",
-                        slot, seq, timeout_ms);
     }
 }
 
