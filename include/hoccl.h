@@ -496,8 +496,8 @@ hoccl_status_t hoccl_ring_hop(const void *partial, const void *local, void *out,
  * intra-node communication): a process exports the allocation holding one
  * of its device buffers, another process on the same device opens it and
  * can then pass the buffer to the collectives above as one of its R
- * pointers.  The handles travel out of band (the PyTorch backend uses the
- * c10d store).  The exporter must not free the allocation while an
+ * pointers.  The handles travel out of band (the PyTorch backend posts
+ * them in a mailbox, below).  The exporter must not free the allocation while an
  * importer has it open.
  *
  * Export the allocation that contains device pointer `ptr`: `handle`

@@ -3,8 +3,8 @@
 // buffers as an IPC handle plus the buffer's offset in it; another process
 // on the same device opens the handle and addresses the buffer directly, so
 // a copy engine or a kernel of that process can read or write it.  The
-// handles travel between processes out of band (the PyTorch backend puts
-// them in the c10d store).  Opened handles are cached per handle, so a
+// handles travel between processes out of band (the PyTorch backend posts
+// them in a shared-memory mailbox).  Opened handles are cached per handle, so a
 // buffer reused call after call is opened once.
 #include <hip/hip_runtime.h>
 
