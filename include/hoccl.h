@@ -29,8 +29,8 @@
  *   caller, must stay valid until the operation completes on `stream`, and
  *   are never retained by the library after that.
  * Counts are in elements of `dtype`.  For copy-only collectives the dtype
- *   only sets the element size (4 bytes for int32/fp32, 2 for bf16) and the
- *   bytes are moved bit for bit.
+ *   only sets the element size (4 bytes for int32/fp32, 2 for bf16, 1 for
+ *   uint8) and the bytes are moved bit for bit.
  * Asynchrony.  Every call returns once the work is enqueued.  The operation
  *   starts after all work previously enqueued on `stream` and all work
  *   enqueued on `stream` afterwards sees its results.  No call synchronises
@@ -100,11 +100,16 @@ typedef enum {
     HOCCL_ERR_UNSUPPORTED = 2, /* valid request the library cannot serve here     */
     HOCCL_ERR_HIP = 3,         /* a HIP / HSA runtime call failed                   */
     HOCCL_ERR_NO_MEMORY = 4,   /* workspace or host allocation failed               */
-    HOCCL_ERR_TIMEOUT = 5,     /* the copy proxy's watchdog expired                 */
+    HOCCL_ERR_TIMEOUT = 5,     /* the copy proxy's watchdog, or a mailbox wait, expired */
     HOCCL_ERR_INTERNAL = 6
 } hoccl_status_t;
 
-typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2 } hoccl_dtype_t;
+/* Element types.  INT32, FP32 and BF16 are the reduction types.  UINT8 is
+ * for the copy-only collectives (all-gather, send/recv, all-to-all(v)),
+ * which move bits and use the dtype only for the element size: it lets a
+ * caller move any byte count.  The reductions (all-reduce,
+ * reduce-scatter, ring hop) return HOCCL_ERR_INVALID_ARG for it. */
+typedef enum { HOCCL_INT32 = 0, HOCCL_FP32 = 1, HOCCL_BF16 = 2, HOCCL_UINT8 = 3 } hoccl_dtype_t;
 
 /* Where pure-copy steps run.  AUTO, SDMA and KERNEL keep the values 0, 1
  * and 2; the HIP runtime's own copy is appended as 3. */

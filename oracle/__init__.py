@@ -24,8 +24,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "hoccl_oracle.c")
 _LIB = os.path.join(_HERE, "libhoccl_oracle.so")
 
-INT32, FP32, BF16 = 0, 1, 2
-_NP = {INT32: np.int32, FP32: np.float32, BF16: np.uint16}
+INT32, FP32, BF16, UINT8 = 0, 1, 2, 3
+_NP = {INT32: np.int32, FP32: np.float32, BF16: np.uint16, UINT8: np.uint8}
 
 _lib = None
 
@@ -76,7 +76,8 @@ def _check(rc, name):
 
 
 def dtype_code(np_dtype):
-    """int32 -> INT32, float32 -> FP32, uint16 (bf16 bit patterns) -> BF16."""
+    """int32 -> INT32, float32 -> FP32, uint16 (bf16 bit patterns) -> BF16,
+    uint8 -> UINT8 (copies only)."""
     np_dtype = np.dtype(np_dtype)
     for k, v in _NP.items():
         if np.dtype(v) == np_dtype:

@@ -48,7 +48,9 @@
 #include <stdint.h>
 #include <string.h>
 
-enum { OR_INT32 = 0, OR_FP32 = 1, OR_BF16 = 2 };
+/* OR_UINT8 is a byte, for the copies only: the sum is defined for the
+ * three arithmetic types, so the reductions refuse it. */
+enum { OR_INT32 = 0, OR_FP32 = 1, OR_BF16 = 2, OR_UINT8 = 3 };
 
 static size_t elem_size(int dtype)
 {
@@ -56,6 +58,7 @@ static size_t elem_size(int dtype)
     case OR_INT32: return 4;
     case OR_FP32: return 4;
     case OR_BF16: return 2;
+    case OR_UINT8: return 1;
     default: return 0;
     }
 }
@@ -143,6 +146,7 @@ int oracle_allreduce(const void *const *send, void *const *recv, size_t count,
 {
     int rc = check_common(send, recv, dtype, R);
     if (rc) return rc;
+    if (dtype == OR_UINT8) return -2;
     if (count == 0) return 0;
     size_t es = elem_size(dtype);
     size_t c = (count + (size_t)R - 1) / (size_t)R;
@@ -162,6 +166,7 @@ int oracle_reduce_scatter(const void *const *send, void *const *recv,
 {
     int rc = check_common(send, recv, dtype, R);
     if (rc) return rc;
+    if (dtype == OR_UINT8) return -2;
     size_t es = elem_size(dtype);
     for (int r = 0; r < R; ++r)
         for (size_t i = 0; i < recvcount; ++i)

@@ -25,12 +25,13 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NO_MEMORY, ERR_TIMEOUT, ERR_INTERNAL = range(7)
-INT32, FP32, BF16 = 0, 1, 2
+INT32, FP32, BF16, UINT8 = 0, 1, 2, 3
 COPY_AUTO, COPY_SDMA, COPY_KERNEL, COPY_HIP = range(4)
 REDUCE_RING, REDUCE_DIRECT, REDUCE_AUTO = range(3)
 OP_ALLREDUCE, OP_REDUCE_SCATTER, OP_ALLGATHER, OP_SENDRECV, OP_ALLTOALL = range(5)
 
 _DTYPES = {torch.int32: INT32, torch.float32: FP32, torch.bfloat16: BF16}
+_COPY_DTYPES = {**_DTYPES, torch.uint8: UINT8}     # the copy-only collectives also move bytes
 HOP_FIRST, HOP_MIDDLE, HOP_LAST, HOP_ONLY = range(4)
 HOPS = {"first": HOP_FIRST, "middle": HOP_MIDDLE, "last": HOP_LAST, "only": HOP_ONLY}
 COPY_PATHS = {"auto": COPY_AUTO, "sdma": COPY_SDMA, "engines": COPY_SDMA,
@@ -253,9 +254,10 @@ def interleave(bytes_per_flow, chunk_bytes):
 
 # ---- collectives ---------------------------------------------------------------
 
-def _dtype_of(tensors):
+def _dtype_of(tensors, copy=False):
     dt = tensors[0].dtype
-    if dt not in _DTYPES:
+    table = _COPY_DTYPES if copy else _DTYPES
+    if dt not in table:
         raise TypeError(f"unsupported dtype {dt}")
     dev = tensors[0].device
     for t in tensors:
@@ -265,7 +267,7 @@ def _dtype_of(tensors):
             raise ValueError("all buffers must live on the same GPU")
         if not t.is_contiguous():
             raise ValueError("buffers must be contiguous")
-    return _DTYPES[dt]
+    return table[dt]
 
 
 def _ptrs(tensors):
@@ -345,7 +347,7 @@ def allgather(send, recv=None, stream=None):
     n = send[0].numel()
     if recv is None:
         recv = [torch.empty(R * n, dtype=send[0].dtype, device=send[0].device) for _ in range(R)]
-    dt = _dtype_of(list(send) + list(recv))
+    dt = _dtype_of(list(send) + list(recv), copy=True)
     if any(t.numel() != n for t in send) or any(t.numel() != R * n for t in recv):
         raise ValueError("buffer sizes do not match")
     _check(_lib.hoccl_allgather(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
@@ -360,7 +362,7 @@ def sendrecv(send, recv, peers, stream=None):
     R = len(send)
     n = send[0].numel()
     live = [t for t in list(send) + list(recv) if t is not None]
-    dt = _dtype_of(live)
+    dt = _dtype_of(live, copy=True)
     rp = (ctypes.c_void_p * R)(*[0 if t is None else t.data_ptr() for t in recv])
     pp = (ctypes.c_int * R)(*peers)
     _check(_lib.hoccl_sendrecv(_ptrs(send), rp, pp, n, dt, R, _stream(stream)), "hoccl_sendrecv")
@@ -375,7 +377,7 @@ def alltoall(send, recv=None, stream=None):
     n = send[0].numel() // R
     if recv is None:
         recv = [torch.empty_like(t) for t in send]
-    dt = _dtype_of(list(send) + list(recv))
+    dt = _dtype_of(list(send) + list(recv), copy=True)
     _check(_lib.hoccl_alltoall(_ptrs(send), _ptrs(recv), n, dt, R, _stream(stream)),
            "hoccl_alltoall")
     return recv
@@ -385,7 +387,7 @@ def alltoall(send, recv=None, stream=None):
 def alltoallv(send, counts, sdispls, recv, rdispls, stream=None):
     """counts/sdispls/rdispls: R*R element counts and offsets, [s*R + d]."""
     R = len(send)
-    dt = _dtype_of(list(send) + list(recv))
+    dt = _dtype_of(list(send) + list(recv), copy=True)
     S = ctypes.c_size_t * (R * R)
     _check(_lib.hoccl_alltoallv(_ptrs(send), S(*counts), S(*sdispls), _ptrs(recv), S(*rdispls),
                                 dt, R, _stream(stream)), "hoccl_alltoallv")

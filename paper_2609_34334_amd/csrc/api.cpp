@@ -933,12 +933,18 @@ hoccl_status_t check_overlaps(const std::vector<Range> &outs, const std::vector<
     return HOCCL_OK;
 }
 
-hoccl_status_t check_common(const void *send, const void *recv, hoccl_dtype_t dt, int R) {
+// `copy`: a copy-only collective, which also takes HOCCL_UINT8.
+hoccl_status_t check_common(const void *send, const void *recv, hoccl_dtype_t dt, int R,
+                            bool copy = false) {
     if (R < 1 || R > kMaxRanks) {
         set_err("R = %d outside [1, %d]", R, kMaxRanks);
         return HOCCL_ERR_INVALID_ARG;
     }
-    if (dt != HOCCL_INT32 && dt != HOCCL_FP32 && dt != HOCCL_BF16) {
+    if (dt == HOCCL_UINT8 && !copy) {
+        set_err("uint8 is for the copy-only collectives; reductions take int32, fp32 or bf16");
+        return HOCCL_ERR_INVALID_ARG;
+    }
+    if (dt != HOCCL_INT32 && dt != HOCCL_FP32 && dt != HOCCL_BF16 && dt != HOCCL_UINT8) {
         set_err("unknown dtype %d", (int)dt);
         return HOCCL_ERR_INVALID_ARG;
     }
@@ -1092,7 +1098,7 @@ const char *hoccl_status_string(hoccl_status_t s) {
     case HOCCL_ERR_UNSUPPORTED: return "unsupported";
     case HOCCL_ERR_HIP: return "HIP/HSA runtime error";
     case HOCCL_ERR_NO_MEMORY: return "out of memory";
-    case HOCCL_ERR_TIMEOUT: return "copy proxy timeout";
+    case HOCCL_ERR_TIMEOUT: return "timeout";
     case HOCCL_ERR_INTERNAL: return "internal error";
     }
     return "unknown status";
@@ -1215,7 +1221,7 @@ hoccl_status_t hoccl_reduce_scatter_noalloc(const void *const *send, void *const
 
 hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv, size_t n,
                                hoccl_dtype_t dt, int R, hipStream_t stream) {
-    TRY(check_common(send, recv, dt, R));
+    TRY(check_common(send, recv, dt, R, true));
     if (n == 0) return HOCCL_OK;
     TRY(check_ptrs(send, R, "send"));
     TRY(check_ptrs((const void *const *)recv, R, "recv"));
@@ -1238,7 +1244,7 @@ hoccl_status_t hoccl_allgather(const void *const *send, void *const *recv, size_
 
 hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv, const int *peers,
                               size_t n, hoccl_dtype_t dt, int R, hipStream_t stream) {
-    TRY(check_common(send, recv, dt, R));
+    TRY(check_common(send, recv, dt, R, true));
     if (!peers) {
         set_err("peers must not be NULL");
         return HOCCL_ERR_INVALID_ARG;
@@ -1277,7 +1283,7 @@ hoccl_status_t hoccl_sendrecv(const void *const *send, void *const *recv, const 
 
 hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv, size_t n,
                               hoccl_dtype_t dt, int R, hipStream_t stream) {
-    TRY(check_common(send, recv, dt, R));
+    TRY(check_common(send, recv, dt, R, true));
     if (n == 0) return HOCCL_OK;
     TRY(check_ptrs(send, R, "send"));
     TRY(check_ptrs((const void *const *)recv, R, "recv"));
@@ -1297,7 +1303,7 @@ hoccl_status_t hoccl_alltoall(const void *const *send, void *const *recv, size_t
 hoccl_status_t hoccl_alltoallv(const void *const *send, const size_t *counts, const size_t *sd,
                                void *const *recv, const size_t *rd, hoccl_dtype_t dt, int R,
                                hipStream_t stream) {
-    TRY(check_common(send, recv, dt, R));
+    TRY(check_common(send, recv, dt, R, true));
     if (!counts || !sd || !rd) {
         set_err("counts and displacements must not be NULL");
         return HOCCL_ERR_INVALID_ARG;
@@ -1329,7 +1335,7 @@ hoccl_status_t hoccl_alltoallv(const void *const *send, const size_t *counts, co
 
 hoccl_status_t hoccl_debug_plan_json(int op, size_t count, hoccl_dtype_t dt, int R, char *buf,
                                      size_t len, size_t *needed) {
-    TRY(check_common((const void *)1, (const void *)1, dt, R));
+    TRY(check_common((const void *)1, (const void *)1, dt, R, op >= 2));
     PlanOptions o = options_from(config(), false);
     Plan p;
     switch (op) {

@@ -22,7 +22,7 @@
 
 namespace hoccl {
 
-size_t dtype_size(hoccl_dtype_t dt) { return dt == HOCCL_BF16 ? 2 : 4; }
+size_t dtype_size(hoccl_dtype_t dt) { return dt == HOCCL_BF16 ? 2 : dt == HOCCL_UINT8 ? 1 : 4; }
 size_t acc_size(hoccl_dtype_t) { return 4; }
 
 static inline int mod(int a, int R) { return ((a % R) + R) % R; }

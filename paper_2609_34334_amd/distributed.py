@@ -32,7 +32,9 @@ have, rank 0 removes the names (the mappings stay, and nothing is left in
 /dev/shm when the processes exit).
 
 Broadcast is a one-row all-to-all(v): the root's buffer is copied into every
-other rank's.
+other rank's.  Scatter and gather are the same with the root's buffer cut
+into blocks (one column for gather); reduce is an all-reduce of copies;
+the list forms of all-gather and all-to-all stage through flat buffers.
 
 Every call synchronises the calling rank's current stream before it
 publishes (its inputs are complete and its outputs free) and returns once
@@ -43,8 +45,9 @@ of float32 or bfloat16 (FSDP's gradient reduce-scatter): the sum, rounded
 once to the dtype, then divided by the world size in that dtype on the
 caller's stream (exact when the world size is a power of two).  The copy
 collectives (broadcast, all-gather, all-to-all, send/recv) move bytes, so
-they take any dtype; the library copies them in 4- or 2-byte units, and a
-copy whose byte counts are odd is refused.  Buffers must be contiguous CUDA
+they take any dtype; the library copies them in 4-, 2- or 1-byte units,
+the widest that divides every count and offset (so all_gather_object and
+broadcast_object_list work too).  Buffers must be contiguous CUDA
 tensors on the shared GPU, in allocations below 2 GiB (larger ones are not
 shared), and must not be freed (``torch.cuda.empty_cache``) while the group
 lives.  ``destroy_process_group`` closes the opened handles before any rank
@@ -71,7 +74,8 @@ from datetime import timedelta
 import torch
 import torch.distributed as dist
 
-from . import (BF16, FP32, INT32, Mailbox, _check, _DTYPES, ipc_close_all, ipc_export, ipc_open, lib)
+from . import (BF16, FP32, INT32, UINT8, Mailbox, _check, _DTYPES, ipc_close_all, ipc_export, ipc_open,
+               lib)
 
 BACKEND = "hoccl"
 ENV = "HOCCL_BACKEND"
@@ -156,12 +160,12 @@ def _nbytes(t):
 
 def _unit(byte_counts):
     """(library dtype, unit bytes) of a copy: copies move bits, so the dtype
-    only sets the unit, the largest of 4 and 2 bytes that divides every
+    only sets the unit, the largest of 4, 2 and 1 bytes that divides every
     count and offset."""
     for size, dt in ((4, INT32), (2, BF16)):
         if all(b % size == 0 for b in byte_counts):
             return dt, size
-    raise ValueError(f"hoccl: copies move 2-byte units; byte counts {sorted(set(byte_counts))[:8]} are odd")
+    return UINT8, 1
 
 
 def _export(t):
@@ -252,6 +256,13 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     def getGroupDesc(self):
         return self._desc
+
+    @property
+    def _device_types(self):
+        """The devices the group serves, as torch reads them to place the
+        tensors of its object collectives (all_gather_object and the like);
+        torch would list its C++ backends, of which this group has none."""
+        return [torch.device("cuda")]
 
     def setGroupDesc(self, desc):
         self._desc = desc
@@ -448,6 +459,93 @@ class HocclProcessGroup(dist.ProcessGroup):
                    "hoccl_alltoallv")
         return self._call(desc, run, [output])
 
+    # ---- rooted and list forms, built on the above ------------------------------------
+    # They stage through flat buffers (torch copies on the caller's stream)
+    # where the library's forms need one buffer per rank.
+
+    def _rooted(self, mine, root, to_root):
+        """One all-to-all(v) whose only nonzero row (to_root False: the
+        root's buffer cut into R blocks, block d to rank d) or column
+        (to_root True: every rank's buffer to block r of the root's) is the
+        root's.  `mine` is this rank's flat buffer: R blocks on the root and
+        one block elsewhere."""
+        R = self._n
+        if not 0 <= root < R:
+            raise ValueError(f"hoccl: root {root} outside 0..{R - 1}")
+        nb = _nbytes(mine) // (R if self._r == root else 1)
+        desc = {"t": _export(mine), "bytes": nb, "type": str(mine.dtype), "dev": mine.device.index}
+
+        def run(descs):
+            if any(d["bytes"] != nb or d["type"] != str(mine.dtype) for d in descs):
+                raise ValueError("hoccl: gather/scatter tensors differ between ranks")
+            dt, u = _unit([nb])
+            p = _ptrs(self._resolve(descs, "t", mine.data_ptr()))
+            S = ctypes.c_size_t * (R * R)
+            n = nb // u
+            if to_root:      # rank s's block to block s of the root's buffer
+                counts = [n if d == root and s != root else 0 for s in range(R) for d in range(R)]
+                sd = [0] * (R * R)
+                rd = [s * n if d == root else 0 for s in range(R) for d in range(R)]
+            else:            # block d of the root's buffer to rank d
+                counts = [n if s == root and d != root else 0 for s in range(R) for d in range(R)]
+                sd = [d * n if s == root else 0 for s in range(R) for d in range(R)]
+                rd = [0] * (R * R)
+            _check(lib().hoccl_alltoallv(p, S(*counts), S(*sd), p, S(*rd), dt, R, _stream()),
+                   "hoccl_alltoallv")
+        return self._call(desc, run)
+
+    def gather(self, output_tensors, input_tensors, opts=None):
+        (inp,) = input_tensors
+        root = getattr(opts, "rootRank", 0)
+        n = inp.numel()
+        if self._r == root:
+            flat = torch.empty(self._n * n, dtype=inp.dtype, device=inp.device)
+            flat[root * n:(root + 1) * n].copy_(inp.reshape(-1))
+            self._rooted(flat, root, True)
+            (outs,) = output_tensors
+            for r, o in enumerate(outs):
+                o.copy_(flat[r * n:(r + 1) * n].view_as(o))
+            return _Done(output_tensors)
+        self._rooted(inp.contiguous().reshape(-1), root, True)
+        return _Done([])
+
+    def scatter(self, output_tensors, input_tensors, opts=None):
+        (out,) = output_tensors
+        root = getattr(opts, "rootRank", 0)
+        if self._r == root:
+            (ins,) = input_tensors
+            flat = torch.cat([x.reshape(-1) for x in ins])
+            self._rooted(flat, root, False)
+            out.copy_(ins[root].view_as(out))
+        else:
+            dst = out if out.is_contiguous() else torch.empty_like(out, memory_format=torch.contiguous_format)
+            self._rooted(dst.reshape(-1), root, False)
+            if dst is not out:
+                out.copy_(dst)
+        return _Done([out])
+
+    def reduce(self, tensors, opts=None):
+        """The sum (or average) into the root's tensor only: an all-reduce of
+        copies, the root's result copied back."""
+        (t,) = tensors
+        tmp = t.clone()
+        self.allreduce([tmp], opts)
+        if self._r == getattr(opts, "rootRank", 0):
+            t.copy_(tmp)
+        return _Done([t])
+
+    def alltoall(self, output_tensors, input_tensors, opts=None):
+        flat_in = torch.cat([x.reshape(-1) for x in input_tensors])
+        flat_out = torch.empty(sum(o.numel() for o in output_tensors), dtype=flat_in.dtype,
+                               device=flat_in.device)
+        self.alltoall_base(flat_out, flat_in, [o.numel() for o in output_tensors],
+                           [x.numel() for x in input_tensors], opts)
+        off = 0
+        for o in output_tensors:
+            o.copy_(flat_out[off:off + o.numel()].view_as(o))
+            off += o.numel()
+        return _Done(output_tensors)
+
     def barrier(self, opts=None):
         return self._call({}, lambda descs: None)
 
@@ -517,4 +615,4 @@ class HocclProcessGroup(dist.ProcessGroup):
 
 
 __all__ = ["BACKEND", "ENV", "HocclProcessGroup", "destroy_process_group", "init_process_group",
-           "register", "selected_backend", "BF16", "FP32", "INT32"]
+           "register", "selected_backend", "BF16", "FP32", "INT32", "UINT8"]

@@ -5,11 +5,12 @@ rank's seeded inputs, so it can compute the oracle's result itself and
 compare its own output with it bit for bit: all_reduce, reduce_scatter_tensor,
 reduce_scatter (list), all_gather_into_tensor, all_gather (list),
 all_to_all_single with uneven splits, send/recv around the ring, broadcast
-from every root, barrier, and torch's functional collectives (all_reduce,
+from every root, gather, scatter, reduce, all_to_all (lists), the object
+collectives, barrier, and torch's functional collectives (all_reduce,
 reduce_scatter_tensor, all_gather_tensor, all_to_all_single, broadcast);
 an all-reduce and an all-gather in a subgroup of the odd ranks.  The copy collectives also run on dtypes the
 library has no arithmetic for (int64, uint8, float16), whose bytes they
-move in 4- or 2-byte units; an odd byte count is refused on every rank.
+move in 4-, 2- or 1-byte units.
 Prints "rank r: backend ok" when everything matched."""
 import os
 import sys
@@ -162,11 +163,44 @@ def main():
         assert_bitwise(from_dev(g, hc.FP32), np.concatenate([from_dev(t, hc.FP32)] * len(odd)),
                        "subgroup all_gather")
     dist.barrier()
-    try:                                    # 3 bytes: no 2-byte unit divides them
-        dist.broadcast(torch.zeros(3, dtype=torch.uint8, device="cuda"), 0)
-        raise AssertionError("an odd-sized broadcast was accepted")
-    except RuntimeError as e:
-        assert "odd" in str(e), e
+    # odd byte counts move as single bytes
+    want = byte_tensor(1000, 0, 3, torch.uint8)
+    t = want.clone() if rank == 0 else torch.zeros(3, dtype=torch.uint8, device="cuda")
+    dist.broadcast(t, 0)
+    assert_same_bytes(t, want, "broadcast of 3 bytes")
+    xs = [byte_tensor(1001, r, 5, torch.uint8) for r in range(R)]
+    g = torch.empty(R * 5, dtype=torch.uint8, device="cuda")
+    dist.all_gather_into_tensor(g, xs[rank])
+    assert_same_bytes(g, torch.cat(xs), "all_gather of 5 bytes")
+    # object collectives (pickles of odd length, through the byte path)
+    objs = [None] * R
+    dist.all_gather_object(objs, {"rank": rank, "pad": "x" * (rank * 7 + 1)})
+    assert objs == [{"rank": r, "pad": "x" * (r * 7 + 1)} for r in range(R)], objs
+    lst = [("config", 3.5, list(range(rank + 3)))] if rank == R - 1 else [None]
+    dist.broadcast_object_list(lst, src=R - 1)
+    assert lst == [("config", 3.5, list(range(R + 2)))], lst
+    # gather, scatter, reduce and the list all-to-all, rooted at the last rank
+    root, n = R - 1, 1001
+    xs = [byte_tensor(1010, r, n, torch.float32) for r in range(R)]
+    parts = [torch.empty(n, device="cuda") for _ in range(R)] if rank == root else None
+    dist.gather(xs[rank], parts, dst=root)
+    if rank == root:
+        assert_same_bytes(torch.cat(parts), torch.cat(xs), "gather")
+    blocks = [byte_tensor(1020 + d, root, n, torch.int64) for d in range(R)]
+    got = torch.empty(n, dtype=torch.int64, device="cuda")
+    dist.scatter(got, blocks if rank == root else None, src=root)
+    assert_same_bytes(got, blocks[rank], "scatter")
+    vals = [W.random_values("fp32", 1030, r, n) for r in range(R)]
+    t = to_dev(vals[rank], hc.FP32)
+    dist.reduce(t, dst=root)
+    want = oracle.allreduce_new(vals, hc.FP32)[root] if rank == root else vals[rank]
+    assert_bitwise(from_dev(t, hc.FP32), want, "reduce")
+    ins = [byte_tensor(1040 + d, rank, d + 2, torch.bfloat16) for d in range(R)]
+    outs = [torch.empty(rank + 2, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    dist.all_to_all(outs, ins)
+    for s in range(R):
+        assert_same_bytes(outs[s], byte_tensor(1040 + rank, s, rank + 2, torch.bfloat16),
+                          f"all_to_all from {s}")
     dist.barrier()
     hdist.destroy_process_group()
     print(f"rank {rank}: backend ok", flush=True)

@@ -27,7 +27,8 @@
 _Static_assert(HOCCL_OK == 0 && HOCCL_ERR_INVALID_ARG == 1 && HOCCL_ERR_UNSUPPORTED == 2 &&
                HOCCL_ERR_HIP == 3 && HOCCL_ERR_NO_MEMORY == 4 && HOCCL_ERR_TIMEOUT == 5 &&
                HOCCL_ERR_INTERNAL == 6, "status values");
-_Static_assert(HOCCL_INT32 == 0 && HOCCL_FP32 == 1 && HOCCL_BF16 == 2, "dtype values");
+_Static_assert(HOCCL_INT32 == 0 && HOCCL_FP32 == 1 && HOCCL_BF16 == 2 && HOCCL_UINT8 == 3,
+               "dtype values");
 _Static_assert(HOCCL_COPY_AUTO == 0 && HOCCL_COPY_SDMA == 1 && HOCCL_COPY_KERNEL == 2 &&
                HOCCL_COPY_HIP == 3, "copy path values");
 _Static_assert(HOCCL_REDUCE_RING == 0 && HOCCL_REDUCE_DIRECT == 1 && HOCCL_REDUCE_AUTO == 2,

@@ -45,6 +45,13 @@ def test_bad_rank_count_and_dtype():
     big = (VP * 65)(*([0x1000] * 65))
     assert L.hoccl_allreduce(big, big, 4, hc.FP32, 65, None) == hc.ERR_INVALID_ARG
     assert L.hoccl_allreduce(p, p, 4, 9, 1, None) == hc.ERR_INVALID_ARG
+    # bytes are for the copies: every reduction refuses them before looking further
+    assert L.hoccl_allreduce(p, p, 4, hc.UINT8, 1, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_reduce_scatter(p, p, 4, hc.UINT8, 1, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_reduce_scatter_noalloc(p, p, 4, hc.UINT8, 1, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_ring_hop(VP(0x1000), VP(0x2000), VP(0x3000), 4, hc.UINT8, hc.HOP_MIDDLE,
+                            None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_allgather(p, p, 4, 4, 1, None) == hc.ERR_INVALID_ARG          # no dtype 4
     assert L.hoccl_allreduce(None, p, 4, hc.FP32, 1, None) == hc.ERR_INVALID_ARG
 
 
@@ -203,10 +210,11 @@ def test_enum_values_match_binding(tmp_path):
     binding's constants equal the header's."""
     names = ["HOCCL_COPY_AUTO", "HOCCL_COPY_SDMA", "HOCCL_COPY_KERNEL", "HOCCL_COPY_HIP",
              "HOCCL_REDUCE_RING", "HOCCL_REDUCE_DIRECT", "HOCCL_REDUCE_AUTO",
-             "HOCCL_INT32", "HOCCL_FP32", "HOCCL_BF16"]
+             "HOCCL_INT32", "HOCCL_FP32", "HOCCL_BF16", "HOCCL_UINT8"]
     got = [int(v) for v in _compile_and_run(tmp_path, "enums",
                                             "".join(f'printf("%d\\n", (int){n});' for n in names))]
-    assert got == [0, 1, 2, 3, 0, 1, 2, 0, 1, 2]
+    assert got == [0, 1, 2, 3, 0, 1, 2, 0, 1, 2, 3]
+    assert [hc.INT32, hc.FP32, hc.BF16, hc.UINT8] == [0, 1, 2, 3]
     assert [hc.COPY_AUTO, hc.COPY_SDMA, hc.COPY_KERNEL, hc.COPY_HIP] == [0, 1, 2, 3]
     assert [hc.REDUCE_RING, hc.REDUCE_DIRECT, hc.REDUCE_AUTO] == [0, 1, 2]
 
@@ -254,15 +262,14 @@ def test_backend_switch_and_registration():
 
 def test_backend_copy_units():
     """The backend's copy collectives move any dtype as bytes: 4-byte units
-    where every count and offset allows, else 2-byte units; odd byte counts
-    are refused.  Reductions keep to the library's three dtypes."""
+    where every count and offset allows, else 2-byte, else single bytes.
+    Reductions keep to the library's three arithmetic dtypes."""
     import torch
     from paper_2609_34334_amd import distributed as hdist
     assert hdist._unit([8, 4, 0]) == (hc.INT32, 4)
     assert hdist._unit([8, 6]) == (hc.BF16, 2)
     assert hdist._unit([]) == (hc.INT32, 4)
-    with pytest.raises(ValueError, match="odd"):
-        hdist._unit([4, 3])
+    assert hdist._unit([4, 3]) == (hc.UINT8, 1)
     with pytest.raises(TypeError, match="int32, float32 or bfloat16"):
         hdist._dtype(torch.zeros(2, dtype=torch.int64))
 

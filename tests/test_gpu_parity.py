@@ -1,6 +1,7 @@
 """GPU parity: every collective through the C ABI against the CPU oracle,
 bit for bit, across dtypes, rank counts, ragged and misaligned sizes, in-place
 forms, copy paths, reduction algorithms and launch shapes."""
+import ctypes
 import time
 
 import numpy as np
@@ -319,6 +320,64 @@ def test_sendrecv_and_alltoall(path, chunk):
         torch.cuda.synchronize()
         for r in range(R):
             assert_bitwise(from_dev(got[r], hc.FP32), ref[r], f"A2A n={n} r={r}")
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_uint8_copies(path):
+    """Bytes on every copy path: odd counts, odd offsets (the kernel's
+    single-byte path), all four copy collectives, canaries untouched."""
+    hc.set_config(copy_path=path)
+    dt = hc.UINT8
+    for R, n in [(3, 1), (8, 4097), (5, 1_000_003)]:
+        lead = 1 + R % 3
+        x = [W.random_bits(95 + n, r, n, 1) for r in range(R)]
+        ref = oracle.allgather_new(x, dt)
+        outs = [padded(R * n, dt, lead) for _ in range(R)]
+        hc.allgather([padded(n, dt, r % 2, 1)[1].copy_(to_dev(x[r], dt)) for r in range(R)],
+                     [o[1] for o in outs])
+        torch.cuda.synchronize()
+        for r in range(R):
+            check_canaries(outs[r][0], lead, R * n, dt)
+            assert_bitwise(from_dev(outs[r][1], dt), ref[r], f"AG u8 {path} R={R} n={n} r={r}")
+        peers = [(r + 1) % R for r in range(R)]
+        ref = [np.full(n, 0x5A, np.uint8) for _ in range(R)]
+        oracle.sendrecv(x, ref, peers, n, dt)
+        outs = [padded(n, dt, lead) for _ in range(R)]
+        hc.sendrecv([to_dev(a, dt) for a in x], [o[1] for o in outs], peers)
+        torch.cuda.synchronize()
+        for r in range(R):
+            check_canaries(outs[r][0], lead, n, dt)
+            assert_bitwise(from_dev(outs[r][1], dt), ref[r], f"P2P u8 {path} R={R} n={n} r={r}")
+        xs = [W.random_bits(96 + n, r, R * n, 1) for r in range(R)]
+        ref = [np.zeros_like(a) for a in xs]
+        oracle.alltoall(xs, ref, n, dt)
+        got = hc.alltoall([to_dev(a, dt) for a in xs])
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(got[r], dt), ref[r], f"A2A u8 {path} R={R} n={n} r={r}")
+    R = 4
+    rng = np.random.default_rng(97)
+    C = rng.integers(0, 5000, size=(R, R))
+    send = [W.random_bits(98, s, int(C[s].sum()), 1) for s in range(R)]
+    counts = [int(C[s][d]) for s in range(R) for d in range(R)]
+    sd = [int(C[s][:d].sum()) for s in range(R) for d in range(R)]
+    rd = [int(C[:s, d].sum()) for s in range(R) for d in range(R)]
+    ref = [np.zeros(int(C[:, d].sum()), np.uint8) for d in range(R)]
+    oracle.alltoallv(send, counts, sd, ref, rd, dt)
+    recv = [torch.zeros(int(C[:, d].sum()), dtype=torch.uint8, device="cuda") for d in range(R)]
+    hc.alltoallv([to_dev(a, dt) for a in send], counts, sd, recv, rd)
+    torch.cuda.synchronize()
+    for r in range(R):
+        assert_bitwise(from_dev(recv[r], dt), ref[r], f"A2Av u8 {path} r={r}")
+
+
+def test_uint8_reductions_refused():
+    x = [torch.zeros(8, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    with pytest.raises(TypeError):
+        hc.allreduce(x)
+    p = (ctypes.c_void_p * 2)(*[t.data_ptr() for t in x])
+    assert hc.lib().hoccl_allreduce(p, p, 8, hc.UINT8, 2, None) == hc.ERR_INVALID_ARG
+    assert hc.lib().hoccl_reduce_scatter(p, p, 4, hc.UINT8, 2, None) == hc.ERR_INVALID_ARG
 
 
 @pytest.mark.parametrize("sched", [0, 1, 2])

@@ -14,8 +14,8 @@ from gpu_util import NAME, TORCH, assert_bitwise, from_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
-NPDT = {hc.INT32: np.int32, hc.FP32: np.float32, hc.BF16: np.uint16}
-ES = {hc.INT32: 4, hc.FP32: 4, hc.BF16: 2}
+NPDT = {hc.INT32: np.int32, hc.FP32: np.float32, hc.BF16: np.uint16, hc.UINT8: np.uint8}
+ES = {hc.INT32: 4, hc.FP32: 4, hc.BF16: 2, hc.UINT8: 1}
 
 
 def draw(i):
@@ -39,6 +39,9 @@ def draw(i):
     # Drawn last so the earlier fields keep their values: the engine
     # proxy's balanced issue (automatic, 64 KiB pieces) or all at once.
     c["cfg"]["proxy_slice_bytes"] = int(g.choice([0, 0, 64 << 10, (1 << 64) - 1]))
+    # A quarter of the copy collectives move single bytes instead.
+    if g.random() < 0.25 and c["op"] in ("allgather", "sendrecv", "alltoall", "alltoallv"):
+        c["dt"] = hc.UINT8
     return c
 
 

@@ -97,7 +97,7 @@ def test_ping_pong_across_processes():
             box.post(0, k, msg)
             if k % 75 == 0:
                 time.sleep(0.002)               # the child's wait sleeps on the futex
-            box.wait(1, k, 10000)
+            box.wait(1, k, 120_000 if k == 1 else 10_000)   # the first reply waits for the child's start
             assert box.read(1) == msg[::-1], k
         assert p.wait(timeout=60) == 0
     finally:

@@ -114,7 +114,7 @@ def test_ring_simulation_matches_oracle(dtype, R):
 @pytest.mark.parametrize("R", [1, 2, 3, 4, 6])
 def test_copy_collectives_match_flow_lists(R):
     for n in [0, 1, 5, 17]:
-        for es, code in [(4, oracle.FP32), (2, oracle.BF16)]:
+        for es, code in [(4, oracle.FP32), (2, oracle.BF16), (1, oracle.UINT8)]:
             x = [W.random_bits(77 + n, r, R * n, es) for r in range(R)]
             # all-to-all
             got = [np.zeros(R * n, dtype=x[0].dtype) for _ in range(R)]
@@ -308,6 +308,35 @@ def test_alltoallv_transposed_restores():
                           [[None] * s for s in rsz], rd)
     for r in range(R):
         assert [int(v) for v in recv[r]] == ref[r]
+
+
+def test_uint8_copies_and_no_uint8_sums():
+    """Bytes move like any element (odd counts and offsets included); the
+    reductions refuse them, as the sum is defined for int32, fp32 and bf16."""
+    R = 3
+    rng = np.random.default_rng(5)
+    C = rng.integers(0, 6, size=(R, R))
+    send = [W.random_bits(88, s, int(C[s].sum()), 1) for s in range(R)]
+    counts = [int(C[s][d]) for s in range(R) for d in range(R)]
+    sd = [int(C[s][:d].sum()) for s in range(R) for d in range(R)]
+    rd = [int(C[:s, d].sum()) for s in range(R) for d in range(R)]
+    rsz = [int(C[:, d].sum()) for d in range(R)]
+    recv = [np.zeros(s, dtype=np.uint8) for s in rsz]
+    oracle.alltoallv(send, counts, sd, recv, rd, oracle.UINT8)
+    ref = brute.alltoallv([list(a) for a in send], counts, sd, [[None] * s for s in rsz], rd)
+    for r in range(R):
+        assert [int(v) for v in recv[r]] == ref[r]
+    x = [W.random_bits(89, r, 7, 1) for r in range(R)]
+    got = [np.full(7, 0xA5, np.uint8) for _ in range(R)]
+    oracle.sendrecv(x, got, [2, -1, 0], 7, oracle.UINT8)
+    ref = brute.sendrecv([list(a) for a in x], [[0xA5] * 7 for _ in range(R)], [2, -1, 0])
+    for r in range(R):
+        assert [int(v) for v in got[r]] == [int(v) for v in ref[r]]
+    assert oracle.dtype_code(np.uint8) == oracle.UINT8
+    with pytest.raises(ValueError):
+        oracle.allreduce_new(x, oracle.UINT8)
+    with pytest.raises(ValueError):
+        oracle.reduce_scatter_new([W.random_bits(90, r, 6, 1) for r in range(R)], oracle.UINT8)
 
 
 def test_sendrecv_pipeline_and_canaries():

@@ -15,7 +15,7 @@ import paper_2609_34334_amd as hc
 import workloads as W
 
 NP = {hc.INT32: np.int32, hc.FP32: np.float32, hc.BF16: np.uint16}
-ES = {hc.INT32: 4, hc.FP32: 4, hc.BF16: 2}
+ES = {hc.INT32: 4, hc.FP32: 4, hc.BF16: 2, hc.UINT8: 1}
 NAME = {hc.INT32: "int32", hc.FP32: "fp32", hc.BF16: "bf16"}
 
 
@@ -140,7 +140,7 @@ def test_reduction_plans_replay_to_oracle(cfg, dt, R):
 
 @pytest.mark.parametrize("R", [1, 2, 3, 8])
 def test_copy_plans_replay_to_oracle(cfg, R):
-    for dt in [hc.FP32, hc.BF16]:
+    for dt in [hc.FP32, hc.BF16, hc.UINT8]:
         for n in [1, 5, 3001]:
             x = [W.random_bits(600 + n, r, n, ES[dt]) for r in range(R)]
             # all-gather

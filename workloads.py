@@ -65,7 +65,7 @@ def random_int32(seed, rank, n, lo=-(2 ** 31), hi=2 ** 31):
 def random_bits(seed, rank, n, itemsize):
     """Arbitrary bit patterns (NaN, Inf and subnormals included) for copies."""
     raw = rng_for(seed, rank).integers(0, 256, n * itemsize, dtype=np.uint8)
-    return raw.view({2: np.uint16, 4: np.uint32}[itemsize]).copy()
+    return raw.view({1: np.uint8, 2: np.uint16, 4: np.uint32}[itemsize]).copy()
 
 
 def random_values(dtype, seed, rank, n):
