@@ -44,7 +44,7 @@ def test_oracle_under_sanitizers(tmp_path):
     cmd = ["gcc", "-std=c11", *SAN, "-fno-fast-math", "-ffp-contract=off",
            os.path.join(HERE, "native", "oracle_bounds.c"), "-o", exe]
     out = _run(cmd, tmp_path, exe)
-    assert "oracle cases run: 672" in out, out
+    assert "oracle cases run: 896" in out, out
 
 
 @pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
