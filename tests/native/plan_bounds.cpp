@@ -127,10 +127,11 @@ void run(const Plan &p, int R, size_t send_bytes, size_t recv_bytes, int in_plac
 
 int main() {
     const int Rs[] = {1, 2, 3, 4, 5, 8, 13, 64};
-    const hoccl_dtype_t dts[] = {HOCCL_INT32, HOCCL_FP32, HOCCL_BF16};
+    const hoccl_dtype_t dts[] = {HOCCL_INT32, HOCCL_FP32, HOCCL_BF16, HOCCL_UINT8};
     for (int R : Rs)
         for (hoccl_dtype_t dt : dts) {
             const size_t es = dtype_size(dt);
+            const bool sums = dt != HOCCL_UINT8;  // bytes: copy collectives only
             const size_t counts[] = {1, 7, (size_t)R * 5 + 3, 1000};
             for (size_t n : counts)
                 for (int ip = 0; ip < 2; ++ip)
@@ -144,11 +145,12 @@ int main() {
                                 o.chunk_bytes = chunk;
                                 for (int direct = 0; direct < 2; ++direct) {
                                     o.allgather_direct = direct != 0;
-                                    run(plan_allreduce(n, dt, R, o), R, n * es, n * es, ip ? 3 : 0);
+                                    if (sums) run(plan_allreduce(n, dt, R, o), R, n * es, n * es, ip ? 3 : 0);
                                     run(plan_allgather(n, dt, R, o), R, n * es, (size_t)R * n * es, ip ? 1 : 0);
                                 }
-                                run(plan_reduce_scatter(n, dt, R, o), R, (size_t)R * n * es, n * es, ip ? 2 : 0);
-                                if (algo == 0)
+                                if (sums)
+                                    run(plan_reduce_scatter(n, dt, R, o), R, (size_t)R * n * es, n * es, ip ? 2 : 0);
+                                if (algo == 0 && sums)
                                     for (int hops : {3, 64}) {  // fused ring hops
                                         PlanOptions f = o;
                                         f.fused_hops = hops;
