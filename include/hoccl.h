@@ -547,7 +547,9 @@ hoccl_status_t hoccl_ipc_close_all(void);
  * be used from several threads, but not to post into one slot at once.
  *
  * hoccl_mailbox_wait polls briefly, then sleeps on the slot (a futex on
- * the shared word); it returns HOCCL_ERR_TIMEOUT after timeout_ms.
+ * the shared word); it returns HOCCL_ERR_TIMEOUT after timeout_ms.  With
+ * timeout_ms 0 it looks once and returns at once (HOCCL_OK or
+ * HOCCL_ERR_TIMEOUT), without setting an error string.
  * hoccl_mailbox_read copies the payload into buf (cap bytes) and stores its
  * length in *len; HOCCL_ERR_INVALID_ARG if it does not fit.  Bad names,
  * slots or sizes are HOCCL_ERR_INVALID_ARG; hoccl_last_error_string() says

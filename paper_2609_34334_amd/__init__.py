@@ -11,6 +11,7 @@ fallback implementation.
 """
 import ctypes
 import os
+import threading
 
 import torch
 
@@ -433,8 +434,8 @@ class Mailbox:
         else:
             _check(_lib.hoccl_mailbox_create(name.encode(), slots, slot_bytes, ctypes.byref(self._h)),
                    "hoccl_mailbox_create")
-        self._buf = ctypes.create_string_buffer(slot_bytes or (1 << 20))
-        self._len = ctypes.c_size_t(0)
+        self._cap = slot_bytes or (1 << 20)
+        self._local = threading.local()     # a read buffer per thread
 
     @staticmethod
     def unlink(name):
@@ -448,10 +449,17 @@ class Mailbox:
         _check(_lib.hoccl_mailbox_wait(self._h, slot, seq & 0xFFFFFFFF, int(timeout_ms)),
                "hoccl_mailbox_wait")
 
+    def ready(self, slot, seq):
+        """Whether the slot has reached `seq` (one look, no waiting)."""
+        return _lib.hoccl_mailbox_wait(self._h, slot, seq & 0xFFFFFFFF, 0) == OK
+
     def read(self, slot):
-        _check(_lib.hoccl_mailbox_read(self._h, slot, self._buf, len(self._buf), ctypes.byref(self._len)),
+        loc = self._local
+        if not hasattr(loc, "buf"):
+            loc.buf, loc.len = ctypes.create_string_buffer(self._cap), ctypes.c_size_t(0)
+        _check(_lib.hoccl_mailbox_read(self._h, slot, loc.buf, self._cap, ctypes.byref(loc.len)),
                "hoccl_mailbox_read")
-        return self._buf.raw[:self._len.value]
+        return loc.buf.raw[:loc.len.value]
 
     def close(self):
         if self._h:

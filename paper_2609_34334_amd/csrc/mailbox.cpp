@@ -178,6 +178,8 @@ hoccl_status_t hoccl_mailbox_wait(hoccl_mailbox_t *box, unsigned slot, unsigned 
                                   unsigned timeout_ms) {
     if (!box || slot >= box->head->slots) return fail(HOCCL_ERR_INVALID_ARG, "mailbox_wait: bad slot");
     SlotHead *s = box->slot(slot);
+    if (timeout_ms == 0)  // a poll: one look, no waiting
+        return seq_reached(__atomic_load_n(&s->seq, __ATOMIC_ACQUIRE), seq) ? HOCCL_OK : HOCCL_ERR_TIMEOUT;
     for (int i = 0; i < kSpins; ++i) {
         if (seq_reached(__atomic_load_n(&s->seq, __ATOMIC_ACQUIRE), seq)) return HOCCL_OK;
         __builtin_ia32_pause();

@@ -22,9 +22,16 @@ paper's intra-node path (Zero-SM Point-to-Point Executor):
   then sleeps on a futex.
 
 Point-to-point: the receiver posts its buffer's handle into the mailbox
-slot of the (sender, receiver) pair; the sender opens it, copies straight
-into it through the library (the engine proxy by default) and posts
-completion, which the receiver waits for.
+slot of the (sender, receiver) pair and returns; the sender hands its
+buffer to the group's send thread and returns.  That thread opens the
+receiver's handle as soon as it is posted, copies straight into it through
+the library (the engine proxy by default) and posts completion, which both
+sides' waits wait for.  Both calls return at once, so batch_isend_irecv,
+and any order of sends, receives and waits across ranks, cannot deadlock.
+The backend's calls into the library (collectives on the calling thread,
+copies on the send thread) take turns under one lock, as the library
+serves one host thread at a time per device; code that calls the library
+directly must not do so while sends are pending.
 
 The c10d store is used once, when the group is created: rank 0 creates the
 mailboxes and publishes their names, every rank opens them, and once all
@@ -69,6 +76,7 @@ import ctypes
 import json
 import os
 import secrets
+import threading
 from datetime import timedelta
 
 import torch
@@ -81,6 +89,9 @@ BACKEND = "hoccl"
 ENV = "HOCCL_BACKEND"
 _VP = ctypes.c_void_p
 _GROUPS = []
+# The library takes calls from one host thread at a time per device; the
+# main thread (collectives) and each group's send thread take turns.
+_LIB_LOCK = threading.RLock()
 COLL_SLOT_BYTES = 64 << 10    # one rank's call description (handles, split sizes)
 P2P_SLOT_BYTES = 2 << 10      # a receive buffer's handle, or a completion status
 
@@ -120,6 +131,66 @@ def _create(store, rank, world_size, timeout):
     g = HocclProcessGroup(store, rank, world_size, timeout)
     _GROUPS.append(g)
     return g
+
+
+class _SendWork(dist._Work):
+    """A send: done once the group's send thread has copied the buffer
+    into the receiver's and posted completion."""
+
+    def __init__(self, t, timeout_s):
+        super().__init__()
+        self._t, self._timeout_s = t, timeout_s
+        self._event, self._status = threading.Event(), None
+        self._fut = torch.futures.Future()
+
+    def _finish(self, status):
+        self._status = status
+        self._event.set()
+        if status == "ok":
+            self._fut.set_result([self._t])
+        else:
+            self._fut.set_exception(RuntimeError(status))
+
+    def wait(self, timeout=None):
+        if not self._event.wait(self._timeout_s):
+            raise RuntimeError("hoccl: send not completed: no matching receive was posted in time")
+        if self._status != "ok":
+            raise RuntimeError(self._status)
+        return True
+
+    def is_completed(self):
+        return self._event.is_set()
+
+    def get_future(self):
+        return self._fut
+
+
+class _RecvWork(dist._Work):
+    """A receive: done once the sender has posted completion."""
+
+    def __init__(self, box, slot, n, t, timeout_ms):
+        super().__init__()
+        self._box, self._slot, self._n, self._t, self._timeout_ms = box, slot, n, t, timeout_ms
+        self._status = None
+        self._fut = torch.futures.Future()
+
+    def wait(self, timeout=None):
+        if self._status is None:
+            self._box.wait(self._slot, self._n, self._timeout_ms)
+            self._status = self._box.read(self._slot).decode(errors="replace")
+            if self._status == "ok":
+                self._fut.set_result([self._t])
+            else:
+                self._fut.set_exception(RuntimeError(self._status))
+        if self._status != "ok":
+            raise RuntimeError(self._status)
+        return True
+
+    def is_completed(self):
+        return self._status is not None or self._box.ready(self._slot, self._n)
+
+    def get_future(self):
+        return self._fut
 
 
 class _Done(dist._Work):
@@ -214,6 +285,7 @@ class HocclProcessGroup(dist.ProcessGroup):
         self._name, self._desc = "", ""
         t = timeout.total_seconds() if isinstance(timeout, timedelta) else timeout
         self._timeout_ms = int(1000 * t) if t else 30 * 60 * 1000
+        self._sends, self._cv, self._sender = [], threading.Condition(), None
         self._open_mailboxes()
 
     def _open_mailboxes(self):
@@ -288,8 +360,9 @@ class HocclProcessGroup(dist.ProcessGroup):
                     descs.append(json.loads(box.read(r)))
                 if len({d["dev"] for d in descs if "dev" in d}) > 1:
                     raise ValueError("hoccl: all ranks must use the same GPU")
-                run(descs)
-                torch.cuda.current_stream().synchronize()
+                with _LIB_LOCK:
+                    run(descs)
+                    torch.cuda.current_stream().synchronize()
                 status = "ok"
             except Exception as e:  # every rank must learn of it, not only rank 0
                 status = f"error: {e}"
@@ -559,42 +632,83 @@ class HocclProcessGroup(dist.ProcessGroup):
         base = 2 * (src * self._n + dst)
         return base, base + 1, n
 
+    # Point to point is asynchronous on both sides, so that no order of
+    # sends, receives and waits across ranks can deadlock: a receive posts
+    # its buffer and returns; a send hands its buffer to the group's send
+    # thread and returns; that thread copies each pending send as soon as
+    # its receiver has posted, and posts completion, which the receive's
+    # wait (and the send's) waits for.
+
     def send(self, tensors, dst, tag=0):
         (t,) = tensors
-        nb = _nbytes(t)
+        _nbytes(t)
         want, done, n = self._p2p_slot(self._r, dst)
-        torch.cuda.current_stream().synchronize()
-        self._pp.wait(want, n, self._timeout_ms)
-        d = json.loads(self._pp.read(want))                    # the receiver's buffer
-        status = "ok"
-        try:
-            if d["bytes"] != nb or d["type"] != str(t.dtype):
-                raise ValueError(f"hoccl: send of {nb} bytes of {t.dtype} to a receive of "
-                                 f"{d['bytes']} bytes of {d['type']}")
-            dt, u = _unit([nb])
-            dst_ptr = _open(d["t"])
-            _check(lib().hoccl_sendrecv(_ptrs([t.data_ptr(), None]), _ptrs([None, dst_ptr]),
-                                        (ctypes.c_int * 2)(1, -1), nb // u, dt, 2, _stream()),
-                   "hoccl_sendrecv")
-            torch.cuda.current_stream().synchronize()
-        except Exception as e:
-            status = f"error: {e}"
-        self._pp.post(done, n, status.encode()[:P2P_SLOT_BYTES])
-        if status != "ok":
-            raise RuntimeError(status)
-        return _Done([t])
+        torch.cuda.current_stream().synchronize()          # the buffer is complete
+        work = _SendWork(t, self._timeout_ms / 1000)
+        with self._cv:
+            if self._sender is None:
+                self._sender = threading.Thread(target=self._send_loop, args=(t.device,),
+                                                name="hoccl-send", daemon=True)
+                self._sender.start()
+            self._sends.append((want, done, n, t, work))
+            self._cv.notify()
+        return work
 
     def recv(self, tensors, src, tag=0):
         (t,) = tensors
         nb = _nbytes(t)
         want, done, n = self._p2p_slot(src, self._r)
-        torch.cuda.current_stream().synchronize()
+        torch.cuda.current_stream().synchronize()          # the buffer is free
         self._pp.post(want, n, json.dumps({"t": _export(t), "bytes": nb, "type": str(t.dtype)}).encode())
-        self._pp.wait(done, n, self._timeout_ms)
-        status = self._pp.read(done).decode(errors="replace")
-        if status != "ok":
-            raise RuntimeError(status)
-        return _Done([t])
+        return _RecvWork(self._pp, done, n, t, self._timeout_ms)
+
+    def _send_loop(self, device):
+        """Copies every pending send whose receiver has posted, in any order
+        across receivers, each on this thread's own stream."""
+        torch.cuda.set_device(device)
+        stream = torch.cuda.Stream(device)
+        while True:
+            with self._cv:
+                while not self._sends:
+                    if self._closed:
+                        return
+                    self._cv.wait()
+                pending = list(self._sends)
+            moved = False
+            for item in pending:
+                want, done, n, t, work = item
+                if not self._pp.ready(want, n):
+                    continue
+                status = self._copy_out(t, want, stream)
+                self._pp.post(done, n, status.encode()[:P2P_SLOT_BYTES])
+                with self._cv:
+                    self._sends.remove(item)
+                work._finish(status)
+                moved = True
+            if not moved:                       # sleep until the oldest receiver posts (or 1 ms)
+                try:
+                    self._pp.wait(pending[0][0], pending[0][2], 1)
+                except Exception:
+                    pass
+
+    def _copy_out(self, t, want, stream):
+        nb = _nbytes(t)
+        try:
+            d = json.loads(self._pp.read(want))            # the receiver's buffer
+            if d["bytes"] != nb or d["type"] != str(t.dtype):
+                raise ValueError(f"hoccl: send of {nb} bytes of {t.dtype} to a receive of "
+                                 f"{d['bytes']} bytes of {d['type']}")
+            if nb:
+                dt, u = _unit([nb])
+                with _LIB_LOCK, torch.cuda.stream(stream):
+                    dst_ptr = _open(d["t"])
+                    _check(lib().hoccl_sendrecv(_ptrs([t.data_ptr(), None]), _ptrs([None, dst_ptr]),
+                                                (ctypes.c_int * 2)(1, -1), nb // u, dt, 2, _stream()),
+                           "hoccl_sendrecv")
+                    stream.synchronize()
+            return "ok"
+        except Exception as e:
+            return f"error: {e}"
 
     # ---- teardown ----------------------------------------------------------------------
 
@@ -604,12 +718,18 @@ class HocclProcessGroup(dist.ProcessGroup):
         have, before any may free its memory."""
         if self._closed:
             return
+        for *_, work in list(self._sends):              # sends still waiting for their receivers
+            work.wait()
         self.barrier()
         ipc_close_all()
         self.barrier()
+        with self._cv:
+            self._closed = True
+            self._cv.notify()
+        if self._sender is not None:
+            self._sender.join()
         self._coll.close()
         self._pp.close()
-        self._closed = True
         if self in _GROUPS:
             _GROUPS.remove(self)
 

@@ -4,7 +4,9 @@ torchrun, all on GPU 0, with HOCCL_BACKEND=1).  Every rank generates every
 rank's seeded inputs, so it can compute the oracle's result itself and
 compare its own output with it bit for bit: all_reduce, reduce_scatter_tensor,
 reduce_scatter (list), all_gather_into_tensor, all_gather (list),
-all_to_all_single with uneven splits, send/recv around the ring, broadcast
+all_to_all_single with uneven splits, send/recv around the ring (blocking,
+and asynchronous in orders that deadlock with synchronous sends, and
+batch_isend_irecv as a pipeline stage uses it), broadcast
 from every root, gather, scatter, reduce, all_to_all (lists), the object
 collectives, barrier, and torch's functional collectives (all_reduce,
 reduce_scatter_tensor, all_gather_tensor, all_to_all_single, broadcast);
@@ -100,6 +102,43 @@ def main():
             dist.recv(got, (rank - 1) % R)
             dist.send(src, (rank + 1) % R)
         assert_bitwise(from_dev(got, hc.BF16), prev, f"recv round {k}")
+    # asynchronous point to point: orders that deadlock with synchronous sends
+    for k in range(2):
+        mine = byte_tensor(1100 + k, rank, 50_001, torch.bfloat16)
+        got = torch.empty_like(mine)
+        rq = dist.irecv(got, (rank - 1) % R)          # every rank receives first ...
+        sq = dist.isend(mine, (rank + 1) % R)         # ... then sends, and waits for the send first
+        sq.wait()
+        rq.wait()
+        assert_same_bytes(got, byte_tensor(1100 + k, (rank - 1) % R, 50_001, torch.bfloat16),
+                          f"ring, receives first, round {k}")
+    # a pipeline stage: gradient to the previous stage, activation from it,
+    # activation to the next, gradient from it (the first and last stages
+    # have one neighbour)
+    nxt, prv = rank + 1, rank - 1
+    a = byte_tensor(1110, rank, 4099, torch.float32)
+    b = byte_tensor(1111, rank, 777, torch.float32)
+    fa, fb = torch.empty_like(a), torch.empty_like(b)
+    ops = []
+    if prv >= 0:
+        ops += [dist.P2POp(dist.isend, b, prv), dist.P2POp(dist.irecv, fa, prv)]
+    if nxt < R:
+        ops += [dist.P2POp(dist.isend, a, nxt), dist.P2POp(dist.irecv, fb, nxt)]
+    for req in dist.batch_isend_irecv(ops):
+        req.wait()
+    if prv >= 0:
+        assert_same_bytes(fa, byte_tensor(1110, prv, 4099, torch.float32), "batch_isend_irecv forward")
+    if nxt < R:
+        assert_same_bytes(fb, byte_tensor(1111, nxt, 777, torch.float32), "batch_isend_irecv backward")
+    if R >= 2 and rank < 2:                           # two stages exchanging, both sending first
+        peer = 1 - rank
+        mine = byte_tensor(1120, rank, 12_345, torch.int32)
+        got = torch.empty_like(mine)
+        sq = dist.isend(mine, peer)
+        rq = dist.irecv(got, peer)
+        sq.wait()
+        rq.wait()
+        assert_same_bytes(got, byte_tensor(1120, peer, 12_345, torch.int32), "exchange, both send first")
     # broadcast from every root; dtypes beyond the library's move as bytes
     for root in range(R):
         for k, (dtype, n) in enumerate(((torch.float32, 4099), (torch.bfloat16, 3 * 65536 + 7),
