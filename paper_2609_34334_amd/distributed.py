@@ -93,7 +93,8 @@ _GROUPS = []
 # main thread (collectives) and each group's send thread take turns.
 _LIB_LOCK = threading.RLock()
 COLL_SLOT_BYTES = 64 << 10    # one rank's call description (handles, split sizes)
-P2P_SLOT_BYTES = 2 << 10      # a receive buffer's handle, or a completion status
+P2P_SLOT_BYTES = 512          # a receive buffer's handle, or a completion status
+P2P_DEPTH = 4                 # receives a rank may have outstanding per sender
 
 
 def selected_backend(requested):
@@ -286,6 +287,7 @@ class HocclProcessGroup(dist.ProcessGroup):
         t = timeout.total_seconds() if isinstance(timeout, timedelta) else timeout
         self._timeout_ms = int(1000 * t) if t else 30 * 60 * 1000
         self._sends, self._cv, self._sender = [], threading.Condition(), None
+        self._recvs = {}                  # (src, dst) -> {message number: its receive}
         self._open_mailboxes()
 
     def _open_mailboxes(self):
@@ -296,7 +298,7 @@ class HocclProcessGroup(dist.ProcessGroup):
             base = f"/hoccl-{os.getpid()}-{secrets.token_hex(6)}"
             try:
                 self._coll = Mailbox(base + "-c", self._n + 1, COLL_SLOT_BYTES)
-                self._pp = Mailbox(base + "-p", 2 * self._n * self._n, P2P_SLOT_BYTES)
+                self._pp = Mailbox(base + "-p", 2 * P2P_DEPTH * self._n * self._n, P2P_SLOT_BYTES)
             except Exception as e:             # the other ranks wait for the name
                 self._store.set("mailbox", f"error: {e}")
                 raise
@@ -626,10 +628,12 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     def _p2p_slot(self, src, dst):
         """(slot of the receiver's buffer, slot of the completion, message
-        number) of the next message from src to dst."""
+        number) of the next message from src to dst.  Each ordered pair has
+        P2P_DEPTH pairs of slots, used in turn, so that a receiver can post
+        that many receives from one sender before the first completes."""
         n = self._p2p.get((src, dst), 0) + 1
         self._p2p[(src, dst)] = n
-        base = 2 * (src * self._n + dst)
+        base = 2 * ((src * self._n + dst) * P2P_DEPTH + n % P2P_DEPTH)
         return base, base + 1, n
 
     # Point to point is asynchronous on both sides, so that no order of
@@ -646,6 +650,18 @@ class HocclProcessGroup(dist.ProcessGroup):
         torch.cuda.current_stream().synchronize()          # the buffer is complete
         work = _SendWork(t, self._timeout_ms / 1000)
         with self._cv:
+            if not self._sends and self._pp.ready(want, n):
+                # The receiver is there and no earlier send waits: copy now,
+                # on the caller's stream.
+                inline = True
+            else:
+                inline = False
+        if inline:
+            status = self._copy_out(t, want, torch.cuda.current_stream())
+            self._pp.post(done, n, status.encode()[:P2P_SLOT_BYTES])
+            work._finish(status)
+            return work
+        with self._cv:
             if self._sender is None:
                 self._sender = threading.Thread(target=self._send_loop, args=(t.device,),
                                                 name="hoccl-send", daemon=True)
@@ -658,9 +674,15 @@ class HocclProcessGroup(dist.ProcessGroup):
         (t,) = tensors
         nb = _nbytes(t)
         want, done, n = self._p2p_slot(src, self._r)
+        mine = self._recvs.setdefault((src, self._r), {})
+        older = mine.pop(n - P2P_DEPTH, None)
+        if older is not None:
+            older.wait()                 # it used the slots this receive reuses
         torch.cuda.current_stream().synchronize()          # the buffer is free
         self._pp.post(want, n, json.dumps({"t": _export(t), "bytes": nb, "type": str(t.dtype)}).encode())
-        return _RecvWork(self._pp, done, n, t, self._timeout_ms)
+        work = _RecvWork(self._pp, done, n, t, self._timeout_ms)
+        mine[n] = work
+        return work
 
     def _send_loop(self, device):
         """Copies every pending send whose receiver has posted, in any order

@@ -139,6 +139,20 @@ def main():
         sq.wait()
         rq.wait()
         assert_same_bytes(got, byte_tensor(1120, peer, 12_345, torch.int32), "exchange, both send first")
+    # more receives outstanding from one sender than a pair has slots, of
+    # different sizes, waited for newest first
+    if rank < 2:
+        sizes = [3, 70_000, 1, 4099, 65_536, 17]
+        if rank == 1:
+            reqs = [dist.irecv(torch.empty(m, dtype=torch.bfloat16, device="cuda"), 0) for m in sizes]
+            for k in reversed(range(len(sizes))):
+                reqs[k].wait()
+                got = reqs[k].get_future().value()[0]
+                assert_same_bytes(got, byte_tensor(1130 + k, 0, sizes[k], torch.bfloat16), f"queued receive {k}")
+        else:
+            sends = [dist.isend(byte_tensor(1130 + k, 0, m, torch.bfloat16), 1) for k, m in enumerate(sizes)]
+            for q in sends:
+                q.wait()
     # broadcast from every root; dtypes beyond the library's move as bytes
     for root in range(R):
         for k, (dtype, n) in enumerate(((torch.float32, 4099), (torch.bfloat16, 3 * 65536 + 7),
