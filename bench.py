@@ -631,14 +631,17 @@ def bench_allgather(hc, W, reps, gemm):
     hc.set_config(allgather_direct=1)
     # Roofline of the engine path: HBM bytes (each copied byte read once and
     # written once) against the 8 TB/s peak, and its copy rate against what
-    # the 16 engines move on one large striped message (512 MiB, each engine
-    # copying one 32 MiB piece), this path's own ceiling.
+    # the 16 engines move when each copies one 256 MiB message of its own
+    # (16 independent sends, 4 GiB in all, so the operation's fixed costs
+    # weigh under 1%), this path's own ceiling.
     with hc.config(copy_path="engines", sdma_engines=16):
-        src = torch.empty(1 << 28, dtype=torch.bfloat16, device="cuda")
-        dst = torch.empty_like(src)
-        med, _ = event_time(lambda: hc.sendrecv([src, src], [dst, dst], [1, -1]), 5)
+        E, m = 16, 1 << 27
+        src = [torch.empty(m, dtype=torch.bfloat16, device="cuda") for _ in range(E)]
+        dst = [torch.empty_like(t) for t in src]
+        ring = [(r + 1) % E for r in range(E)]
+        med, _ = event_time(lambda: hc.sendrecv(src, dst, ring), 5)
         del src, dst
-    ceiling = (1 << 29) / med / 1e9
+    ceiling = E * m * 2 / med / 1e9
     roof = {}
     for name in ("engines", "engines16"):
         r = res[name]
