@@ -50,8 +50,11 @@
  *   earlier call that made no progress for proxy_timeout_ms are reported
  *   once, as HOCCL_ERR_TIMEOUT, by the next SDMA call (which then
  *   enqueues nothing).
- * Threads.  One host thread at a time may call into the library per device.
- *   Collectives issued on different streams that overlap in time are
+ * Threads.  Calls from several host threads on one device take turns: each
+ *   holds a per-device lock while it plans and enqueues (not while the
+ *   work runs), and calls run in the order they take it.  Statistics and
+ *   error strings are per thread.  hoccl_finalize must not overlap other
+ *   calls.  Collectives issued on different streams that overlap in time are
  *   ordered by the library where they share its workspace or its internal
  *   copy / handshake streams, in the order the calls were issued: a call
  *   must not wait, through the caller's own stream dependencies, for a call

@@ -48,6 +48,9 @@ struct TimingPair {
 };
 
 struct DeviceState {
+    // Held by every call while it plans and enqueues on this device, so
+    // calls from several host threads take turns.
+    std::recursive_mutex call_mu;
     int device = -1;
     int num_cus = 0;
     std::vector<hipStream_t> copy_streams;
@@ -780,6 +783,7 @@ hoccl_status_t execute(Build build, bool in_place, const Buffers &B0, hipStream_
     DeviceState *stp = nullptr;
     TRY(get_state(&stp, capturing || noalloc));
     DeviceState &st = *stp;
+    std::lock_guard<std::recursive_mutex> call_lock(st.call_mu);
     hoccl_config_t cfg = config();
     std::memset(&t_stats, 0, sizeof t_stats);
     // Timing events of a captured call would be recorded only on replay; a
@@ -1081,6 +1085,7 @@ hoccl_status_t hoccl_get_kernel_times(float *ms, int cap, int *n) {
     }
     *n = 0;
     if (!st) return HOCCL_OK;
+    std::lock_guard<std::recursive_mutex> call_lock(st->call_mu);
     *n = (int)st->timing_used;
     if (cap <= 0) return HOCCL_OK;  // query the count only; keep the record
     for (size_t i = 0; i < st->timing_used; ++i) {
@@ -1156,6 +1161,7 @@ hoccl_status_t hoccl_ring_hop(const void *partial, const void *local, void *out,
     DeviceState *stp = nullptr;
     TRY(get_state(&stp, capturing));
     DeviceState &st = *stp;
+    std::lock_guard<std::recursive_mutex> call_lock(st.call_mu);
     hoccl_config_t cfg = config();
     if (capturing) cfg.kernel_timing = 0;
     std::memset(&t_stats, 0, sizeof t_stats);
@@ -1417,6 +1423,7 @@ hoccl_status_t hoccl_debug_stream_ceiling(int mode, const void *a, const void *b
     }
     DeviceState *st = nullptr;
     TRY(get_state(&st));
+    std::lock_guard<std::recursive_mutex> call_lock(st->call_mu);
     hoccl_config_t cfg = config();
     const int threads = cfg.threads_per_workgroup ? cfg.threads_per_workgroup : 256;
     const int wg = workgroups_for(*st, cfg, (bytes / 16 + 3) / 4, threads);

@@ -28,10 +28,8 @@ receiver's handle as soon as it is posted, copies straight into it through
 the library (the engine proxy by default) and posts completion, which both
 sides' waits wait for.  Both calls return at once, so batch_isend_irecv,
 and any order of sends, receives and waits across ranks, cannot deadlock.
-The backend's calls into the library (collectives on the calling thread,
-copies on the send thread) take turns under one lock, as the library
-serves one host thread at a time per device; code that calls the library
-directly must not do so while sends are pending.
+The library serialises calls from several host threads on one device, so
+the calling thread's collectives and the send thread's copies take turns.
 
 The c10d store is used once, when the group is created: rank 0 creates the
 mailboxes and publishes their names, every rank opens them, and once all
@@ -89,9 +87,6 @@ BACKEND = "hoccl"
 ENV = "HOCCL_BACKEND"
 _VP = ctypes.c_void_p
 _GROUPS = []
-# The library takes calls from one host thread at a time per device; the
-# main thread (collectives) and each group's send thread take turns.
-_LIB_LOCK = threading.RLock()
 COLL_SLOT_BYTES = 64 << 10    # one rank's call description (handles, split sizes)
 P2P_SLOT_BYTES = 512          # a receive buffer's handle, or a completion status
 P2P_DEPTH = 4                 # receives a rank may have outstanding per sender
@@ -362,9 +357,8 @@ class HocclProcessGroup(dist.ProcessGroup):
                     descs.append(json.loads(box.read(r)))
                 if len({d["dev"] for d in descs if "dev" in d}) > 1:
                     raise ValueError("hoccl: all ranks must use the same GPU")
-                with _LIB_LOCK:
-                    run(descs)
-                    torch.cuda.current_stream().synchronize()
+                run(descs)
+                torch.cuda.current_stream().synchronize()
                 status = "ok"
             except Exception as e:  # every rank must learn of it, not only rank 0
                 status = f"error: {e}"
@@ -722,7 +716,7 @@ class HocclProcessGroup(dist.ProcessGroup):
                                  f"{d['bytes']} bytes of {d['type']}")
             if nb:
                 dt, u = _unit([nb])
-                with _LIB_LOCK, torch.cuda.stream(stream):
+                with torch.cuda.stream(stream):
                     dst_ptr = _open(d["t"])
                     _check(lib().hoccl_sendrecv(_ptrs([t.data_ptr(), None]), _ptrs([None, dst_ptr]),
                                                 (ctypes.c_int * 2)(1, -1), nb // u, dt, 2, _stream()),

@@ -4,7 +4,8 @@ round into buffers of its own) and the EP all-to-all(v), on the default copy
 path (AUTO: the SDMA engine proxy with its host-function handshake), start
 together with a loop of bf16 8192^3 GEMMs on another hardware queue behind
 one host gate, as the benchmark's interference runs do.  Every output
-element is then compared with the oracle."""
+element is then compared with the oracle.  Also: calls from several host
+threads at once, which the library serialises per device."""
 import numpy as np
 import pytest
 import torch
@@ -114,3 +115,54 @@ def test_alltoallv_ep_beside_gemm():
     oracle.alltoallv(send_np, counts, sd, ref, rd, hc.BF16)
     for r in range(R):
         assert_bitwise(from_dev(recv[r], hc.BF16), ref[r], f"EP all-to-all(v) beside the GEMM, rank {r}")
+
+
+@pytest.mark.parametrize("path", ["engines", "kernel"])
+def test_calls_from_several_host_threads(path):
+    """Four host threads call the library at once, each on its own stream
+    with its own buffers: reduce-scatters, all-gathers and send/recvs in a
+    loop.  The library serialises the calls per device; every result must
+    match the oracle."""
+    import threading
+    R, n, loops = 4, 20_011, 12
+    x = [W.random_values("bf16", 1200, r, R * n) for r in range(R)]
+    rs_ref = oracle.reduce_scatter_new(x, hc.BF16)
+    g = [W.random_bits(1201, r, n, 2) for r in range(R)]
+    ag_ref = oracle.allgather_new(g, hc.BF16)
+    errors, results = [], {}
+
+    def worker(k):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                send = [to_dev(a, hc.BF16) for a in x]
+                shards = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+                gs = [to_dev(a, hc.BF16) for a in g]
+                full = [torch.empty(R * n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+                moved = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+                for _ in range(loops):
+                    hc.reduce_scatter(send, shards, stream=s)
+                    hc.allgather(gs, full, stream=s)
+                    hc.sendrecv(gs, moved, [(r + k + 1) % R for r in range(R)], stream=s)
+                s.synchronize()
+                results[k] = ([from_dev(t, hc.BF16) for t in shards], [from_dev(t, hc.BF16) for t in full],
+                              [from_dev(t, hc.BF16) for t in moved])
+        except Exception as e:          # reported by the main thread
+            errors.append(repr(e))
+
+    with hc.config(copy_path=path):
+        hc.reduce_scatter([to_dev(a, hc.BF16) for a in x])     # initialise on this thread first
+        torch.cuda.synchronize()
+        threads = [threading.Thread(target=worker, args=(k,)) for k in range(4)]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join(timeout=120)
+        assert not any(t.is_alive() for t in threads), "a thread did not finish"
+    assert not errors, errors
+    for k in range(4):
+        shards, full, moved = results[k]
+        for r in range(R):
+            assert_bitwise(shards[r], rs_ref[r], f"thread {k} reduce-scatter rank {r}")
+            assert_bitwise(full[r], ag_ref[r], f"thread {k} all-gather rank {r}")
+            assert_bitwise(moved[(r + k + 1) % R], g[r], f"thread {k} send/recv from rank {r}")
