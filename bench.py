@@ -1696,16 +1696,16 @@ def backend_rank():
     b = torch.ones(1 << 20, device="cuda")
     out["broadcast_fp32_4MiB_us"] = per_call(lambda: dist.broadcast(b, 0))
     out["barrier_us"] = per_call(lambda: dist.barrier())
-    m = torch.ones(1024, device="cuda")
-
-    def ping():
-        if rank == 0:
-            dist.send(m, 1)
-            dist.recv(m, 1)
-        elif rank == 1:
-            dist.recv(m, 0)
-            dist.send(m, 0)
-    out["send_recv_4KiB_round_trip_us"] = per_call(ping)
+    for name, m in (("4KiB", torch.ones(1024, device="cuda")),
+                    ("16MiB", torch.ones(1 << 23, dtype=torch.bfloat16, device="cuda"))):
+        def ping():
+            if rank == 0:
+                dist.send(m, 1)
+                dist.recv(m, 1)
+            elif rank == 1:
+                dist.recv(m, 0)
+                dist.send(m, 0)
+        out[f"send_recv_{name}_round_trip_us"] = per_call(ping)
     dist.barrier()
     hdist.destroy_process_group()
     if rank == 0:
