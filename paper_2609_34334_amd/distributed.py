@@ -75,6 +75,7 @@ import json
 import os
 import secrets
 import threading
+import time
 from datetime import timedelta
 
 import torch
@@ -90,6 +91,7 @@ _GROUPS = []
 COLL_SLOT_BYTES = 64 << 10    # one rank's call description (handles, split sizes)
 P2P_SLOT_BYTES = 512          # a receive buffer's handle, or a completion status
 P2P_DEPTH = 4                 # receives a rank may have outstanding per sender
+SEND_SPIN_S = 50e-6           # how long a send waits for its receiver before handing off
 
 
 def selected_backend(requested):
@@ -644,12 +646,19 @@ class HocclProcessGroup(dist.ProcessGroup):
         torch.cuda.current_stream().synchronize()          # the buffer is complete
         work = _SendWork(t, self._timeout_ms / 1000)
         with self._cv:
-            if not self._sends and self._pp.ready(want, n):
-                # The receiver is there and no earlier send waits: copy now,
-                # on the caller's stream.
-                inline = True
-            else:
-                inline = False
+            idle = not self._sends
+        inline = False
+        if idle:
+            # No earlier send waits: if the receiver is there, or arrives
+            # within SEND_SPIN_S, copy now on the caller's stream (a hand-off
+            # to the send thread costs more than that).
+            t0 = time.perf_counter()
+            while True:
+                if self._pp.ready(want, n):
+                    inline = True
+                    break
+                if time.perf_counter() - t0 > SEND_SPIN_S:
+                    break
         if inline:
             status = self._copy_out(t, want, torch.cuda.current_stream())
             self._pp.post(done, n, status.encode()[:P2P_SLOT_BYTES])
