@@ -289,8 +289,9 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     def _open_mailboxes(self):
         """Rank 0 creates the collective mailbox (a slot per rank plus the
-        status slot) and the point-to-point one (two slots per ordered pair);
-        every rank opens them; rank 0 removes the names once all have."""
+        status slot) and the point-to-point one (P2P_DEPTH pairs of slots
+        per ordered pair of ranks); every rank opens them; rank 0 removes
+        the names once all have."""
         if self._r == 0:
             base = f"/hoccl-{os.getpid()}-{secrets.token_hex(6)}"
             try:
