@@ -1,6 +1,6 @@
 """Randomised GPU parity: 160 seeded cases (HOCCL_RANDOM_CASES=N for more),
-each drawing a collective, dtype,
-rank count (up to 64), ragged count, misaligned buffer offset, copy path,
+each drawing a collective, dtype (bytes for a quarter of the copies), rank
+count (up to 64), ragged count, misaligned buffer offset, copy path,
 reduction algorithm, launch shape, group options and the engine proxy's
 issue mode, run through the C ABI and compared bit for bit with the
 oracle."""
