@@ -1,7 +1,8 @@
 """The "hoccl" torch.distributed backend across processes sharing the one
 GPU: ranks launched by torchrun (HOCCL_BACKEND=1 turns the requested
 backend into hoccl).  Every collective's output compared with the oracle by
-each rank (tests/backend_worker.py); DistributedDataParallel training
+each rank (tests/backend_worker.py), a seeded random sequence of calls
+(tests/backend_random_worker.py); DistributedDataParallel training
 (tests/ddp_worker.py) and FSDP2 training (tests/fsdp_worker.py) over the
 backend."""
 import os
@@ -55,3 +56,8 @@ def test_ddp_over_the_backend(ranks):
 @pytest.mark.parametrize("ranks", [2, 4])
 def test_fsdp_over_the_backend(ranks, dtype):
     run_ranks("fsdp_worker.py", ranks, "fsdp ok", dtype)
+
+
+@pytest.mark.parametrize("ranks", [2, 4])
+def test_random_calls_over_the_backend(ranks):
+    run_ranks("backend_random_worker.py", ranks, "random ok", "120")
