@@ -71,6 +71,7 @@ Use::
     hdist.destroy_process_group()
 """
 import ctypes
+import functools
 import json
 import os
 import secrets
@@ -268,6 +269,23 @@ def _average(opts, t):
     raise ValueError(f"hoccl: only sums, and averages of float32 or bfloat16 ({op} on {t.dtype})")
 
 
+def _together(method):
+    """A collective whose checks fail on this rank before it joins the call
+    still joins it, with the error as its description, so that every rank
+    fails at once instead of waiting for this one."""
+    @functools.wraps(method)
+    def wrapper(self, *args, **kwargs):
+        joined = self._seq
+        try:
+            return method(self, *args, **kwargs)
+        except Exception as e:
+            if self._seq == joined:
+                msg = f"rank {self._r}: {e}"
+                self._call(lambda: {"error": msg}, lambda descs: None)
+            raise
+    return wrapper
+
+
 class HocclProcessGroup(dist.ProcessGroup):
     """The process group of the "hoccl" backend (see the module docstring)."""
 
@@ -329,6 +347,9 @@ class HocclProcessGroup(dist.ProcessGroup):
     def getGroupDesc(self):
         return self._desc
 
+    def setGroupDesc(self, desc):
+        self._desc = desc
+
     @property
     def _device_types(self):
         """The devices the group serves, as torch reads them to place the
@@ -336,28 +357,34 @@ class HocclProcessGroup(dist.ProcessGroup):
         torch would list its C++ backends, of which this group has none."""
         return [torch.device("cuda")]
 
-    def setGroupDesc(self, desc):
-        self._desc = desc
-
     # ---- the collective protocol ----------------------------------------------
 
     def _call(self, desc, run, result=None):
-        """Post this rank's `desc`; rank 0 gathers every rank's and runs
-        `run(descs)`; every rank waits for completion.  The work's future
-        holds `result` (the output tensors).  A rank posts call k + 1 only
-        after it has seen call k's status, so rank 0 has read every slot
-        before it is written again."""
+        """Post this rank's description (`desc()`: its buffers' handles and
+        sizes); rank 0 gathers every rank's and runs `run(descs)`; every
+        rank waits for completion.  The work's future holds `result` (the
+        output tensors).  A rank that cannot describe its buffers posts the
+        error instead, so every rank fails at once rather than wait.  A rank
+        posts call k + 1 only after it has seen call k's status, so rank 0
+        has read every slot before it is written again."""
         self._seq += 1
         k, R, box = self._seq, self._n, self._coll
         torch.cuda.current_stream().synchronize()
+        try:
+            mine = desc()
+        except Exception as e:
+            mine = {"error": f"rank {self._r}: {e}"}
         if self._r != 0:
-            box.post(self._r, k, json.dumps(desc).encode())
+            box.post(self._r, k, json.dumps(mine).encode()[:COLL_SLOT_BYTES])
         else:
             try:
-                descs = [desc]
+                descs = [mine]
                 for r in range(1, R):
                     box.wait(r, k, self._timeout_ms)
                     descs.append(json.loads(box.read(r)))
+                for d in descs:
+                    if "error" in d:
+                        raise ValueError(d["error"])
                 if len({d["dev"] for d in descs if "dev" in d}) > 1:
                     raise ValueError("hoccl: all ranks must use the same GPU")
                 run(descs)
@@ -379,11 +406,12 @@ class HocclProcessGroup(dist.ProcessGroup):
 
     # ---- collectives ---------------------------------------------------------------
 
+    @_together
     def allreduce(self, tensors, opts=None):
         (t,) = tensors
         avg = _average(opts, t)
         dt = _dtype(t)
-        desc = {"t": _export(t), "numel": t.numel(), "dt": dt, "dev": t.device.index}
+        desc = lambda: {"t": _export(t), "numel": t.numel(), "dt": dt, "dev": t.device.index}
 
         def run(descs):
             if any(d["numel"] != t.numel() or d["dt"] != dt for d in descs):
@@ -400,6 +428,7 @@ class HocclProcessGroup(dist.ProcessGroup):
             self.allreduce([t], opts)
         return _Done(list(tensors))
 
+    @_together
     def broadcast(self, tensors, opts=None):
         """The root's tensor into every rank's: an all-to-all(v) whose only
         nonzero row is the root's, every copy reading the root's whole
@@ -409,7 +438,7 @@ class HocclProcessGroup(dist.ProcessGroup):
         if not 0 <= root < self._n:
             raise ValueError(f"hoccl: broadcast root {root} outside 0..{self._n - 1}")
         nb = _nbytes(t)
-        desc = {"t": _export(t), "bytes": nb, "type": str(t.dtype), "dev": t.device.index}
+        desc = lambda: {"t": _export(t), "bytes": nb, "type": str(t.dtype), "dev": t.device.index}
 
         def run(descs):
             R = self._n
@@ -423,12 +452,13 @@ class HocclProcessGroup(dist.ProcessGroup):
             _check(lib().hoccl_alltoallv(p, counts, zero, p, zero, dt, R, _stream()), "hoccl_alltoallv")
         return self._call(desc, run, [t])
 
+    @_together
     def _reduce_scatter_base(self, output, input, opts=None):
         avg = _average(opts, input)
         dt = _dtype(input)
         if _dtype(output) != dt or input.numel() != self._n * output.numel():
             raise ValueError("hoccl: reduce_scatter needs an input of world_size times the output")
-        desc = {"in": _export(input), "out": _export(output), "numel": output.numel(), "dt": dt,
+        desc = lambda: {"in": _export(input), "out": _export(output), "numel": output.numel(), "dt": dt,
                 "dev": input.device.index}
 
         def run(descs):
@@ -456,11 +486,12 @@ class HocclProcessGroup(dist.ProcessGroup):
         flat = torch.cat([x.reshape(-1) for x in ins])
         return self._reduce_scatter_base(out, flat, opts)
 
+    @_together
     def _allgather_base(self, output, input, opts=None):
         nb = _nbytes(input)
         if output.dtype != input.dtype or _nbytes(output) != self._n * nb:
             raise ValueError("hoccl: all_gather needs an output of world_size times the input")
-        desc = {"in": _export(input), "out": _export(output), "bytes": nb, "type": str(input.dtype),
+        desc = lambda: {"in": _export(input), "out": _export(output), "bytes": nb, "type": str(input.dtype),
                 "dev": input.device.index}
 
         def run(descs):
@@ -488,6 +519,7 @@ class HocclProcessGroup(dist.ProcessGroup):
             o.copy_(flat[r * inp.numel():(r + 1) * inp.numel()].view_as(o))
         return _Done([outs])
 
+    @_together
     def alltoall_base(self, output, input, output_split_sizes, input_split_sizes, opts=None):
         if output.dtype != input.dtype:
             raise ValueError("hoccl: all_to_all tensors differ in dtype")
@@ -500,7 +532,7 @@ class HocclProcessGroup(dist.ProcessGroup):
             raise ValueError("hoccl: all_to_all rows differ in size")
         split_in = list(input_split_sizes) or [input.size(0) // self._n] * self._n
         split_out = list(output_split_sizes) or [output.size(0) // self._n] * self._n
-        desc = {"in": _export(input), "out": _export(output), "type": str(input.dtype),
+        desc = lambda: {"in": _export(input), "out": _export(output), "type": str(input.dtype),
                 "dev": input.device.index,
                 "sin": [s * row_in * es for s in split_in], "sout": [s * row_out * es for s in split_out]}
 
@@ -535,6 +567,7 @@ class HocclProcessGroup(dist.ProcessGroup):
     # They stage through flat buffers (torch copies on the caller's stream)
     # where the library's forms need one buffer per rank.
 
+    @_together
     def _rooted(self, mine, root, to_root):
         """One all-to-all(v) whose only nonzero row (to_root False: the
         root's buffer cut into R blocks, block d to rank d) or column
@@ -545,7 +578,7 @@ class HocclProcessGroup(dist.ProcessGroup):
         if not 0 <= root < R:
             raise ValueError(f"hoccl: root {root} outside 0..{R - 1}")
         nb = _nbytes(mine) // (R if self._r == root else 1)
-        desc = {"t": _export(mine), "bytes": nb, "type": str(mine.dtype), "dev": mine.device.index}
+        desc = lambda: {"t": _export(mine), "bytes": nb, "type": str(mine.dtype), "dev": mine.device.index}
 
         def run(descs):
             if any(d["bytes"] != nb or d["type"] != str(mine.dtype) for d in descs):
@@ -619,7 +652,7 @@ class HocclProcessGroup(dist.ProcessGroup):
         return _Done(output_tensors)
 
     def barrier(self, opts=None):
-        return self._call({}, lambda descs: None)
+        return self._call(dict, lambda descs: None)
 
     # ---- point to point ----------------------------------------------------------------
 

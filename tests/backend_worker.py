@@ -254,6 +254,19 @@ def main():
     for s in range(R):
         assert_same_bytes(outs[s], byte_tensor(1040 + rank, s, rank + 2, torch.bfloat16),
                           f"all_to_all from {s}")
+    # a check failing on one rank only: every rank fails at once, none waits
+    import time
+    t0 = time.perf_counter()
+    bad = torch.zeros(8, dtype=torch.int64 if rank == R - 1 else torch.float32, device="cuda")
+    try:
+        dist.all_reduce(bad)
+        raise AssertionError("an int64 all_reduce was accepted")
+    except RuntimeError as e:
+        assert f"rank {R - 1}" in str(e) and "int32, float32 or bfloat16" in str(e), e
+    assert time.perf_counter() - t0 < 10, "a rank waited for the failing one"
+    x = torch.ones(4, device="cuda")
+    dist.all_reduce(x)                      # the group goes on afterwards
+    assert bool((x == R).all()), x
     dist.barrier()
     hdist.destroy_process_group()
     print(f"rank {rank}: backend ok", flush=True)
