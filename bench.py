@@ -1498,8 +1498,8 @@ def stream_ceilings():
     for line in open(CEILINGS_SUMMARY):
         if line.startswith("| 2048 MiB |"):
             cells = [c.strip().split()[0] for c in line.strip().strip("|").split("|")[1:]]
-            return dict(zip(("read", "write", "copy", "two_reads_one_write", "in_place_rmw"),
-                            (float(c) for c in cells)))
+            return dict(zip(("read", "write", "copy", "copy_nt_stores", "two_reads_one_write",
+                             "two_reads_one_write_nt_stores", "in_place_rmw"), (float(c) for c in cells)))
     return None
 
 
@@ -1598,8 +1598,9 @@ def pmc_workload(hc, W):
 
 def ceilings_workload(hc, sizes=(64 << 20, 128 << 20, 256 << 20, 2 << 30), reps=50):
     """The memory system's streaming ceilings (hoccl_debug_stream_ceiling):
-    read only, write only, copy, two reads and a write (fp32 add) and an
-    in-place fp32 read-modify-write, per operand size: 64, 128 and 256 MiB,
+    read only, write only, copy, two reads and a write (fp32 add), the two
+    with non-temporal stores too, and an in-place fp32 read-modify-write,
+    per operand size: 64, 128 and 256 MiB,
     which the 256 MB Infinity Cache holds once warm, and 2 GiB, which it
     cannot.  Each: 3 warm-up launches, then `reps` back-to-back launches
     between two events (per-launch time includes the launch gap; the
@@ -1613,9 +1614,9 @@ def ceilings_workload(hc, sizes=(64 << 20, 128 << 20, 256 << 20, 2 << 30), reps=
     out = {}
     for size in sizes:
         row = {}
-        for mode in ("read", "write", "copy", "add", "rmw"):
-            a = A[:size] if mode in ("read", "copy", "add") else None
-            b = B[:size] if mode == "add" else None
+        for mode in ("read", "write", "copy", "copy_nt", "add", "add_nt", "rmw"):
+            a = A[:size] if mode in ("read", "copy", "copy_nt", "add", "add_nt") else None
+            b = B[:size] if mode in ("add", "add_nt") else None
             c = C[:size]
 
             def fn():

@@ -609,7 +609,9 @@ hoccl_status_t hoccl_debug_interleave(int nflows, const double *bytes, double ch
  * kernels are read against (the paper reports bandwidth against what the
  * hardware moves, Evaluation, Communication Benchmark).  One launch over
  * `bytes` bytes per operand: mode 0 reads a; 1 writes c; 2 copies a to c;
- * 3 writes c = a + b (fp32); 4 adds 1 to c in place (fp32).  Device
+ * 3 writes c = a + b (fp32); 4 adds 1 to c in place (fp32); 5 and 6 are
+ * modes 2 and 3 with non-temporal stores (faster to HBM once the data
+ * outgrows the Infinity Cache, slower while it fits).  Device
  * pointers, 16-byte aligned, `bytes` a multiple of 16; mode 0 needs c as a
  * 4-byte sink it never writes in practice.  Launch shape from
  * workgroups_per_step and threads_per_workgroup (automatic: about 4

@@ -467,13 +467,14 @@ class Mailbox:
             self._h = ctypes.c_void_p()
 
 
-CEILING_MODES = {"read": 0, "write": 1, "copy": 2, "add": 3, "rmw": 4}
+CEILING_MODES = {"read": 0, "write": 1, "copy": 2, "add": 3, "rmw": 4, "copy_nt": 5, "add_nt": 6}
 
 
 def stream_ceiling(mode, a=None, b=None, c=None, nbytes=None, stream=None):
     """One launch of a streaming-ceiling kernel (hoccl_debug_stream_ceiling):
     'read' a, 'write' c, 'copy' a -> c, 'add' c = a + b (fp32), 'rmw' c += 1
-    (fp32).  nbytes defaults to the size of the first tensor given."""
+    (fp32), 'copy_nt' and 'add_nt' with non-temporal stores.  nbytes
+    defaults to the size of the first tensor given."""
     m = CEILING_MODES[mode] if isinstance(mode, str) else int(mode)
     ts = [t for t in (a, b, c) if t is not None]
     if nbytes is None:

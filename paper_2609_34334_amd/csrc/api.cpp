@@ -1407,12 +1407,12 @@ hoccl_status_t hoccl_debug_schedule_json(int G, const double *C, const int *node
 
 hoccl_status_t hoccl_debug_stream_ceiling(int mode, const void *a, const void *b, void *c, size_t bytes,
                                           hipStream_t stream) {
-    if (mode < 0 || mode > 4) {
+    if (mode < 0 || mode > 6) {
         set_err("unknown mode %d", mode);
         return HOCCL_ERR_INVALID_ARG;
     }
     if (bytes == 0) return HOCCL_OK;
-    const bool need_a = mode == 0 || mode == 2 || mode == 3, need_b = mode == 3, need_c = true;
+    const bool need_a = mode != 1 && mode != 4, need_b = mode == 3 || mode == 6, need_c = true;
     if ((need_a && !a) || (need_b && !b) || (need_c && !c)) {
         set_err("a pointer the mode needs is NULL");
         return HOCCL_ERR_INVALID_ARG;
@@ -1432,7 +1432,7 @@ hoccl_status_t hoccl_debug_stream_ceiling(int mode, const void *a, const void *b
     t_stats.workgroups_per_step = wg;
     t_stats.cus_available = st->num_cus;
     t_stats.cus_used_max = std::min(wg, st->num_cus);
-    static const unsigned long long per_byte[] = {1, 1, 2, 3, 2};
+    static const unsigned long long per_byte[] = {1, 1, 2, 3, 2, 2, 3};
     t_stats.hbm_bytes_algorithmic = per_byte[mode] * (unsigned long long)bytes;
     return HOCCL_OK;
 }

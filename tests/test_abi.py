@@ -236,6 +236,9 @@ def test_stream_ceiling_rejects_bad_arguments_without_a_device():
     assert L.hoccl_debug_stream_ceiling(2, V(0x1000), None, V(0x2008), 64, None) == hc.ERR_INVALID_ARG
     assert L.hoccl_debug_stream_ceiling(2, V(0x1000), None, V(0x2000), 60, None) == hc.ERR_INVALID_ARG
     assert L.hoccl_debug_stream_ceiling(3, V(0x1000), None, V(0x2000), 64, None) == hc.ERR_INVALID_ARG
+    assert L.hoccl_debug_stream_ceiling(6, V(0x1000), None, V(0x2000), 64, None) == hc.ERR_INVALID_ARG  # add_nt needs b
+    assert L.hoccl_debug_stream_ceiling(5, None, None, V(0x2000), 64, None) == hc.ERR_INVALID_ARG       # copy_nt needs a
+    assert L.hoccl_debug_stream_ceiling(7, V(0x1000), V(0x1000), V(0x2000), 64, None) == hc.ERR_INVALID_ARG
     assert L.hoccl_debug_stream_ceiling(1, None, None, V(0x2000), 0, None) == hc.OK
 
 

@@ -20,6 +20,15 @@ def test_stream_ceiling_kernels():
     hc.stream_ceiling("copy", a=a, c=c, nbytes=n * 4)
     torch.cuda.synchronize()
     assert torch.equal(c[:n], a) and bool((c[n:] == 0).all())
+    c.zero_()
+    hc.stream_ceiling("copy_nt", a=a, c=c, nbytes=n * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(c[:n], a) and bool((c[n:] == 0).all())
+    hc.stream_ceiling("add_nt", a=a, b=b, c=c, nbytes=n * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(c[:n], a + b) and bool((c[n:] == 0).all())
+    assert hc.last_stats()["hbm_bytes_algorithmic"] == 3 * n * 4
+    c.zero_()
     hc.stream_ceiling("add", a=a, b=b, c=c, nbytes=n * 4)
     torch.cuda.synchronize()
     assert torch.equal(c[:n], a + b)
