@@ -23,8 +23,9 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--quick]
        python bench.py --sweep            (algbw against message size)
 Profiling workloads (one phase each): --pmc-workload, --occupancy-workload,
 --copy-workload, --ar-groups-workload, --interference-workload,
---ceilings-workload, --after-free-workload, --backend-workload (the
-torch.distributed backend's per-call time over rank processes).
+--ceilings-workload, --after-free-workload, --copy-kernel-workload,
+--backend-workload (the torch.distributed backend's per-call time over rank
+processes).
 """
 import argparse
 import json
@@ -1664,6 +1665,47 @@ def occupancy_workload(hc, W):
                       "kernel_source_sha256_16": kernel_source_hash()}))
 
 
+def copy_kernel_workload(hc, W):
+    """The CU copy kernel on the copy workloads, back to back (median of
+    HIP events per call): a 2 GiB and a 64 MiB copy, the FSDP all-gather,
+    the PP schedule (32 rounds of seven 16 MiB hops) and the EP
+    all-to-all(v), all on copy path `kernel`.  Run once per build of the
+    kernel's knobs (HOCCL_COPY_UNROLL, HOCCL_COPY_NT_IN, HOCCL_COPY_NT_OUT)
+    to compare them."""
+    import torch
+    res = {}
+    hc.set_config(copy_path="kernel")
+
+    def t(label, fn, reps=20):
+        med, _ = event_time(fn, reps)
+        res[label] = round(med * 1e6, 1)
+    a = torch.empty(1 << 30, dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    t("copy_2GiB_us", lambda: hc.sendrecv([a, a], [b, b], [1, -1]))
+    a2, b2 = a[:1 << 25], b[:1 << 25]
+    t("copy_64MiB_us", lambda: hc.sendrecv([a2, a2], [b2, b2], [1, -1]), 50)
+    del a, b, a2, b2
+    R, total = 8, 201_326_592
+    send = [bf16_dev(v) for v in W.ag_parameters(R, total)]
+    recv = [torch.empty(total, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    t("fsdp_allgather_us", lambda: hc.allgather(send, recv))
+    del send, recv
+    ps = [bf16_dev(v) for v in W.p2p_activations(R)]
+    pr = [torch.empty_like(v) for v in ps]
+    fwd, bwd = [r + 1 if r + 1 < R else -1 for r in range(R)], [r - 1 for r in range(R)]
+
+    def pp():
+        for _ in range(16):
+            hc.sendrecv(ps, pr, fwd)
+            hc.sendrecv(ps, pr, bwd)
+    t("pp_schedule_us", pp, 5)
+    s_np, counts, sd, rd, rsz = W.a2a_tokens(R)
+    asend = [bf16_dev(v) for v in s_np]
+    arecv = [torch.empty(z, dtype=torch.bfloat16, device="cuda") for z in rsz]
+    t("ep_alltoallv_us", lambda: hc.alltoallv(asend, counts, sd, arecv, rd))
+    return res
+
+
 def backend_rank():
     """One rank of --backend-workload (started by torchrun with
     HOCCL_BACKEND=1): per-call host time of the torch.distributed backend,
@@ -1761,6 +1803,8 @@ def main():
                     help="run only the copy collectives the zero-CU trace is taken on")
     ap.add_argument("--after-free-workload", action="store_true",
                     help="the SDMA engines right after a large device-memory free, static against balanced")
+    ap.add_argument("--copy-kernel-workload", action="store_true",
+                    help="the CU copy kernel on the copy workloads (to compare its build knobs)")
     ap.add_argument("--backend-workload", action="store_true",
                     help="per-call time of the torch.distributed backend, 2 and 4 rank processes")
     args = ap.parse_args()
@@ -1808,6 +1852,9 @@ def main():
         return
     if args.after_free_workload:
         print(json.dumps({"sdma_after_free": bench_after_free(hc, W)}), flush=True)
+        return
+    if args.copy_kernel_workload:
+        print(json.dumps({"copy_kernel": copy_kernel_workload(hc, W)}), flush=True)
         return
     log("reduce-scatter headline")
     rs = bench_reduce_scatter(hc, W, args.steps, args.warmup)
