@@ -12,7 +12,9 @@ the build command for it.
 Parity status: every function here is pinned by ``tests/test_oracle_pins.py``
 (closed forms, invariants, exhaustive conversion check, brute force, the
 Higham error bound and hand-derived ring-order fixtures under
-``tests/golden/``).
+``tests/golden/``; the bf16-partials fold by the pure-Python ring that
+rounds every hop, a hand-worked example, special cases and its own error
+bound).
 """
 import ctypes
 import os
@@ -54,6 +56,8 @@ def lib():
             "oracle_alltoall": [vpp, vpp, sz, ctypes.c_int, ctypes.c_int],
             "oracle_alltoallv": [vpp, ctypes.POINTER(sz), ctypes.POINTER(sz), vpp,
                                  ctypes.POINTER(sz), ctypes.c_int, ctypes.c_int],
+            "oracle_allreduce_bf16_hops": [vpp, vpp, sz, ctypes.c_int],
+            "oracle_reduce_scatter_bf16_hops": [vpp, vpp, sz, ctypes.c_int],
         }.items():
             f = getattr(L, name)
             f.argtypes = args
@@ -128,6 +132,18 @@ def f32_to_bf16(x):
 
 # ---- whole-array conveniences: allocate outputs, return them ----------------
 
+def allreduce_bf16_hops(send, recv, count):
+    """bf16 all-reduce with bf16 partials rounded at every hop."""
+    _check(lib().oracle_allreduce_bf16_hops(_ptrs(send), _ptrs(recv), count, len(send)),
+           "allreduce_bf16_hops")
+
+
+def reduce_scatter_bf16_hops(send, recv, recvcount):
+    """bf16 reduce-scatter with bf16 partials rounded at every hop."""
+    _check(lib().oracle_reduce_scatter_bf16_hops(_ptrs(send), _ptrs(recv), recvcount, len(send)),
+           "reduce_scatter_bf16_hops")
+
+
 def allreduce_new(send, dtype):
     count = send[0].size
     recv = [np.zeros_like(s) for s in send]
@@ -148,4 +164,18 @@ def allgather_new(send, dtype):
     n = send[0].size
     recv = [np.zeros(R * n, dtype=send[0].dtype) for _ in send]
     allgather(send, recv, n, dtype)
+    return recv
+
+
+def allreduce_bf16_hops_new(send):
+    recv = [np.zeros_like(s) for s in send]
+    allreduce_bf16_hops(send, recv, send[0].size)
+    return recv
+
+
+def reduce_scatter_bf16_hops_new(send):
+    R = len(send)
+    n = send[0].size // R
+    recv = [np.zeros(n, dtype=np.uint16) for _ in send]
+    reduce_scatter_bf16_hops(send, recv, n)
     return recv

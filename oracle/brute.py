@@ -84,9 +84,11 @@ def _narrow(dtype, v):
     return float_to_bf16_bits(v) if dtype == BF16 else v
 
 
-def ring_reduce_scatter(x, n, dtype):
+def ring_reduce_scatter(x, n, dtype, bf16_hops=False):
     """x: R lists of R*n values.  Returns R lists of n values (rank r owns
-    block r).  Simulates the R-1 reduce steps of a ring r -> r+1."""
+    block r).  Simulates the R-1 reduce steps of a ring r -> r+1.  With
+    bf16_hops (bf16 only), every partial a rank passes on is rounded to
+    bf16 first."""
     R = len(x)
     if R == 1:
         return [list(x[0][:n])]
@@ -103,6 +105,8 @@ def ring_reduce_scatter(x, n, dtype):
             blk, part = inbox[r]
             mine = x[r][blk * n:(blk + 1) * n]
             part = [_add(dtype, p, _widen(dtype, v)) for p, v in zip(part, mine)]
+            if bf16_hops:
+                part = [bf16_bits_to_float(float_to_bf16_bits(p)) for p in part]
             outbox[r] = (blk, part)
         if step == R - 2:
             out = [None] * R
@@ -115,7 +119,7 @@ def ring_reduce_scatter(x, n, dtype):
     raise AssertionError("unreachable")
 
 
-def ring_allreduce(x, dtype):
+def ring_allreduce(x, dtype, bf16_hops=False):
     """x: R lists of n values.  Chunk size c = ceil(n / R); ragged chunks are
     simulated as blocks padded to c elements whose pad is discarded."""
     R = len(x)
@@ -125,7 +129,7 @@ def ring_allreduce(x, dtype):
     c = -(-n // R)
     pad = 0 if dtype != BF16 else 0
     xp = [list(xr) + [pad] * (R * c - n) for xr in x]
-    owned = ring_reduce_scatter(xp, c, dtype)       # rank j owns chunk j
+    owned = ring_reduce_scatter(xp, c, dtype, bf16_hops)   # rank j owns chunk j
     # ring all-gather: at step s, rank r forwards chunk (r - s) to rank r+1.
     have = [{r: owned[r]} for r in range(R)]
     for s in range(R - 1):

@@ -30,6 +30,11 @@
  *      * bf16 operands are widened exactly to fp32, all additions are fp32,
  *        and one round-to-nearest-even fp32 -> bf16 conversion happens at
  *        the end (fp32 accumulation);
+ *      * a second bf16 mode (the *_bf16_hops functions) passes bf16
+ *        partials from hop to hop: every partial is rounded to bf16 right
+ *        after its fp32 add, so R ranks round R-1 times (fewer bytes per
+ *        hop, more rounding error);
+ *      * copies also take bytes (OR_UINT8); the sums refuse them;
  *      * all-reduce splits count n into R chunks of c = ceil(n/R) elements,
  *        chunk j = [j*c, min(n, (j+1)*c)), so the last chunks may be short or
  *        empty;
@@ -129,6 +134,20 @@ static void ring_sum_one(const void *const *x, int dtype, int R, int j,
         }
         *(uint16_t *)out = oracle_f32_to_bf16(acc);
     }
+}
+
+/* The same fold with bf16 partials: the partial is rounded to bf16 (round to
+ * nearest, ties to even) after every add, as when each hop passes a bf16
+ * partial to the next rank.  Two ranks need one add and one rounding, the
+ * same as the fold above. */
+static uint16_t ring_sum_one_bf16_hops(const void *const *x, int R, int j, size_t i)
+{
+    uint16_t part = ((const uint16_t *)x[(j + 1) % R])[i];
+    for (int k = 2; k <= R; ++k) {
+        const uint16_t *xr = (const uint16_t *)x[(j + k) % R];
+        part = oracle_f32_to_bf16(bf16_to_f32(part) + bf16_to_f32(xr[i]));
+    }
+    return part;
 }
 
 static int check_common(const void *send, const void *recv, int dtype, int R)
@@ -255,5 +274,32 @@ int oracle_alltoallv(const void *const *send, const size_t *sendcounts,
                        (const unsigned char *)send[s] + (sdispls[k] + i) * es,
                        es);
         }
+    return 0;
+}
+
+/* all-reduce and reduce-scatter of bf16 with bf16 partials rounded at every
+ * hop (ring_sum_one_bf16_hops), in the ring order and chunking of
+ * oracle_allreduce / oracle_reduce_scatter. */
+int oracle_allreduce_bf16_hops(const void *const *send, void *const *recv, size_t count, int R)
+{
+    int rc = check_common(send, recv, OR_BF16, R);
+    if (rc) return rc;
+    if (count == 0) return 0;
+    size_t c = (count + (size_t)R - 1) / (size_t)R;
+    for (size_t i = 0; i < count; ++i) {
+        uint16_t v = ring_sum_one_bf16_hops(send, R, (int)(i / c), i);
+        for (int r = 0; r < R; ++r)
+            ((uint16_t *)recv[r])[i] = v;
+    }
+    return 0;
+}
+
+int oracle_reduce_scatter_bf16_hops(const void *const *send, void *const *recv, size_t recvcount, int R)
+{
+    int rc = check_common(send, recv, OR_BF16, R);
+    if (rc) return rc;
+    for (int r = 0; r < R; ++r)
+        for (size_t i = 0; i < recvcount; ++i)
+            ((uint16_t *)recv[r])[i] = ring_sum_one_bf16_hops(send, R, r, (size_t)r * recvcount + i);
     return 0;
 }

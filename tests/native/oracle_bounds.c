@@ -57,6 +57,10 @@ static void run_case(int op, int dtype, int R, size_t n)
     }
     if (op == 4) rc = oracle_alltoall((const void *const *)send, recv, n, dtype, R);
     if (dtype == OR_UINT8 && op < 2) rc = rc == -2 ? 0 : 1;  /* bytes have no sum: refused */
+    if (dtype == OR_BF16 && op == 0 && rc == 0)               /* bf16 partials rounded per hop */
+        rc = oracle_allreduce_bf16_hops((const void *const *)send, recv, n, R);
+    if (dtype == OR_BF16 && op == 1 && rc == 0)
+        rc = oracle_reduce_scatter_bf16_hops((const void *const *)send, recv, n, R);
     if (rc != 0) {
         fprintf(stderr, "op %d dtype %d R %d n %zu: rc %d\n", op, dtype, R, n, rc);
         exit(1);

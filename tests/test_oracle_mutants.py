@@ -3,7 +3,8 @@
 Each mutant is a copy of ``oracle/hoccl_oracle.c`` with one plausible
 mistake written into it: a fold that starts at the wrong rank or runs the
 wrong way, a dropped term, a wrong sign, the wrong block or chunk length, an
-operand taken from the wrong rank, a truncating or ties-away conversion.  The
+operand taken from the wrong rank, a truncating or ties-away conversion,
+and the same for the fold with bf16 partials.  The
 copy is built into a temporary library that stands in for the oracle's own
 while the fast pins of ``test_oracle_pins.py`` run against it.  A mutant that
 passed every pin would be a mistake the pins cannot see, so each must fail
@@ -26,9 +27,9 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "hoccl_oracle.c")
 # (name, text in the oracle, replacement, how many times the text occurs)
 MUTANTS = [
     ("fold starts at rank j, not j+1",
-     "x[(j + k) % R]", "x[(j + k - 1) % R]", 3),
+     "x[(j + k) % R]", "x[(j + k - 1) % R]", 4),
     ("fold runs backwards (j, j-1, ..., j+1)",
-     "x[(j + k) % R]", "x[(j + R + 1 - k) % R]", 3),
+     "x[(j + k) % R]", "x[(j + R + 1 - k) % R]", 4),
     ("fold drops rank j's own term",
      "for (int k = 1; k <= R; ++k)", "for (int k = 1; k < R; ++k)", 3),
     ("int32 partials subtracted",
@@ -45,7 +46,7 @@ MUTANTS = [
     ("bf16 conversion turns NaN into infinity",
      "return (uint16_t)((u >> 16) | 0x0040u);", "return (uint16_t)((u >> 16) & 0xff80u);", 1),
     ("all-reduce chunk length one too long",
-     "size_t c = (count + (size_t)R - 1) / (size_t)R;", "size_t c = count / (size_t)R + 1;", 1),
+     "size_t c = (count + (size_t)R - 1) / (size_t)R;", "size_t c = count / (size_t)R + 1;", 2),
     ("all-reduce writes rank 0's output only",
      "for (int r = 0; r < R; ++r)\n            memcpy((unsigned char *)recv[r] + i * es, v, es);",
      "for (int r = 0; r < 1; ++r)\n            memcpy((unsigned char *)recv[r] + i * es, v, es);", 1),
@@ -62,6 +63,10 @@ MUTANTS = [
      "(const unsigned char *)send[d] + ((size_t)s * count + i) * es,", 1),
     ("all-to-all(v) drops each block's last element",
      "for (size_t i = 0; i < sendcounts[k]; ++i)", "for (size_t i = 0; i + 1 < sendcounts[k]; ++i)", 1),
+    ("bf16 partials: the fold starts at rank j's own term",
+     "uint16_t part = ((const uint16_t *)x[(j + 1) % R])[i];", "uint16_t part = ((const uint16_t *)x[j % R])[i];", 1),
+    ("bf16 partials: the fold drops rank j's own term",
+     "for (int k = 2; k <= R; ++k)", "for (int k = 2; k < R; ++k)", 1),
     ("send/recv runs the wrong direction",
      "memcpy((unsigned char *)recv[d] + i * es,\n                   (const unsigned char *)send[r] + i * es, es);",
      "memcpy((unsigned char *)recv[r] + i * es,\n                   (const unsigned char *)send[d] + i * es, es);", 1),
@@ -95,6 +100,10 @@ def battery():
         ("bf16 rounding model", P.test_bf16_rounding_matches_python_model),
         ("ring simulation",
          lambda: [P.test_ring_simulation_matches_oracle(d, R) for d in ("int32", "fp32", "bf16") for R in (3, 4)]),
+        ("bf16 partials: ring simulation", lambda: [P.test_bf16_hops_ring_simulation_matches_oracle(R) for R in (3, 4)]),
+        ("bf16 partials: worked example", P.test_bf16_hops_worked_example),
+        ("bf16 partials: special cases", P.test_bf16_hops_special_cases),
+        ("bf16 partials: error bound", lambda: P.test_bf16_hops_within_bound(3)),
     ]
 
 

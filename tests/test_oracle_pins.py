@@ -397,3 +397,63 @@ def test_bf16_rounding_exhaustive_against_torch():
             assert ((o & 0x7F80) == 0x7F80).all() and ((o & 0x7F) != 0).all()
         else:
             assert np.array_equal(ours, ref), hex(start)
+
+
+# ------------------------------------------- bf16 partials rounded at every hop
+
+@pytest.mark.parametrize("R", [1, 2, 3, 4, 6])
+def test_bf16_hops_ring_simulation_matches_oracle(R):
+    """The fold with bf16 partials against the pure-Python ring that rounds
+    every partial it passes on (reduce-scatter and ragged all-reduce)."""
+    for n in list(range(0, 12)) + [29]:
+        x = [W.random_values("bf16", 3000 + 7 * R + n, r, R * n) for r in range(R)]
+        got = oracle.reduce_scatter_bf16_hops_new(x)
+        ref = brute.ring_reduce_scatter([_to_py(a, "bf16") for a in x], n, dtype=oracle.BF16, bf16_hops=True)
+        for r in range(R):
+            assert np.array_equal(got[r], _from_py(ref[r], "bf16")), (n, r)
+        x = [W.random_values("bf16", 3100 + 7 * R + n, r, n) for r in range(R)]
+        got = oracle.allreduce_bf16_hops_new(x)
+        ref = brute.ring_allreduce([_to_py(a, "bf16") for a in x], oracle.BF16, bf16_hops=True)
+        for r in range(R):
+            assert np.array_equal(got[r], _from_py(ref[r], "bf16")), (n, r)
+
+
+def test_bf16_hops_worked_example():
+    """Three ranks, rank 0's block: the fold takes x1 = 1, x2 = 2^-8, x0 = 2^-8.
+    With one rounding at the end the sum 1 + 2^-7 is a bf16 value; rounded at
+    every hop, 1 + 2^-8 is a tie between 1 and 1 + 2^-7 and goes to the even
+    1, twice, so the result is 1."""
+    one, eps = 0x3F80, 0x3B80                          # 1.0 and 2^-8 in bf16
+    x = [np.array([eps], np.uint16), np.array([one], np.uint16), np.array([eps], np.uint16)]
+    x = [np.concatenate([a, np.zeros(2, np.uint16)]) for a in x]      # R * recvcount = 3
+    assert oracle.reduce_scatter_new(x, oracle.BF16)[0][0] == 0x3F81  # 1 + 2^-7
+    assert oracle.reduce_scatter_bf16_hops_new(x)[0][0] == one
+
+
+def test_bf16_hops_special_cases():
+    """Two ranks round once in either mode; sums of small integers are exact
+    in either mode; rank-count 1 is the identity."""
+    x = [W.normal_bf16(24, r, 5000, 1.0) for r in range(2)]
+    assert np.array_equal(oracle.allreduce_bf16_hops_new(x)[0], oracle.allreduce_new(x, oracle.BF16)[0])
+    rng = np.random.default_rng(4)
+    ints = [rng.integers(-16, 16, 700) for _ in range(8)]   # every partial |.| <= 128
+    xs = [W.to_bf16_bits(a) for a in ints]
+    assert np.array_equal(W.bf16_bits_to_f32(oracle.allreduce_bf16_hops_new(xs)[3]),
+                          sum(ints).astype(np.float32))
+    one = [W.normal_bf16(25, 0, 33, 1.0)]
+    assert np.array_equal(oracle.allreduce_bf16_hops_new(one)[0], one[0])
+
+
+@pytest.mark.parametrize("R", [3, 8])
+def test_bf16_hops_within_bound(R):
+    """Each of the R-1 hops rounds the partial once to bf16 (8 significant
+    bits: at most 2^-8 of its magnitude) after an fp32 add (2^-24): the
+    result lies within (R-1)(2^-8 + 2^-24) times the sum of magnitudes of
+    the exact sum."""
+    n = 300
+    x = [W.normal_bf16(26, r, n, 1.0) for r in range(R)]
+    out = oracle.allreduce_bf16_hops_new(x)
+    for i in range(n):
+        vals = [Fraction(float(W.bf16_bits_to_f32(a[i]))) for a in x]
+        bound = (R - 1) * Fraction(2.0 ** -8 + 2.0 ** -24) * sum(abs(v) for v in vals)
+        assert abs(Fraction(float(W.bf16_bits_to_f32(out[0][i]))) - sum(vals)) <= bound
