@@ -965,6 +965,59 @@ def bench_fused_hops(hc, send_np, steps, warmup):
                          "folded per launch (bit-identical to k = 1)", **out)
 
 
+def bench_bf16_partials(hc, send_np, steps, warmup, samples=8192):
+    """The headline reduce-scatter with bf16 partials (every hop's sum
+    rounded to bf16) against fp32 partials (one rounding), on the ring and
+    the direct fold: time per call (HIP events on the launching stream over
+    `steps` back-to-back calls), algorithmic bytes, and the error of sampled
+    outputs against the exact fp64 sum, in units of 2^-8 * sum |x| (the
+    bound of one bf16 rounding of the sum's magnitude)."""
+    import numpy as np
+    import torch
+    R = len(send_np)
+    n = send_np[0].size // R
+    send = [bf16_dev(a) for a in send_np]
+    recv = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    stream = torch.cuda.current_stream()
+    g = np.random.default_rng(5)
+    ranks = g.integers(0, R, samples)
+    idx = g.integers(0, n, samples)
+    pos = ranks * n + idx
+    vals = np.stack([((a.view(np.uint16)[pos].astype(np.uint32) << 16).view(np.float32))
+                     for a in send_np]).astype(np.float64)     # R x samples
+    exact = vals.sum(axis=0)
+    scale = np.abs(vals).sum(axis=0) * 2.0 ** -8
+    out = {}
+    for algo in ("ring", "direct"):
+        for bp in (0, 1):
+            with hc.config(reduce_algo=algo, bf16_partials=bp, fused_hops=1, kernel_timing=0):
+                def step():
+                    hc.reduce_scatter(send, recv, stream=stream)
+                for _ in range(warmup):
+                    step()
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(steps):
+                    step()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                st = hc.last_stats()
+            t = e0.elapsed_time(e1) / 1e3 / steps
+            got = torch.stack(recv).float().cpu().numpy()[ranks, idx].astype(np.float64)
+            err = np.abs(got - exact) / np.where(scale > 0, scale, 1.0)
+            b = st["hbm_bytes_algorithmic"]
+            out[f"{algo}_{'bf16' if bp else 'fp32'}_partials"] = dict(
+                us=round(t * 1e6, 2), bytes_per_op=b, achieved_GBs=round(b / t / 1e9, 1),
+                frac=round(b / t / 1e9 / HBM_PEAK_GBS, 4), launches=st["reduce_launches"],
+                err_max=round(float(err.max()), 4), err_mean=round(float(err.mean()), 5))
+    return dict(workload="reduce-scatter bf16 R=8, 25,165,824 elements per rank: bf16 partials "
+                         "(rounded at every hop) against fp32 partials (rounded once), ring and "
+                         "direct fold; error of %d sampled outputs against the exact sum, in units "
+                         "of 2^-8 * sum |x|" % samples, **out)
+
+
 def bench_rs_graph(hc, send_np, steps):
     """The headline ring reduce-scatter captured ten steps at a time into a
     HIP graph and replayed, against the same steps issued eagerly on the
@@ -1913,6 +1966,12 @@ def main():
             extra["reduce_scatter_fused_hops"] = bench_fused_hops(hc, rs["x"], args.steps, args.warmup)
         except Exception as e:
             extra["reduce_scatter_fused_hops"] = {"error": repr(e)}
+        log("reduce-scatter with bf16 partials")
+        try:
+            extra["reduce_scatter_bf16_partials"] = bench_bf16_partials(hc, rs["x"], args.steps,
+                                                                        args.warmup)
+        except Exception as e:
+            extra["reduce_scatter_bf16_partials"] = {"error": repr(e)}
         log("reduce-scatter in a graph")
         try:
             extra["reduce_scatter_graph"] = bench_rs_graph(hc, rs["x"], args.steps)

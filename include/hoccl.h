@@ -291,6 +291,27 @@ typedef struct {
                                    all-gather, the reduce-scatter /
                                    all-reduce gathers) and graph captures
                                    are always issued at once               */
+    int bf16_partials;          /* bf16 reduce-scatter / all-reduce partials:
+                                   0 (default): the partial sums travel in
+                                   fp32 and each output is rounded to bf16
+                                   once, after its last addition (the
+                                   result is the sum in ring order rounded
+                                   once);
+                                   1: every addition's result is rounded to
+                                   bf16 (round to nearest, ties to even)
+                                   before the next one, as when each rank
+                                   of the ring forwards its partial in the
+                                   collective's own element type: the ring
+                                   step moves 6 bytes per element instead
+                                   of 8 to 10 and keeps no fp32 workspace,
+                                   at up to R-1 roundings of error instead
+                                   of one.  The same ring order and the
+                                   same roundings on the ring, the direct
+                                   fold and every grouping; fused hops
+                                   (fused_hops) are not used in this mode.
+                                   Other dtypes ignore it.  hoccl_ring_hop
+                                   is unaffected: its HOCCL_HOP_ONLY is the
+                                   bf16-partial hop                         */
 } hoccl_config_t;
 
 /* The first eight fields are the core statistics; the rest extend them. */
@@ -331,8 +352,8 @@ typedef struct {
  *   HOCCL_COPY_STREAMS, HOCCL_SDMA_ENGINES, HOCCL_AG_DIRECT,
  *   HOCCL_AR_GROUPS, HOCCL_KERNEL_TIMING, HOCCL_PROXY_HANDSHAKE,
  *   HOCCL_PROXY_WAIT_LIMIT_US, HOCCL_RING_GROUP_BYTES, HOCCL_FUSED_HOPS,
- *   HOCCL_A2A_SCHEDULE, HOCCL_PROXY_SLICE_BYTES (the fields of the same
- *   meaning),
+ *   HOCCL_A2A_SCHEDULE, HOCCL_PROXY_SLICE_BYTES, HOCCL_BF16_PARTIALS
+ *   (the fields of the same meaning),
  *   HOCCL_COPY_PATH = auto | sdma (or engines) | kernel | hip,
  *   HOCCL_REDUCE_ALGO = ring | direct | auto,
  *   HOCCL_DEBUG = 1 (log every executed plan as JSON to stderr),

@@ -58,7 +58,8 @@ class Config(ctypes.Structure):
                 ("proxy_wait_limit_us", ctypes.c_uint),
                 ("fused_hops", ctypes.c_int),
                 ("a2a_schedule", ctypes.c_int),
-                ("proxy_slice_bytes", ctypes.c_size_t)]
+                ("proxy_slice_bytes", ctypes.c_size_t),
+                ("bf16_partials", ctypes.c_int)]
 
 
 class Stats(ctypes.Structure):

@@ -121,6 +121,7 @@ hoccl_config_t default_config() {
     c.fused_hops = 1;
     c.a2a_schedule = 0;
     c.proxy_slice_bytes = 0;
+    c.bf16_partials = 0;
     return c;
 }
 
@@ -142,6 +143,7 @@ bool config_valid(const hoccl_config_t &c) {
     if (c.proxy_slice_bytes != 0 && c.proxy_slice_bytes != SIZE_MAX &&
         (c.proxy_slice_bytes < ((size_t)64 << 10) || c.proxy_slice_bytes % 4096 != 0))
         return false;
+    if (c.bf16_partials != 0 && c.bf16_partials != 1) return false;
     return true;
 }
 
@@ -168,6 +170,7 @@ void load_config_locked() {
     c.proxy_wait_limit_us = (unsigned)env_long("HOCCL_PROXY_WAIT_LIMIT_US", c.proxy_wait_limit_us);
     c.fused_hops = (int)env_long("HOCCL_FUSED_HOPS", c.fused_hops);
     c.a2a_schedule = (int)env_long("HOCCL_A2A_SCHEDULE", c.a2a_schedule);
+    c.bf16_partials = (int)env_long("HOCCL_BF16_PARTIALS", c.bf16_partials);
     if (const char *v = std::getenv("HOCCL_RING_GROUP_BYTES")) c.ring_group_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_PROXY_SLICE_BYTES")) c.proxy_slice_bytes = std::strtoull(v, nullptr, 0);
     if (const char *v = std::getenv("HOCCL_COPY_PATH")) {
@@ -370,7 +373,8 @@ int auto_workgroups(const DeviceState &st, const hoccl_config_t &cfg, const Plan
     for (const ReduceStep &s : p.reduce_steps) {
         unsigned long long n = 0;
         for (const ReduceSeg &g : s.segs) n += g.n;
-        need(n, s.hops > 1 ? multihop_elems_per_thread(p.dtype) : reduce_step_elems_per_thread(p.dtype, s.phase));
+        need(n, s.hops > 1 ? multihop_elems_per_thread(p.dtype)
+                           : reduce_step_elems_per_thread(p.dtype, s.phase, p.bf16_partials));
     }
     if (p.has_fold) need(p.fold.total, fold_elems_per_thread(p.dtype));
     if (cfg.copy_path == HOCCL_COPY_KERNEL)
@@ -487,7 +491,7 @@ hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const 
             a.nseg = ns;
             TimingPair *tp;
             TRY(timed_begin(st, cfg, s, &tp));
-            HIP_TRY(launch_reduce_step(p.dtype, step.phase, a, wg, threads, s));
+            HIP_TRY(launch_reduce_step(p.dtype, step.phase, a, wg, threads, s, p.bf16_partials));
             TRY(timed_end(tp, s));
             t_stats.reduce_launches++;
         }
@@ -518,7 +522,7 @@ hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const 
         a.out_at_chunk = p.fold.out_at_chunk ? 1 : 0;
         TimingPair *tp;
         TRY(timed_begin(st, cfg, s, &tp));
-        HIP_TRY(launch_fold(p.dtype, a, wg, threads, s));
+        HIP_TRY(launch_fold(p.dtype, a, wg, threads, s, p.bf16_partials));
         TRY(timed_end(tp, s));
         t_stats.reduce_launches++;
     }
@@ -1001,6 +1005,7 @@ PlanOptions options_from(const hoccl_config_t &cfg, bool in_place) {
     o.algo = cfg.reduce_algo;
     o.fused_hops = cfg.fused_hops;
     o.a2a_schedule = cfg.a2a_schedule;
+    o.bf16_partials = cfg.bf16_partials != 0;
     return o;
 }
 

@@ -100,6 +100,7 @@ struct Plan {
     std::vector<CopyOp> copies;            // in issue order
     int nchains = 0;
     size_t ws_bytes = 0;                   // workspace the plan needs
+    bool bf16_partials = false;            // bf16 partials, rounded at every add
     unsigned long long hbm_bytes = 0;      // algorithmic HBM bytes
     unsigned long long copy_bytes = 0;
 };
@@ -120,6 +121,9 @@ struct PlanOptions {
     // balanced chains; 1 and 2 the stages of the collective scheduler's
     // decomposition (copies tagged with their stage; 2 runs them serially).
     int a2a_schedule = 0;
+    // bf16 reductions keep their partials in bf16, rounding every addition
+    // (hoccl_config_t.bf16_partials); one hop per ring launch.
+    bool bf16_partials = false;
 };
 
 // HOCCL_REDUCE_AUTO folds directly up to this many ranks.  On one GPU the
@@ -130,7 +134,9 @@ constexpr int kDirectMaxRanks = 64;
 bool use_direct(hoccl_reduce_algo_t algo, int R);
 
 size_t dtype_size(hoccl_dtype_t dt);
-size_t acc_size(hoccl_dtype_t dt);
+// Bytes of one partial-sum element: 4 (fp32 for bf16), 2 for bf16 with
+// bf16 partials.
+size_t acc_size(hoccl_dtype_t dt, bool bf16_partials = false);
 
 // Planner entry points (plan.cpp); pure host code.
 Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o);
@@ -227,17 +233,20 @@ struct HandshakeArgs {
     uint64_t limit_ticks;   // give up after this many device wall-clock ticks
 };
 
+// bf16_partials: a bf16 step keeps every operand and result in bf16 (the
+// middle and last phases read, and the first and middle write, bf16
+// partials); a bf16 fold rounds after every addition.
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg,
-                              int threads, hipStream_t s);
+                              int threads, hipStream_t s, bool bf16_partials = false);
 hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
-                       hipStream_t s);
+                       hipStream_t s, bool bf16_partials = false);
 hipError_t launch_multihop(hoccl_dtype_t dt, Phase ph, const MultiArgs &a, int wg, int threads,
                            hipStream_t s);
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s);
 
 // Work one thread does in one pass of each kernel's main loop (elements of
 // the collective's dtype, or bytes for the copy kernel).
-size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph);
+size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph, bool bf16_partials = false);
 size_t fold_elems_per_thread(hoccl_dtype_t dt);
 size_t multihop_elems_per_thread(hoccl_dtype_t dt);
 size_t copy_bytes_per_thread();

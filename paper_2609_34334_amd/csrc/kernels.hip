@@ -368,12 +368,19 @@ __global__ void __launch_bounds__(1024) multihop_kernel(MultiArgsT<CAP>) {
 // ---- direct fold ------------------------------------------------------------------
 // Chunk j reads x[(j+1)%R], x[(j+2)%R], ..., x[j] at the chunk's elements and
 // adds them left to right; loads are issued in batches of KB ranks so several
-// are in flight before the adds consume them in order.
-template <class T, int VE, int NR, class FA>
+// are in flight before the adds consume them in order.  RH rounds every
+// addition's result to the element type before the next addition (the
+// partials a ring of bf16 forwarding ranks would hold).
+template <class T, int VE, int NR, bool RH, class FA>
 __device__ __forceinline__ void fold_chunk(const FA &a, int j, int lb, int nb) {
     using S = typename T::S;
     using A = typename T::A;
     using P = Pack<S, VE>;
+    auto add = [](A acc, S x) -> A {
+        A y = acc + T::widen(x);
+        if constexpr (RH) y = T::widen(T::narrow(y));
+        return y;
+    };
     const int R = NR > 0 ? NR : a.R;
     const uint64_t e0 = (uint64_t)j * a.c;
     if (e0 >= a.total) return;
@@ -403,7 +410,7 @@ __device__ __forceinline__ void fold_chunk(const FA &a, int j, int lb, int nb) {
     const uint64_t stride = (uint64_t)nb * bd;
     auto scalar = [&](uint64_t k) {
         A acc = T::widen(src(0)[k]);
-        for (int q = 1; q < R; ++q) acc = acc + T::widen(src(q)[k]);
+        for (int q = 1; q < R; ++q) acc = add(acc, src(q)[k]);
         S y = T::narrow(acc);
         for (int q = 0; q < nout; ++q) dst(q)[k] = y;
     };
@@ -436,7 +443,7 @@ __device__ __forceinline__ void fold_chunk(const FA &a, int j, int lb, int nb) {
 #pragma unroll
                 for (int k = 1; k < NR; ++k)
 #pragma unroll
-                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[k].v[e]);
+                    for (int e = 0; e < VE; ++e) acc[e] = add(acc[e], v[k].v[e]);
                 P y;
 #pragma unroll
                 for (int e = 0; e < VE; ++e) y.v[e] = T::narrow(acc[e]);
@@ -467,12 +474,12 @@ __device__ __forceinline__ void fold_chunk(const FA &a, int j, int lb, int nb) {
 #pragma unroll
                 for (int q = 0; q < KB; ++q)
 #pragma unroll
-                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v[q].v[e]);
+                    for (int e = 0; e < VE; ++e) acc[e] = add(acc[e], v[q].v[e]);
             }
             for (; k < R; ++k) {
                 P v = ((const P *)(src(k) + h))[i];
 #pragma unroll
-                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T::widen(v.v[e]);
+                for (int e = 0; e < VE; ++e) acc[e] = add(acc[e], v.v[e]);
             }
         }
         P y;
@@ -491,10 +498,15 @@ __device__ __forceinline__ const A &kernargs() {
     return *(const A *)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
-template <class T, int VE, int NR, int CAP>
+template <class T, int VE, int NR, int CAP, bool RH>
 __global__ void __launch_bounds__(1024) fold_kernel(FoldArgsT<CAP>) {
     const FoldArgsT<CAP> &a = kernargs<FoldArgsT<CAP>>();
-    for_each_segment(a.R, [&](int j, int lb, int nb) { fold_chunk<T, VE, NR>(a, j, lb, nb); });
+    // Forced inline: for_each_segment calls the body from two places, and
+    // the eight-rank rounding fold was otherwise left an out-of-line call
+    // with a scratch frame.
+    for_each_segment(a.R, [&](int j, int lb, int nb) __attribute__((always_inline)) {
+        fold_chunk<T, VE, NR, RH>(a, j, lb, nb);
+    });
 }
 
 // ---- CU copy ----------------------------------------------------------------------
@@ -611,10 +623,31 @@ static hipError_t launch_rs(const ReduceArgs &a, int wg, int threads, hipStream_
 }
 
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg, int threads,
-                              hipStream_t s) {
+                              hipStream_t s, bool bf16_partials) {
     constexpr int UB = HOCCL_RS_UNROLL_BF16, U4 = HOCCL_RS_UNROLL_32;
     constexpr int VP = kVeBf16Partial, VB = kVeBf16Only, V4 = kVe32;
-    if (dt == HOCCL_BF16) {
+    if (dt == HOCCL_BF16 && bf16_partials) {
+        // Every operand and result in bf16: each step rounds its sum, as a
+        // ring that forwards bf16 partials does.  The same in-flight rule
+        // as below, on 8-element vectors.
+        uint64_t n = 0;
+        for (int k = 0; k < a.nseg; ++k) n += a.seg[k].n;
+        const bool deep = n > (uint64_t)wg * (uint64_t)threads * (uint64_t)(VB * UB);
+        if (deep) {
+            switch (ph) {
+            case PH_FIRST: return launch_rs<TBF16, TBF16, TBF16, VB, 2 * UB, kNtFirst>(a, wg, threads, s);
+            case PH_MIDDLE: return launch_rs<TBF16, TBF16, TBF16, VB, 2 * UB, kNtMiddle>(a, wg, threads, s);
+            case PH_LAST: return launch_rs<TBF16, TBF16, TBF16, VB, 2 * UB, kNtLast>(a, wg, threads, s);
+            case PH_ONLY: break;
+            }
+        }
+        switch (ph) {
+        case PH_FIRST: return launch_rs<TBF16, TBF16, TBF16, VB, UB, kNtFirst>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_rs<TBF16, TBF16, TBF16, VB, UB, kNtMiddle>(a, wg, threads, s);
+        case PH_LAST: return launch_rs<TBF16, TBF16, TBF16, VB, UB, kNtLast>(a, wg, threads, s);
+        case PH_ONLY: return launch_rs<TBF16, TBF16, TBF16, VB, UB, kNtOnly>(a, wg, threads, s);
+        }
+    } else if (dt == HOCCL_BF16) {
         // A launch that leaves each thread several passes (a small
         // workgroup budget) keeps twice the vectors in flight per thread:
         // there the bytes in flight per wave, not the number of waves, set
@@ -712,32 +745,35 @@ size_t multihop_elems_per_thread(hoccl_dtype_t) { return 8; }
 
 // Elements one thread covers in one pass of each kernel's main loop; the
 // executor sizes automatic launches to about one pass per thread.
-size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph) {
+size_t reduce_step_elems_per_thread(hoccl_dtype_t dt, Phase ph, bool bf16_partials) {
     if (dt == HOCCL_BF16)
-        return (size_t)(ph == PH_ONLY ? kVeBf16Only : kVeBf16Partial) * HOCCL_RS_UNROLL_BF16;
+        return (size_t)(ph == PH_ONLY || bf16_partials ? kVeBf16Only : kVeBf16Partial) *
+               HOCCL_RS_UNROLL_BF16;
     return (size_t)kVe32 * HOCCL_RS_UNROLL_32;
 }
 size_t fold_elems_per_thread(hoccl_dtype_t dt) { return 16 / dtype_size(dt); }
 size_t copy_bytes_per_thread() { return 16 * kCopyUnroll; }
 
 // R = 2, 3, 4 and 8 have kernels of their own, whose arguments hold R ranks.
-template <class T, int VE, int NR>
+template <class T, int VE, int NR, bool RH>
 static hipError_t launch_fold_r(const FoldArgs &a, int wg, int threads, hipStream_t s) {
-    return launch((const void *)fold_kernel<T, VE, NR, NR>, fit<NR>(a), wg, threads, s);
+    return launch((const void *)fold_kernel<T, VE, NR, NR, RH>, fit<NR>(a), wg, threads, s);
 }
 
-template <class T, int VE>
+template <class T, int VE, bool RH = false>
 static hipError_t launch_fold_t(const FoldArgs &a, int wg, int threads, hipStream_t s) {
     switch (a.R) {
-    case 2: return launch_fold_r<T, VE, 2>(a, wg, threads, s);
-    case 3: return launch_fold_r<T, VE, 3>(a, wg, threads, s);
-    case 4: return launch_fold_r<T, VE, 4>(a, wg, threads, s);
-    case 8: return launch_fold_r<T, VE, 8>(a, wg, threads, s);
-    default: return launch((const void *)fold_kernel<T, VE, 0, kMaxRanks>, a, wg, threads, s);
+    case 2: return launch_fold_r<T, VE, 2, RH>(a, wg, threads, s);
+    case 3: return launch_fold_r<T, VE, 3, RH>(a, wg, threads, s);
+    case 4: return launch_fold_r<T, VE, 4, RH>(a, wg, threads, s);
+    case 8: return launch_fold_r<T, VE, 8, RH>(a, wg, threads, s);
+    default: return launch((const void *)fold_kernel<T, VE, 0, kMaxRanks, RH>, a, wg, threads, s);
     }
 }
 
-hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads, hipStream_t s) {
+hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads, hipStream_t s,
+                       bool bf16_partials) {
+    if (dt == HOCCL_BF16 && bf16_partials) return launch_fold_t<TBF16, 8, true>(a, wg, threads, s);
     if (dt == HOCCL_BF16) return launch_fold_t<TBF16, 8>(a, wg, threads, s);
     if (dt == HOCCL_FP32) return launch_fold_t<TF32, 4>(a, wg, threads, s);
     if (dt == HOCCL_INT32) return launch_fold_t<TI32, 4>(a, wg, threads, s);

@@ -23,7 +23,9 @@
 namespace hoccl {
 
 size_t dtype_size(hoccl_dtype_t dt) { return dt == HOCCL_BF16 ? 2 : dt == HOCCL_UINT8 ? 1 : 4; }
-size_t acc_size(hoccl_dtype_t) { return 4; }
+size_t acc_size(hoccl_dtype_t dt, bool bf16_partials) {
+    return dt == HOCCL_BF16 && bf16_partials ? 2 : 4;
+}
 
 static inline int mod(int a, int R) { return ((a % R) + R) % R; }
 
@@ -40,8 +42,8 @@ static BufRef ref(uint8_t kind, int rank, size_t off) {
 }
 
 // Bytes one reduction segment must move: two reads and one write.
-static unsigned long long seg_bytes(hoccl_dtype_t dt, Phase ph, size_t n) {
-    size_t e = dtype_size(dt), a = acc_size(dt);
+static unsigned long long seg_bytes(hoccl_dtype_t dt, bool bf16p, Phase ph, size_t n) {
+    size_t e = dtype_size(dt), a = acc_size(dt, bf16p);
     switch (ph) {
     case PH_FIRST: return (unsigned long long)n * (e + e + a);
     case PH_MIDDLE: return (unsigned long long)n * (a + e + a);
@@ -125,7 +127,7 @@ static void finish_chains(Plan &p) {
 static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
                         const std::vector<size_t> &chunk_len, size_t g0, size_t glen,
                         int group, bool out_at_chunk, int H) {
-    size_t es = dtype_size(dt), as = acc_size(dt);
+    size_t es = dtype_size(dt), as = acc_size(dt, p.bf16_partials);
     for (int s0 = 0; s0 <= R - 2; s0 += H) {
         const int s1 = std::min(s0 + H, R - 1);  // hops s0 .. s1-1
         const bool first = s0 == 0, last = s1 == R - 1;
@@ -155,24 +157,27 @@ static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
             } else {
                 sg.out = ref(BUF_WS, 0, e * as);
             }
-            p.hbm_bytes += seg_bytes(dt, st.phase, n) + (unsigned long long)n * es * sg.more.size();
+            p.hbm_bytes += seg_bytes(dt, p.bf16_partials, st.phase, n) +
+                           (unsigned long long)n * es * sg.more.size();
             st.segs.push_back(std::move(sg));
         }
         if (!st.segs.empty()) p.reduce_steps.push_back(std::move(st));
     }
 }
 
-// Hops per ring launch from the option (0 and 1: one), at most kMaxHops.
-static int hops_per_launch(const PlanOptions &o) {
+// Hops per ring launch from the option (0 and 1: one), at most kMaxHops;
+// one with bf16 partials, whose every addition is rounded in memory's type.
+static int hops_per_launch(const Plan &p, const PlanOptions &o) {
+    if (p.bf16_partials) return 1;
     return std::max(1, std::min(o.fused_hops, kMaxHops));
 }
 
 // Groups a ring reduction over chunks of c elements is split into so that
 // one group's partials (R chunk slices of acc-size elements) take at most
 // `limit` bytes.  Two ranks keep no partials.
-static int cache_groups(int R, size_t c, hoccl_dtype_t dt, size_t limit) {
+static int cache_groups(int R, size_t c, hoccl_dtype_t dt, bool bf16p, size_t limit) {
     if (limit == 0 || R <= 2 || c == 0) return 1;
-    unsigned long long bytes = (unsigned long long)R * c * acc_size(dt);
+    unsigned long long bytes = (unsigned long long)R * c * acc_size(dt, bf16p);
     unsigned long long G = (bytes + limit - 1) / limit;
     if (G > c) G = c;
     return (int)std::max(1ull, std::min(G, 1ull << 20));
@@ -184,6 +189,7 @@ Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o
     p.dtype = dt;
     p.R = R;
     p.count = n;
+    p.bf16_partials = o.bf16_partials && dt == HOCCL_BF16;
     if (n == 0) return p;
     size_t es = dtype_size(dt);
     if (R == 1) {
@@ -203,13 +209,13 @@ Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o
         return p;
     }
     std::vector<size_t> len((size_t)R, n);
-    const int G = cache_groups(R, n, dt, o.group_partial_bytes);
+    const int G = cache_groups(R, n, dt, p.bf16_partials, o.group_partial_bytes);
     const size_t gl = (n + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;
-    const int H = hops_per_launch(o);
+    const int H = hops_per_launch(p, o);
     for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, n, len, (size_t)g * gl, gl, g, true, H);
     // Partials cross launches only when the hops take more than one.
-    p.ws_bytes = (R - 1 > H) ? (size_t)R * n * acc_size(dt) : 0;
+    p.ws_bytes = (R - 1 > H) ? (size_t)R * n * acc_size(dt, p.bf16_partials) : 0;
     return p;
 }
 
@@ -219,6 +225,7 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
     p.dtype = dt;
     p.R = R;
     p.count = count;
+    p.bf16_partials = o.bf16_partials && dt == HOCCL_BF16;
     if (count == 0) return p;
     size_t es = dtype_size(dt);
     if (R == 1) {
@@ -249,11 +256,11 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
     // per rank), else one (2 MiB per rank: 0.18 ms with one, 0.24 with two).
     const int want = o.allreduce_groups > 0 ? o.allreduce_groups
                                             : (count * es >= ((size_t)32 << 20) ? 2 : 1);
-    int G = std::max(want, cache_groups(R, c, dt, o.group_partial_bytes));
+    int G = std::max(want, cache_groups(R, c, dt, p.bf16_partials, o.group_partial_bytes));
     if ((size_t)G > c) G = (int)c;
     size_t cg = (c + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;
-    const int H = hops_per_launch(o);
+    const int H = hops_per_launch(p, o);
     for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, c, len, (size_t)g * cg, cg, g, false, H);
     // Gather phase: chunk j (group g) travels j -> j+1 -> ... -> j-1.
     int maxp = 1;
@@ -281,7 +288,7 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
                          o.allgather_direct ? 0 : s, o.chunk_bytes, maxp);
             }
         }
-    p.ws_bytes = (R - 1 > H) ? (size_t)R * c * acc_size(dt) : 0;
+    p.ws_bytes = (R - 1 > H) ? (size_t)R * c * acc_size(dt, p.bf16_partials) : 0;
     finish_chains(p);
     return p;
 }
@@ -498,7 +505,8 @@ std::string plan_to_json(const Plan &p) {
     os << "{\"op\":" << (int)p.op << ",\"dtype\":" << (int)p.dtype << ",\"R\":" << p.R
        << ",\"count\":" << p.count << ",\"ngroups\":" << p.ngroups << ",\"ws_bytes\":" << p.ws_bytes
        << ",\"hbm_bytes\":" << p.hbm_bytes << ",\"copy_bytes\":" << p.copy_bytes
-       << ",\"nchains\":" << p.nchains << ",\"reduce_steps\":[";
+       << ",\"nchains\":" << p.nchains << ",\"bf16_partials\":" << (p.bf16_partials ? 1 : 0)
+       << ",\"reduce_steps\":[";
     for (size_t i = 0; i < p.reduce_steps.size(); ++i) {
         const auto &s = p.reduce_steps[i];
         if (i) os << ",";

@@ -14,7 +14,7 @@
 #include "../../include/hoccl.h"
 
 /* Sizes the Python binding mirrors (tests/test_abi.py checks the same). */
-#define HOCCL_CONFIG_SIZE 88
+#define HOCCL_CONFIG_SIZE 96
 #define HOCCL_STATS_SIZE 56
 
 #define R 5

@@ -51,7 +51,7 @@ void mix(char *out, const char *a, const char *b, size_t eo, size_t ea, size_t e
 }
 
 void replay(const Plan &p, const Bufs &B) {
-    const size_t es = dtype_size(p.dtype), as = acc_size(p.dtype);
+    const size_t es = dtype_size(p.dtype), as = acc_size(p.dtype, p.bf16_partials);
     for (const ReduceStep &st : p.reduce_steps) {
         size_t e0 = (st.phase == PH_FIRST || st.phase == PH_ONLY) ? es : as;
         size_t eo = (st.phase == PH_LAST || st.phase == PH_ONLY) ? es : as;
@@ -158,6 +158,13 @@ int main() {
                                         run(plan_reduce_scatter(n, dt, R, f), R, (size_t)R * n * es, n * es,
                                             ip ? 2 : 0);
                                     }
+                                if (algo == 0 && dt == HOCCL_BF16) {  // bf16 partials (fused hops ignored)
+                                    PlanOptions b = o;
+                                    b.bf16_partials = true;
+                                    b.fused_hops = 3;
+                                    run(plan_allreduce(n, dt, R, b), R, n * es, n * es, ip ? 3 : 0);
+                                    run(plan_reduce_scatter(n, dt, R, b), R, (size_t)R * n * es, n * es, ip ? 2 : 0);
+                                }
                                 if (ip) continue;
                                 std::vector<int> shift((size_t)R), rev((size_t)R);
                                 for (int r = 0; r < R; ++r) {

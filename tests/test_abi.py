@@ -124,6 +124,12 @@ def test_config_roundtrip_and_validation():
             hc.set_config(threads_per_workgroup=100)
         with pytest.raises(hc.HocclError):
             hc.set_config(chunk_bytes=100)
+        for bad in (-1, 2):
+            with pytest.raises(hc.HocclError):
+                hc.set_config(bf16_partials=bad)
+        assert hc.get_config()["bf16_partials"] == 0
+        hc.set_config(bf16_partials=1)
+        assert hc.get_config()["bf16_partials"] == 1
         assert hc.get_config()["workgroups_per_step"] == 64
     finally:
         hc.set_config(**saved)

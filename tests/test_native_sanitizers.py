@@ -35,7 +35,7 @@ def test_planner_and_scheduler_under_sanitizers(tmp_path):
            os.path.join(HERE, "native", "plan_bounds.cpp"), os.path.join(CSRC, "plan.cpp"),
            os.path.join(CSRC, "schedule.cpp"), "-o", exe]
     out = _run(cmd, tmp_path, exe)
-    assert "plans replayed: 17920" in out, out
+    assert "plans replayed: 18432" in out, out
 
 
 @pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc not available")

@@ -48,10 +48,19 @@ def replay(plan, send, recv):
         assert off + nbytes <= arr.size, (ref, nbytes, arr.size)
         return arr[off:off + nbytes]
 
+    # bf16 partials: the partials are bf16 like the operands, and every
+    # addition's result is rounded (narrow then widen) before the next.
+    bf16p = bool(plan["bf16_partials"])
+
+    def rounded(v):
+        if not bf16p:
+            return v
+        return widen(narrow(v, dt, False).view(np.uint16), dt, False)
+
     for st in plan["reduce_steps"]:
         ph = st["phase"]
-        in0_acc = ph in ("middle", "last")
-        out_acc = ph in ("first", "middle")
+        in0_acc = ph in ("middle", "last") and not bf16p
+        out_acc = ph in ("first", "middle") and not bf16p
         for g in st["segs"]:
             n = g["n"]
             r = widen(region(g["in0"], n * (4 if in0_acc else es)).copy(), dt, in0_acc)
@@ -61,7 +70,7 @@ def replay(plan, send, recv):
                 if dt == hc.INT32:
                     r = (r.astype(np.uint64) + b.astype(np.uint64)) & 0xFFFFFFFF
                 else:
-                    r = r + b
+                    r = rounded(r + b)
             region(g["out"], n * (4 if out_acc else es))[:] = narrow(r, dt, out_acc)
     f = plan["fold"]
     if f is not None:
@@ -80,7 +89,7 @@ def replay(plan, send, recv):
                 elif dt == hc.INT32:
                     acc = (acc + x.astype(np.uint64)) & 0xFFFFFFFF
                 else:
-                    acc = acc + x
+                    acc = rounded(acc + x)
             y = narrow(acc, dt, False)
             oe = 0 if f["out_at_chunk"] else e0
             outs = range(R) if f["write_all"] else [j]
@@ -297,3 +306,57 @@ def test_alltoall_stages_are_matchings_and_complete(R):
         arr = cov.setdefault(c["dst"][1], np.zeros(R * n * 2, np.int32))
         arr[c["dst"][2]:c["dst"][2] + c["bytes"]] += 1
     assert all((a == 1).all() for a in cov.values()) and len(cov) == R
+
+
+BF16P_CONFIGS = [
+    dict(bf16_partials=1, reduce_algo="ring"),
+    dict(bf16_partials=1, reduce_algo="direct"),
+    dict(bf16_partials=1, reduce_algo="auto"),
+    dict(bf16_partials=1, reduce_algo="ring", fused_hops=3, allreduce_chunk_groups=2),
+    dict(bf16_partials=1, reduce_algo="ring", ring_group_bytes=1000, chunk_bytes=4096),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(BF16P_CONFIGS)), ids=lambda i: "bf16p%d" % i)
+@pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 8])
+def test_bf16_partial_plans_replay_to_oracle(ci, R):
+    """With bf16 partials, bf16 plans replay to the oracle's sums whose every
+    hop is rounded to bf16; fp32 and int32 plans are the usual ones."""
+    with hc.config(**BF16P_CONFIGS[ci]):
+        for n in [1, 7, R * 5 + 3, 3001]:
+            seed = 900 + R * 7 + n
+            x = [W.random_values("bf16", seed, r, n) for r in range(R)]
+            plan = hc.plan_json(hc.OP_ALLREDUCE, n, hc.BF16, R)
+            assert plan["bf16_partials"] == 1
+            assert all(st["hops"] == 1 for st in plan["reduce_steps"])
+            ref = oracle.allreduce_bf16_hops_new(x)
+            recv = [np.zeros(n * 2, np.uint8) for _ in range(R)]
+            replay(plan, as_bytes(x), recv)
+            for r in range(R):
+                assert np.array_equal(recv[r], as_bytes([ref[r]])[0]), ("allreduce", n, r)
+            x = [W.random_values("bf16", seed + 1, r, R * n) for r in range(R)]
+            ref = oracle.reduce_scatter_bf16_hops_new(x)
+            recv = [np.zeros(n * 2, np.uint8) for _ in range(R)]
+            replay(hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, R), as_bytes(x), recv)
+            for r in range(R):
+                assert np.array_equal(recv[r], as_bytes([ref[r]])[0]), ("reduce_scatter", n, r)
+            for dt in (hc.FP32, hc.INT32):
+                plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, dt, R)
+                assert plan["bf16_partials"] == 0
+                x = [W.random_values(NAME[dt], seed + 2, r, R * n) for r in range(R)]
+                ref = oracle.reduce_scatter_new(x, dt)
+                recv = [np.zeros(n * 4, np.uint8) for _ in range(R)]
+                replay(plan, as_bytes(x), recv)
+                for r in range(R):
+                    assert np.array_equal(recv[r], as_bytes([ref[r]])[0]), (NAME[dt], n, r)
+
+
+def test_bf16_partial_bytes():
+    """bf16 ring reduce-scatter with bf16 partials moves 2+2+2 bytes per
+    element on each of its R-1 hops and keeps R*n bf16 partials."""
+    R, n = 8, 1 << 20
+    with hc.config(bf16_partials=1, reduce_algo="ring", ring_group_bytes=(1 << 64) - 1, fused_hops=4):
+        plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, R)
+        assert plan["hbm_bytes"] == R * n * 6 * (R - 1)
+        assert plan["ws_bytes"] == R * n * 2
+        assert len(plan["reduce_steps"]) == R - 1
