@@ -1,9 +1,10 @@
 """Randomised GPU parity: 160 seeded cases (HOCCL_RANDOM_CASES=N for more),
 each drawing a collective, dtype (bytes for a quarter of the copies), rank
 count (up to 64), ragged count, misaligned buffer offset, copy path,
-reduction algorithm, launch shape, group options and the engine proxy's
-issue mode, run through the C ABI and compared bit for bit with the
-oracle."""
+reduction algorithm, launch shape, group options, the engine proxy's issue
+mode and, for a quarter, bf16 partials rounded at every hop, run through
+the C ABI and compared bit for bit with the oracle (its per-hop-rounding
+sums where that mode meets bf16)."""
 import os
 
 import numpy as np
@@ -45,6 +46,8 @@ def draw(i):
     # A quarter of the copy collectives move single bytes instead.
     if g.random() < 0.25 and c["op"] in ("allgather", "sendrecv", "alltoall", "alltoallv"):
         c["dt"] = hc.UINT8
+    # A quarter of the cases keep bf16 partials in bf16 (rounded every hop).
+    c["cfg"]["bf16_partials"] = int(g.random() < 0.25)
     return c
 
 
@@ -78,14 +81,15 @@ def test_random_case(i):
     if c["cfg"]["a2a_schedule"] == 2 and c["cfg"]["copy_path"] in ("engines", "auto"):
         c["cfg"]["a2a_schedule"] = 1
     es = ES[dt]
+    hops = dt == hc.BF16 and c["cfg"]["bf16_partials"] == 1
     with hc.config(**c["cfg"]):
         if op == "allreduce":
             x = [W.random_values(NAME[dt], seed, r, n) for r in range(R)]
-            ref = oracle.allreduce_new(x, dt)
+            ref = oracle.allreduce_bf16_hops_new(x) if hops else oracle.allreduce_new(x, dt)
             out = hc.allreduce(dev_views(x, dt, lead), empty_views(n, R, dt, lead))
         elif op == "reduce_scatter":
             x = [W.random_values(NAME[dt], seed, r, R * n) for r in range(R)]
-            ref = oracle.reduce_scatter_new(x, dt)
+            ref = oracle.reduce_scatter_bf16_hops_new(x) if hops else oracle.reduce_scatter_new(x, dt)
             out = hc.reduce_scatter(dev_views(x, dt, lead), empty_views(n, R, dt, lead))
         elif op == "allgather":
             x = [W.random_bits(seed, r, n, es).view(NPDT[dt]) for r in range(R)]

@@ -19,6 +19,9 @@ configs = st.fixed_dictionaries({
     "ring_group_bytes": st.sampled_from([0, 1000, 4096, 65536]),
     "reduce_algo": st.sampled_from(["ring", "direct"]),
     "allgather_direct": st.sampled_from([0, 1]),
+    "fused_hops": st.sampled_from([1, 2, 3, 64]),
+    "a2a_schedule": st.sampled_from([0, 1, 2]),
+    "bf16_partials": st.sampled_from([0, 1]),
 })
 
 
@@ -31,15 +34,16 @@ def test_random_plans_replay_to_oracle(op, dt, R, n, seed, cfg):
     if R >= 16:
         n = min(n, 97)                     # keep R * R * n small
     es = ES[dt]
+    hops = dt == hc.BF16 and cfg["bf16_partials"] == 1
     with hc.config(**cfg):
         plan = hc.plan_json(op, n, dt, R)
     if op == hc.OP_ALLREDUCE:
         x = [W.random_values(NAME[dt], seed, r, n) for r in range(R)]
-        ref = oracle.allreduce_new(x, dt)
+        ref = oracle.allreduce_bf16_hops_new(x) if hops else oracle.allreduce_new(x, dt)
         recv = [np.zeros(n * es, np.uint8) for _ in range(R)]
     elif op == hc.OP_REDUCE_SCATTER:
         x = [W.random_values(NAME[dt], seed, r, R * n) for r in range(R)]
-        ref = oracle.reduce_scatter_new(x, dt)
+        ref = oracle.reduce_scatter_bf16_hops_new(x) if hops else oracle.reduce_scatter_new(x, dt)
         recv = [np.zeros(n * es, np.uint8) for _ in range(R)]
     elif op == hc.OP_ALLGATHER:
         x = [W.random_bits(seed, r, n, es) for r in range(R)]
