@@ -433,10 +433,11 @@ hoccl_status_t hoccl_reduce_scatter(const void *const *send, void *const *recv,
  * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
  * operation, arguments and results as hoccl_reduce_scatter, bit for bit,
  * but the call allocates nothing and creates no stream or event.  Where the
- * ring keeps fp32 partials (bf16 over more than two ranks; int32 / fp32 in
+ * ring keeps partials (bf16 over more than two ranks; int32 / fp32 in
  * place) they live in a static device array of 128 MiB that every device
  * the library runs on holds from initialisation until the process ends.  A
- * call that needs more (R * recvcount * 4 bytes beyond 128 MiB) returns
+ * call that needs more (R * recvcount * 4 bytes, or 2 for bf16 with
+ * bf16_partials, beyond 128 MiB) returns
  * HOCCL_ERR_INVALID_ARG and enqueues nothing; the reduction the
  * configuration picks decides whether any is needed (the direct fold needs
  * none).  The library must already be initialised on the current device

@@ -71,6 +71,27 @@ def test_noalloc_matches_reduce_scatter_on_calls_in_a_row(algo):
             assert_bitwise(from_dev(got[r], dt), from_dev(want[r], dt), f"rank {r}")
 
 
+def test_noalloc_bf16_partials_fit_twice_the_elements():
+    """bf16 partials take 2 bytes per element: a bf16 ring reduce-scatter
+    whose fp32 partials would overflow the scratch fits with them, and
+    matches hoccl_reduce_scatter in that mode, on two calls in a row, the
+    second smaller."""
+    hc.init(0)
+    hc.set_config(reduce_algo="ring", bf16_partials=1)
+    for R, n in ((8, 4_200_000), (5, 3001)):
+        print(f"noalloc bf16 partials R={R} n={n}", flush=True)
+        x = [W.random_values("bf16", 77 + R, r, R * n) for r in range(R)]
+        send = [to_dev(a, hc.BF16) for a in x]
+        want, got = canary_like(n, hc.BF16, R), canary_like(n, hc.BF16, R)
+        assert call("hoccl_reduce_scatter", send, want, n, hc.BF16) == hc.OK
+        torch.cuda.synchronize()
+        assert call("hoccl_reduce_scatter_noalloc", send, got, n, hc.BF16) == hc.OK, \
+            hc.lib().hoccl_last_error_string()
+        torch.cuda.synchronize()
+        for r in range(R):
+            assert_bitwise(from_dev(got[r], hc.BF16), from_dev(want[r], hc.BF16), f"rank {r}")
+
+
 def test_noalloc_rejects_what_the_scratch_cannot_hold():
     """A bf16 ring reduce-scatter whose fp32 partials (R * recvcount * 4
     bytes) exceed the 128 MiB scratch is refused before anything is
