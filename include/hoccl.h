@@ -145,7 +145,8 @@ typedef enum {
 typedef enum {
     HOCCL_REDUCE_RING = 0,   /* R-1 ring steps (or fused_hops steps per
                                 launch), one kernel launch per step over all
-                                ranks; fp32 partials for bf16              */
+                                ranks; fp32 partials for bf16 (bf16 ones
+                                with bf16_partials)                        */
     HOCCL_REDUCE_DIRECT = 1, /* one launch folds all R inputs in the ring
                                 order (fewer HBM bytes)                    */
     HOCCL_REDUCE_AUTO = 2    /* DIRECT where the one-GPU fold is faster:
@@ -218,7 +219,7 @@ typedef struct {
                                    explicit 2 returns HOCCL_ERR_UNSUPPORTED */
     size_t ring_group_bytes;    /* ring reduce-scatter / all-reduce run their
                                    R-1 steps group by group over slices of
-                                   every chunk, one group's fp32 partials
+                                   every chunk, one group's partials
                                    taking at most this many bytes, so they
                                    stay in the 256 MB last-level cache from
                                    step to step (same fold order, same bits).
