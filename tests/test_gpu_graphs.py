@@ -54,6 +54,27 @@ def test_reduce_scatter_in_a_graph(algo):
     replay_check(lambda s: hc.reduce_scatter(send, outs, stream=s), outs, ref, hc.BF16, algo)
 
 
+@pytest.mark.parametrize("algo", ["ring", "direct"])
+def test_bf16_partials_in_a_graph(algo):
+    """bf16 partials rounded at every hop: reduce-scatter and all-reduce
+    (whose gather copies go to the default copy path) replay to the
+    oracle's per-hop-rounding sums."""
+    hc.set_config(reduce_algo=algo, bf16_partials=1)
+    R, n = 8, 100_003
+    x = [W.random_values("bf16", 304, r, R * n) for r in range(R)]
+    ref = oracle.reduce_scatter_bf16_hops_new(x)
+    send = [to_dev(a, hc.BF16) for a in x]
+    outs = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    replay_check(lambda s: hc.reduce_scatter(send, outs, stream=s), outs, ref, hc.BF16,
+                 "RS bf16 partials " + algo)
+    xa = [W.random_values("bf16", 305, r, 70_001) for r in range(R)]
+    refa = oracle.allreduce_bf16_hops_new(xa)
+    senda = [to_dev(a, hc.BF16) for a in xa]
+    outa = [torch.empty(70_001, dtype=torch.bfloat16, device="cuda") for _ in range(R)]
+    replay_check(lambda s: hc.allreduce(senda, outa, stream=s), outa, refa, hc.BF16,
+                 "AR bf16 partials " + algo)
+
+
 @pytest.mark.parametrize("path", ["auto", "engines", "hip", "kernel"])
 def test_allgather_and_allreduce_in_a_graph(path):
     """On AUTO and the engine proxy the copies are recorded as a host node
