@@ -304,9 +304,9 @@ typedef struct {
                                    of the ring forwards its partial in the
                                    collective's own element type: the ring
                                    step moves 6 bytes per element instead
-                                   of 8 to 10 and keeps no fp32 workspace,
-                                   at up to R-1 roundings of error instead
-                                   of one.  The same ring order and the
+                                   of 8 to 10 and its workspace is half the
+                                   size, at up to R-1 roundings of error
+                                   instead of one.  The same ring order and the
                                    same roundings on the ring, the direct
                                    fold and every grouping; fused hops
                                    (fused_hops) are not used in this mode.
