@@ -136,9 +136,12 @@ static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
         st.step = s0;
         st.hops = s1 - s0;
         st.phase = first ? (last ? PH_ONLY : PH_FIRST) : (last ? PH_LAST : PH_MIDDLE);
-        for (int r = 0; r < R; ++r) {
+        // Segments in chunk order: launch block b serves segment b mod R
+        // and lands on XCD b mod 8, so at R = 8 chunk j's partial is
+        // written and read again by the same XCD at every step.
+        for (int j = 0; j < R; ++j) {
             // The rank performing hop s0 of chunk j is r = j + s0 + 2.
-            int j = mod(r - s0 - 2, R);
+            int r = mod(j + s0 + 2, R);
             size_t L = chunk_len[(size_t)j];
             if (g0 >= L) continue;
             size_t n = std::min(glen, L - g0);
