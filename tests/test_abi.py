@@ -322,3 +322,30 @@ def test_ipc_export_rejects_host_memory():
     off, size = C.c_size_t(0), C.c_size_t(0)
     host = (C.c_char * 256)()
     assert hc.lib().hoccl_ipc_export(C.addressof(host), buf, C.byref(off), C.byref(size)) != hc.OK
+
+
+def _config_under_env(env):
+    """The configuration a fresh process reads from HOCCL_* variables."""
+    import json
+    import subprocess
+    import sys
+    code = ("import json, paper_2609_34334_amd as hc; "
+            "c = hc.get_config(); print(json.dumps({k: c[k] for k in "
+            "('bf16_partials', 'fused_hops', 'a2a_schedule')}))")
+    e = dict(os.environ)
+    for k in list(e):
+        if k.startswith("HOCCL_"):
+            del e[k]
+    e.update(env)
+    out = subprocess.run([sys.executable, "-c", code], env=e, cwd=ROOT, capture_output=True,
+                         text=True, timeout=300, check=True)
+    return json.loads(out.stdout.strip().splitlines()[-1])
+
+
+def test_environment_sets_bf16_partials_and_invalid_sets_fall_back():
+    assert _config_under_env({}) == {"bf16_partials": 0, "fused_hops": 1, "a2a_schedule": 0}
+    assert _config_under_env({"HOCCL_BF16_PARTIALS": "1", "HOCCL_FUSED_HOPS": "3"}) == \
+        {"bf16_partials": 1, "fused_hops": 3, "a2a_schedule": 0}
+    # one invalid value discards the whole set, as the header states
+    assert _config_under_env({"HOCCL_BF16_PARTIALS": "2", "HOCCL_FUSED_HOPS": "3"}) == \
+        {"bf16_partials": 0, "fused_hops": 1, "a2a_schedule": 0}
