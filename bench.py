@@ -988,9 +988,9 @@ def bench_bf16_partials(hc, send_np, steps, warmup, samples=8192):
     exact = vals.sum(axis=0)
     scale = np.abs(vals).sum(axis=0) * 2.0 ** -8
     out = {}
-    for algo in ("ring", "direct"):
+    for algo, k in (("ring", 1), ("ring", 2), ("ring", 7), ("direct", 1)):
         for bp in (0, 1):
-            with hc.config(reduce_algo=algo, bf16_partials=bp, fused_hops=1, kernel_timing=0):
+            with hc.config(reduce_algo=algo, bf16_partials=bp, fused_hops=k, kernel_timing=0):
                 def step():
                     hc.reduce_scatter(send, recv, stream=stream)
                 for _ in range(warmup):
@@ -1008,14 +1008,15 @@ def bench_bf16_partials(hc, send_np, steps, warmup, samples=8192):
             got = torch.stack(recv).float().cpu().numpy()[ranks, idx].astype(np.float64)
             err = np.abs(got - exact) / np.where(scale > 0, scale, 1.0)
             b = st["hbm_bytes_algorithmic"]
-            out[f"{algo}_{'bf16' if bp else 'fp32'}_partials"] = dict(
+            label = algo if k == 1 else f"{algo}_k{k}"
+            out[f"{label}_{'bf16' if bp else 'fp32'}_partials"] = dict(
                 us=round(t * 1e6, 2), bytes_per_op=b, achieved_GBs=round(b / t / 1e9, 1),
                 frac=round(b / t / 1e9 / HBM_PEAK_GBS, 4), launches=st["reduce_launches"],
                 err_max=round(float(err.max()), 4), err_mean=round(float(err.mean()), 5))
     return dict(workload="reduce-scatter bf16 R=8, 25,165,824 elements per rank: bf16 partials "
-                         "(rounded at every hop) against fp32 partials (rounded once), ring and "
-                         "direct fold; error of %d sampled outputs against the exact sum, in units "
-                         "of 2^-8 * sum |x|" % samples, **out)
+                         "(rounded at every hop) against fp32 partials (rounded once), ring (one, "
+                         "two or seven hops per launch: k2, k7) and direct fold; error of %d sampled "
+                         "outputs against the exact sum, in units of 2^-8 * sum |x|" % samples, **out)
 
 
 def bench_rs_graph(hc, send_np, steps):

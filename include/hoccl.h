@@ -307,9 +307,8 @@ typedef struct {
                                    of 8 to 10 and its workspace is half the
                                    size, at up to R-1 roundings of error
                                    instead of one.  The same ring order and the
-                                   same roundings on the ring, the direct
-                                   fold and every grouping; fused hops
-                                   (fused_hops) are not used in this mode.
+                                   same roundings on the ring, fused hops,
+                                   the direct fold and every grouping.
                                    Other dtypes ignore it.  hoccl_ring_hop
                                    is unaffected: its HOCCL_HOP_ONLY is the
                                    bf16-partial hop                         */

@@ -473,7 +473,7 @@ hoccl_status_t run_reductions(DeviceState &st, const hoccl_config_t &cfg, const 
             a.nseg = ns;
             TimingPair *tp;
             TRY(timed_begin(st, cfg, s, &tp));
-            HIP_TRY(launch_multihop(p.dtype, step.phase, a, wg, threads, s));
+            HIP_TRY(launch_multihop(p.dtype, step.phase, a, wg, threads, s, p.bf16_partials));
             TRY(timed_end(tp, s));
             t_stats.reduce_launches++;
         }

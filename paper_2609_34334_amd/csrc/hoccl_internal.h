@@ -122,7 +122,7 @@ struct PlanOptions {
     // decomposition (copies tagged with their stage; 2 runs them serially).
     int a2a_schedule = 0;
     // bf16 reductions keep their partials in bf16, rounding every addition
-    // (hoccl_config_t.bf16_partials); one hop per ring launch.
+    // (hoccl_config_t.bf16_partials).
     bool bf16_partials = false;
 };
 
@@ -235,13 +235,13 @@ struct HandshakeArgs {
 
 // bf16_partials: a bf16 step keeps every operand and result in bf16 (the
 // middle and last phases read, and the first and middle write, bf16
-// partials); a bf16 fold rounds after every addition.
+// partials); a bf16 fold, or fused step, rounds after every addition.
 hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, int wg,
                               int threads, hipStream_t s, bool bf16_partials = false);
 hipError_t launch_fold(hoccl_dtype_t dt, const FoldArgs &a, int wg, int threads,
                        hipStream_t s, bool bf16_partials = false);
 hipError_t launch_multihop(hoccl_dtype_t dt, Phase ph, const MultiArgs &a, int wg, int threads,
-                           hipStream_t s);
+                           hipStream_t s, bool bf16_partials = false);
 hipError_t launch_copy(const CopyArgs &a, int wg, int threads, hipStream_t s);
 
 // Work one thread does in one pass of each kernel's main loop (elements of

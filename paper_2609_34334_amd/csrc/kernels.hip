@@ -254,13 +254,20 @@ __global__ void __launch_bounds__(1024) reduce_step_kernel(ReduceArgsT<CAP>) {
 // partial's round trips through memory between the fused hops are gone.
 // nloc is the same for every lane, so the guards on the unrolled
 // contribution loop are uniform branches.
-template <class T0, class T1, class TO, int VE, int U, int NT, int MAXL>
+template <class T0, class T1, class TO, int VE, int U, int NT, int MAXL, bool RH>
 __device__ __forceinline__ void multihop_segment(const MSegArg &s, int lb, int nb) {
     constexpr bool NT0 = NT & 1, NT1 = NT & 2, NTO = NT & 4;
     using S0 = typename T0::S;
     using S1 = typename T1::S;
     using SO = typename TO::S;
     using A = typename T1::A;
+    // RH: every addition's result is rounded to the contribution's type
+    // before the next (bf16 partials), as separate hops would round it.
+    auto add = [](A acc, S1 x) -> A {
+        A y = acc + T1::widen(x);
+        if constexpr (RH) y = T1::widen(T1::narrow(y));
+        return y;
+    };
     using P0 = Pack<S0, VE>;
     using P1 = Pack<S1, VE>;
     using PO = Pack<SO, VE>;
@@ -290,7 +297,7 @@ __device__ __forceinline__ void multihop_segment(const MSegArg &s, int lb, int n
         A acc = T0::widen(in0[k]);
 #pragma unroll
         for (int m = 0; m < MAXL; ++m)
-            if (m < nl) acc = acc + T1::widen(loc[m][k]);
+            if (m < nl) acc = add(acc, loc[m][k]);
         out[k] = TO::narrow(acc);
     };
     for (uint64_t k = t; k < h; k += stride) scalar(k);
@@ -314,7 +321,7 @@ __device__ __forceinline__ void multihop_segment(const MSegArg &s, int lb, int n
         for (int m = 0; m < MAXL; ++m)
             if (m < nl)
 #pragma unroll
-                for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T1::widen(b[m].v[e]);
+                for (int e = 0; e < VE; ++e) acc[e] = add(acc[e], b[m].v[e]);
         PO y;
 #pragma unroll
         for (int e = 0; e < VE; ++e) y.v[e] = TO::narrow(acc[e]);
@@ -342,7 +349,7 @@ __device__ __forceinline__ void multihop_segment(const MSegArg &s, int lb, int n
             for (int m = 0; m < MAXL; ++m)
                 if (m < nl)
 #pragma unroll
-                    for (int e = 0; e < VE; ++e) acc[e] = acc[e] + T1::widen(b[u][m].v[e]);
+                    for (int e = 0; e < VE; ++e) acc[e] = add(acc[e], b[u][m].v[e]);
             PO y;
 #pragma unroll
             for (int e = 0; e < VE; ++e) y.v[e] = TO::narrow(acc[e]);
@@ -357,11 +364,11 @@ __device__ __forceinline__ void multihop_segment(const MSegArg &s, int lb, int n
     }
 }
 
-template <class T0, class T1, class TO, int VE, int U, int NT, int MAXL, int CAP>
+template <class T0, class T1, class TO, int VE, int U, int NT, int MAXL, int CAP, bool RH>
 __global__ void __launch_bounds__(1024) multihop_kernel(MultiArgsT<CAP>) {
     const MultiArgsT<CAP> &a = kernargs<MultiArgsT<CAP>>();
-    for_each_segment(a.nseg, [&](int seg, int lb, int nb) {
-        multihop_segment<T0, T1, TO, VE, U, NT, MAXL>(a.seg[seg], lb, nb);
+    for_each_segment(a.nseg, [&](int seg, int lb, int nb) __attribute__((always_inline)) {
+        multihop_segment<T0, T1, TO, VE, U, NT, MAXL, RH>(a.seg[seg], lb, nb);
     });
 }
 
@@ -694,28 +701,35 @@ hipError_t launch_reduce_step(hoccl_dtype_t dt, Phase ph, const ReduceArgs &a, i
 // they need stay within the 128 VGPRs a 1024-thread launch bound allows
 // without spilling: bf16 2 whatever the bound; 32-bit types 4, 2 and 1 for
 // at most 2, 4 and 8 contributions.
-template <class T0, class T1, class TO, int NT, int MAXL>
+template <class T0, class T1, class TO, int NT, int MAXL, bool RH>
 static hipError_t launch_mh_l(const MultiArgs &a, int wg, int threads, hipStream_t s) {
     constexpr int U = sizeof(typename T1::S) == 2 ? 2 : (MAXL <= 2 ? 4 : (MAXL <= 4 ? 2 : 1));
     if (a.nseg <= kSmallSegs)
-        return launch((const void *)multihop_kernel<T0, T1, TO, 4, U, NT, MAXL, kSmallSegs>,
+        return launch((const void *)multihop_kernel<T0, T1, TO, 4, U, NT, MAXL, kSmallSegs, RH>,
                       fit<kSmallSegs>(a), wg, threads, s);
-    return launch((const void *)multihop_kernel<T0, T1, TO, 4, U, NT, MAXL, kMaxMultiSegs>, a, wg, threads,
-                  s);
+    return launch((const void *)multihop_kernel<T0, T1, TO, 4, U, NT, MAXL, kMaxMultiSegs, RH>, a, wg,
+                  threads, s);
 }
 
-template <class T0, class T1, class TO, int NT>
+template <class T0, class T1, class TO, int NT, bool RH = false>
 static hipError_t launch_mh(const MultiArgs &a, int wg, int threads, hipStream_t s) {
     int nl = 0;
     for (int k = 0; k < a.nseg; ++k) nl = a.seg[k].nloc > nl ? a.seg[k].nloc : nl;
-    if (nl <= 2) return launch_mh_l<T0, T1, TO, NT, 2>(a, wg, threads, s);
-    if (nl <= 4) return launch_mh_l<T0, T1, TO, NT, 4>(a, wg, threads, s);
-    return launch_mh_l<T0, T1, TO, NT, kMaxHops>(a, wg, threads, s);
+    if (nl <= 2) return launch_mh_l<T0, T1, TO, NT, 2, RH>(a, wg, threads, s);
+    if (nl <= 4) return launch_mh_l<T0, T1, TO, NT, 4, RH>(a, wg, threads, s);
+    return launch_mh_l<T0, T1, TO, NT, kMaxHops, RH>(a, wg, threads, s);
 }
 
 hipError_t launch_multihop(hoccl_dtype_t dt, Phase ph, const MultiArgs &a, int wg, int threads,
-                           hipStream_t s) {
-    if (dt == HOCCL_BF16) {
+                           hipStream_t s, bool bf16_partials) {
+    if (dt == HOCCL_BF16 && bf16_partials) {
+        switch (ph) {
+        case PH_FIRST: return launch_mh<TBF16, TBF16, TBF16, kNtFirst, true>(a, wg, threads, s);
+        case PH_MIDDLE: return launch_mh<TBF16, TBF16, TBF16, kNtMiddle, true>(a, wg, threads, s);
+        case PH_LAST: return launch_mh<TBF16, TBF16, TBF16, kNtLast, true>(a, wg, threads, s);
+        case PH_ONLY: return launch_mh<TBF16, TBF16, TBF16, kNtOnly, true>(a, wg, threads, s);
+        }
+    } else if (dt == HOCCL_BF16) {
         switch (ph) {
         case PH_FIRST: return launch_mh<TBF16, TBF16, TF32, kNtFirst>(a, wg, threads, s);
         case PH_MIDDLE: return launch_mh<TF32, TBF16, TF32, kNtMiddle>(a, wg, threads, s);

@@ -168,10 +168,8 @@ static void ring_reduce(Plan &p, hoccl_dtype_t dt, int R, size_t stride,
     }
 }
 
-// Hops per ring launch from the option (0 and 1: one), at most kMaxHops;
-// one with bf16 partials, whose every addition is rounded in memory's type.
-static int hops_per_launch(const Plan &p, const PlanOptions &o) {
-    if (p.bf16_partials) return 1;
+// Hops per ring launch from the option (0 and 1: one), at most kMaxHops.
+static int hops_per_launch(const PlanOptions &o) {
     return std::max(1, std::min(o.fused_hops, kMaxHops));
 }
 
@@ -215,7 +213,7 @@ Plan plan_reduce_scatter(size_t n, hoccl_dtype_t dt, int R, const PlanOptions &o
     const int G = cache_groups(R, n, dt, p.bf16_partials, o.group_partial_bytes);
     const size_t gl = (n + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;
-    const int H = hops_per_launch(p, o);
+    const int H = hops_per_launch(o);
     for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, n, len, (size_t)g * gl, gl, g, true, H);
     // Partials cross launches only when the hops take more than one.
     p.ws_bytes = (R - 1 > H) ? (size_t)R * n * acc_size(dt, p.bf16_partials) : 0;
@@ -263,7 +261,7 @@ Plan plan_allreduce(size_t count, hoccl_dtype_t dt, int R, const PlanOptions &o)
     if ((size_t)G > c) G = (int)c;
     size_t cg = (c + (size_t)G - 1) / (size_t)G;
     p.ngroups = G;
-    const int H = hops_per_launch(p, o);
+    const int H = hops_per_launch(o);
     for (int g = 0; g < G; ++g) ring_reduce(p, dt, R, c, len, (size_t)g * cg, cg, g, false, H);
     // Gather phase: chunk j (group g) travels j -> j+1 -> ... -> j-1.
     int maxp = 1;

@@ -50,8 +50,8 @@ def run_ar(x, lead=0):
 @pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 8, 13, 16])
 def test_bf16_partials_match_the_oracle(algo, R):
     """Every size from one element to several tiles with a ragged tail; the
-    ring takes R-1 one-hop launches whatever fused_hops says."""
-    hc.set_config(bf16_partials=1, reduce_algo=algo, copy_path="hip", fused_hops=3)
+    ring takes R-1 one-hop launches."""
+    hc.set_config(bf16_partials=1, reduce_algo=algo, copy_path="hip", fused_hops=1)
     differs = False
     for n in [1, 7, R * 37 + 3, 4099, 65536 + 5]:
         seed = 9400 + 13 * R + n
@@ -72,6 +72,28 @@ def test_bf16_partials_match_the_oracle(algo, R):
     # the mode is observable: from three ranks on, the per-hop roundings
     # change some sums against a single rounding
     assert differs or R <= 2
+
+
+@pytest.mark.parametrize("hops", [2, 3, 7, 64])
+@pytest.mark.parametrize("R", [3, 4, 8, 13])
+def test_bf16_partials_with_fused_hops(hops, R):
+    """k hops per launch round every addition as k separate hops would:
+    the oracle's per-hop-rounding bits, in ceil((R-1)/k) launches of at
+    most 8 hops, ragged and misaligned."""
+    hc.set_config(bf16_partials=1, reduce_algo="ring", copy_path="hip", fused_hops=hops)
+    k = min(hops, 8)
+    for n in [1, 7, R * 37 + 3, 65536 + 5]:
+        x = [W.random_values("bf16", 9540 + R + hops, r, R * n) for r in range(R)]
+        ref = oracle.reduce_scatter_bf16_hops_new(x)
+        got = run_rs(x, lead=3)
+        assert hc.last_stats()["reduce_launches"] == -(-(R - 1) // k)
+        for r in range(R):
+            assert_bitwise(got[r], ref[r], f"fused RS k={hops} R={R} n={n} r={r}")
+        xa = [W.random_values("bf16", 9550 + R + hops, r, n) for r in range(R)]
+        refa = oracle.allreduce_bf16_hops_new(xa)
+        gota = run_ar(xa, lead=1)
+        for r in range(R):
+            assert_bitwise(gota[r], refa[r], f"fused AR k={hops} R={R} n={n} r={r}")
 
 
 @pytest.mark.parametrize("path", ["hip", "engines", "kernel"])

@@ -313,6 +313,7 @@ BF16P_CONFIGS = [
     dict(bf16_partials=1, reduce_algo="direct"),
     dict(bf16_partials=1, reduce_algo="auto"),
     dict(bf16_partials=1, reduce_algo="ring", fused_hops=3, allreduce_chunk_groups=2),
+    dict(bf16_partials=1, reduce_algo="ring", fused_hops=64),
     dict(bf16_partials=1, reduce_algo="ring", ring_group_bytes=1000, chunk_bytes=4096),
 ]
 
@@ -328,7 +329,8 @@ def test_bf16_partial_plans_replay_to_oracle(ci, R):
             x = [W.random_values("bf16", seed, r, n) for r in range(R)]
             plan = hc.plan_json(hc.OP_ALLREDUCE, n, hc.BF16, R)
             assert plan["bf16_partials"] == 1
-            assert all(st["hops"] == 1 for st in plan["reduce_steps"])
+            k = max(1, min(BF16P_CONFIGS[ci].get("fused_hops", 1), 8))
+            assert all(st["hops"] <= k for st in plan["reduce_steps"])
             ref = oracle.allreduce_bf16_hops_new(x)
             recv = [np.zeros(n * 2, np.uint8) for _ in range(R)]
             replay(plan, as_bytes(x), recv)
@@ -353,10 +355,16 @@ def test_bf16_partial_plans_replay_to_oracle(ci, R):
 
 def test_bf16_partial_bytes():
     """bf16 ring reduce-scatter with bf16 partials moves 2+2+2 bytes per
-    element on each of its R-1 hops and keeps R*n bf16 partials."""
+    element on each of its R-1 hops and keeps R*n bf16 partials; with 4
+    hops per launch, 2+2+3*2+2 and then 2+2+2*2+2 bytes in 2 launches."""
     R, n = 8, 1 << 20
-    with hc.config(bf16_partials=1, reduce_algo="ring", ring_group_bytes=(1 << 64) - 1, fused_hops=4):
+    with hc.config(bf16_partials=1, reduce_algo="ring", ring_group_bytes=(1 << 64) - 1, fused_hops=1):
         plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, R)
         assert plan["hbm_bytes"] == R * n * 6 * (R - 1)
         assert plan["ws_bytes"] == R * n * 2
         assert len(plan["reduce_steps"]) == R - 1
+    with hc.config(bf16_partials=1, reduce_algo="ring", ring_group_bytes=(1 << 64) - 1, fused_hops=4):
+        plan = hc.plan_json(hc.OP_REDUCE_SCATTER, n, hc.BF16, R)
+        assert plan["hbm_bytes"] == R * n * (12 + 10)
+        assert plan["ws_bytes"] == R * n * 2
+        assert [st["hops"] for st in plan["reduce_steps"]] == [4, 3]
