@@ -2,9 +2,9 @@
 each drawing a collective, dtype (bytes for a quarter of the copies), rank
 count (up to 64), ragged count, misaligned buffer offset, copy path,
 reduction algorithm, launch shape, group options, the engine proxy's issue
-mode and, for a quarter, bf16 partials rounded at every hop, run through
-the C ABI and compared bit for bit with the oracle (its per-hop-rounding
-sums where that mode meets bf16)."""
+mode, the ring hops fused per launch and, for a quarter, bf16 partials
+rounded at every hop, run through the C ABI and compared bit for bit with
+the oracle (its per-hop-rounding sums where that mode meets bf16)."""
 import os
 
 import numpy as np
@@ -48,6 +48,8 @@ def draw(i):
         c["dt"] = hc.UINT8
     # A quarter of the cases keep bf16 partials in bf16 (rounded every hop).
     c["cfg"]["bf16_partials"] = int(g.random() < 0.25)
+    # Ring hops folded per launch (the same bits as one per launch).
+    c["cfg"]["fused_hops"] = int(g.choice([1, 1, 2, 3, 8]))
     return c
 
 
