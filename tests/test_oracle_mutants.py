@@ -102,6 +102,7 @@ def battery():
          lambda: [P.test_ring_simulation_matches_oracle(d, R) for d in ("int32", "fp32", "bf16") for R in (3, 4)]),
         ("bf16 partials: ring simulation", lambda: [P.test_bf16_hops_ring_simulation_matches_oracle(R) for R in (3, 4)]),
         ("bf16 partials: worked example", P.test_bf16_hops_worked_example),
+        ("bf16 partials: four-rank example", P.test_bf16_hops_worked_example_four_ranks),
         ("bf16 partials: special cases", P.test_bf16_hops_special_cases),
         ("bf16 partials: error bound", lambda: P.test_bf16_hops_within_bound(3)),
     ]

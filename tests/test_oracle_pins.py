@@ -430,6 +430,24 @@ def test_bf16_hops_worked_example():
     assert oracle.reduce_scatter_bf16_hops_new(x)[0][0] == one
 
 
+def test_bf16_hops_worked_example_four_ranks():
+    """Four ranks, block 0: the ring folds x1 = 1, then x2 = x3 = x0 = 2^-8.
+    Rounded at every hop, each 1 + 2^-8 is a tie that goes to the even 1, so
+    the result is 1 (0x3F80).  Rounded once, 1 + 3*2^-8 is a tie between
+    1 + 2^-7 and 1 + 2^-6 that goes to the even 1 + 2^-6 (0x3F82).  A fold
+    that starts one rank later, or runs backwards, adds the three small
+    terms first (exactly, 3*2^-8) and also gives 0x3F82, so only the ring's
+    order with per-hop rounding gives 0x3F80.  All-reduce's block 0 is the
+    same sum."""
+    one, eps = 0x3F80, 0x3B80
+    vals = [eps, one, eps, eps]                              # x0, x1, x2, x3 at block 0
+    x = [np.concatenate([[v], np.zeros(3)]).astype(np.uint16) for v in vals]
+    assert oracle.reduce_scatter_new(x, oracle.BF16)[0][0] == 0x3F82
+    assert oracle.reduce_scatter_bf16_hops_new(x)[0][0] == 0x3F80
+    assert all(r[0] == 0x3F80 for r in oracle.allreduce_bf16_hops_new(x))
+    assert all(r[0] == 0x3F82 for r in oracle.allreduce_new(x, oracle.BF16))
+
+
 def test_bf16_hops_special_cases():
     """Two ranks round once in either mode; sums of small integers are exact
     in either mode; rank-count 1 is the identity."""
