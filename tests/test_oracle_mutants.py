@@ -67,6 +67,12 @@ MUTANTS = [
      "uint16_t part = ((const uint16_t *)x[(j + 1) % R])[i];", "uint16_t part = ((const uint16_t *)x[j % R])[i];", 1),
     ("bf16 partials: the fold drops rank j's own term",
      "for (int k = 2; k <= R; ++k)", "for (int k = 2; k < R; ++k)", 1),
+    ("bf16 partials: each hop subtracts its contribution",
+     "part = oracle_f32_to_bf16(bf16_to_f32(part) + bf16_to_f32(xr[i]));",
+     "part = oracle_f32_to_bf16(bf16_to_f32(part) - bf16_to_f32(xr[i]));", 1),
+    ("bf16 partials: the hops run backwards (j+1, j, j-1, ..., j+2)",
+     "(const uint16_t *)x[(j + k) % R];\n        part =",
+     "(const uint16_t *)x[(j + R + 2 - k) % R];\n        part =", 1),
     ("send/recv runs the wrong direction",
      "memcpy((unsigned char *)recv[d] + i * es,\n                   (const unsigned char *)send[r] + i * es, es);",
      "memcpy((unsigned char *)recv[r] + i * es,\n                   (const unsigned char *)send[d] + i * es, es);", 1),
